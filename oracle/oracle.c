@@ -1,0 +1,781 @@
+/*
+ * CPU oracle for the line-granularity network model -- TEST INFRASTRUCTURE.
+ *
+ * This file is the plain, slow, single-threaded reference that the GPU
+ * library is checked against.  Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg may load it; the product never does.  It
+ * shares no code, header or table with the GPU library.
+ *
+ * What it computes (paper: Sec. 4.4 "Wavefront Request" -- a 128 B
+ * cache-line transfer is the unit the network simulates; Sec. 4.5 "Detailed
+ * Simple Network Modeling" -- the network is a graph of endpoints and
+ * switches with a routing function; Sec. 2.1 -- the Simple backend is an
+ * alpha-beta model; Sec. 1/2 list ring and direct collectives).  The paper
+ * leaves the queueing discipline unstated, so the model below is the reading
+ * this project adopts (all readings are listed with the design notes):
+ *
+ *   link l : FIFO of (line, ready) entries; integer bandwidth b (lines per
+ *            cycle), latency L (cycles), capacity cap (lines in flight plus
+ *            waiting).  Entered at cycle t -> may leave at t + L.
+ *   cycle t (every decision uses the state at the start of t):
+ *     requests  each FIFO offers its first <= b entries with ready <= t
+ *               (stopping at the first not-ready one); each injection stream
+ *               (src endpoint, first link) offers its first <= b released
+ *               lines in ascending id (stopping at the first unreleased one).
+ *               The k-th offered line requests the next link of its path, or
+ *               the sink when the current link is its last hop.
+ *     grants    per link f: order the requests (lowest line id first, or
+ *               round-robin: ascending (k, (port - rr_f) mod P)) and grant
+ *               the first min(b_f, cap_f - occ_f, #requests); the sink
+ *               grants everything.
+ *     departures from every source exactly the longest granted prefix
+ *               (k = 0, 1, ...) departs; a grant beyond it is void.
+ *     enter     departing lines join their target FIFO in grant order with
+ *               ready = t + L; counters; round-robin pointer moves past the
+ *               port of the last appended line.
+ *     eject     a line leaving to the sink completes at t + 1.
+ *     time      next cycle is t + 1 if anything departed, else the earliest
+ *               future FIFO-head ready time; no such time while lines remain
+ *               is a deadlock.
+ *   routing   minimal hop paths; among equal-length next hops, a choice by
+ *             the MurmurHash3 32-bit finalizer of (src << 16 | dst).
+ *   release   a line may be injected once all its predecessor lines have
+ *             completed (rel = max predecessor completion, 0 if none).
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <time.h>
+
+#define OR_OK 0
+#define OR_ERR_INVALID_ARG 1
+#define OR_ERR_TOPOLOGY 2
+#define OR_ERR_UNREACHABLE 3
+#define OR_ERR_SIZE 4
+#define OR_ERR_OOM 5
+#define OR_ERR_DEADLOCK 7
+#define OR_ERR_MAX_CYCLES 8
+#define OR_ERR_INVARIANT 100
+
+#define NEVER 0xFFFFFFFFu
+#define SINK (-1)
+
+/* ---------------------------------------------------------------- hashing */
+
+/* MurmurHash3 (Appleby) 32-bit finalizer: xor-shift 16, multiply by
+ * 0x85ebca6b, xor-shift 13, multiply by 0xc2b2ae35, xor-shift 16. */
+uint32_t oracle_fmix32(uint32_t h)
+{
+    h ^= h >> 16;
+    h *= 0x85ebca6bu;
+    h ^= h >> 13;
+    h *= 0xc2b2ae35u;
+    h ^= h >> 16;
+    return h;
+}
+
+/* ---------------------------------------------------------------- routing */
+
+/* Hop distance from every node to endpoint d: breadth-first search from d
+ * over the reversed links (in_ptr/in_tail list, for each node w, the tails
+ * of the links entering w).  dist = -1 when d is unreachable. */
+static void bfs_to(int32_t n, const int32_t *in_ptr, const int32_t *in_tail,
+                   int32_t d, int32_t *dist, int32_t *queue)
+{
+    for (int32_t v = 0; v < n; v++) dist[v] = -1;
+    dist[d] = 0;
+    int32_t qh = 0, qt = 0;
+    queue[qt++] = d;
+    while (qh < qt) {
+        int32_t w = queue[qh++];
+        for (int32_t q = in_ptr[w]; q < in_ptr[w + 1]; q++) {
+            int32_t u = in_tail[q];
+            if (dist[u] >= 0) continue;
+            dist[u] = dist[w] + 1;
+            queue[qt++] = u;
+        }
+    }
+}
+
+/* Path of flow (s, d) given dist-to-d.  At each node the candidates are the
+ * out-links (ascending id) whose head is one hop closer to d; at the j-th
+ * node with two or more candidates, the choice is byte (j mod 4) of the hash
+ * modulo the candidate count, and the hash is re-mixed before every fourth
+ * choice point after the first.  Returns the hop count. */
+static int32_t trace_path(const int32_t *row_ptr, const int32_t *col_idx,
+                          const int32_t *dist, int32_t s, int32_t d,
+                          int32_t *out)
+{
+    uint32_t h = oracle_fmix32(((uint32_t)s << 16) | (uint32_t)d);
+    int32_t v = s, len = 0, j = 0;
+    int32_t cand[4096];
+    while (v != d) {
+        int32_t nc = 0;
+        for (int32_t l = row_ptr[v]; l < row_ptr[v + 1]; l++)
+            if (dist[col_idx[l]] == dist[v] - 1) cand[nc++] = l;
+        int32_t pick;
+        if (nc == 1) {
+            pick = cand[0];
+        } else {
+            if (j > 0 && j % 4 == 0) h = oracle_fmix32(h);
+            pick = cand[((h >> (8 * (j % 4))) & 255u) % (uint32_t)nc];
+            j++;
+        }
+        out[len++] = pick;
+        v = col_idx[pick];
+    }
+    return len;
+}
+
+/* All E*E flow paths.  path_ptr has E*E+1 entries (flow = s*E + d).  A pair
+ * with s == d or with no path gets an empty path.  Returns OR_ERR_SIZE if
+ * path_cap is too small (path_ptr[E*E] then holds the need). */
+int oracle_paths(int32_t n, int32_t E, const int32_t *row_ptr,
+                 const int32_t *col_idx, int64_t *path_ptr, int32_t *path_link,
+                 int64_t path_cap)
+{
+    int32_t *dist = malloc(sizeof(int32_t) * (size_t)n * (size_t)E);
+    int32_t *queue = malloc(sizeof(int32_t) * (size_t)n);
+    int32_t *tmp = malloc(sizeof(int32_t) * (size_t)(n + 1));
+    if (!dist || !queue || !tmp) { free(dist); free(queue); free(tmp); return OR_ERR_OOM; }
+    int rc = OR_OK;
+    int32_t m = row_ptr[n];
+    int32_t *in_ptr = calloc((size_t)n + 1, sizeof(int32_t));
+    int32_t *in_tail = malloc(sizeof(int32_t) * (size_t)(m + 1));
+    int32_t *fill = calloc((size_t)n, sizeof(int32_t));
+    for (int32_t l = 0; l < m; l++) in_ptr[col_idx[l] + 1]++;
+    for (int32_t v = 0; v < n; v++) in_ptr[v + 1] += in_ptr[v];
+    for (int32_t u = 0; u < n; u++)
+        for (int32_t l = row_ptr[u]; l < row_ptr[u + 1]; l++)
+            in_tail[in_ptr[col_idx[l]] + fill[col_idx[l]]++] = u;
+    for (int32_t d = 0; d < E; d++) bfs_to(n, in_ptr, in_tail, d, dist + (size_t)d * n, queue);
+    free(in_ptr); free(in_tail); free(fill);
+    int64_t pos = 0;
+    for (int32_t s = 0; s < E && rc == OR_OK; s++) {
+        for (int32_t d = 0; d < E; d++) {
+            path_ptr[(int64_t)s * E + d] = pos;
+            if (s == d) continue;
+            const int32_t *dd = dist + (size_t)d * n;
+            if (dd[s] < 0) continue;  /* unreachable: empty path */
+            int32_t len = trace_path(row_ptr, col_idx, dd, s, d, tmp);
+            if (pos + len <= path_cap) memcpy(path_link + pos, tmp, sizeof(int32_t) * (size_t)len);
+            pos += len;
+        }
+    }
+    path_ptr[(int64_t)E * E] = pos;
+    if (rc == OR_OK && pos > path_cap) rc = OR_ERR_SIZE;
+    free(dist); free(queue); free(tmp);
+    return rc;
+}
+
+/* ------------------------------------------------------ workload expansion */
+
+enum { COLL_RING = 0, COLL_DIRECT = 1, COLL_HIER = 2, COLL_A2A = 3, COLL_CUSTOM = -1 };
+
+typedef struct {
+    int coll;
+    int32_t E;              /* endpoints */
+    int32_t p;              /* participants (ring/direct: all endpoints) */
+    const int32_t *rho;     /* ring order (NULL = rank order) */
+    int64_t C;              /* ring/direct/a2a chunk lines */
+    int64_t G, M, C1, C2, B2, B3;  /* hierarchical */
+    int64_t T;
+    /* custom */
+    const int32_t *csrc, *cdst;
+    const int64_t *pptr, *pidx;
+} work_t;
+
+static int32_t rho_of(const work_t *w, int64_t i) { return w->rho ? w->rho[i] : (int32_t)i; }
+
+/* Transaction-id spaces are step-major: for each collective the id is a
+ * mixed-radix number whose most significant digit is the algorithm step, so
+ * that lowest-id arbitration favours earlier steps. */
+static int setup_work(work_t *w, int coll, uint64_t bytes, int32_t group, int32_t E,
+                      const int32_t *order)
+{
+    memset(w, 0, sizeof(*w));
+    w->coll = coll; w->E = E; w->p = E; w->rho = order;
+    if (bytes == 0 || bytes % 128 != 0) return OR_ERR_SIZE;
+    int64_t N = (int64_t)(bytes / 128);  /* lines */
+    if (E < 2) return OR_ERR_INVALID_ARG;
+    switch (coll) {
+    case COLL_RING:
+        if (N % E) return OR_ERR_SIZE;
+        w->C = N / E;
+        w->T = (2 * (int64_t)E - 2) * E * w->C;
+        break;
+    case COLL_DIRECT:
+        if (N % E) return OR_ERR_SIZE;
+        w->C = N / E;
+        w->T = 2 * (int64_t)(E - 1) * E * w->C;
+        break;
+    case COLL_HIER:
+        if (group < 2 || E % group || E / group < 2) return OR_ERR_INVALID_ARG;
+        w->M = group; w->G = E / group;
+        if (N % w->M) return OR_ERR_SIZE;
+        w->C1 = N / w->M;
+        if (w->C1 % w->G) return OR_ERR_SIZE;
+        w->C2 = w->C1 / w->G;
+        w->B2 = (w->M - 1) * w->G * w->M * w->C1;
+        w->B3 = w->B2 + (2 * w->G - 2) * w->M * w->G * w->C2;
+        w->T = w->B3 + (w->M - 1) * w->G * w->M * w->C1;
+        break;
+    case COLL_A2A:
+        w->C = N;
+        w->T = (int64_t)(E - 1) * E * w->C;
+        break;
+    default:
+        return OR_ERR_INVALID_ARG;
+    }
+    if (w->T >= (int64_t)0xFFFFFFFF) return OR_ERR_SIZE;
+    return OR_OK;
+}
+
+static int64_t pmod(int64_t a, int64_t m) { int64_t r = a % m; return r < 0 ? r + m : r; }
+
+/* Decode transaction x into (src, dst) and its predecessor list.
+ * Returns the number of predecessors written to preds (at most 64 for the
+ * collectives; custom lists are bounded by the caller's array). */
+static int32_t decode(const work_t *w, int64_t x, int32_t *src, int32_t *dst, int64_t *preds)
+{
+    int32_t np = 0;
+    if (w->coll == COLL_CUSTOM) {
+        *src = w->csrc[x]; *dst = w->cdst[x];
+        for (int64_t q = w->pptr[x]; q < w->pptr[x + 1]; q++) preds[np++] = w->pidx[q];
+        return np;
+    }
+    if (w->coll == COLL_RING) {
+        /* id = (s*p + i)*C + j; sends rho(i) -> rho(i+1); waits for the same
+         * line of the previous step received from rho(i-1). */
+        int64_t p = w->p, C = w->C;
+        int64_t j = x % C, q = x / C, i = q % p, s = q / p;
+        *src = rho_of(w, i); *dst = rho_of(w, (i + 1) % p);
+        if (s >= 1) preds[np++] = ((s - 1) * p + pmod(i - 1, p)) * C + j;
+        return np;
+    }
+    if (w->coll == COLL_DIRECT) {
+        /* id = ((ph*(p-1) + (k-1))*p + i)*C + j; i -> i+k.  Reduce-scatter
+         * (ph 0) has no predecessors; all-gather line j of chunk i waits for
+         * every reduce-scatter line j of chunk i delivered to i. */
+        int64_t p = w->p, C = w->C;
+        int64_t j = x % C, q = x / C, i = q % p;
+        q /= p;
+        int64_t k = q % (p - 1) + 1, ph = q / (p - 1);
+        *src = rho_of(w, i); *dst = rho_of(w, (i + k) % p);
+        if (ph == 1)
+            for (int64_t i2 = 0; i2 < p; i2++) {
+                if (i2 == i) continue;
+                int64_t k2 = pmod(i - i2, p);
+                preds[np++] = ((0 * (p - 1) + (k2 - 1)) * p + i2) * C + j;
+            }
+        return np;
+    }
+    if (w->coll == COLL_HIER) {
+        int64_t G = w->G, M = w->M, C1 = w->C1, C2 = w->C2;
+        if (x < w->B2) {
+            /* phase 1: intra-domain reduce-scatter, (d, r) -> (d, r+k) */
+            int64_t q = x / C1, r = q % M;
+            q /= M;
+            int64_t d = q % G, k = q / G + 1;
+            *src = (int32_t)(d * M + r); *dst = (int32_t)(d * M + (r + k) % M);
+            return 0;
+        }
+        if (x < w->B3) {
+            /* phase 2: ring over domains on rail r, (d, r) -> (d+1, r) */
+            int64_t y = x - w->B2;
+            int64_t j = y % C2, q = y / C2, d = q % G;
+            q /= G;
+            int64_t r = q % M, s = q / M;
+            *src = (int32_t)(d * M + r); *dst = (int32_t)(((d + 1) % G) * M + r);
+            if (s <= G - 1) {
+                /* reduce-scatter steps and the first all-gather step send
+                 * sub-chunk (d - s) mod G combined with this node's own copy,
+                 * which must first be reduced inside the domain: all phase-1
+                 * lines sub*C2 + j of chunk r delivered to (d, r) */
+                int64_t sub = pmod(d - s, G);
+                for (int64_t r2 = 0; r2 < M; r2++) {
+                    if (r2 == r) continue;
+                    int64_t k = pmod(r - r2, M);
+                    preds[np++] = (((k - 1) * G + d) * M + r2) * C1 + sub * C2 + j;
+                }
+            }
+            if (s >= 1)  /* the same line received from (d - 1, r) one step earlier */
+                preds[np++] = w->B2 + (((s - 1) * M + r) * G + pmod(d - 1, G)) * C2 + j;
+            return np;
+        }
+        /* phase 3: intra-domain all-gather of chunk r, (d, r) -> (d, r+k) */
+        int64_t y = x - w->B3;
+        int64_t j = y % C1, q = y / C1, r = q % M;
+        q /= M;
+        int64_t d = q % G, k = q / G + 1;
+        *src = (int32_t)(d * M + r); *dst = (int32_t)(d * M + (r + k) % M);
+        int64_t sub = j / C2, jj = j % C2, dm = pmod(d - 1, G), s;
+        if (sub == (d + 1) % G) {
+            /* owned after reduce-scatter: the last reduce-scatter line from
+             * (d - 1, r) combined with this node's domain-reduced copy */
+            s = G - 2;
+            for (int64_t r2 = 0; r2 < M; r2++) {
+                if (r2 == r) continue;
+                int64_t k2 = pmod(r - r2, M);
+                preds[np++] = (((k2 - 1) * G + d) * M + r2) * C1 + j;
+            }
+        } else {
+            s = G - 1 + pmod(d - sub, G);               /* arrives during all-gather */
+        }
+        preds[np++] = w->B2 + ((s * M + r) * G + dm) * C2 + jj;
+        return np;
+    }
+    /* all-to-all, linear shift: id = ((k-1)*E + i)*C + j; i -> i+k */
+    {
+        int64_t E = w->E, C = w->C;
+        int64_t j = x % C, q = x / C, i = q % E, k = q / E + 1;
+        (void)j;
+        *src = (int32_t)i; *dst = (int32_t)((i + k) % E);
+        return 0;
+    }
+}
+
+/* Public decoder (tests use it to pin the expansion). */
+int oracle_txn(int coll, uint64_t bytes, int32_t group, int32_t E, const int32_t *order,
+               int64_t x, int32_t *src, int32_t *dst, int32_t *npred, int64_t *preds,
+               int64_t *T_out)
+{
+    work_t w;
+    int rc = setup_work(&w, coll, bytes, group, E, order);
+    if (rc) return rc;
+    if (T_out) *T_out = w.T;
+    if (x < 0 || x >= w.T) return OR_ERR_INVALID_ARG;
+    *npred = decode(&w, x, src, dst, preds);
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------- simulation */
+
+/* FIFO entry: line id, first cycle it may leave, hop index of this link on
+ * its path, and the path itself (start in the path table, hop count). */
+typedef struct { uint32_t x; uint32_t ready; int32_t hop; int32_t plen; int64_t pp; } entry_t;
+
+typedef struct {
+    int32_t src;        /* source id: FIFO l -> l, stream of link f -> m + f */
+    int32_t k;          /* position in the source's offer */
+    uint32_t x;         /* line id */
+    int32_t target;     /* link id, or SINK */
+    int32_t port;       /* input port at the target's tail node */
+    int32_t hop;        /* hop index of the target on the line's path */
+    int32_t plen;       /* path of the line: hop count and start */
+    int64_t pp;
+    int granted;
+    int departs;
+} req_t;
+
+typedef struct {
+    uint64_t processed_cycles;
+    uint64_t line_hops;
+    double seconds;     /* event loop only */
+} oracle_stats;
+
+/* A decoded stream head: its predecessors and its path. */
+typedef struct {
+    uint32_t x;
+    int32_t np;
+    int64_t *preds;
+    int64_t pp;
+    int32_t plen;
+} hcache_t;
+
+static const hcache_t *head_info(hcache_t *c, int64_t *slot, const work_t *w, uint32_t x,
+                                 const int64_t *path_ptr, int32_t E)
+{
+    if (c->x == x) return c;
+    int32_t s, d;
+    if (w->coll == COLL_CUSTOM) {
+        /* custom lists may have any number of predecessors */
+        int64_t n = w->pptr[x + 1] - w->pptr[x];
+        free(c->preds);
+        c->preds = malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+        slot = c->preds;
+    } else {
+        c->preds = slot;
+    }
+    c->np = decode(w, x, &s, &d, slot);
+    c->pp = path_ptr[(int64_t)s * E + d];
+    c->plen = (int32_t)(path_ptr[(int64_t)s * E + d + 1] - c->pp);
+    c->x = x;
+    return c;
+}
+
+/* rel(x) = max completion over predecessors; "never" while any is pending. */
+static uint64_t release_of(const hcache_t *c, const uint32_t *completion)
+{
+    uint64_t rel = 0;
+    for (int32_t q = 0; q < c->np; q++) {
+        uint32_t v = completion[c->preds[q]];
+        if (v == NEVER) return UINT64_MAX;
+        if (v > rel) rel = v;
+    }
+    return rel;
+}
+
+static int key_less(const req_t *a, const req_t *b, int arb, int32_t rr, int32_t P)
+{
+    if (arb == 0) return a->x < b->x;
+    if (a->k != b->k) return a->k < b->k;
+    return pmod(a->port - rr, P) < pmod(b->port - rr, P);
+}
+
+/*
+ * Run one scenario.  Inputs: CSR topology (endpoints are nodes 0..E-1), the
+ * per-link bw/lat/cap, the arbitration policy (0 lowest id, 1 round-robin),
+ * and either a collective (coll >= 0) or a custom transaction list
+ * (coll == -1: n_txn lines with src/dst and predecessor CSR).  Outputs:
+ * completion[T] (cycle, NEVER if not delivered), tx_lines[m], busy[m],
+ * makespan.  max_cycles bounds the processed cycle (0 = 2^32 - 2).
+ * check != 0 verifies the per-cycle and end-of-run invariants.
+ */
+int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t *col_idx,
+                    const int32_t *bw, const int32_t *lat, const int32_t *cap, int32_t arb,
+                    int32_t coll, uint64_t bytes, int32_t group, const int32_t *order,
+                    int64_t n_txn, const int32_t *csrc, const int32_t *cdst,
+                    const int64_t *pred_ptr, const int64_t *pred_idx,
+                    uint64_t max_cycles, int32_t check,
+                    uint32_t *completion, uint64_t *tx_lines, uint64_t *busy,
+                    uint32_t *makespan, oracle_stats *stats)
+{
+    if (n < 1 || E < 1 || E > n || !row_ptr || !col_idx) return OR_ERR_INVALID_ARG;
+    int32_t m = row_ptr[n];
+    for (int32_t l = 0; l < m; l++) {
+        if (bw[l] < 1 || lat[l] < 1 || cap[l] < 1) return OR_ERR_TOPOLOGY;
+        if (col_idx[l] < 0 || col_idx[l] >= n) return OR_ERR_TOPOLOGY;
+    }
+    for (int32_t u = 0; u < n; u++)
+        for (int32_t l = row_ptr[u]; l < row_ptr[u + 1]; l++)
+            if (col_idx[l] == u) return OR_ERR_TOPOLOGY;
+    if (max_cycles == 0 || max_cycles > 0xFFFFFFFEull) max_cycles = 0xFFFFFFFEull;
+
+    work_t w;
+    int rc;
+    if (coll == COLL_CUSTOM) {
+        memset(&w, 0, sizeof(w));
+        w.coll = COLL_CUSTOM; w.E = E; w.T = n_txn;
+        w.csrc = csrc; w.cdst = cdst; w.pptr = pred_ptr; w.pidx = pred_idx;
+        for (int64_t x = 0; x < n_txn; x++) {
+            if (csrc[x] < 0 || csrc[x] >= E || cdst[x] < 0 || cdst[x] >= E || csrc[x] == cdst[x])
+                return OR_ERR_INVALID_ARG;
+            for (int64_t q = pred_ptr[x]; q < pred_ptr[x + 1]; q++)
+                if (pred_idx[q] < 0 || pred_idx[q] >= n_txn) return OR_ERR_INVALID_ARG;
+        }
+    } else {
+        rc = setup_work(&w, coll, bytes, group, E, order);
+        if (rc) return rc;
+    }
+    int64_t T = w.T;
+
+    /* routes */
+    int64_t *path_ptr = malloc(sizeof(int64_t) * ((size_t)E * E + 1));
+    if (!path_ptr) return OR_ERR_OOM;
+    int64_t pcap = (int64_t)E * (E - 1) * 8 + 16;
+    int32_t *path_link = malloc(sizeof(int32_t) * (size_t)pcap);
+    rc = oracle_paths(n, E, row_ptr, col_idx, path_ptr, path_link, pcap);
+    if (rc == OR_ERR_SIZE) {
+        pcap = path_ptr[(int64_t)E * E];
+        free(path_link);
+        path_link = malloc(sizeof(int32_t) * (size_t)pcap);
+        rc = oracle_paths(n, E, row_ptr, col_idx, path_ptr, path_link, pcap);
+    }
+    if (rc) { free(path_ptr); free(path_link); return rc; }
+
+    /* input ports: in-links of v sorted by id, then the injection port */
+    int32_t *port_of = malloc(sizeof(int32_t) * (size_t)(m + 1));
+    int32_t *nports = calloc((size_t)n, sizeof(int32_t));
+    int32_t *tail_of = malloc(sizeof(int32_t) * (size_t)(m + 1));
+    for (int32_t u = 0; u < n; u++)
+        for (int32_t l = row_ptr[u]; l < row_ptr[u + 1]; l++) tail_of[l] = u;
+    for (int32_t l = 0; l < m; l++) port_of[l] = nports[col_idx[l]]++;
+    for (int32_t v = 0; v < E; v++) nports[v]++;
+
+    /* injection streams: per first link, the lines in ascending id */
+    int64_t *s_ptr = calloc((size_t)m + 1, sizeof(int64_t));
+    uint32_t *s_list = malloc(sizeof(uint32_t) * (size_t)(T > 0 ? T : 1));
+    int64_t *s_cur = calloc((size_t)m, sizeof(int64_t));
+    int64_t *preds = malloc(sizeof(int64_t) * 4096);
+    int64_t line_hops = 0;
+    for (int64_t x = 0; x < T; x++) {
+        int32_t s, d;
+        decode(&w, x, &s, &d, preds);
+        int64_t f0 = path_ptr[(int64_t)s * E + d];
+        if (path_ptr[(int64_t)s * E + d + 1] == f0) {   /* needed pair without a path */
+            rc = OR_ERR_UNREACHABLE;
+            break;
+        }
+        s_ptr[path_link[f0] + 1]++;
+        line_hops += path_ptr[(int64_t)s * E + d + 1] - f0;
+    }
+    if (rc) {
+        free(path_ptr); free(path_link); free(port_of); free(nports); free(tail_of);
+        free(s_ptr); free(s_list); free(s_cur); free(preds);
+        return rc;
+    }
+    for (int32_t l = 0; l < m; l++) s_ptr[l + 1] += s_ptr[l];
+    for (int64_t x = 0; x < T; x++) {
+        int32_t s, d;
+        decode(&w, x, &s, &d, preds);
+        int32_t f = path_link[path_ptr[(int64_t)s * E + d]];
+        s_list[s_ptr[f] + s_cur[f]++] = (uint32_t)x;
+    }
+    memset(s_cur, 0, sizeof(int64_t) * (size_t)m);
+
+    /* FIFOs */
+    int64_t *q_off = malloc(sizeof(int64_t) * ((size_t)m + 1));
+    q_off[0] = 0;
+    for (int32_t l = 0; l < m; l++) q_off[l + 1] = q_off[l] + cap[l];
+    entry_t *qbuf = malloc(sizeof(entry_t) * (size_t)(q_off[m] > 0 ? q_off[m] : 1));
+    int32_t *qhead = calloc((size_t)m, sizeof(int32_t));
+    int32_t *qocc = calloc((size_t)m, sizeof(int32_t));
+    int32_t *rr = calloc((size_t)m, sizeof(int32_t));
+
+    int32_t bmax = 1;
+    for (int32_t l = 0; l < m; l++) if (bw[l] > bmax) bmax = bw[l];
+    size_t rcap = (size_t)2 * m * bmax + 1;
+    req_t *reqs = malloc(sizeof(req_t) * rcap);
+    /* per-target request slots: at most (input ports of its tail) * bmax */
+    int32_t *bucket_n = calloc((size_t)m, sizeof(int32_t));
+    int64_t *bucket_off = malloc(sizeof(int64_t) * ((size_t)m + 1));
+    bucket_off[0] = 0;
+    for (int32_t f = 0; f < m; f++) bucket_off[f + 1] = bucket_off[f] + (int64_t)nports[tail_of[f]] * bmax;
+    int32_t *bucket = malloc(sizeof(int32_t) * (size_t)(bucket_off[m] + 1));
+    int32_t *touched = malloc(sizeof(int32_t) * ((size_t)m + 1));
+    int32_t *active = malloc(sizeof(int32_t) * ((size_t)2 * m + 1));
+    int32_t *src_first = malloc(sizeof(int32_t) * (size_t)2 * m);
+    int32_t *src_cnt = calloc((size_t)2 * m, sizeof(int32_t));
+    /* decoded stream heads (re-used while a head waits) */
+    int32_t maxp = (w.coll == COLL_RING) ? 1 : (w.coll == COLL_DIRECT) ? w.p - 1
+                 : (w.coll == COLL_HIER) ? (int32_t)w.M : 0;  /* custom heads allocate their own */
+    if (maxp < 1) maxp = 1;
+    hcache_t *hcache = malloc(sizeof(hcache_t) * (size_t)m * bmax);
+    int64_t *hpred = malloc(sizeof(int64_t) * (size_t)m * bmax * maxp);
+    for (size_t i = 0; i < (size_t)m * bmax; i++) { hcache[i].x = NEVER; hcache[i].preds = NULL; }
+    uint32_t *admit0 = check ? malloc(sizeof(uint32_t) * (size_t)(T > 0 ? T : 1)) : NULL;
+    int32_t *adm_cnt = check ? calloc((size_t)m, sizeof(int32_t)) : NULL;
+
+    for (int64_t x = 0; x < T; x++) completion[x] = NEVER;
+    for (int32_t l = 0; l < m; l++) { tx_lines[l] = 0; busy[l] = 0; }
+    if (admit0) for (int64_t x = 0; x < T; x++) admit0[x] = NEVER;
+
+    int64_t remaining = T;
+    uint64_t t = 0, processed = 0;
+    rc = OR_OK;
+    struct timespec t0, t1;
+    clock_gettime(CLOCK_MONOTONIC, &t0);
+
+    while (remaining > 0) {
+        if (t > max_cycles) { rc = OR_ERR_MAX_CYCLES; break; }
+        processed++;
+        size_t nr = 0;
+        int32_t ntouched = 0, nactive = 0;
+        /* --- requests from FIFOs */
+        for (int32_t l = 0; l < m; l++) {
+            if (qocc[l] == 0) continue;
+            src_first[l] = (int32_t)nr;
+            src_cnt[l] = 0;
+            for (int32_t k = 0; k < bw[l] && k < qocc[l]; k++) {
+                entry_t *e = &qbuf[q_off[l] + (qhead[l] + k) % cap[l]];
+                if (e->ready > t) break;
+                req_t *r = &reqs[nr++];
+                r->src = l; r->k = k; r->x = e->x;
+                r->hop = e->hop + 1;
+                r->pp = e->pp; r->plen = e->plen;
+                r->target = (r->hop < e->plen) ? path_link[e->pp + r->hop] : SINK;
+                r->port = port_of[l];
+                r->granted = 0; r->departs = 0;
+                src_cnt[l]++;
+            }
+            if (src_cnt[l]) active[nactive++] = l;
+        }
+        /* --- requests from injection streams */
+        for (int32_t f = 0; f < m; f++) {
+            int32_t sid = m + f;
+            int64_t len = s_ptr[f + 1] - s_ptr[f];
+            if (s_cur[f] >= len) continue;
+            src_first[sid] = (int32_t)nr;
+            src_cnt[sid] = 0;
+            for (int32_t k = 0; k < bw[f] && s_cur[f] + k < len; k++) {
+                uint32_t x = s_list[s_ptr[f] + s_cur[f] + k];
+                const hcache_t *hc = head_info(&hcache[(size_t)f * bmax + k], hpred + ((size_t)f * bmax + k) * maxp,
+                                               &w, x, path_ptr, E);
+                uint64_t rel = release_of(hc, completion);
+                if (rel > t) break;
+                req_t *r = &reqs[nr++];
+                r->src = sid; r->k = k; r->x = x;
+                r->hop = 0; r->target = f;
+                r->pp = hc->pp; r->plen = hc->plen;
+                r->port = nports[tail_of[f]] - 1;
+                r->granted = 0; r->departs = 0;
+                src_cnt[sid]++;
+            }
+            if (src_cnt[sid]) active[nactive++] = sid;
+        }
+        /* --- grants: bucket requests by target link, order, grant a prefix */
+        for (size_t i = 0; i < nr; i++) {
+            if (reqs[i].target == SINK) { reqs[i].granted = 1; continue; }
+            int32_t f = reqs[i].target;
+            if (bucket_n[f] == 0) touched[ntouched++] = f;
+            bucket[bucket_off[f] + bucket_n[f]++] = (int32_t)i;
+        }
+        for (int32_t ti = 0; ti < ntouched; ti++) {
+            int32_t f = touched[ti];
+            int32_t cnt = bucket_n[f];
+            int32_t *bk = bucket + bucket_off[f];
+            int32_t P = nports[tail_of[f]];
+            for (int32_t a = 1; a < cnt; a++) {      /* insertion sort by key */
+                int32_t v = bk[a], b = a - 1;
+                while (b >= 0 && key_less(&reqs[v], &reqs[bk[b]], arb, rr[f], P)) {
+                    bk[b + 1] = bk[b];
+                    b--;
+                }
+                bk[b + 1] = v;
+            }
+            int32_t g = bw[f];
+            if (cap[f] - qocc[f] < g) g = cap[f] - qocc[f];
+            if (cnt < g) g = cnt;
+            for (int32_t a = 0; a < g; a++) reqs[bk[a]].granted = 1;
+        }
+        /* --- departures: longest granted prefix of each source */
+        int64_t departed = 0;
+        for (int32_t ai = 0; ai < nactive; ai++) {
+            int32_t sid = active[ai];
+            for (int32_t k = 0; k < src_cnt[sid]; k++) {
+                req_t *r = &reqs[src_first[sid] + k];
+                if (!r->granted) break;
+                r->departs = 1;
+            }
+        }
+        /* --- enter target FIFOs in grant order */
+        for (int32_t ti = 0; ti < ntouched; ti++) {
+            int32_t f = touched[ti];
+            int32_t cnt = bucket_n[f];
+            bucket_n[f] = 0;
+            int32_t *bk = bucket + bucket_off[f];
+            int32_t entered = 0, last_port = -1;
+            for (int32_t a = 0; a < cnt; a++) {
+                req_t *r = &reqs[bk[a]];
+                if (!r->departs) continue;
+                entry_t *e = &qbuf[q_off[f] + (qhead[f] + qocc[f]) % cap[f]];
+                e->x = r->x; e->ready = (uint32_t)(t + (uint64_t)lat[f]); e->hop = r->hop;
+                e->pp = r->pp; e->plen = r->plen;
+                qocc[f]++;
+                entered++;
+                last_port = r->port;
+                if (admit0 && r->hop == 0) admit0[r->x] = (uint32_t)t;
+            }
+            if (entered) {
+                tx_lines[f] += (uint64_t)entered;
+                busy[f] += 1;
+                if (arb == 1) rr[f] = (last_port + 1) % nports[tail_of[f]];
+                if (check) {
+                    if (entered > bw[f]) rc = OR_ERR_INVARIANT;         /* admissions <= b */
+                    if (qocc[f] > cap[f]) rc = OR_ERR_INVARIANT;         /* occupancy <= cap */
+                }
+            }
+        }
+        /* --- pop sources, eject to sink */
+        for (int32_t ai = 0; ai < nactive; ai++) {
+            int32_t sid = active[ai];
+            int32_t dep = 0;
+            for (int32_t k = 0; k < src_cnt[sid]; k++) {
+                req_t *r = &reqs[src_first[sid] + k];
+                if (!r->departs) break;
+                dep++;
+                if (r->target == SINK) {
+                    if (check && completion[r->x] != NEVER) rc = OR_ERR_INVARIANT;  /* once */
+                    completion[r->x] = (uint32_t)(t + 1);
+                    remaining--;
+                }
+            }
+            if (!dep) continue;
+            departed += dep;
+            if (sid < m) {
+                if (check && dep > bw[sid]) rc = OR_ERR_INVARIANT;       /* departures <= b */
+                qhead[sid] = (qhead[sid] + dep) % cap[sid];
+                qocc[sid] -= dep;
+            } else {
+                s_cur[sid - m] += dep;
+            }
+        }
+        if (check) {
+            /* FIFO order: ready times never decrease from head to tail */
+            for (int32_t l = 0; l < m && rc == OR_OK; l++)
+                for (int32_t k = 1; k < qocc[l]; k++) {
+                    entry_t *a = &qbuf[q_off[l] + (qhead[l] + k - 1) % cap[l]];
+                    entry_t *b = &qbuf[q_off[l] + (qhead[l] + k) % cap[l]];
+                    if (a->ready > b->ready) { rc = OR_ERR_INVARIANT; break; }
+                }
+        }
+        if (rc) break;
+        if (remaining == 0) break;
+        /* --- time advance */
+        if (departed > 0) {
+            t++;
+            continue;
+        }
+        uint64_t next = UINT64_MAX;
+        for (int32_t l = 0; l < m; l++)
+            for (int32_t k = 0; k < bw[l] && k < qocc[l]; k++) {
+                entry_t *e = &qbuf[q_off[l] + (qhead[l] + k) % cap[l]];
+                if (e->ready > t) { if (e->ready < next) next = e->ready; break; }
+            }
+        for (int32_t f = 0; f < m; f++) {
+            int64_t len = s_ptr[f + 1] - s_ptr[f];
+            for (int32_t k = 0; k < bw[f] && s_cur[f] + k < len; k++) {
+                uint32_t x = s_list[s_ptr[f] + s_cur[f] + k];
+                const hcache_t *hc = head_info(&hcache[(size_t)f * bmax + k], hpred + ((size_t)f * bmax + k) * maxp,
+                                               &w, x, path_ptr, E);
+                uint64_t rel = release_of(hc, completion);
+                if (rel > t) { if (rel < next) next = rel; break; }
+            }
+        }
+        if (next == UINT64_MAX) { rc = OR_ERR_DEADLOCK; break; }
+        t = next;
+    }
+    clock_gettime(CLOCK_MONOTONIC, &t1);
+
+    uint32_t mk = 0;
+    for (int64_t x = 0; x < T; x++)
+        if (completion[x] != NEVER && completion[x] > mk) mk = completion[x];
+    *makespan = mk;
+
+    if (check && rc == OR_OK) {
+        /* sum of admissions equals the sum of path lengths */
+        uint64_t sum = 0;
+        for (int32_t l = 0; l < m; l++) {
+            sum += tx_lines[l];
+            if (busy[l] > tx_lines[l] || tx_lines[l] > (uint64_t)bw[l] * busy[l]) rc = OR_ERR_INVARIANT;
+        }
+        if (sum != (uint64_t)line_hops) rc = OR_ERR_INVARIANT;
+        /* completion >= release + path latency + 1, release = max pred completion */
+        for (int64_t x = 0; x < T && rc == OR_OK; x++) {
+            int32_t s, d;
+            int32_t np = decode(&w, x, &s, &d, preds);
+            uint64_t rel = 0;
+            for (int32_t q = 0; q < np; q++)
+                if (completion[preds[q]] > rel) rel = completion[preds[q]];
+            uint64_t lsum = 0;
+            for (int64_t q = path_ptr[(int64_t)s * E + d]; q < path_ptr[(int64_t)s * E + d + 1]; q++)
+                lsum += (uint64_t)lat[path_link[q]];
+            if (admit0[x] < rel) rc = OR_ERR_INVARIANT;
+            if ((uint64_t)completion[x] < rel + lsum + 1) rc = OR_ERR_INVARIANT;
+        }
+    }
+
+    if (stats) {
+        stats->processed_cycles = processed;
+        stats->line_hops = (uint64_t)line_hops;
+        stats->seconds = (double)(t1.tv_sec - t0.tv_sec) + 1e-9 * (double)(t1.tv_nsec - t0.tv_nsec);
+    }
+    free(path_ptr); free(path_link); free(port_of); free(nports); free(tail_of);
+    free(s_ptr); free(s_list); free(s_cur); free(preds); free(q_off); free(qbuf);
+    free(qhead); free(qocc); free(rr); free(reqs); free(bucket_n); free(bucket_off);
+    free(bucket); free(touched); free(active);
+    for (size_t i = 0; w.coll == COLL_CUSTOM && i < (size_t)m * bmax; i++) free(hcache[i].preds);
+    free(hcache); free(hpred); free(src_first); free(src_cnt); free(admit0); free(adm_cnt);
+    return rc;
+}
