@@ -1,0 +1,164 @@
+/*
+ * simgpu -- line-granularity network simulation on one MI355X (gfx950).
+ *
+ * C ABI of libsimgpu.so.  Every call returns a sim_status; no C++ exception
+ * crosses this boundary.  Plain pointers and sizes only.
+ *
+ * What is simulated.  The paper ("ASTRA-sim 3.0") makes the cache-line-sized
+ * wavefront request the unit that the network backend simulates (Sec. 4.4,
+ * "Wavefront Request") and extends the Simple network backend to a graph of
+ * endpoints, switches and links with a modular routing function (Sec. 4.5);
+ * the Simple backend itself is an alpha-beta model (Sec. 2.1).  This library
+ * advances every 128 B line of a collective hop by hop through such a graph.
+ * The paper does not state the queueing discipline; the model implemented
+ * here is:
+ *   - link l = bounded FIFO with integer bandwidth b_l (lines/cycle), latency
+ *     L_l (cycles) and capacity cap_l (lines in flight plus waiting);
+ *   - per cycle t, from the state at the start of t: every FIFO offers its
+ *     first <= b ready entries, every injection stream (source endpoint,
+ *     first link) its first <= b released lines in id order; each link grants
+ *     min(b, cap - occupancy, #requests) requests, ordered by lowest line id
+ *     or round-robin over its tail node's input ports (key (k, port offset));
+ *     the longest granted prefix of each source departs; lines enter the
+ *     target FIFO in grant order and may leave at t + L; a line leaving its
+ *     last link completes at t + 1;
+ *   - cycles in which nothing can change are skipped;
+ *   - routes are minimal-hop paths; ties between next hops are broken by the
+ *     MurmurHash3 32-bit finalizer of (src << 16 | dst) (hash ECMP);
+ *   - a line is injected once all its predecessor lines have completed.
+ *
+ * Threading: a context is used by one host thread at a time; there is no
+ * global mutable state, so distinct contexts may be used concurrently.
+ */
+#ifndef SIMGPU_H
+#define SIMGPU_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct sim_ctx sim_ctx; /* opaque, owned by the library */
+
+typedef enum {
+    SIM_OK = 0,
+    SIM_ERR_INVALID_ARG = 1, /* null pointer, bad enum, out-of-range argument    */
+    SIM_ERR_TOPOLOGY = 2,    /* malformed CSR, self-loop, parameter out of range */
+    SIM_ERR_UNREACHABLE = 3, /* a needed endpoint pair has no path               */
+    SIM_ERR_SIZE = 4,        /* message not divisible into whole lines/chunks    */
+    SIM_ERR_OOM = 5,         /* host or device allocation failed                 */
+    SIM_ERR_DEVICE = 6,      /* HIP runtime error                                */
+    SIM_ERR_DEADLOCK = 7,    /* device: no departure and no future event         */
+    SIM_ERR_MAX_CYCLES = 8,  /* device: cycle guard exceeded                     */
+    SIM_ERR_STATE = 9        /* call out of order (e.g. run before load)         */
+} sim_status;
+
+typedef enum { SIM_ARB_LOWEST_ID = 0, SIM_ARB_ROUND_ROBIN = 1 } sim_arb;
+
+/* Collectives (the paper's textbook algorithms, Sec. 1; the hierarchical
+ * form composes direct and ring steps over scale-up domains).  Transaction
+ * ids are step-major so that lowest-id arbitration favours earlier steps. */
+typedef enum {
+    SIM_COLL_RING_ALLREDUCE = 0,   /* reduce-scatter + all-gather ring, 2(p-1) steps */
+    SIM_COLL_DIRECT_ALLREDUCE = 1, /* all-pairs reduce-scatter then all-gather       */
+    SIM_COLL_HIER_ALLREDUCE = 2,   /* direct RS in domain, ring per rail, direct AG  */
+    SIM_COLL_ALLTOALL = 3          /* linear-shift all-to-all                        */
+} sim_coll;
+
+/* Limits checked by sim_create. */
+#define SIM_MAX_BW 64           /* lines per cycle */
+#define SIM_MAX_LAT (1 << 20)   /* cycles          */
+#define SIM_MAX_CAP (1 << 16)   /* lines           */
+#define SIM_LINE_BYTES 128
+
+/*
+ * Create a context from a directed graph (paper Sec. 4.6: the infrastructure
+ * as a directed attributed graph whose vertices are hardware units and whose
+ * edges carry bandwidth/latency annotations).
+ *   n_nodes, n_endpoints : nodes 0..n_endpoints-1 are endpoints (they inject
+ *                          and eject lines); the rest are switches.
+ *   row_ptr[n_nodes+1], col_idx[m] : CSR out-adjacency; m = row_ptr[n_nodes];
+ *                          link id = CSR index; col_idx[l] = head node of l.
+ *                          No self-loops.  Parallel links are allowed.
+ *   n_scenarios          : S >= 1 independent scenarios sharing topology,
+ *                          routing and workload (batched design sweeps).
+ *   bw, lat, cap         : [S*m] int32, scenario-major; 1 <= bw <= SIM_MAX_BW,
+ *                          1 <= lat <= SIM_MAX_LAT, 1 <= cap <= SIM_MAX_CAP.
+ *   arb                  : sim_arb.
+ * Host arrays are copied; the caller keeps ownership.  Routing distances are
+ * built here.  Uses the current HIP device.  *out is set only on SIM_OK.
+ */
+sim_status sim_create(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_ptr,
+                      const int32_t *col_idx, int32_t n_scenarios, const int32_t *bw,
+                      const int32_t *lat, const int32_t *cap, int32_t arb, sim_ctx **out);
+
+/*
+ * Load a collective (replaces any previous workload).
+ *   coll       : sim_coll.
+ *   bytes      : per endpoint (all-reduce) or per ordered pair (all-to-all);
+ *                must be a multiple of 128 B times the collective's chunk
+ *                divisor (p for ring/direct, M*G for hierarchical), else
+ *                SIM_ERR_SIZE.
+ *   group_size : hierarchical only: endpoints per domain M (endpoint d*M + r);
+ *                0 otherwise.
+ *   order      : ring/direct: participant order, a permutation of the
+ *                endpoints (NULL = rank order); must be NULL otherwise.
+ * Builds the routes of every flow used (SIM_ERR_UNREACHABLE if one has no
+ * path), the injection streams and the predecessor tables, and uploads them.
+ */
+sim_status sim_load_collective(sim_ctx *ctx, int32_t coll, uint64_t bytes, int32_t group_size,
+                               const int32_t *order);
+
+/*
+ * Load a custom transaction list: line x (0 <= x < n) goes src[x] -> dst[x]
+ * (endpoints, src != dst) and may be injected once every line in
+ * pred_idx[pred_ptr[x] .. pred_ptr[x+1]) has completed (paper Sec. 4.2: the
+ * custom collective algorithms are dependency-ordered transfer lists).  A
+ * cyclic predecessor relation is reported as SIM_ERR_DEADLOCK by the run.
+ */
+sim_status sim_load_transactions(sim_ctx *ctx, int64_t n, const int32_t *src, const int32_t *dst,
+                                 const int64_t *pred_ptr, const int64_t *pred_idx);
+
+/* Sizes of the loaded problem: transactions T, links m, scenarios S and
+ * line-hops per scenario (sum of path lengths).  Any pointer may be NULL. */
+sim_status sim_sizes(const sim_ctx *ctx, int64_t *n_txn, int32_t *n_links, int32_t *n_scenarios,
+                     uint64_t *line_hops);
+
+/*
+ * Enqueue one full simulation of every scenario on hip_stream (a
+ * hipStream_t; NULL = the null stream) and return.  Outputs are caller-owned
+ * device buffers that must stay valid until the stream reaches this work:
+ *   d_completion  [S*T] u32 : completion cycle of every line (scenario-major)
+ *   d_tx_lines    [S*m] u64 : lines admitted onto each link
+ *   d_busy_cycles [S*m] u64 : cycles in which each link admitted >= 1 line
+ *   d_makespan    [S]   u32 : max completion per scenario
+ * max_cycles bounds the simulated cycle (0 = the largest supported guard).
+ * Argument errors return synchronously.  Deadlock / guard overrun are found
+ * on the device: read them with sim_status_after_sync once the stream has
+ * been synchronised; the outputs of a failed scenario are unspecified.
+ */
+sim_status sim_run(sim_ctx *ctx, void *hip_stream, uint32_t *d_completion, uint64_t *d_tx_lines,
+                   uint64_t *d_busy_cycles, uint32_t *d_makespan, uint64_t max_cycles);
+
+/* After the caller has synchronised the run's stream: SIM_OK, or the first
+ * device-detected error (DEADLOCK / MAX_CYCLES) over the scenarios.  If
+ * status/cycles are non-NULL they receive per-scenario statuses ([S] int32)
+ * and processed-cycle counts ([S] u64) on the host. */
+sim_status sim_status_after_sync(sim_ctx *ctx, int32_t *status, uint64_t *cycles);
+
+/* Route of flow src -> dst as link ids (host copy; *len = hop count).
+ * SIM_ERR_SIZE if cap < hop count (then *len still holds the count). */
+sim_status sim_route(const sim_ctx *ctx, int32_t src, int32_t dst, int32_t *links, int32_t cap,
+                     int32_t *len);
+
+/* Last error message of this context (owned by the context; never NULL). */
+const char *sim_last_error(const sim_ctx *ctx);
+
+/* Free the context and all its device memory.  NULL is allowed. */
+void sim_destroy(sim_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SIMGPU_H */

@@ -1,0 +1,622 @@
+// Host side of libsimgpu: topology validation, routing tables, workload
+// expansion into injection streams, device uploads and the C ABI.
+//
+// Paper: the infrastructure is a directed attributed graph (Sec. 4.6); the
+// Simple backend routes over it with a modular routing function (Sec. 4.5);
+// the unit of transfer is the 128 B wavefront request (Sec. 4.4); the
+// collectives are the textbook ring / direct algorithms (Sec. 1).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "../../include/simgpu.h"
+#include "sim_internal.h"
+
+using simgpu::DevNet;
+
+namespace {
+
+// MurmurHash3's 32-bit finalizer (Appleby): spreads (src, dst) over the
+// candidate next hops.
+inline uint32_t finalize32(uint32_t v) {
+    v ^= v >> 16;
+    v *= 0x85ebca6bu;
+    v ^= v >> 13;
+    v *= 0xc2b2ae35u;
+    v ^= v >> 16;
+    return v;
+}
+
+}  // namespace
+
+struct sim_ctx {
+    int32_t n = 0, E = 0, m = 0, S = 0, arb = 0;
+    int device = 0;
+    std::vector<int32_t> row_ptr, col_idx, tail;
+    std::vector<int32_t> bw, lat, cap;
+    std::vector<int32_t> hops;  // [E*n]: hop count from node v to endpoint d (-1 none)
+
+    // loaded workload
+    bool loaded = false;
+    int64_t T = 0;
+    uint64_t line_hops = 0;
+    std::unordered_map<uint64_t, int32_t> flow_slot;  // (src << 32 | dst) -> slot
+    std::vector<int32_t> flow_path;                   // [nflows] start in path_link
+    std::vector<int32_t> path_link;
+
+    DevNet dn{};
+    std::vector<void *> dev_static;  // freed on reload / destroy
+    std::vector<void *> dev_state;
+    std::string err = "";
+    bool ran = false;
+};
+
+namespace {
+
+sim_status fail(sim_ctx *c, sim_status s, const std::string &msg) {
+    if (c) c->err = msg;
+    return s;
+}
+
+void free_list(std::vector<void *> &v) {
+    for (void *p : v) (void)hipFree(p);
+    v.clear();
+}
+
+template <class T>
+sim_status upload(sim_ctx *c, std::vector<void *> &owner, const std::vector<T> &h, T **out) {
+    size_t bytes = std::max<size_t>(h.size() * sizeof(T), 16);
+    void *p = nullptr;
+    if (hipMalloc(&p, bytes) != hipSuccess) return fail(c, SIM_ERR_OOM, "hipMalloc failed");
+    owner.push_back(p);
+    if (!h.empty() && hipMemcpy(p, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice) != hipSuccess)
+        return fail(c, SIM_ERR_DEVICE, "hipMemcpy failed");
+    *out = static_cast<T *>(p);
+    return SIM_OK;
+}
+
+template <class T>
+sim_status alloc(sim_ctx *c, std::vector<void *> &owner, size_t count, T **out) {
+    void *p = nullptr;
+    if (hipMalloc(&p, std::max<size_t>(count * sizeof(T), 16)) != hipSuccess)
+        return fail(c, SIM_ERR_OOM, "hipMalloc failed (" + std::to_string(count * sizeof(T)) + " B)");
+    owner.push_back(p);
+    *out = static_cast<T *>(p);
+    return SIM_OK;
+}
+
+// Hop distances to every endpoint: breadth-first search from the endpoint
+// over reversed links.
+void build_hops(sim_ctx *c) {
+    const int32_t n = c->n, m = c->m;
+    std::vector<int32_t> in_ptr(n + 1, 0), in_src(m);
+    for (int32_t l = 0; l < m; l++) in_ptr[c->col_idx[l] + 1]++;
+    for (int32_t v = 0; v < n; v++) in_ptr[v + 1] += in_ptr[v];
+    std::vector<int32_t> fill(in_ptr.begin(), in_ptr.end() - 1);
+    for (int32_t l = 0; l < m; l++) in_src[fill[c->col_idx[l]]++] = c->tail[l];
+    c->hops.assign((size_t)c->E * n, -1);
+    std::vector<int32_t> frontier;
+    frontier.reserve(n);
+    for (int32_t d = 0; d < c->E; d++) {
+        int32_t *h = &c->hops[(size_t)d * n];
+        frontier.clear();
+        frontier.push_back(d);
+        h[d] = 0;
+        for (size_t q = 0; q < frontier.size(); q++) {
+            int32_t w = frontier[q];
+            for (int32_t e = in_ptr[w]; e < in_ptr[w + 1]; e++) {
+                int32_t u = in_src[e];
+                if (h[u] < 0) {
+                    h[u] = h[w] + 1;
+                    frontier.push_back(u);
+                }
+            }
+        }
+    }
+}
+
+// Minimal-hop route of flow s -> d.  Among out-links whose head is one hop
+// nearer to d (ascending link id), the i-th tie-break uses byte (i mod 4) of
+// the finalized (s << 16 | d), re-finalized before every fourth tie-break
+// after the first.
+bool trace_route(const sim_ctx *c, int32_t s, int32_t d, std::vector<int32_t> &out) {
+    out.clear();
+    const int32_t *h = &c->hops[(size_t)d * c->n];
+    if (h[s] < 0) return false;
+    uint32_t key = finalize32(((uint32_t)s << 16) | (uint32_t)d);
+    int32_t ties = 0;
+    int32_t v = s;
+    while (v != d) {
+        const int32_t want = h[v] - 1;
+        int32_t count = 0;
+        for (int32_t l = c->row_ptr[v]; l < c->row_ptr[v + 1]; l++)
+            if (h[c->col_idx[l]] == want) count++;
+        int32_t pick = 0;
+        if (count > 1) {
+            if (ties > 0 && (ties & 3) == 0) key = finalize32(key);
+            pick = (int32_t)(((key >> (8 * (ties & 3))) & 0xFFu) % (uint32_t)count);
+            ties++;
+        }
+        int32_t chosen = -1;
+        for (int32_t l = c->row_ptr[v]; l < c->row_ptr[v + 1]; l++)
+            if (h[c->col_idx[l]] == want && pick-- == 0) {
+                chosen = l;
+                break;
+            }
+        out.push_back(chosen);
+        v = c->col_idx[chosen];
+    }
+    return true;
+}
+
+// The workload as id ranges: consecutive line ids of one flow whose
+// predecessors are, line for line, consecutive lines of earlier ranges.
+struct Ranges {
+    std::vector<uint32_t> start, len;
+    std::vector<int32_t> src, dst;
+    std::vector<int64_t> pref_beg;   // [nr+1] into pref_rng/pref_delta
+    std::vector<int64_t> pref_rng;   // predecessor range
+    std::vector<uint32_t> pref_delta;  // line start+o waits for line pref_start+delta+o
+    void add(uint64_t s, uint64_t l, int32_t a, int32_t b) {
+        start.push_back((uint32_t)s);
+        len.push_back((uint32_t)l);
+        src.push_back(a);
+        dst.push_back(b);
+        pref_beg.push_back((int64_t)pref_rng.size());
+    }
+    void pred(int64_t r, uint64_t delta) {
+        pref_rng.push_back(r);
+        pref_delta.push_back((uint32_t)delta);
+    }
+    void close() { pref_beg.push_back((int64_t)pref_rng.size()); }
+};
+
+inline int64_t wrap(int64_t a, int64_t m) { return ((a % m) + m) % m; }
+
+sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t group,
+                             const int32_t *order, Ranges &R) {
+    const int64_t E = c->E;
+    if (bytes == 0 || bytes % SIM_LINE_BYTES) return fail(c, SIM_ERR_SIZE, "bytes must be a positive multiple of 128");
+    const int64_t N = (int64_t)(bytes / SIM_LINE_BYTES);
+    if (E < 2) return fail(c, SIM_ERR_INVALID_ARG, "a collective needs at least 2 endpoints");
+    std::vector<int32_t> rho(E);
+    for (int64_t i = 0; i < E; i++) rho[i] = (int32_t)i;
+    if (order) {
+        if (coll != SIM_COLL_RING_ALLREDUCE && coll != SIM_COLL_DIRECT_ALLREDUCE)
+            return fail(c, SIM_ERR_INVALID_ARG, "order applies to ring/direct only");
+        std::vector<char> seen(E, 0);
+        for (int64_t i = 0; i < E; i++) {
+            if (order[i] < 0 || order[i] >= E || seen[order[i]])
+                return fail(c, SIM_ERR_INVALID_ARG, "order is not a permutation of the endpoints");
+            seen[order[i]] = 1;
+            rho[i] = order[i];
+        }
+    }
+    if (coll == SIM_COLL_RING_ALLREDUCE) {
+        const int64_t p = E;
+        if (N % p) return fail(c, SIM_ERR_SIZE, "ring: lines not divisible by participants");
+        const int64_t C = N / p;
+        for (int64_t s = 0; s < 2 * p - 2; s++)
+            for (int64_t i = 0; i < p; i++) {
+                R.add((s * p + i) * C, C, rho[i], rho[(i + 1) % p]);
+                if (s > 0) R.pred((s - 1) * p + wrap(i - 1, p), 0);
+            }
+    } else if (coll == SIM_COLL_DIRECT_ALLREDUCE) {
+        const int64_t p = E;
+        if (N % p) return fail(c, SIM_ERR_SIZE, "direct: lines not divisible by participants");
+        const int64_t C = N / p;
+        for (int64_t ph = 0; ph < 2; ph++)
+            for (int64_t k = 1; k < p; k++)
+                for (int64_t i = 0; i < p; i++) {
+                    int64_t idx = (ph * (p - 1) + (k - 1)) * p + i;
+                    R.add(idx * C, C, rho[i], rho[(i + k) % p]);
+                    if (ph == 1)
+                        for (int64_t i2 = 0; i2 < p; i2++)
+                            if (i2 != i) R.pred(((wrap(i - i2, p) - 1) * p + i2), 0);
+                }
+    } else if (coll == SIM_COLL_HIER_ALLREDUCE) {
+        const int64_t M = group;
+        if (M < 2 || E % M || E / M < 2)
+            return fail(c, SIM_ERR_INVALID_ARG, "hierarchical: group_size must split endpoints into >= 2 domains of >= 2");
+        const int64_t G = E / M;
+        if (N % M) return fail(c, SIM_ERR_SIZE, "hierarchical: lines not divisible by group size");
+        const int64_t C1 = N / M;
+        if (C1 % G) return fail(c, SIM_ERR_SIZE, "hierarchical: chunk not divisible by domain count");
+        const int64_t C2 = C1 / G;
+        const int64_t R1 = (M - 1) * G * M, R2 = (2 * G - 2) * M * G;
+        const int64_t B2 = R1 * C1, B3 = B2 + R2 * C2;
+        // phase 1: direct reduce-scatter inside each domain
+        for (int64_t k = 1; k < M; k++)
+            for (int64_t d = 0; d < G; d++)
+                for (int64_t r = 0; r < M; r++)
+                    R.add((((k - 1) * G + d) * M + r) * C1, C1, (int32_t)(d * M + r),
+                          (int32_t)(d * M + (r + k) % M));
+        // phase 2: ring over the domains on each rail r
+        for (int64_t s = 0; s < 2 * G - 2; s++)
+            for (int64_t r = 0; r < M; r++)
+                for (int64_t d = 0; d < G; d++) {
+                    R.add(B2 + ((s * M + r) * G + d) * C2, C2, (int32_t)(d * M + r),
+                          (int32_t)(((d + 1) % G) * M + r));
+                    // Up to the first all-gather step the sent sub-chunk (d - s) mod G
+                    // includes this node's own copy, reduced inside the domain first.
+                    if (s <= G - 1)
+                        for (int64_t r2 = 0; r2 < M; r2++)
+                            if (r2 != r) R.pred(((wrap(r - r2, M) - 1) * G + d) * M + r2, wrap(d - s, G) * C2);
+                    if (s >= 1) R.pred(R1 + ((s - 1) * M + r) * G + wrap(d - 1, G), 0);
+                }
+        // phase 3: direct all-gather inside each domain, split per sub-chunk
+        for (int64_t k = 1; k < M; k++)
+            for (int64_t d = 0; d < G; d++)
+                for (int64_t r = 0; r < M; r++)
+                    for (int64_t sub = 0; sub < G; sub++) {
+                        R.add(B3 + (((k - 1) * G + d) * M + r) * C1 + sub * C2, C2, (int32_t)(d * M + r),
+                              (int32_t)(d * M + (r + k) % M));
+                        const bool owned = sub == (d + 1) % G;  // fully reduced here by the ring
+                        int64_t s = owned ? G - 2 : G - 1 + wrap(d - sub, G);
+                        if (owned)
+                            for (int64_t r2 = 0; r2 < M; r2++)
+                                if (r2 != r) R.pred(((wrap(r - r2, M) - 1) * G + d) * M + r2, sub * C2);
+                        R.pred(R1 + (s * M + r) * G + wrap(d - 1, G), 0);
+                    }
+    } else if (coll == SIM_COLL_ALLTOALL) {
+        const int64_t C = N;
+        for (int64_t k = 1; k < E; k++)
+            for (int64_t i = 0; i < E; i++) R.add(((k - 1) * E + i) * C, C, (int32_t)i, (int32_t)((i + k) % E));
+    } else {
+        return fail(c, SIM_ERR_INVALID_ARG, "unknown collective");
+    }
+    R.close();
+    return SIM_OK;
+}
+
+// Turn ranges into device tables: flow slots, paths, streams, predecessor
+// descriptors, FIFO/request layouts; allocate per-scenario state.
+sim_status finish_load(sim_ctx *c, Ranges &R) {
+    free_list(c->dev_static);
+    free_list(c->dev_state);
+    c->loaded = false;
+    const int64_t nr = (int64_t)R.start.size();
+    int64_t T = 0;
+    for (int64_t i = 0; i < nr; i++) {
+        if ((int64_t)R.start[i] != T) return fail(c, SIM_ERR_INVALID_ARG, "internal: ranges not contiguous");
+        T += R.len[i];
+    }
+    if (T >= (int64_t)0xFFFFFFFFll) return fail(c, SIM_ERR_SIZE, "more than 2^32-2 transactions");
+    c->T = T;
+
+    // flow slots and paths
+    c->flow_slot.clear();
+    c->flow_path.clear();
+    c->path_link.clear();
+    std::vector<int32_t> rflow(nr);
+    std::vector<int32_t> hopsv;
+    std::vector<int32_t> flow_hops;
+    for (int64_t i = 0; i < nr; i++) {
+        uint64_t key = ((uint64_t)(uint32_t)R.src[i] << 32) | (uint32_t)R.dst[i];
+        auto it = c->flow_slot.find(key);
+        if (it == c->flow_slot.end()) {
+            if (!trace_route(c, R.src[i], R.dst[i], hopsv))
+                return fail(c, SIM_ERR_UNREACHABLE, "no path from endpoint " + std::to_string(R.src[i]) +
+                                                        " to endpoint " + std::to_string(R.dst[i]));
+            int32_t slot = (int32_t)c->flow_path.size();
+            c->flow_path.push_back((int32_t)c->path_link.size());
+            c->path_link.insert(c->path_link.end(), hopsv.begin(), hopsv.end());
+            c->path_link.push_back(-(1 + slot));
+            flow_hops.push_back((int32_t)hopsv.size());
+            it = c->flow_slot.emplace(key, slot).first;
+        }
+        rflow[i] = it->second;
+    }
+    const int32_t nflows = (int32_t)c->flow_path.size();
+    if (c->path_link.size() >= (size_t)INT32_MAX) return fail(c, SIM_ERR_SIZE, "path table too large");
+
+    // per-flow sequence numbers (flows deliver in id order) and predecessor descriptors
+    std::vector<uint32_t> seq0(nr);
+    {
+        std::vector<uint64_t> cnt(nflows, 0);
+        for (int64_t i = 0; i < nr; i++) {
+            seq0[i] = (uint32_t)cnt[rflow[i]];
+            cnt[rflow[i]] += R.len[i];
+        }
+    }
+    c->line_hops = 0;
+    for (int64_t i = 0; i < nr; i++) c->line_hops += (uint64_t)R.len[i] * (uint64_t)flow_hops[rflow[i]];
+
+    // streams: ranges grouped by first link, ascending id inside a stream
+    const int32_t m = c->m;
+    std::vector<int64_t> first_cnt(m + 1, 0);
+    for (int64_t i = 0; i < nr; i++) first_cnt[c->path_link[c->flow_path[rflow[i]]] + 1]++;
+    std::vector<int32_t> s_link, s_rbeg, s_rend;
+    std::vector<int64_t> pos(m, -1);
+    int64_t acc = 0;
+    for (int32_t l = 0; l < m; l++) {
+        if (first_cnt[l + 1] == 0) continue;
+        s_link.push_back(l);
+        s_rbeg.push_back((int32_t)acc);
+        pos[l] = acc;
+        acc += first_cnt[l + 1];
+        s_rend.push_back((int32_t)acc);
+    }
+    if (acc >= INT32_MAX) return fail(c, SIM_ERR_SIZE, "too many ranges");
+    std::vector<uint32_t> r_start(nr), r_len(nr);
+    std::vector<int32_t> r_path(nr), r_pd(nr + 1);
+    std::vector<int32_t> pd_flow;
+    std::vector<uint32_t> pd_base;
+    std::vector<int64_t> order(nr);
+    for (int64_t i = 0; i < nr; i++) {
+        int32_t f = c->path_link[c->flow_path[rflow[i]]];
+        order[pos[f]++] = i;
+    }
+    for (int64_t j = 0; j < nr; j++) {
+        int64_t i = order[j];
+        r_start[j] = R.start[i];
+        r_len[j] = R.len[i];
+        r_path[j] = c->flow_path[rflow[i]];
+        r_pd[j] = (int32_t)pd_flow.size();
+        for (int64_t q = R.pref_beg[i]; q < R.pref_beg[i + 1]; q++) {
+            int64_t pr = R.pref_rng[q];
+            if ((uint64_t)R.pref_delta[q] + R.len[i] > R.len[pr])
+                return fail(c, SIM_ERR_INVALID_ARG, "internal: predecessor range too short");
+            pd_flow.push_back(rflow[pr]);
+            pd_base.push_back(seq0[pr] + R.pref_delta[q]);
+        }
+    }
+    r_pd[nr] = (int32_t)pd_flow.size();
+
+    // links carrying traffic; ports; FIFO and request layouts
+    std::vector<char> used(m, 0);
+    for (int32_t v : c->path_link)
+        if (v >= 0) used[v] = 1;
+    std::vector<int32_t> fsrc;
+    for (int32_t l = 0; l < m; l++)
+        if (used[l]) fsrc.push_back(l);
+    std::vector<int32_t> nports(c->n, 0), port_at_head(m), nports_tail(m);
+    for (int32_t l = 0; l < m; l++) port_at_head[l] = nports[c->col_idx[l]]++;
+    for (int32_t v = 0; v < c->E; v++) nports[v]++;  // injection port last
+    for (int32_t l = 0; l < m; l++) nports_tail[l] = nports[c->tail[l]];
+    int32_t bmax = 1;
+    for (int32_t v : c->bw) bmax = std::max(bmax, v);
+    std::vector<int32_t> fifo_off(m, 0), fifo_mask(m, 0), req_off(m, 0);
+    int64_t ftot = 0, rtot = 0;
+    for (int32_t l = 0; l < m; l++) {
+        int32_t capmax = 1;
+        for (int32_t s = 0; s < c->S; s++) capmax = std::max(capmax, c->cap[(size_t)s * m + l]);
+        int32_t ring = 1;
+        while (ring < capmax) ring <<= 1;
+        if (!used[l]) ring = 1;
+        fifo_off[l] = (int32_t)ftot;
+        fifo_mask[l] = ring - 1;
+        ftot += ring;
+        req_off[l] = (int32_t)rtot;
+        if (used[l]) rtot += (int64_t)nports_tail[l] * bmax;
+    }
+    if (ftot >= INT32_MAX || rtot >= INT32_MAX) return fail(c, SIM_ERR_SIZE, "state too large");
+
+    // everything below touches the device
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return fail(c, SIM_ERR_DEVICE, "no HIP device");
+    if (c->device >= 0 && dev != c->device)
+        return fail(c, SIM_ERR_DEVICE, "current HIP device differs from the context's device");
+    c->device = dev;
+    DevNet d{};
+    d.m = m;
+    d.n_fsrc = (int32_t)fsrc.size();
+    d.ns = (int32_t)s_link.size();
+    d.nflows = nflows;
+    d.S = c->S;
+    d.arb = c->arb;
+    d.bmax = bmax;
+    d.fifo_total = (int32_t)ftot;
+    d.req_total = (int32_t)rtot;
+    d.T = T;
+    sim_status st;
+    auto &own = c->dev_static;
+#define UP(vec, field)                                         \
+    if ((st = upload(c, own, vec, &tmp_##field)) != SIM_OK) return st; \
+    d.field = tmp_##field;
+    int32_t *tmp_fsrc_link, *tmp_port_at_head, *tmp_nports_tail, *tmp_fifo_off, *tmp_fifo_mask, *tmp_req_off;
+    int32_t *tmp_s_link, *tmp_s_rbeg, *tmp_s_rend, *tmp_r_path, *tmp_r_pd, *tmp_pd_flow, *tmp_path_link;
+    uint32_t *tmp_r_start, *tmp_r_len, *tmp_pd_base;
+    int32_t *tmp_bw, *tmp_lat, *tmp_cap;
+    UP(fsrc, fsrc_link);
+    UP(port_at_head, port_at_head);
+    UP(nports_tail, nports_tail);
+    UP(fifo_off, fifo_off);
+    UP(fifo_mask, fifo_mask);
+    UP(req_off, req_off);
+    UP(s_link, s_link);
+    UP(s_rbeg, s_rbeg);
+    UP(s_rend, s_rend);
+    UP(r_start, r_start);
+    UP(r_len, r_len);
+    UP(r_path, r_path);
+    UP(r_pd, r_pd);
+    UP(pd_flow, pd_flow);
+    UP(pd_base, pd_base);
+    UP(c->path_link, path_link);
+    UP(c->bw, bw);
+    UP(c->lat, lat);
+    UP(c->cap, cap);
+#undef UP
+    const size_t S = (size_t)c->S;
+    const size_t nsrc = (size_t)m + (size_t)d.ns;
+    auto &ost = c->dev_state;
+    if ((st = alloc(c, ost, S * ftot, &d.fifo_x)) || (st = alloc(c, ost, S * ftot, &d.fifo_rdy)) ||
+        (st = alloc(c, ost, S * ftot, &d.fifo_pp)) || (st = alloc(c, ost, S * m, &d.qhead)) ||
+        (st = alloc(c, ost, S * m, &d.qtail)) || (st = alloc(c, ost, S * m, &d.rr)) ||
+        (st = alloc(c, ost, S * d.ns, &d.cur_rng)) || (st = alloc(c, ost, S * d.ns, &d.cur_off)) ||
+        (st = alloc(c, ost, S * nflows, &d.delivered)) || (st = alloc(c, ost, S * m, &d.req_cnt)) ||
+        (st = alloc(c, ost, S * rtot, &d.req_rec)) || (st = alloc(c, ost, S * nsrc * bmax, &d.sreq_x)) ||
+        (st = alloc(c, ost, S * nsrc * bmax, &d.sreq_pp)) || (st = alloc(c, ost, S * nsrc, &d.sreq_n)) ||
+        (st = alloc(c, ost, S * nsrc * bmax, &d.grant)) || (st = alloc(c, ost, S * m, &d.gcount)) ||
+        (st = alloc(c, ost, S * m * bmax, &d.glist)) || (st = alloc(c, ost, S * m * bmax, &d.gdep)) ||
+        (st = alloc(c, ost, S, &d.status)) || (st = alloc(c, ost, S, &d.cycles)))
+        return st;
+    c->dn = d;
+    c->loaded = true;
+    c->ran = false;
+    return SIM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sim_status sim_create(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_ptr, const int32_t *col_idx,
+                      int32_t n_scenarios, const int32_t *bw, const int32_t *lat, const int32_t *cap,
+                      int32_t arb, sim_ctx **out) {
+    if (!out || !row_ptr || !col_idx || !bw || !lat || !cap) return SIM_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (n_nodes < 1 || n_endpoints < 1 || n_endpoints > n_nodes || n_scenarios < 1) return SIM_ERR_INVALID_ARG;
+    if (arb != SIM_ARB_LOWEST_ID && arb != SIM_ARB_ROUND_ROBIN) return SIM_ERR_INVALID_ARG;
+    if (n_endpoints > 65536) return SIM_ERR_INVALID_ARG;  // (src << 16 | dst) hash key
+    if (row_ptr[0] != 0) return SIM_ERR_TOPOLOGY;
+    for (int32_t v = 0; v < n_nodes; v++)
+        if (row_ptr[v + 1] < row_ptr[v]) return SIM_ERR_TOPOLOGY;
+    const int32_t m = row_ptr[n_nodes];
+    for (int32_t v = 0; v < n_nodes; v++)
+        for (int32_t l = row_ptr[v]; l < row_ptr[v + 1]; l++)
+            if (col_idx[l] < 0 || col_idx[l] >= n_nodes || col_idx[l] == v) return SIM_ERR_TOPOLOGY;
+    const size_t pm = (size_t)n_scenarios * (size_t)m;
+    for (size_t i = 0; i < pm; i++)
+        if (bw[i] < 1 || bw[i] > SIM_MAX_BW || lat[i] < 1 || lat[i] > SIM_MAX_LAT || cap[i] < 1 ||
+            cap[i] > SIM_MAX_CAP)
+            return SIM_ERR_TOPOLOGY;
+    sim_ctx *c = new (std::nothrow) sim_ctx();
+    if (!c) return SIM_ERR_OOM;
+    c->device = -1;  // bound to the current HIP device by the first load
+    c->n = n_nodes;
+    c->E = n_endpoints;
+    c->m = m;
+    c->S = n_scenarios;
+    c->arb = arb;
+    c->row_ptr.assign(row_ptr, row_ptr + n_nodes + 1);
+    c->col_idx.assign(col_idx, col_idx + m);
+    c->tail.resize(m);
+    for (int32_t v = 0; v < n_nodes; v++)
+        for (int32_t l = row_ptr[v]; l < row_ptr[v + 1]; l++) c->tail[l] = v;
+    c->bw.assign(bw, bw + pm);
+    c->lat.assign(lat, lat + pm);
+    c->cap.assign(cap, cap + pm);
+    build_hops(c);
+    *out = c;
+    return SIM_OK;
+}
+
+sim_status sim_load_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t group_size, const int32_t *order) {
+    if (!c) return SIM_ERR_INVALID_ARG;
+    if (coll != SIM_COLL_HIER_ALLREDUCE && group_size != 0)
+        return fail(c, SIM_ERR_INVALID_ARG, "group_size applies to the hierarchical all-reduce only");
+    Ranges R;
+    sim_status st = expand_collective(c, coll, bytes, group_size, order, R);
+    if (st != SIM_OK) return st;
+    return finish_load(c, R);
+}
+
+sim_status sim_load_transactions(sim_ctx *c, int64_t n, const int32_t *src, const int32_t *dst,
+                                 const int64_t *pred_ptr, const int64_t *pred_idx) {
+    if (!c || n < 0 || (n > 0 && (!src || !dst || !pred_ptr))) return SIM_ERR_INVALID_ARG;
+    if (n >= (int64_t)0xFFFFFFFFll) return fail(c, SIM_ERR_SIZE, "more than 2^32-2 transactions");
+    if (n > 0 && pred_ptr[0] != 0) return fail(c, SIM_ERR_INVALID_ARG, "pred_ptr[0] must be 0");
+    Ranges R;
+    for (int64_t x = 0; x < n; x++) {
+        if (src[x] < 0 || src[x] >= c->E || dst[x] < 0 || dst[x] >= c->E || src[x] == dst[x])
+            return fail(c, SIM_ERR_INVALID_ARG, "transaction " + std::to_string(x) + ": bad endpoints");
+        if (pred_ptr[x + 1] < pred_ptr[x]) return fail(c, SIM_ERR_INVALID_ARG, "pred_ptr not monotone");
+        R.add((uint64_t)x, 1, src[x], dst[x]);
+        for (int64_t q = pred_ptr[x]; q < pred_ptr[x + 1]; q++) {
+            if (!pred_idx || pred_idx[q] < 0 || pred_idx[q] >= n)
+                return fail(c, SIM_ERR_INVALID_ARG, "predecessor out of range");
+            R.pred(pred_idx[q], 0);
+        }
+    }
+    R.close();
+    return finish_load(c, R);
+}
+
+sim_status sim_sizes(const sim_ctx *c, int64_t *n_txn, int32_t *n_links, int32_t *n_scenarios, uint64_t *line_hops) {
+    if (!c) return SIM_ERR_INVALID_ARG;
+    if (n_links) *n_links = c->m;
+    if (n_scenarios) *n_scenarios = c->S;
+    if (!c->loaded) return SIM_ERR_STATE;
+    if (n_txn) *n_txn = c->T;
+    if (line_hops) *line_hops = c->line_hops;
+    return SIM_OK;
+}
+
+sim_status sim_run(sim_ctx *c, void *stream, uint32_t *d_completion, uint64_t *d_tx_lines,
+                   uint64_t *d_busy_cycles, uint32_t *d_makespan, uint64_t max_cycles) {
+    if (!c) return SIM_ERR_INVALID_ARG;
+    if (!c->loaded) return fail(c, SIM_ERR_STATE, "sim_run before a workload was loaded");
+    if ((!d_completion && c->T > 0) || !d_tx_lines || !d_busy_cycles || !d_makespan)
+        return fail(c, SIM_ERR_INVALID_ARG, "null output buffer");
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev != c->device)
+        return fail(c, SIM_ERR_DEVICE, "current HIP device differs from the context's device");
+    DevNet d = c->dn;
+    d.completion = d_completion;
+    d.tx_lines = d_tx_lines;
+    d.busy = d_busy_cycles;
+    d.makespan = d_makespan;
+    d.max_cycles = (max_cycles == 0 || max_cycles > simgpu::kCycleLimit) ? simgpu::kCycleLimit : max_cycles;
+    // Between two departing cycles at most fifo_total event jumps can happen
+    // (each lands on a distinct FIFO-head ready time); departing cycles are at
+    // most line_hops + T.
+    d.watchdog = (c->line_hops + (uint64_t)c->T + 1) * ((uint64_t)d.fifo_total + 2) + 1000000ull;
+    int e = simgpu::launch_engine(d, stream);
+    if (e != 0) return fail(c, SIM_ERR_DEVICE, std::string("kernel launch failed: ") + hipGetErrorString((hipError_t)e));
+    c->ran = true;
+    return SIM_OK;
+}
+
+sim_status sim_status_after_sync(sim_ctx *c, int32_t *status, uint64_t *cycles) {
+    if (!c) return SIM_ERR_INVALID_ARG;
+    if (!c->loaded || !c->ran) return fail(c, SIM_ERR_STATE, "no run to report on");
+    std::vector<int32_t> st(c->S);
+    if (hipMemcpy(st.data(), c->dn.status, sizeof(int32_t) * c->S, hipMemcpyDeviceToHost) != hipSuccess)
+        return fail(c, SIM_ERR_DEVICE, "hipMemcpy of status failed");
+    if (status) std::memcpy(status, st.data(), sizeof(int32_t) * c->S);
+    if (cycles &&
+        hipMemcpy(cycles, c->dn.cycles, sizeof(uint64_t) * c->S, hipMemcpyDeviceToHost) != hipSuccess)
+        return fail(c, SIM_ERR_DEVICE, "hipMemcpy of cycles failed");
+    for (int32_t s = 0; s < c->S; s++) {
+        if (st[s] == simgpu::kRunDeadlock) return fail(c, SIM_ERR_DEADLOCK, "scenario " + std::to_string(s) + " deadlocked");
+        if (st[s] == simgpu::kRunMaxCycles)
+            return fail(c, SIM_ERR_MAX_CYCLES, "scenario " + std::to_string(s) + " exceeded max_cycles");
+        if (st[s] == simgpu::kRunWatchdog)
+            return fail(c, SIM_ERR_DEVICE, "scenario " + std::to_string(s) + ": engine watchdog fired");
+        if (st[s] != simgpu::kRunOk) return fail(c, SIM_ERR_DEVICE, "scenario " + std::to_string(s) + " did not finish");
+    }
+    return SIM_OK;
+}
+
+sim_status sim_route(const sim_ctx *c, int32_t src, int32_t dst, int32_t *links, int32_t cap, int32_t *len) {
+    if (!c || !len || src < 0 || dst < 0 || src >= c->E || dst >= c->E) return SIM_ERR_INVALID_ARG;
+    std::vector<int32_t> hops;
+    if (src == dst) {
+        *len = 0;
+        return SIM_OK;
+    }
+    if (!trace_route(c, src, dst, hops)) return SIM_ERR_UNREACHABLE;
+    *len = (int32_t)hops.size();
+    if ((int32_t)hops.size() > cap || (!links && !hops.empty())) return SIM_ERR_SIZE;
+    std::copy(hops.begin(), hops.end(), links);
+    return SIM_OK;
+}
+
+const char *sim_last_error(const sim_ctx *c) { return c ? c->err.c_str() : "null context"; }
+
+void sim_destroy(sim_ctx *c) {
+    if (!c) return;
+    free_list(c->dev_static);
+    free_list(c->dev_state);
+    delete c;
+}
+
+}  // extern "C"

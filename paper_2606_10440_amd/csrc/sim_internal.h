@@ -1,0 +1,97 @@
+// Internal tables shared by the library's host builder (api.cpp) and its
+// device engine (engine.hip).  Not part of the public ABI.
+#pragma once
+#include <stdint.h>
+
+namespace simgpu {
+
+constexpr uint32_t kNever = 0xFFFFFFFFu;
+// Largest cycle a run may process: completion = cycle + 1 and ready =
+// cycle + latency must both fit in u32.
+constexpr uint64_t kCycleLimit = 0xFFFFFFFEull - (1ull << 20);
+
+// Per-scenario device status.
+// kRunWatchdog: more processed cycles than any correct run can need (every
+// processed cycle either moves a line or jumps to a strictly later FIFO-head
+// ready time), i.e. an engine fault; it ends the kernel instead of spinning.
+enum : int32_t { kRunOk = 0, kRunDeadlock = 7, kRunMaxCycles = 8, kRunWatchdog = 10, kRunRunning = -1 };
+
+// Everything a kernel needs, passed by value as the kernel argument.
+// "Static" tables are shared by all scenarios; "state" arrays have one slice
+// per scenario (scenario-major).
+struct DevNet {
+    // sizes
+    int32_t m;           // links
+    int32_t n_fsrc;      // links that carry traffic (FIFO sources / targets)
+    int32_t ns;          // injection streams
+    int32_t nflows;      // flow slots (distinct (src, dst) pairs used)
+    int32_t S;           // scenarios
+    int32_t arb;         // 0 lowest id, 1 round-robin
+    int32_t bmax;        // max bandwidth over links and scenarios
+    int32_t fifo_total;  // FIFO entries per scenario
+    int32_t req_total;   // request slots per scenario
+    int64_t T;           // transactions per scenario
+    uint64_t max_cycles; // simulated-cycle guard
+    uint64_t watchdog;   // processed-cycle bound (see kRunWatchdog)
+
+    // static topology tables
+    const int32_t *fsrc_link;     // [n_fsrc] link ids carrying traffic
+    const int32_t *port_at_head;  // [m] input-port index of l at head(l)
+    const int32_t *nports_tail;   // [m] number of input ports at tail(l)
+    const int32_t *fifo_off;      // [m] offset of l's ring in a scenario's FIFO storage
+    const int32_t *fifo_mask;     // [m] ring size - 1 (power of two >= max cap)
+    const int32_t *req_off;       // [m] offset of l's request slots
+    // injection streams: lines with the same source and first link, in id order,
+    // as a list of id ranges
+    const int32_t *s_link;        // [ns] first link
+    const int32_t *s_rbeg;        // [ns] first range
+    const int32_t *s_rend;        // [ns] one past last range
+    const uint32_t *r_start;      // [nr] first line id
+    const uint32_t *r_len;        // [nr] lines in range
+    const int32_t *r_path;        // [nr] index of the range's first hop in path_link
+    const int32_t *r_pd;          // [nr+1] predecessor descriptors of the range
+    // predecessor descriptor: line start+o may be injected once flow pd_flow has
+    // delivered more than pd_base + o lines (flows deliver in id order)
+    const int32_t *pd_flow;
+    const uint32_t *pd_base;
+    // paths: hop link ids, each path terminated by -(1 + flow slot)
+    const int32_t *path_link;
+
+    // per-scenario parameters [S*m]
+    const int32_t *bw, *lat, *cap;
+
+    // per-scenario state
+    uint32_t *fifo_x;     // [S*fifo_total] line id
+    uint32_t *fifo_rdy;   // [S*fifo_total] first cycle the entry may leave
+    int32_t *fifo_pp;     // [S*fifo_total] path index of the link the entry is on
+    uint32_t *qhead;      // [S*m] popped count
+    uint32_t *qtail;      // [S*m] pushed count
+    uint32_t *rr;         // [S*m] round-robin pointer
+    int32_t *cur_rng;     // [S*ns] stream cursor: range
+    uint32_t *cur_off;    // [S*ns] stream cursor: offset in range
+    uint32_t *delivered;  // [S*nflows] lines delivered per flow
+
+    // per-scenario scratch
+    uint32_t *req_cnt;    // [S*m] requests received this cycle
+    uint64_t *req_rec;    // [S*req_total] (key << 32) | (source << 8) | k
+    uint32_t *sreq_x;     // [S*(m+ns)*bmax] requested line
+    int32_t *sreq_pp;     // [S*(m+ns)*bmax] path index of the requested hop
+    int32_t *sreq_n;      // [S*(m+ns)] requests made this cycle
+    int32_t *grant;       // [S*(m+ns)*bmax] -1 none, -2 sink, else grant rank
+    uint32_t *gcount;     // [S*m] grants issued this cycle
+    uint32_t *glist;      // [S*m*bmax] (source << 8) | k by grant rank
+    uint8_t *gdep;        // [S*m*bmax] granted request actually departs
+
+    // outputs
+    uint32_t *completion; // [S*T]
+    uint64_t *tx_lines;   // [S*m]
+    uint64_t *busy;       // [S*m]
+    uint32_t *makespan;   // [S]
+    int32_t *status;      // [S]
+    uint64_t *cycles;     // [S] processed cycles
+};
+
+// Launch the engine for all scenarios on `stream`; returns a hipError_t value.
+int launch_engine(const DevNet &d, void *stream);
+
+}  // namespace simgpu

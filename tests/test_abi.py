@@ -1,0 +1,138 @@
+"""Host-side checks of libsimgpu that need no GPU.
+
+* the library loads and exports every function include/simgpu.h declares;
+* its routing builder (sim_create + sim_route, host only) gives the same
+  paths as the CPU oracle's independent router on every benchmark topology
+  and on random graphs;
+* argument / topology / size / reachability errors are reported before any
+  device work.
+"""
+from __future__ import annotations
+
+import os
+import re
+
+import numpy as np
+import pytest
+
+import sim_inputs as si
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def simlib():
+    from paper_2606_10440_amd import sim
+    if not os.path.exists(sim.LIB_PATH):
+        from paper_2606_10440_amd import build
+        build.build()
+    return sim
+
+
+def test_exports_match_header(simlib):
+    hdr = open(os.path.join(ROOT, "include", "simgpu.h")).read()
+    declared = set(re.findall(r"^\s*(?:sim_status|const char \*|void)\s*(sim_\w+)\s*\(", hdr, re.M))
+    assert declared == set(simlib.EXPORTS)
+    lib = simlib.lib()
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C5"])
+def test_routes_equal_oracle(simlib, oracle_lib, name):
+    w = si.config(name)
+    ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw[:w.n_links],
+                            w.lat[:w.n_links], w.cap[:w.n_links], w.arb)
+    try:
+        E = w.n_endpoints
+        rc, pp, pl = oracle_lib.paths(w.n_nodes, E, w.row_ptr, w.col_idx)
+        assert rc == 0
+        for s in range(E):
+            for d in range(E):
+                want = pl[pp[s * E + d]:pp[s * E + d + 1]]
+                got = simlib.sim_route(ctx, s, d)
+                assert np.array_equal(got, want), (s, d)
+    finally:
+        simlib.sim_destroy(ctx)
+
+
+def test_routes_equal_oracle_fat_tree_sample(simlib, oracle_lib):
+    w = si.config("C4")
+    ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, w.arb)
+    try:
+        E = w.n_endpoints
+        rc, pp, pl = oracle_lib.paths(w.n_nodes, E, w.row_ptr, w.col_idx)
+        rng = np.random.default_rng(3)
+        for s, d in rng.integers(0, E, size=(3000, 2)):
+            want = pl[pp[s * E + d]:pp[s * E + d + 1]]
+            assert np.array_equal(simlib.sim_route(ctx, int(s), int(d)), want)
+    finally:
+        simlib.sim_destroy(ctx)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_routes_equal_oracle_random(simlib, oracle_lib, seed):
+    rng = np.random.default_rng(seed)
+    n_end = int(rng.integers(2, 9))
+    n, rp, ci, bw, lat, cap = si.random_graph(rng, n_end, int(rng.integers(0, 6)), int(rng.integers(0, 10)))
+    ctx = simlib.sim_create(n, n_end, rp, ci, 1, bw, lat, cap, 0)
+    try:
+        rc, pp, pl = oracle_lib.paths(n, n_end, rp, ci)
+        for s in range(n_end):
+            for d in range(n_end):
+                want = pl[pp[s * n_end + d]:pp[s * n_end + d + 1]]
+                assert np.array_equal(simlib.sim_route(ctx, s, d), want)
+    finally:
+        simlib.sim_destroy(ctx)
+
+
+def test_create_rejects_bad_inputs(simlib):
+    rp = np.array([0, 1, 2], np.int32)
+    ci = np.array([1, 0], np.int32)
+    one = np.ones(2, np.int32)
+    with pytest.raises(simlib.SimError) as e:
+        simlib.sim_create(2, 2, rp, np.array([0, 0], np.int32), 1, one, one, one, 0)   # self loop
+    assert e.value.status == simlib.SIM_ERR_TOPOLOGY
+    with pytest.raises(simlib.SimError) as e:
+        simlib.sim_create(2, 2, rp, ci, 1, one * 0, one, one, 0)                       # b = 0
+    assert e.value.status == simlib.SIM_ERR_TOPOLOGY
+    with pytest.raises(simlib.SimError) as e:
+        simlib.sim_create(2, 2, rp, ci, 1, one, one, one, 5)                           # arbitration
+    assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+    with pytest.raises(simlib.SimError) as e:
+        simlib.sim_create(2, 3, rp, ci, 1, one, one, one, 0)                           # E > n
+    assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+
+
+def test_load_errors_before_device(simlib):
+    w = si.config("C2")
+    ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, w.arb)
+    try:
+        for nbytes in (0, 100, 128 * 7):
+            with pytest.raises(simlib.SimError) as e:
+                simlib.sim_load_collective(ctx, si.COLL_RING_ALLREDUCE, nbytes)
+            assert e.value.status == simlib.SIM_ERR_SIZE
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_collective(ctx, 9, 1024)
+        assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_collective(ctx, si.COLL_RING_ALLREDUCE, 1024, order=[0, 1, 2, 3, 4, 5, 6, 6])
+        assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_run(ctx, 0, 0, 0, 0, 0)
+        assert e.value.status == simlib.SIM_ERR_STATE
+    finally:
+        simlib.sim_destroy(ctx)
+    rp = np.array([0, 1, 1], np.int32)  # 0 -> 1 only: 1 cannot reach 0
+    ci = np.array([1], np.int32)
+    one = np.ones(1, np.int32)
+    ctx = simlib.sim_create(2, 2, rp, ci, 1, one, one, one, 0)
+    try:
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_transactions(ctx, [1], [0], [0, 0], [])
+        assert e.value.status == simlib.SIM_ERR_UNREACHABLE
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_transactions(ctx, [0], [0], [0, 0], [])
+        assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+    finally:
+        simlib.sim_destroy(ctx)

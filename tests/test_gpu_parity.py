@@ -1,0 +1,278 @@
+"""GPU parity: libsimgpu (HIP kernels, called through the C ABI) against the
+CPU oracle, bit for bit.
+
+Small and scaled cases run the oracle in the test and compare every
+completion cycle, tx_lines, busy_cycles and makespan.  The five full-size
+workloads compare SHA-256 digests of the complete outputs (and a sample of
+values) with ``tests/golden/*.json``, which tests/golden/make_golden.py
+wrote by running the oracle alone.
+"""
+from __future__ import annotations
+
+import hashlib
+import json
+import os
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+
+import sim_inputs as si
+
+pytestmark = pytest.mark.gpu
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    return torch
+
+
+@pytest.fixture(scope="module")
+def simmod(torch_cuda):
+    from paper_2606_10440_amd import sim
+    sim.lib()  # raises if the library was not built
+    return sim
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def run_gpu(simmod, w, max_cycles=0, txns=None):
+    s = simmod.Simulator(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw, w.lat, w.cap, w.arb,
+                         w.n_scenarios)
+    if txns is not None:
+        s.load_transactions(*txns)
+    else:
+        s.load_collective(w.coll, w.bytes, w.group_size, w.order)
+    r = s.run(max_cycles=max_cycles)
+    s.close()
+    return r
+
+
+def compare_scenario(r, s, want, T):
+    assert want.status_name == "OK"
+    assert r.scenario_status[s] == 0
+    comp = r.completion[s, :T].cpu().numpy().view(np.uint32)
+    bad = np.nonzero(comp != want.completion)[0]
+    assert bad.size == 0, f"scenario {s}: {bad.size} completions differ, first id {bad[:5]} " \
+                          f"gpu {comp[bad[:5]]} oracle {want.completion[bad[:5]]}"
+    assert np.array_equal(r.tx_lines[s].cpu().numpy().astype(np.uint64), want.tx_lines)
+    assert np.array_equal(r.busy_cycles[s].cpu().numpy().astype(np.uint64), want.busy_cycles)
+    assert int(r.makespan[s].item()) == want.makespan
+
+
+def compare_deadlocked(r, s, want):
+    """Same status, same counters, same cycle for every line that completed."""
+    assert r.scenario_status[s] == 7
+    comp = r.completion[s, :len(want.completion)].cpu().numpy().view(np.uint32)
+    done = want.completion != 0xFFFFFFFF
+    assert np.array_equal(comp[done], want.completion[done])
+    assert np.array_equal(r.tx_lines[s].cpu().numpy().astype(np.uint64), want.tx_lines)
+    assert np.array_equal(r.busy_cycles[s].cpu().numpy().astype(np.uint64), want.busy_cycles)
+
+
+def check_vs_oracle(simmod, oracle_lib, w, scenarios=None, expect_ok=True):
+    r = run_gpu(simmod, w)
+    if expect_ok:
+        assert r.status == 0, simmod.STATUS_NAMES[r.status]
+    n_ok = 0
+    for s in (range(w.n_scenarios) if scenarios is None else scenarios):
+        want = oracle_lib.simulate_workload(w, s)
+        if want.status_name == "DEADLOCK":
+            compare_deadlocked(r, s, want)
+        else:
+            compare_scenario(r, s, want, len(want.completion))
+            n_ok += 1
+    return r, n_ok
+
+
+# ----------------------------------------------------------------- small cases
+
+def test_c1_full(simmod, oracle_lib):
+    r, _ = check_vs_oracle(simmod, oracle_lib, si.config("C1"))
+    assert int(r.makespan[0]) == 266
+
+
+def test_c2_full(simmod, oracle_lib):
+    w = si.config("C2")
+    r, _ = check_vs_oracle(simmod, oracle_lib, w)
+    ids = np.arange(r.completion.shape[1], dtype=np.int64)
+    comp = r.completion[0].cpu().numpy().view(np.uint32)
+    assert np.array_equal(comp, 16384 * (ids // (16384 * 8)) + ids % 16384 + 51)
+
+
+@pytest.mark.parametrize("p,C,b,L,coll", [(3, 5, 1, 4, 0), (4, 8, 2, 3, 0), (5, 10, 1, 7, 1), (4, 6, 3, 2, 1),
+                                          (2, 9, 1, 1, 0), (6, 12, 2, 20, 1)])
+def test_mesh_collectives(simmod, oracle_lib, p, C, b, L, coll):
+    w = si.full_mesh(p, b=b, L=L, cap=max(1, b * (L + 1) // 2), coll=coll, nbytes=128 * C * p)
+    check_vs_oracle(simmod, oracle_lib, w)
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_dags(simmod, oracle_lib, seed):
+    rng = np.random.default_rng(1000 + seed)
+    n_end = int(rng.integers(2, 7))
+    S = int(rng.integers(1, 4))
+    n, rp, ci, bw, lat, cap = si.random_graph(rng, n_end, int(rng.integers(0, 4)), int(rng.integers(0, 6)),
+                                              bmax=4, Lmax=5, capmax=6, S=S)
+    src, dst, pptr, pidx = si.random_dag(rng, n_end, int(rng.integers(1, 300)), max_preds=3)
+    arb = seed % 2
+    w = si.Workload("rand", n, n_end, rp, ci, S, bw, lat, cap, arb, -1, 0)
+    say(f"random dag seed={seed} n={n} E={n_end} S={S} T={len(src)} arb={arb}")
+    r = run_gpu(simmod, w, txns=(src, dst, pptr, pidx))
+    m = int(rp[-1])
+    for s in range(S):
+        want = oracle_lib.simulate(n, n_end, rp, ci, bw[s * m:(s + 1) * m], lat[s * m:(s + 1) * m],
+                                   cap[s * m:(s + 1) * m], arb, txns=(src, dst, pptr, pidx))
+        if want.status_name == "DEADLOCK":
+            compare_deadlocked(r, s, want)
+            continue
+        compare_scenario(r, s, want, len(src))
+
+
+@pytest.mark.parametrize("k,nbytes,cap,lo,hi", [(4, 128 * 16, 5, 2, 9), (6, 128 * 4, 8, 5, 30),
+                                                (8, 128 * 2, 32, 100, 300)])
+def test_small_fat_trees(simmod, oracle_lib, k, nbytes, cap, lo, hi):
+    w = si.fat_tree(k, nbytes=nbytes, cap=cap, lat_lo=lo, lat_hi=hi)
+    check_vs_oracle(simmod, oracle_lib, w)
+
+
+def test_scaled_hierarchical(simmod, oracle_lib):
+    w = si.scaled(si.config("C3"), bytes=128 * 64 * 8 * 3)
+    check_vs_oracle(simmod, oracle_lib, w)
+
+
+def test_scaled_hierarchical_small_domains(simmod, oracle_lib):
+    w = si.domains_leaf_spine(G=3, M=4, n_leaf=3, n_spine=2, intra=(2, 3, 4), fabric=(1, 7, 6),
+                              nbytes=128 * 12 * 5)
+    check_vs_oracle(simmod, oracle_lib, w)
+
+
+def test_batched_torus_subset(simmod, oracle_lib):
+    w = si.take_scenarios(si.config("C5"), range(24))
+    w = si.scaled(w, bytes=128 * 16 * 64)
+    check_vs_oracle(simmod, oracle_lib, w)
+
+
+@pytest.mark.parametrize("arb,coll,depths,nbytes", [(0, si.COLL_DIRECT_ALLREDUCE, (8, 13, 16, 32), 128 * 120),
+                                                    (1, si.COLL_ALLTOALL, (8, 13, 16, 32), 128 * 3),
+                                                    (1, si.COLL_ALLTOALL, (16, 32, 64), 128 * 8),
+                                                    (1, si.COLL_DIRECT_ALLREDUCE, (1, 2, 3, 7, 16), 128 * 120),
+                                                    (0, si.COLL_ALLTOALL, (1, 2, 3, 7, 16), 128 * 3)])
+def test_torus_random_params(simmod, oracle_lib, arb, coll, depths, nbytes):
+    # A torus with wrap links has cyclic buffer dependencies: with tiny
+    # buffers many scenarios deadlock, which must be detected identically.
+    w = si.torus2d(4, 3, n_scenarios=40, seed=11 + arb + 2 * coll, bws=(1, 2, 3, 4), lat_lo=1, lat_hi=12,
+                   depths=depths, nbytes=nbytes, arb=arb, coll=coll)
+    r, n_ok = check_vs_oracle(simmod, oracle_lib, w, expect_ok=False)
+    if depths[0] >= 8:
+        assert n_ok > 0
+
+
+# ----------------------------------------------------------------- error paths
+
+def test_deadlock_detected(simmod, oracle_lib):
+    rp = np.array([0, 1, 2, 3], np.int32)
+    ci = np.array([1, 2, 0], np.int32)
+    one = np.ones(3, np.int32)
+    src = np.array([0, 1, 2] * 4, np.int32)
+    dst = np.array([2, 0, 1] * 4, np.int32)
+    pptr = np.zeros(13, np.int64)
+    w = si.Workload("ring3", 3, 3, rp, ci, 1, one, one, one, 0, -1, 0)
+    want = oracle_lib.simulate(3, 3, rp, ci, one, one, one, 0, txns=(src, dst, pptr, np.zeros(0, np.int64)))
+    assert want.status_name == "DEADLOCK"
+    r = run_gpu(simmod, w, txns=(src, dst, pptr, np.zeros(0, np.int64)))
+    assert r.status == simmod.SIM_ERR_DEADLOCK and r.scenario_status[0] == 7
+
+
+def test_cyclic_predecessors_deadlock(simmod):
+    rp = np.array([0, 1, 2, 3], np.int32)
+    ci = np.array([1, 2, 0], np.int32)
+    four = np.full(3, 4, np.int32)
+    w = si.Workload("ring3", 3, 3, rp, ci, 1, four, four, four, 0, -1, 0)
+    r = run_gpu(simmod, w, txns=(np.array([0, 1]), np.array([1, 2]), np.array([0, 1, 2]), np.array([1, 0])))
+    assert r.status == simmod.SIM_ERR_DEADLOCK
+
+
+def test_max_cycles_guard(simmod):
+    w = si.config("C1")
+    assert run_gpu(simmod, w, max_cycles=100).status == simmod.SIM_ERR_MAX_CYCLES
+    r = run_gpu(simmod, w, max_cycles=265)
+    assert r.status == 0 and int(r.makespan[0]) == 266
+
+
+def test_empty_workload(simmod):
+    w = si.config("C1")
+    r = run_gpu(simmod, w, txns=(np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(1, np.int64),
+                                 np.zeros(0, np.int64)))
+    assert r.status == 0 and int(r.makespan[0]) == 0
+    assert int(r.tx_lines.sum()) == 0
+
+
+def test_deterministic_repeat(simmod):
+    w = si.take_scenarios(si.config("C5"), range(64))
+    w = si.scaled(w, bytes=128 * 16 * 32)
+    s = simmod.Simulator.from_workload(w)
+    a = s.run()
+    ca = a.completion.clone()
+    b = s.run()
+    s.close()
+    assert a.status == b.status == 0
+    assert bool((ca == b.completion).all())
+
+
+# ----------------------------------------------------------------- full size
+
+def _digest(a: np.ndarray) -> str:
+    return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
+
+
+def _golden(name):
+    with open(os.path.join(HERE, "golden", f"{name}.json")) as f:
+        return json.load(f)
+
+
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4"])
+def test_full_size_digest(simmod, torch_cuda, name):
+    g = _golden(name)
+    w = si.config(name)
+    say(f"full-size {name}: running on GPU")
+    r = run_gpu(simmod, w)
+    assert r.status == 0
+    comp = r.completion[0].cpu().numpy().view(np.uint32)
+    idx = np.array(g["sample_idx"])
+    assert np.array_equal(comp[idx].astype(np.int64), np.array(g["sample_completion"]))
+    assert int(r.makespan[0]) == g["makespan"][0]
+    assert _digest(comp.astype("<u4")) == g["completion_sha256"][0]
+    assert _digest(r.tx_lines[0].cpu().numpy().astype("<u8")) == g["tx_lines_sha256"][0]
+    assert _digest(r.busy_cycles[0].cpu().numpy().astype("<u8")) == g["busy_cycles_sha256"][0]
+
+
+def test_full_size_batched_digest(simmod, torch_cuda):
+    g = _golden("C5")
+    w = si.config("C5")
+    say("full-size C5: running 4096 scenarios on GPU")
+    r = run_gpu(simmod, w)
+    assert r.status == 0
+    mk = r.makespan.cpu().numpy()
+    assert np.array_equal(mk, np.array(g["makespan"]))
+    tx = r.tx_lines.cpu().numpy().astype("<u8")
+    busy = r.busy_cycles.cpu().numpy().astype("<u8")
+    S = w.n_scenarios
+    chunk = 256
+    bad = []
+    with ThreadPoolExecutor(16) as ex:
+        for c0 in range(0, S, chunk):
+            host = r.completion[c0:c0 + chunk].cpu().numpy().view(np.uint32)
+            dig = list(ex.map(lambda i: _digest(host[i].astype("<u4")), range(host.shape[0])))
+            for i, d in enumerate(dig):
+                s = c0 + i
+                if d != g["completion_sha256"][s] or _digest(tx[s]) != g["tx_lines_sha256"][s] or \
+                        _digest(busy[s]) != g["busy_cycles_sha256"][s]:
+                    bad.append(s)
+    assert not bad, f"{len(bad)} scenarios differ, first {bad[:10]}"
