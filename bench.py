@@ -1,0 +1,211 @@
+"""Benchmark: simulated line-hop events per second on one MI355X.
+
+One step = one full simulation (``sim_run``) of the workload's whole batch:
+every line of every scenario advanced hop by hop to completion, inputs and
+state resident in HBM.  The default workload is the batched design sweep
+(4096 scenarios of a 4x4 torus, ring all-reduce of 4 MiB per endpoint,
+seeded bandwidth/latency/depth per scenario), the largest workload by
+line-hop events; ``--workload C1..C4`` selects the others.
+
+Prints one JSON line with the metric, a roofline entry for the engine
+kernel (algorithmic bytes per launch / measured launch time vs the 8 TB/s
+HBM peak) and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, 8 TB/s
+COMPLETION_BYTES = 4            # u32 completion cycle written per line
+KERNEL_NAME = "engine"          # substring of the dominant kernel's symbol
+
+DESCR = {
+    "C1": "4-endpoint full mesh, direct all-reduce 64 KiB, b=1 L=10 cap=16, lowest-id",
+    "C2": "8-endpoint full mesh, ring all-reduce 16 MiB, b=1 L=50 cap=64, lowest-id",
+    "C3": "8 full-mesh domains of 8 + 8-leaf/4-spine fabric, hierarchical all-reduce 64 MiB, round-robin",
+    "C4": "k=16 fat-tree (1024 hosts, 320 switches), all-to-all 64 KiB per pair, L in [100,300], cap 32",
+    "C5": "4096 scenarios x 4x4 torus, ring all-reduce 4 MiB, seeded b in {1,2,4}, L in [20,200], depth in {16,32,64}",
+}
+
+
+def algorithmic_bytes(T: int, S: int, m: int) -> int:
+    """Bytes the method must move per launch: one u32 completion per line
+    plus the per-link u64 counters and per-scenario makespan; scenario state
+    and routing tables are on-chip or reused and not counted."""
+    return S * (T * COMPLETION_BYTES + m * 16 + 4)
+
+
+def engine_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("engine.hip", "sim_internal.h"):
+        with open(os.path.join(ROOT, "paper_2606_10440_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload: str, launch_s: float):
+    """HBM traffic per launch from the committed rocprofv3 counter summary,
+    only if it was taken on the current engine source."""
+    path = os.path.join(ROOT, "profiles", f"engine_{workload}_hbm_counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        c = json.load(f)
+    if c.get("engine_source_hash") != engine_source_hash():
+        return None
+    return c.get("traffic_bytes_per_launch")
+
+
+def cpu_baseline(w, sample_seconds: float):
+    """Time the CPU oracle (single thread) on whole scenarios of the same
+    workload until about sample_seconds of event-loop time has accumulated."""
+    import oracle
+    oracle.build(force=False)
+    total_hops = 0
+    total_s = 0.0
+    n = 0
+    for s in range(w.n_scenarios):
+        r = oracle.simulate_workload(w, s)
+        total_hops += r.line_hops
+        total_s += r.seconds
+        n += 1
+        if total_s >= sample_seconds:
+            break
+    return {"value": total_hops / total_s, "unit": "line-hop events/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} of {w.n_scenarios} scenario(s), full size, event loop only "
+                      f"({total_hops} line-hops in {total_s:.1f} s)"}
+
+
+def copy_calibration():
+    """A plain device copy of known size, for scaling the HBM counters."""
+    import torch
+    n = 1 << 28  # 1 GiB of int32
+    a = torch.ones(n, dtype=torch.int32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="C5", choices=sorted(DESCR))
+    ap.add_argument("--cpu-sample-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-verify", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true")
+    a = ap.parse_args()
+
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(f"bench.py: this build runs on exactly one GPU (asked for {a.gpus}); "
+              "batched scenarios would shard across GPUs with no exchange, but no "
+              "multi-GPU path is built", file=sys.stderr)
+        sys.exit(2)
+    if a.calibrate_copy:
+        copy_calibration()
+        return
+
+    import torch
+    import sim_inputs as si
+    from paper_2606_10440_amd import sim
+
+    assert torch.cuda.is_available(), "bench.py needs a HIP device"
+    w = si.config(a.workload)
+    t0 = time.time()
+    s = sim.Simulator.from_workload(w)
+    T, m, S, line_hops = s.sizes()
+    outs = s.alloc_outputs()
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+    print(f"[bench] {a.workload}: T={T} S={S} m={m} line_hops/scenario={line_hops} setup {setup_s:.1f}s",
+          file=sys.stderr, flush=True)
+
+    stream = torch.cuda.current_stream()
+    for i in range(a.warmup):
+        s.enqueue(outs, stream=stream)
+        stream.synchronize()
+        print(f"[bench] warmup {i} done", file=sys.stderr, flush=True)
+    if a.warmup > 0:
+        rc, st, cyc = sim.sim_status_after_sync(s.ctx, S)
+        if rc != 0:
+            raise SystemExit(f"simulation failed: {sim.STATUS_NAMES[rc]} {sim.sim_last_error(s.ctx)}")
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(a.steps):
+        s.enqueue(outs, stream=stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    gpu_ms = ev0.elapsed_time(ev1)
+    rc, st, cyc = sim.sim_status_after_sync(s.ctx, S)
+    if rc != 0:
+        raise SystemExit(f"simulation failed: {sim.STATUS_NAMES[rc]}")
+    print(f"[bench] timed {a.steps} steps: {gpu_ms:.1f} ms (wall {wall * 1e3:.1f} ms)", file=sys.stderr, flush=True)
+
+    verified = None
+    if not a.no_verify:
+        gpath = os.path.join(ROOT, "tests", "golden", f"{a.workload}.json")
+        if os.path.exists(gpath):
+            with open(gpath) as f:
+                g = json.load(f)
+            mk = outs[3].cpu().numpy()
+            ok = np.array_equal(mk, np.array(g["makespan"]))
+            for sc in sorted({0, S // 2, S - 1}):
+                comp = outs[0][sc, :T].cpu().numpy().view(np.uint32).astype("<u4")
+                ok = ok and hashlib.sha256(comp.tobytes()).hexdigest() == g["completion_sha256"][sc]
+            verified = bool(ok)
+
+    ms_per_step = gpu_ms / a.steps
+    launch_s = ms_per_step / 1e3
+    total_hops = line_hops * S
+    value = total_hops * a.steps / (gpu_ms / 1e3)
+    alg = algorithmic_bytes(T, S, m)
+    achieved = alg / launch_s / 1e9
+    out = {
+        "metric": "simulated line-hop events/sec on 1 MI355X (bit-exact vs CPU oracle)",
+        "value": value,
+        "unit": "line-hop events/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {"workload": f"{a.workload}: {DESCR[a.workload]}", "scenarios": S, "transactions": T * S,
+                   "line_hops": total_hops, "links": m,
+                   "processed_cycles_max": int(cyc.max()), "processed_cycles_sum": int(cyc.sum()),
+                   "bit_exact_vs_golden": verified},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": load_traffic(a.workload, launch_s),
+                     "kernel": KERNEL_NAME, "algorithmic_bytes_per_launch": alg},
+    }
+    s.close()
+    if not a.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, a.cpu_sample_seconds)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()
