@@ -9,6 +9,8 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <cstdlib>
+#include <cstdio>
 #include <cstring>
 #include <new>
 #include <string>
@@ -398,6 +400,76 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     }
     if (ftot >= INT32_MAX || rtot >= INT32_MAX) return fail(c, SIM_ERR_SIZE, "state too large");
 
+    // Lane-engine tables: lane i owns traffic link fsrc[i] (its FIFO, its
+    // injection stream and the arbitration for entering it).
+    const int32_t nl = (int32_t)fsrc.size();
+    std::vector<int32_t> link_lane(m, -1);
+    for (int32_t i = 0; i < nl; i++) link_lane[fsrc[i]] = i;
+    std::vector<int32_t> path_lane(c->path_link.size());
+    for (size_t q = 0; q < c->path_link.size(); q++) {
+        int32_t v = c->path_link[q];
+        path_lane[q] = v >= 0 ? link_lane[v] : v;
+    }
+    // feeders of each target lane: lanes whose lines continue onto it, plus its stream
+    std::vector<std::vector<int32_t>> feeders(nl);
+    for (size_t q = 0; q + 1 < path_lane.size(); q++)
+        if (path_lane[q] >= 0 && path_lane[q + 1] >= 0) feeders[path_lane[q + 1]].push_back(path_lane[q]);
+    std::vector<int32_t> ln_P(nl), ln_port(nl), ln_fifo(nl), ln_mask(nl), ln_req(nl), ln_reqcap(nl),
+        ln_srbeg(nl, 0), ln_srend(nl, 0);
+    for (size_t j = 0; j < s_link.size(); j++) {
+        ln_srbeg[link_lane[s_link[j]]] = s_rbeg[j];
+        ln_srend[link_lane[s_link[j]]] = s_rend[j];
+    }
+    int32_t bm = 1;
+    while (bm < bmax) bm <<= 1;
+    int64_t lf = 0, lr = 0;
+    for (int32_t i = 0; i < nl; i++) {
+        const int32_t l = fsrc[i];
+        auto &fv = feeders[i];
+        std::sort(fv.begin(), fv.end());
+        fv.erase(std::unique(fv.begin(), fv.end()), fv.end());
+        ln_P[i] = nports_tail[l];
+        ln_port[i] = port_at_head[l];
+        ln_fifo[i] = (int32_t)lf;
+        ln_mask[i] = fifo_mask[l];
+        lf += fifo_mask[l] + 1;
+        const int32_t nfeed = (int32_t)fv.size() + (ln_srend[i] > ln_srbeg[i] ? 1 : 0);
+        ln_req[i] = (int32_t)lr;
+        ln_reqcap[i] = nfeed * bmax;
+        lr += (int64_t)nfeed * bmax;
+    }
+    // LDS layout of the lane engine (16-byte FIFO entries and request records)
+    auto align16 = [](int64_t v) { return (v + 15) & ~(int64_t)15; };
+    int64_t off = lf * 16;
+    const int64_t o_path = off;
+    const int64_t path_bytes = (int64_t)path_lane.size() * 4;
+    const bool path_in_lds = path_bytes <= 16384;
+    if (path_in_lds) off = align16(off + path_bytes);
+    const int64_t o_deliv = off;
+    off = align16(off + (int64_t)nflows * 4);
+    const int64_t o_reqcnt = off;
+    off = align16(off + (int64_t)nl * 4);
+    const int64_t o_reqb = off;
+    off = align16(off + (int64_t)nl * 8);
+    const int64_t o_req = off;
+    off = align16(off + lr * 16);
+    const int64_t o_glist = off;
+    off = align16(off + (int64_t)nl * bm * 4);
+    const int64_t o_grant = off;
+    off = align16(off + (int64_t)2 * nl * bm * 4);
+    const int64_t o_gdep = off;
+    off = align16(off + (int64_t)nl * bm * 4);
+    const int64_t o_red = off;
+    off = align16(off + 64);
+    const int64_t lds_bytes = off;
+    int engine = (nl >= 1 && nl <= 1024 && lds_bytes <= 160 * 1024 && bm <= 64) ? simgpu::kEngineLane
+                                                                                 : simgpu::kEngineWorkgroup;
+    if (const char *ev = std::getenv("SIMGPU_ENGINE")) {
+        if (!std::strcmp(ev, "workgroup")) engine = simgpu::kEngineWorkgroup;
+        if (!std::strcmp(ev, "lane") && engine != simgpu::kEngineLane)
+            return fail(c, SIM_ERR_INVALID_ARG, "SIMGPU_ENGINE=lane: scenario state does not fit in LDS");
+    }
+
     // everything below touches the device
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess) return fail(c, SIM_ERR_DEVICE, "no HIP device");
@@ -415,6 +487,27 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     d.fifo_total = (int32_t)ftot;
     d.req_total = (int32_t)rtot;
     d.T = T;
+    d.engine = engine;
+    d.nl = nl;
+    d.lane_threads = ((nl + 63) / 64) * 64;
+    if (const char *ev = std::getenv("SIMGPU_LANE_THREADS")) {
+        const int v = std::atoi(ev);
+        if (v >= d.lane_threads && v <= 1024 && v % 64 == 0) d.lane_threads = v;
+    }
+    d.bm = bm;
+    d.lds_bytes = (int32_t)lds_bytes;
+    d.o_path = (int32_t)o_path;
+    d.o_deliv = (int32_t)o_deliv;
+    d.o_reqcnt = (int32_t)o_reqcnt;
+    d.o_reqb = (int32_t)o_reqb;
+    d.o_req = (int32_t)o_req;
+    d.o_glist = (int32_t)o_glist;
+    d.o_grant = (int32_t)o_grant;
+    d.o_gdep = (int32_t)o_gdep;
+    d.o_red = (int32_t)o_red;
+    d.path_len = (int32_t)path_lane.size();
+    d.path_in_lds = path_in_lds ? 1 : 0;
+    d.req_slots = (int32_t)lr;
     sim_status st;
     auto &own = c->dev_static;
 #define UP(vec, field)                                         \
@@ -443,11 +536,25 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     UP(c->bw, bw);
     UP(c->lat, lat);
     UP(c->cap, cap);
+    int32_t *tmp_ln_P, *tmp_ln_port, *tmp_ln_fifo, *tmp_ln_mask, *tmp_ln_req, *tmp_ln_reqcap, *tmp_ln_srbeg,
+        *tmp_ln_srend, *tmp_link_lane, *tmp_path_lane;
+    UP(ln_P, ln_P);
+    UP(ln_port, ln_port);
+    UP(ln_fifo, ln_fifo);
+    UP(ln_mask, ln_mask);
+    UP(ln_req, ln_req);
+    UP(ln_reqcap, ln_reqcap);
+    UP(ln_srbeg, ln_srbeg);
+    UP(ln_srend, ln_srend);
+    UP(link_lane, link_lane);
+    UP(path_lane, path_lane);
 #undef UP
     const size_t S = (size_t)c->S;
     const size_t nsrc = (size_t)m + (size_t)d.ns;
     auto &ost = c->dev_state;
-    if ((st = alloc(c, ost, S * ftot, &d.fifo_x)) || (st = alloc(c, ost, S * ftot, &d.fifo_rdy)) ||
+    if ((st = alloc(c, ost, S, &d.status)) || (st = alloc(c, ost, S, &d.cycles))) return st;
+    if (engine == simgpu::kEngineWorkgroup &&
+        ((st = alloc(c, ost, S * ftot, &d.fifo_x)) || (st = alloc(c, ost, S * ftot, &d.fifo_rdy)) ||
         (st = alloc(c, ost, S * ftot, &d.fifo_pp)) || (st = alloc(c, ost, S * m, &d.qhead)) ||
         (st = alloc(c, ost, S * m, &d.qtail)) || (st = alloc(c, ost, S * m, &d.rr)) ||
         (st = alloc(c, ost, S * d.ns, &d.cur_rng)) || (st = alloc(c, ost, S * d.ns, &d.cur_off)) ||
@@ -455,8 +562,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         (st = alloc(c, ost, S * rtot, &d.req_rec)) || (st = alloc(c, ost, S * nsrc * bmax, &d.sreq_x)) ||
         (st = alloc(c, ost, S * nsrc * bmax, &d.sreq_pp)) || (st = alloc(c, ost, S * nsrc, &d.sreq_n)) ||
         (st = alloc(c, ost, S * nsrc * bmax, &d.grant)) || (st = alloc(c, ost, S * m, &d.gcount)) ||
-        (st = alloc(c, ost, S * m * bmax, &d.glist)) || (st = alloc(c, ost, S * m * bmax, &d.gdep)) ||
-        (st = alloc(c, ost, S, &d.status)) || (st = alloc(c, ost, S, &d.cycles)))
+        (st = alloc(c, ost, S * m * bmax, &d.glist)) || (st = alloc(c, ost, S * m * bmax, &d.gdep))))
         return st;
     c->dn = d;
     c->loaded = true;
@@ -589,6 +695,8 @@ sim_status sim_status_after_sync(sim_ctx *c, int32_t *status, uint64_t *cycles) 
         if (st[s] == simgpu::kRunDeadlock) return fail(c, SIM_ERR_DEADLOCK, "scenario " + std::to_string(s) + " deadlocked");
         if (st[s] == simgpu::kRunMaxCycles)
             return fail(c, SIM_ERR_MAX_CYCLES, "scenario " + std::to_string(s) + " exceeded max_cycles");
+        if (st[s] == simgpu::kRunInternal)
+            return fail(c, SIM_ERR_DEVICE, "scenario " + std::to_string(s) + ": request slot overflow (internal)");
         if (st[s] == simgpu::kRunWatchdog)
             return fail(c, SIM_ERR_DEVICE, "scenario " + std::to_string(s) + ": engine watchdog fired");
         if (st[s] != simgpu::kRunOk) return fail(c, SIM_ERR_DEVICE, "scenario " + std::to_string(s) + " did not finish");

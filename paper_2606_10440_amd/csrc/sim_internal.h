@@ -14,7 +14,7 @@ constexpr uint64_t kCycleLimit = 0xFFFFFFFEull - (1ull << 20);
 // kRunWatchdog: more processed cycles than any correct run can need (every
 // processed cycle either moves a line or jumps to a strictly later FIFO-head
 // ready time), i.e. an engine fault; it ends the kernel instead of spinning.
-enum : int32_t { kRunOk = 0, kRunDeadlock = 7, kRunMaxCycles = 8, kRunWatchdog = 10, kRunRunning = -1 };
+enum : int32_t { kRunOk = 0, kRunDeadlock = 7, kRunMaxCycles = 8, kRunWatchdog = 10, kRunInternal = 11, kRunRunning = -1 };
 
 // Everything a kernel needs, passed by value as the kernel argument.
 // "Static" tables are shared by all scenarios; "state" arrays have one slice
@@ -82,14 +82,40 @@ struct DevNet {
     uint32_t *glist;      // [S*m*bmax] (source << 8) | k by grant rank
     uint8_t *gdep;        // [S*m*bmax] granted request actually departs
 
+    // lane engine: one lane per traffic-carrying link, a scenario's whole
+    // state in one workgroup's LDS and registers
+    int32_t engine;       // kEngineWorkgroup or kEngineLane
+    int32_t nl;           // lanes (= n_fsrc), lane i owns link fsrc_link[i]
+    int32_t lane_threads; // workgroup size of the lane engine (multiple of 64, >= nl)
+    int32_t bm;           // compile-time bandwidth bound (power of two >= bmax)
+    int32_t lds_bytes;    // dynamic LDS per workgroup
+    int32_t o_path, o_deliv, o_reqcnt, o_reqb, o_req, o_glist, o_grant, o_gdep, o_red;  // LDS byte offsets
+    int32_t path_len;     // entries of path_lane
+    int32_t path_in_lds;  // path table copied into LDS
+    int32_t req_slots;    // request slots in LDS
+    const int32_t *ln_P;      // [nl] input ports at the tail of the lane's link
+    const int32_t *ln_port;   // [nl] port index of the lane's link at its head
+    const int32_t *ln_fifo;   // [nl] first LDS FIFO entry
+    const int32_t *ln_mask;   // [nl] ring size - 1
+    const int32_t *ln_req;    // [nl] first request slot of the lane as a target
+    const int32_t *ln_reqcap; // [nl] request slots of the lane
+    const int32_t *ln_srbeg;  // [nl] stream ranges of the lane's link (empty if none)
+    const int32_t *ln_srend;
+    const int32_t *link_lane; // [m] lane of a link, -1 if no traffic
+    const int32_t *path_lane; // path table with link ids replaced by lanes
+
     // outputs
     uint32_t *completion; // [S*T]
     uint64_t *tx_lines;   // [S*m]
     uint64_t *busy;       // [S*m]
     uint32_t *makespan;   // [S]
-    int32_t *status;      // [S]
+    int32_t *status;      // [S] (kRunInternal: an LDS request slot overflowed)
     uint64_t *cycles;     // [S] processed cycles
 };
+
+enum : int32_t { kEngineWorkgroup = 0, kEngineLane = 1 };
+// Registers cache up to this many predecessor descriptors of a stream's range.
+constexpr int kPredCache = 8;
 
 // Launch the engine for all scenarios on `stream`; returns a hipError_t value.
 int launch_engine(const DevNet &d, void *stream);

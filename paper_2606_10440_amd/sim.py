@@ -18,7 +18,7 @@ from typing import Optional
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libsimgpu.so")
+LIB_PATH = os.environ.get("SIMGPU_LIB", os.path.join(_HERE, "libsimgpu.so"))
 
 SIM_OK, SIM_ERR_INVALID_ARG, SIM_ERR_TOPOLOGY, SIM_ERR_UNREACHABLE, SIM_ERR_SIZE = 0, 1, 2, 3, 4
 SIM_ERR_OOM, SIM_ERR_DEVICE, SIM_ERR_DEADLOCK, SIM_ERR_MAX_CYCLES, SIM_ERR_STATE = 5, 6, 7, 8, 9
