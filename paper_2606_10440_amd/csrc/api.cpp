@@ -400,75 +400,146 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     }
     if (ftot >= INT32_MAX || rtot >= INT32_MAX) return fail(c, SIM_ERR_SIZE, "state too large");
 
-    // Lane-engine tables: lane i owns traffic link fsrc[i] (its FIFO, its
-    // injection stream and the arbitration for entering it).
+    // Which links carry traffic, and which of them start an injection stream.
     const int32_t nl = (int32_t)fsrc.size();
+    std::vector<char> has_stream(m, 0);
+    for (int32_t f : s_link) has_stream[f] = 1;
+    int32_t bm = 1;
+    while (bm < bmax) bm <<= 1;
+    bool rr_ports_fit = true;  // every input-port set fits a 64-bit mask
+    for (int32_t l : fsrc)
+        if (nports_tail[l] > 64) rr_ports_fit = false;
+    const bool any_preds = !pd_flow.empty();
+
+    // Engine choice.  Lane engine with FIFO rings in LDS when a scenario fits
+    // a workgroup's LDS; the compact b = 1 engine for large single-line-rate
+    // graphs; the lane engine with FIFO rings in HBM when only its mailboxes
+    // fit; else the generic workgroup engine.
+    auto align16 = [](int64_t v) { return (v + 15) & ~(int64_t)15; };
+    const int64_t kLds = 160 * 1024;
+    int64_t lf = 0;
+    for (int32_t l : fsrc) lf += fifo_mask[l] + 1;
+    // mailbox slots of the lane engine: feeders of each target lane x bmax
     std::vector<int32_t> link_lane(m, -1);
     for (int32_t i = 0; i < nl; i++) link_lane[fsrc[i]] = i;
+    std::vector<std::vector<int32_t>> feeders(nl);
+    for (size_t q = 0; q + 1 < c->path_link.size(); q++) {
+        const int32_t a = c->path_link[q], b2 = c->path_link[q + 1];
+        if (a >= 0 && b2 >= 0) feeders[link_lane[b2]].push_back(link_lane[a]);
+    }
+    int64_t lr = 0;
+    for (int32_t i = 0; i < nl; i++) {
+        auto &fv = feeders[i];
+        std::sort(fv.begin(), fv.end());
+        fv.erase(std::unique(fv.begin(), fv.end()), fv.end());
+        lr += (int64_t)((int32_t)fv.size() + (has_stream[fsrc[i]] ? 1 : 0)) * bmax;
+    }
+    const int64_t path_bytes = (int64_t)c->path_link.size() * 4;
+    struct LaneLayout { int64_t o_path, o_deliv, o_reqcnt, o_reqb, o_req, o_glist, o_grant, o_gdep, o_red, bytes; bool path_lds; };
+    auto lane_layout = [&](bool fifo_lds) {
+        LaneLayout L{};
+        int64_t off = fifo_lds ? lf * 16 : 0;
+        L.o_path = off;
+        L.path_lds = path_bytes <= 16384;
+        if (L.path_lds) off = align16(off + path_bytes);
+        L.o_deliv = off;
+        off = align16(off + (int64_t)nflows * 4);
+        L.o_reqcnt = off;
+        off = align16(off + (int64_t)nl * 4);
+        L.o_reqb = off;
+        off = align16(off + (int64_t)nl * 8);
+        L.o_req = off;
+        off = align16(off + lr * 16);
+        L.o_glist = off;
+        off = align16(off + (int64_t)nl * bm * 4);
+        L.o_grant = off;
+        off = align16(off + (int64_t)2 * nl * bm * 4);
+        L.o_gdep = off;
+        off = align16(off + (int64_t)nl * bm * 4);
+        L.o_red = off;
+        L.bytes = align16(off + 64);
+        return L;
+    };
+    const LaneLayout lay_lds = lane_layout(true), lay_hbm = lane_layout(false);
+    // compact engine LDS: one request word per target lane (+ grant words and
+    // the in-link lane table for round-robin), delivered counters if they fit
+    // words (lowest-id: two buffers) | grant words + in-lane table (round-robin)
+    // | per-lane counters | delivered counters if they fit | reduction slots
+    // round-robin: request masks + posts (8 B per lane) + in-lane table (u16);
+    // lowest-id: two buffers of request words; then one counter per lane
+    // (+ in-lane offsets, u16) then one counter per lane
+    const int64_t b1_words = (c->arb == SIM_ARB_ROUND_ROBIN ? (int64_t)nl * 16 + align16((int64_t)m * 2) +
+                                                                  align16((int64_t)nl * 2)
+                                                            : (int64_t)nl * 16) +
+                             (int64_t)nl * 4;
+    int32_t b1_ring = 1;
+    for (int32_t l : fsrc) b1_ring = std::max(b1_ring, fifo_mask[l] + 1);
+    const bool b1_deliv_lds = any_preds && align16(b1_words) + (int64_t)nflows * 4 + 64 <= kLds;
+    const int64_t b1_bytes = align16(align16(b1_words) + (b1_deliv_lds ? (int64_t)nflows * 4 : 0)) + 64;
+    const bool b1_ok = bmax == 1 && (int64_t)s_link.size() <= 1024 && nl <= 8 * 1024 && nl < 65536 && b1_bytes <= kLds &&
+                       (c->arb == SIM_ARB_LOWEST_ID || rr_ports_fit);
+    int engine = simgpu::kEngineWorkgroup;
+    if (nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds) engine = simgpu::kEngineLane;
+    else if (nl >= 1 && b1_ok) engine = simgpu::kEngineB1;
+    else if (nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds) engine = simgpu::kEngineLaneHbm;
+    if (const char *ev = std::getenv("SIMGPU_ENGINE")) {
+        int want = -1;
+        if (!std::strcmp(ev, "workgroup")) want = simgpu::kEngineWorkgroup;
+        if (!std::strcmp(ev, "lane")) want = simgpu::kEngineLane;
+        if (!std::strcmp(ev, "lanehbm")) want = simgpu::kEngineLaneHbm;
+        if (!std::strcmp(ev, "b1")) want = simgpu::kEngineB1;
+        const bool ok = want == simgpu::kEngineWorkgroup ||
+                        (want == simgpu::kEngineLane && engine == simgpu::kEngineLane) ||
+                        (want == simgpu::kEngineLaneHbm && nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds) ||
+                        (want == simgpu::kEngineB1 && nl >= 1 && b1_ok);
+        if (want < 0 || !ok) return fail(c, SIM_ERR_INVALID_ARG, std::string("SIMGPU_ENGINE=") + ev + " is not usable here");
+        engine = want;
+    }
+
+    // Lane order: traffic links ascending; the compact engine puts the links
+    // that start a stream first so that stream j is owned by thread j.
+    std::vector<int32_t> lane_link(fsrc);
+    if (engine == simgpu::kEngineB1)
+        std::stable_partition(lane_link.begin(), lane_link.end(), [&](int32_t l) { return has_stream[l] != 0; });
+    for (int32_t i = 0; i < nl; i++) link_lane[lane_link[i]] = i;
     std::vector<int32_t> path_lane(c->path_link.size());
     for (size_t q = 0; q < c->path_link.size(); q++) {
         int32_t v = c->path_link[q];
         path_lane[q] = v >= 0 ? link_lane[v] : v;
     }
-    // feeders of each target lane: lanes whose lines continue onto it, plus its stream
-    std::vector<std::vector<int32_t>> feeders(nl);
-    for (size_t q = 0; q + 1 < path_lane.size(); q++)
-        if (path_lane[q] >= 0 && path_lane[q + 1] >= 0) feeders[path_lane[q + 1]].push_back(path_lane[q]);
     std::vector<int32_t> ln_P(nl), ln_port(nl), ln_fifo(nl), ln_mask(nl), ln_req(nl), ln_reqcap(nl),
         ln_srbeg(nl, 0), ln_srend(nl, 0);
     for (size_t j = 0; j < s_link.size(); j++) {
         ln_srbeg[link_lane[s_link[j]]] = s_rbeg[j];
         ln_srend[link_lane[s_link[j]]] = s_rend[j];
     }
-    int32_t bm = 1;
-    while (bm < bmax) bm <<= 1;
-    int64_t lf = 0, lr = 0;
-    for (int32_t i = 0; i < nl; i++) {
-        const int32_t l = fsrc[i];
-        auto &fv = feeders[i];
-        std::sort(fv.begin(), fv.end());
-        fv.erase(std::unique(fv.begin(), fv.end()), fv.end());
-        ln_P[i] = nports_tail[l];
-        ln_port[i] = port_at_head[l];
-        ln_fifo[i] = (int32_t)lf;
-        ln_mask[i] = fifo_mask[l];
-        lf += fifo_mask[l] + 1;
-        const int32_t nfeed = (int32_t)fv.size() + (ln_srend[i] > ln_srbeg[i] ? 1 : 0);
-        ln_req[i] = (int32_t)lr;
-        ln_reqcap[i] = nfeed * bmax;
-        lr += (int64_t)nfeed * bmax;
+    {
+        int64_t f = 0, r = 0;
+        for (int32_t i = 0; i < nl; i++) {
+            const int32_t l = lane_link[i];
+            ln_P[i] = nports_tail[l];
+            ln_port[i] = port_at_head[l];
+            ln_fifo[i] = (int32_t)f;
+            ln_mask[i] = fifo_mask[l];
+            f += fifo_mask[l] + 1;
+            // feeders were collected in ascending-link lane order
+            const int32_t nfeed = (int32_t)feeders[std::lower_bound(fsrc.begin(), fsrc.end(), l) - fsrc.begin()].size() +
+                                  (has_stream[l] ? 1 : 0);
+            ln_req[i] = (int32_t)r;
+            ln_reqcap[i] = nfeed * bmax;
+            r += (int64_t)nfeed * bmax;
+        }
     }
-    // LDS layout of the lane engine (16-byte FIFO entries and request records)
-    auto align16 = [](int64_t v) { return (v + 15) & ~(int64_t)15; };
-    int64_t off = lf * 16;
-    const int64_t o_path = off;
-    const int64_t path_bytes = (int64_t)path_lane.size() * 4;
-    const bool path_in_lds = path_bytes <= 16384;
-    if (path_in_lds) off = align16(off + path_bytes);
-    const int64_t o_deliv = off;
-    off = align16(off + (int64_t)nflows * 4);
-    const int64_t o_reqcnt = off;
-    off = align16(off + (int64_t)nl * 4);
-    const int64_t o_reqb = off;
-    off = align16(off + (int64_t)nl * 8);
-    const int64_t o_req = off;
-    off = align16(off + lr * 16);
-    const int64_t o_glist = off;
-    off = align16(off + (int64_t)nl * bm * 4);
-    const int64_t o_grant = off;
-    off = align16(off + (int64_t)2 * nl * bm * 4);
-    const int64_t o_gdep = off;
-    off = align16(off + (int64_t)nl * bm * 4);
-    const int64_t o_red = off;
-    off = align16(off + 64);
-    const int64_t lds_bytes = off;
-    int engine = (nl >= 1 && nl <= 1024 && lds_bytes <= 160 * 1024 && bm <= 64) ? simgpu::kEngineLane
-                                                                                 : simgpu::kEngineWorkgroup;
-    if (const char *ev = std::getenv("SIMGPU_ENGINE")) {
-        if (!std::strcmp(ev, "workgroup")) engine = simgpu::kEngineWorkgroup;
-        if (!std::strcmp(ev, "lane") && engine != simgpu::kEngineLane)
-            return fail(c, SIM_ERR_INVALID_ARG, "SIMGPU_ENGINE=lane: scenario state does not fit in LDS");
-    }
+    // round-robin port -> lane table of the compact engine: for every node,
+    // the lanes of its in-links in port order (-1 for links without traffic)
+    std::vector<int32_t> node_inoff(c->n + 1, 0), in_lane(m, -1), ln_inoff(nl, 0);
+    for (int32_t l = 0; l < m; l++) node_inoff[c->col_idx[l] + 1]++;
+    for (int32_t v = 0; v < c->n; v++) node_inoff[v + 1] += node_inoff[v];
+    for (int32_t l = 0; l < m; l++) in_lane[node_inoff[c->col_idx[l]] + port_at_head[l]] = link_lane[l];
+    for (int32_t i = 0; i < nl; i++) ln_inoff[i] = node_inoff[c->tail[lane_link[i]]];
+    const LaneLayout &lay = engine == simgpu::kEngineLane ? lay_lds : lay_hbm;
+    const bool path_in_lds = lay.path_lds;
+    const int64_t lds_bytes = engine == simgpu::kEngineB1 ? b1_bytes : lay.bytes;
 
     // everything below touches the device
     int dev = -1;
@@ -489,6 +560,19 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     d.T = T;
     d.engine = engine;
     d.nl = nl;
+    d.has_preds = any_preds ? 1 : 0;
+    d.b1_ns = (int32_t)s_link.size();
+    d.b1_lpt = (nl + 1023) / 1024;
+    d.b1_deliv_lds = b1_deliv_lds ? 1 : 0;
+    d.o_word = 0;
+    d.o_gnt = (int32_t)((int64_t)nl * 8);   // round-robin posts
+    d.o_inl = (int32_t)((int64_t)nl * 16);
+    d.o_b1ino = (int32_t)((int64_t)nl * 16 + align16((int64_t)m * 2));
+    d.o_b1cnt = (int32_t)(c->arb == SIM_ARB_ROUND_ROBIN ? d.o_b1ino + align16((int64_t)nl * 2) : (int64_t)nl * 16);
+    d.b1_ring_lg = 0;
+    while ((1 << d.b1_ring_lg) < b1_ring) d.b1_ring_lg++;
+    d.o_b1deliv = (int32_t)align16(b1_words);
+    d.o_b1red = (int32_t)(b1_bytes - 64);
     d.lane_threads = ((nl + 63) / 64) * 64;
     if (const char *ev = std::getenv("SIMGPU_LANE_THREADS")) {
         const int v = std::atoi(ev);
@@ -496,18 +580,20 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     }
     d.bm = bm;
     d.lds_bytes = (int32_t)lds_bytes;
-    d.o_path = (int32_t)o_path;
-    d.o_deliv = (int32_t)o_deliv;
-    d.o_reqcnt = (int32_t)o_reqcnt;
-    d.o_reqb = (int32_t)o_reqb;
-    d.o_req = (int32_t)o_req;
-    d.o_glist = (int32_t)o_glist;
-    d.o_grant = (int32_t)o_grant;
-    d.o_gdep = (int32_t)o_gdep;
-    d.o_red = (int32_t)o_red;
+    d.o_path = (int32_t)lay.o_path;
+    d.o_deliv = (int32_t)lay.o_deliv;
+    d.o_reqcnt = (int32_t)lay.o_reqcnt;
+    d.o_reqb = (int32_t)lay.o_reqb;
+    d.o_req = (int32_t)lay.o_req;
+    d.o_glist = (int32_t)lay.o_glist;
+    d.o_grant = (int32_t)lay.o_grant;
+    d.o_gdep = (int32_t)lay.o_gdep;
+    d.o_red = (int32_t)lay.o_red;
     d.path_len = (int32_t)path_lane.size();
     d.path_in_lds = path_in_lds ? 1 : 0;
     d.req_slots = (int32_t)lr;
+    // lane engines: rings of the traffic links only, in lane order
+    if (engine != simgpu::kEngineWorkgroup) d.fifo_total = (int32_t)lf;
     sim_status st;
     auto &own = c->dev_static;
 #define UP(vec, field)                                         \
@@ -548,11 +634,23 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     UP(ln_srend, ln_srend);
     UP(link_lane, link_lane);
     UP(path_lane, path_lane);
+    int32_t *tmp_ln_link, *tmp_in_lane, *tmp_ln_inoff;
+    UP(lane_link, ln_link);
+    UP(in_lane, in_lane);
+    UP(ln_inoff, ln_inoff);
 #undef UP
     const size_t S = (size_t)c->S;
     const size_t nsrc = (size_t)m + (size_t)d.ns;
     auto &ost = c->dev_state;
     if ((st = alloc(c, ost, S, &d.status)) || (st = alloc(c, ost, S, &d.cycles))) return st;
+    if (engine == simgpu::kEngineLaneHbm)
+        if ((st = alloc(c, ost, S * (size_t)lf, &d.gfifo))) return st;
+    if (engine == simgpu::kEngineB1) {  // uniform rings: lane i owns entries [i << lg, (i + 1) << lg)
+        d.fifo_total = nl << d.b1_ring_lg;
+        if ((st = alloc(c, ost, S * (size_t)d.fifo_total, &d.gfifo))) return st;
+    }
+    if (engine == simgpu::kEngineB1 && any_preds && !b1_deliv_lds)
+        if ((st = alloc(c, ost, S * (size_t)nflows, &d.gdeliv))) return st;
     if (engine == simgpu::kEngineWorkgroup &&
         ((st = alloc(c, ost, S * ftot, &d.fifo_x)) || (st = alloc(c, ost, S * ftot, &d.fifo_rdy)) ||
         (st = alloc(c, ost, S * ftot, &d.fifo_pp)) || (st = alloc(c, ost, S * m, &d.qhead)) ||

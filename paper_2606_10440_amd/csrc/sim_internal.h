@@ -103,6 +103,19 @@ struct DevNet {
     const int32_t *ln_srend;
     const int32_t *link_lane; // [m] lane of a link, -1 if no traffic
     const int32_t *path_lane; // path table with link ids replaced by lanes
+    const int32_t *ln_link;   // [nl] link of a lane
+    uint4 *gfifo;             // [S*fifo_total] FIFO rings in HBM (lane-HBM and compact engines)
+
+    // compact engine (every bandwidth 1): thread t owns lanes t, t+1024, ...
+    int32_t has_preds;        // some line has predecessors
+    int32_t b1_ns;            // stream lanes (lanes 0..b1_ns-1 start a stream)
+    int32_t b1_lpt;           // lanes per thread
+    int32_t b1_deliv_lds;     // delivered counters in LDS (else gdeliv)
+    int32_t o_word, o_gnt, o_inl, o_b1deliv, o_b1cnt, o_b1ino, o_b1red;  // LDS byte offsets
+    int32_t b1_ring_lg;       // log2 of the (uniform) ring size
+    const int32_t *in_lane;   // [m] lanes of each node's in-links in port order (-1: no traffic)
+    const int32_t *ln_inoff;  // [nl] offset of the lane's tail node in in_lane
+    uint32_t *gdeliv;         // [S*nflows] delivered counters in HBM
 
     // outputs
     uint32_t *completion; // [S*T]
@@ -113,7 +126,7 @@ struct DevNet {
     uint64_t *cycles;     // [S] processed cycles
 };
 
-enum : int32_t { kEngineWorkgroup = 0, kEngineLane = 1 };
+enum : int32_t { kEngineWorkgroup = 0, kEngineLane = 1, kEngineLaneHbm = 2, kEngineB1 = 3 };
 // Registers cache up to this many predecessor descriptors of a stream's range.
 constexpr int kPredCache = 8;
 

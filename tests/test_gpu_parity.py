@@ -276,3 +276,79 @@ def test_full_size_batched_digest(simmod, torch_cuda):
                         _digest(busy[s]) != g["busy_cycles_sha256"][s]:
                     bad.append(s)
     assert not bad, f"{len(bad)} scenarios differ, first {bad[:10]}"
+
+
+# ----------------------------------------------------------------- every engine
+
+ENGINES = ["workgroup", "lane", "lanehbm", "b1"]
+
+
+def run_engine(simmod, w, engine, txns=None):
+    old = os.environ.get("SIMGPU_ENGINE")
+    os.environ["SIMGPU_ENGINE"] = engine
+    try:
+        return run_gpu(simmod, w, txns=txns)
+    finally:
+        if old is None:
+            del os.environ["SIMGPU_ENGINE"]
+        else:
+            os.environ["SIMGPU_ENGINE"] = old
+
+
+def check_engine(simmod, oracle_lib, w, engine, txns=None):
+    say(f"engine {engine}: {w.name} S={w.n_scenarios}")
+    r = run_engine(simmod, w, engine, txns)
+    m = w.n_links
+    n_ok = 0
+    for s in range(w.n_scenarios):
+        sl = slice(s * m, (s + 1) * m)
+        if txns is None:
+            want = oracle_lib.simulate_workload(w, s)
+        else:
+            want = oracle_lib.simulate(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw[sl], w.lat[sl],
+                                       w.cap[sl], w.arb, txns=txns)
+        if want.status_name == "DEADLOCK":
+            compare_deadlocked(r, s, want)
+        else:
+            compare_scenario(r, s, want, len(want.completion))
+            n_ok += 1
+    return n_ok
+
+
+@pytest.mark.parametrize("engine", ENGINES)
+@pytest.mark.parametrize("arb", [0, 1])
+def test_engines_fat_tree_b1(simmod, oracle_lib, engine, arb):
+    w = si.fat_tree(4, nbytes=128 * 12, cap=5, lat_lo=2, lat_hi=9, arb=arb)
+    assert check_engine(simmod, oracle_lib, w, engine) == 1
+
+
+@pytest.mark.parametrize("engine", ENGINES)
+@pytest.mark.parametrize("arb", [0, 1])
+def test_engines_torus_ring_b1(simmod, oracle_lib, engine, arb):
+    w = si.torus2d(4, 4, n_scenarios=6, seed=21 + arb, bws=(1,), lat_lo=1, lat_hi=30, depths=(2, 4, 32),
+                   nbytes=128 * 16 * 20, arb=arb)
+    check_engine(simmod, oracle_lib, w, engine)
+
+
+@pytest.mark.parametrize("engine", ENGINES)
+@pytest.mark.parametrize("seed", range(12))
+def test_engines_random_dag_b1(simmod, oracle_lib, engine, seed):
+    rng = np.random.default_rng(5000 + seed)
+    n_end = int(rng.integers(2, 7))
+    n, rp, ci, bw, lat, cap = si.random_graph(rng, n_end, int(rng.integers(0, 4)), int(rng.integers(0, 6)),
+                                              bmax=1, Lmax=5, capmax=6, S=2)
+    src, dst, pptr, pidx = si.random_dag(rng, n_end, int(rng.integers(1, 300)), max_preds=3)
+    w = si.Workload("rand_b1", n, n_end, rp, ci, 2, bw, lat, cap, seed % 2, -1, 0)
+    check_engine(simmod, oracle_lib, w, engine, txns=(src, dst, pptr, pidx))
+
+
+@pytest.mark.parametrize("engine", ["workgroup", "lane", "lanehbm"])
+@pytest.mark.parametrize("seed", range(12))
+def test_engines_random_dag_multirate(simmod, oracle_lib, engine, seed):
+    rng = np.random.default_rng(6000 + seed)
+    n_end = int(rng.integers(2, 7))
+    n, rp, ci, bw, lat, cap = si.random_graph(rng, n_end, int(rng.integers(0, 4)), int(rng.integers(0, 6)),
+                                              bmax=4, Lmax=5, capmax=6, S=2)
+    src, dst, pptr, pidx = si.random_dag(rng, n_end, int(rng.integers(1, 300)), max_preds=3)
+    w = si.Workload("rand_mr", n, n_end, rp, ci, 2, bw, lat, cap, seed % 2, -1, 0)
+    check_engine(simmod, oracle_lib, w, engine, txns=(src, dst, pptr, pidx))
