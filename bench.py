@@ -27,7 +27,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, 8 TB/s
 COMPLETION_BYTES = 4            # u32 completion cycle written per line
-KERNEL_NAME = "engine"          # substring of the dominant kernel's symbol
+KERNEL_NAME = "engine_"         # substring of the engine kernels' symbols
 
 DESCR = {
     "C1": "4-endpoint full mesh, direct all-reduce 64 KiB, b=1 L=10 cap=16, lowest-id",
@@ -46,10 +46,15 @@ def algorithmic_bytes(T: int, S: int, m: int) -> int:
 
 
 def engine_source_hash() -> str:
+    """Digest of the device engine sources (counters taken on other sources
+    are not reported)."""
     h = hashlib.sha256()
-    for f in ("engine.hip", "sim_internal.h"):
-        with open(os.path.join(ROOT, "paper_2606_10440_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    csrc = os.path.join(ROOT, "paper_2606_10440_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(f.encode())
+                h.update(fh.read())
     return h.hexdigest()[:16]
 
 

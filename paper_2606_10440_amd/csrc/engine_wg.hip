@@ -1,0 +1,311 @@
+// Device engine of libsimgpu: advances every line of every scenario one
+// processed cycle at a time.
+//
+// One workgroup owns one scenario and runs it to completion inside a single
+// launch; the four phases of a cycle are separated by workgroup barriers:
+//   R  sources (link FIFOs and injection streams) offer up to b lines and
+//      post requests to their target links;
+//   G  every target link ranks its requests and grants min(b, free, #req);
+//   D  every source departs its longest granted prefix; lines leaving their
+//      last hop complete (cycle + 1) and bump their flow's delivered count;
+//   E  targets append the departing lines in grant order (ready = t + L).
+// Then the next cycle is t + 1 if anything departed, otherwise the earliest
+// FIFO-head ready time (no such time = deadlock).
+//
+// Predecessor release uses per-flow delivered counters: lines of one flow
+// (same source, destination and hence path) are injected in id order and
+// FIFOs never reorder, so a flow delivers its lines in id order and "line
+// with flow sequence q has completed" is "delivered > q" at cycle start.
+#include <hip/hip_runtime.h>
+
+#include "sim_internal.h"
+
+namespace simgpu {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+__global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
+    const int s = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int m = d.m;
+    const int bmax = d.bmax;
+    const size_t sm = (size_t)s * m;
+    const int32_t *__restrict__ bw = d.bw + sm;
+    const int32_t *__restrict__ lat = d.lat + sm;
+    const int32_t *__restrict__ cap = d.cap + sm;
+    const size_t fo = (size_t)s * d.fifo_total;
+    uint32_t *fx = d.fifo_x + fo;
+    uint32_t *frdy = d.fifo_rdy + fo;
+    int32_t *fpp = d.fifo_pp + fo;
+    uint32_t *qhead = d.qhead + sm;
+    uint32_t *qtail = d.qtail + sm;
+    uint32_t *rr = d.rr + sm;
+    int32_t *cur_rng = d.cur_rng + (size_t)s * d.ns;
+    uint32_t *cur_off = d.cur_off + (size_t)s * d.ns;
+    uint32_t *delivered = d.delivered + (size_t)s * d.nflows;
+    uint32_t *req_cnt = d.req_cnt + sm;
+    uint64_t *req_rec = d.req_rec + (size_t)s * d.req_total;
+    const size_t nsrc = (size_t)m + d.ns;
+    uint32_t *sreq_x = d.sreq_x + (size_t)s * nsrc * bmax;
+    int32_t *sreq_pp = d.sreq_pp + (size_t)s * nsrc * bmax;
+    int32_t *sreq_n = d.sreq_n + (size_t)s * nsrc;
+    int32_t *grant = d.grant + (size_t)s * nsrc * bmax;
+    uint32_t *gcount = d.gcount + sm;
+    uint32_t *glist = d.glist + sm * bmax;
+    uint8_t *gdep = d.gdep + sm * bmax;
+    uint32_t *comp = d.completion + (size_t)s * d.T;
+    uint64_t *tx = d.tx_lines + sm;
+    uint64_t *busy = d.busy + sm;
+    const int32_t *__restrict__ path = d.path_link;
+
+    __shared__ uint32_t sh_t, sh_next, sh_anydep, sh_ndone;
+    __shared__ int32_t sh_state;
+
+    for (int l = tid; l < m; l += kThreads) {
+        qhead[l] = 0;
+        qtail[l] = 0;
+        rr[l] = 0;
+        req_cnt[l] = 0;
+        gcount[l] = 0;
+        tx[l] = 0;
+        busy[l] = 0;
+    }
+    for (size_t i = tid; i < (size_t)m * bmax; i += kThreads) gdep[i] = 0;
+    for (size_t i = tid; i < nsrc * bmax; i += kThreads) grant[i] = -1;
+    for (size_t i = tid; i < nsrc; i += kThreads) sreq_n[i] = 0;
+    for (int j = tid; j < d.ns; j += kThreads) {
+        cur_rng[j] = d.s_rbeg[j];
+        cur_off[j] = 0;
+    }
+    for (int f = tid; f < d.nflows; f += kThreads) delivered[f] = 0;
+    if (tid == 0) {
+        sh_t = 0;
+        sh_state = d.T > 0 ? kRunRunning : kRunOk;
+        sh_next = kNever;
+        sh_anydep = 0;
+        sh_ndone = 0;
+    }
+    __syncthreads();
+
+    uint64_t done = 0, processed = 0;  // meaningful in thread 0
+    const int nact = d.n_fsrc + d.ns;
+    while (sh_state == kRunRunning) {
+        const uint32_t t = sh_t;
+        // ---------------------------------------------------------------- R
+        for (int a = tid; a < nact; a += kThreads) {
+            if (a < d.n_fsrc) {
+                const int l = d.fsrc_link[a];
+                const uint32_t h = qhead[l];
+                const uint32_t occ = qtail[l] - h;
+                const int b = bw[l];
+                const int base = d.fifo_off[l], mask = d.fifo_mask[l];
+                int nr = 0;
+                for (int k = 0; k < b && (uint32_t)k < occ; k++) {
+                    const int e = base + (int)((h + k) & (uint32_t)mask);
+                    const uint32_t rdy = frdy[e];
+                    if (rdy > t) {
+                        atomicMin(&sh_next, rdy);
+                        break;
+                    }
+                    const uint32_t x = fx[e];
+                    const int pp = fpp[e] + 1;
+                    const int tgt = path[pp];
+                    const size_t si = (size_t)l * bmax + k;
+                    sreq_x[si] = x;
+                    sreq_pp[si] = pp;
+                    if (tgt < 0) {
+                        grant[si] = -2;  // the sink takes everything
+                    } else {
+                        const uint32_t P = (uint32_t)d.nports_tail[tgt];
+                        const uint32_t key =
+                            d.arb == 0 ? x
+                                       : (uint32_t)k * P + ((uint32_t)d.port_at_head[l] + P - rr[tgt]) % P;
+                        const uint32_t slot = atomicAdd(&req_cnt[tgt], 1u);
+                        req_rec[d.req_off[tgt] + slot] = ((uint64_t)key << 32) | ((uint32_t)l << 8) | (uint32_t)k;
+                    }
+                    nr++;
+                }
+                sreq_n[l] = nr;
+            } else {
+                const int j = a - d.n_fsrc;
+                const int f = d.s_link[j];
+                const int src = m + j;
+                int R = cur_rng[j];
+                uint32_t o = cur_off[j];
+                const int rend = d.s_rend[j];
+                const int b = bw[f];
+                const uint32_t P = (uint32_t)d.nports_tail[f];
+                int nr = 0;
+                for (int k = 0; k < b && R < rend; k++) {
+                    bool ok = true;
+                    for (int q = d.r_pd[R]; q < d.r_pd[R + 1]; q++)
+                        if (delivered[d.pd_flow[q]] <= d.pd_base[q] + o) {
+                            ok = false;
+                            break;
+                        }
+                    if (!ok) break;
+                    const uint32_t x = d.r_start[R] + o;
+                    const size_t si = (size_t)src * bmax + k;
+                    sreq_x[si] = x;
+                    sreq_pp[si] = d.r_path[R];
+                    const uint32_t key = d.arb == 0 ? x : (uint32_t)k * P + ((P - 1) + P - rr[f]) % P;
+                    const uint32_t slot = atomicAdd(&req_cnt[f], 1u);
+                    req_rec[d.req_off[f] + slot] = ((uint64_t)key << 32) | ((uint32_t)src << 8) | (uint32_t)k;
+                    nr++;
+                    if (++o == d.r_len[R]) {
+                        R++;
+                        o = 0;
+                    }
+                }
+                sreq_n[src] = nr;
+            }
+        }
+        __syncthreads();
+        // ---------------------------------------------------------------- G
+        for (int a = tid; a < d.n_fsrc; a += kThreads) {
+            const int f = d.fsrc_link[a];
+            const uint32_t c = req_cnt[f];
+            if (c == 0) continue;
+            req_cnt[f] = 0;
+            const int occ = (int)(qtail[f] - qhead[f]);
+            int g = bw[f];
+            if (cap[f] - occ < g) g = cap[f] - occ;
+            if ((int)c < g) g = (int)c;
+            const uint64_t *rec = req_rec + d.req_off[f];
+            for (uint32_t i = 0; i < c; i++) {
+                const uint64_t ri = rec[i];
+                const uint32_t ki = (uint32_t)(ri >> 32);
+                int rank = 0;
+                for (uint32_t jj = 0; jj < c; jj++) rank += ((uint32_t)(rec[jj] >> 32) < ki) ? 1 : 0;
+                if (rank < g) {
+                    const uint32_t sk = (uint32_t)ri;
+                    glist[(size_t)f * bmax + rank] = sk;
+                    grant[(size_t)(sk >> 8) * bmax + (sk & 255u)] = rank;
+                }
+            }
+            gcount[f] = (uint32_t)(g > 0 ? g : 0);
+        }
+        __syncthreads();
+        // ---------------------------------------------------------------- D
+        for (int a = tid; a < nact; a += kThreads) {
+            const int src = a < d.n_fsrc ? d.fsrc_link[a] : m + (a - d.n_fsrc);
+            const int nr = sreq_n[src];
+            if (nr == 0) continue;
+            sreq_n[src] = 0;
+            int dep = 0, sinks = 0;
+            bool open = true;
+            for (int k = 0; k < nr; k++) {
+                const size_t si = (size_t)src * bmax + k;
+                const int gr = grant[si];
+                grant[si] = -1;
+                if (!open || gr == -1) {
+                    open = false;
+                    continue;
+                }
+                dep++;
+                const int pv = path[sreq_pp[si]];
+                if (gr == -2) {
+                    comp[sreq_x[si]] = t + 1;
+                    delivered[-pv - 1]++;
+                    sinks++;
+                } else {
+                    gdep[(size_t)pv * bmax + gr] = 1;
+                }
+            }
+            if (dep) {
+                sh_anydep = 1;
+                if (src < m) {
+                    qhead[src] += (uint32_t)dep;
+                } else {
+                    const int j = src - m;
+                    int R = cur_rng[j];
+                    uint32_t o = cur_off[j] + (uint32_t)dep;
+                    while (R < d.s_rend[j] && o >= d.r_len[R]) {
+                        o -= d.r_len[R];
+                        R++;
+                    }
+                    cur_rng[j] = R;
+                    cur_off[j] = o;
+                }
+                if (sinks) atomicAdd(&sh_ndone, (uint32_t)sinks);
+            }
+        }
+        __syncthreads();
+        // ---------------------------------------------------------------- E
+        for (int a = tid; a < d.n_fsrc; a += kThreads) {
+            const int f = d.fsrc_link[a];
+            const int g = (int)gcount[f];
+            if (g == 0) continue;
+            gcount[f] = 0;
+            const uint32_t P = (uint32_t)d.nports_tail[f];
+            uint32_t tl = qtail[f];
+            const int base = d.fifo_off[f], mask = d.fifo_mask[f];
+            const uint32_t ready = t + (uint32_t)lat[f];
+            int cnt = 0;
+            uint32_t last_port = 0;
+            for (int r = 0; r < g; r++) {
+                const size_t gi = (size_t)f * bmax + r;
+                if (!gdep[gi]) continue;
+                gdep[gi] = 0;
+                const uint32_t sk = glist[gi];
+                const int src = (int)(sk >> 8);
+                const size_t si = (size_t)src * bmax + (sk & 255u);
+                const int e = base + (int)(tl & (uint32_t)mask);
+                fx[e] = sreq_x[si];
+                frdy[e] = ready;
+                fpp[e] = sreq_pp[si];
+                tl++;
+                cnt++;
+                last_port = src < m ? (uint32_t)d.port_at_head[src] : P - 1;
+            }
+            if (cnt) {
+                qtail[f] = tl;
+                tx[f] += (uint64_t)cnt;
+                busy[f] += 1;
+                if (d.arb == 1) rr[f] = (last_port + 1) % P;
+            }
+        }
+        __syncthreads();
+        // ---------------------------------------------------------------- time
+        if (tid == 0) {
+            processed++;
+            done += sh_ndone;
+            uint32_t nt = t;
+            int32_t state = kRunRunning;
+            if (done == (uint64_t)d.T) {
+                state = kRunOk;
+                d.makespan[s] = t + 1;
+            } else if (sh_anydep) {
+                nt = t + 1;
+            } else if (sh_next == kNever) {
+                state = kRunDeadlock;
+            } else {
+                nt = sh_next;
+            }
+            if (state == kRunRunning && (uint64_t)nt > d.max_cycles) state = kRunMaxCycles;
+            if (state == kRunRunning && processed > d.watchdog) state = kRunWatchdog;
+            sh_t = nt;
+            sh_state = state;
+            sh_next = kNever;
+            sh_anydep = 0;
+            sh_ndone = 0;
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        if (d.T == 0) d.makespan[s] = 0;
+        d.status[s] = sh_state;
+        d.cycles[s] = processed;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_workgroup(const DevNet &d, hipStream_t st) {
+    hipLaunchKernelGGL(engine_wg, dim3((unsigned)d.S), dim3(kThreads), 0, st, d);
+    return hipGetLastError();
+}
+
+}  // namespace simgpu

@@ -134,3 +134,13 @@ constexpr int kPredCache = 8;
 int launch_engine(const DevNet &d, void *stream);
 
 }  // namespace simgpu
+
+#include <hip/hip_runtime.h>
+
+namespace simgpu {
+// per-engine launchers (one translation unit each)
+hipError_t launch_workgroup(const DevNet &d, hipStream_t st);
+hipError_t launch_lane_any(const DevNet &d, hipStream_t st);
+hipError_t launch_b1_any(const DevNet &d, hipStream_t st);
+
+}  // namespace simgpu
