@@ -5,7 +5,7 @@
  * crosses this boundary.  Plain pointers and sizes only.
  *
  * What is simulated.  The paper ("ASTRA-sim 3.0") makes the cache-line-sized
- * wavefront request the unit that the network backend simulates (Sec. 4.4,
+ * wavefront request the unit that the network backend simulates (Sec. 4.4.3,
  * "Wavefront Request") and extends the Simple network backend to a graph of
  * endpoints, switches and links with a modular routing function (Sec. 4.5);
  * the Simple backend itself is an alpha-beta model (Sec. 2.1).  This library

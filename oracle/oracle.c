@@ -6,7 +6,7 @@
  * benchmark's CPU-baseline leg may load it; the product never does.  It
  * shares no code, header or table with the GPU library.
  *
- * What it computes (paper: Sec. 4.4 "Wavefront Request" -- a 128 B
+ * What it computes (paper: Sec. 4.4.3 "Wavefront Request" -- a 128 B
  * cache-line transfer is the unit the network simulates; Sec. 4.5 "Detailed
  * Simple Network Modeling" -- the network is a graph of endpoints and
  * switches with a routing function; Sec. 2.1 -- the Simple backend is an

@@ -3,7 +3,7 @@
 //
 // Paper: the infrastructure is a directed attributed graph (Sec. 4.6); the
 // Simple backend routes over it with a modular routing function (Sec. 4.5);
-// the unit of transfer is the 128 B wavefront request (Sec. 4.4); the
+// the unit of transfer is the 128 B wavefront request (Sec. 4.4.3); the
 // collectives are the textbook ring / direct algorithms (Sec. 1).
 #include <hip/hip_runtime.h>
 
