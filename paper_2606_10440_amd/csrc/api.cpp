@@ -434,6 +434,204 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         fv.erase(std::unique(fv.begin(), fv.end()), fv.end());
         lr += (int64_t)((int32_t)fv.size() + (has_stream[fsrc[i]] ? 1 : 0)) * bmax;
     }
+    // Wave engine tables: every lane's local flows (at most four cross a
+    // link), the feeders of every lane as a target, each range's local flow
+    // at its first lane, and the scenario slots of every wave (scenarios
+    // with the most lines per cycle of bandwidth on their busiest link first,
+    // so that the longest runs start first).
+    struct WaveLayout {
+        bool ok = false;
+        int32_t G = 0, W = 0, nfs = 0;
+        int32_t nblk = 0, wpb = 0;
+        int64_t o_word = 0, o_red = 0, o_deliv = 0, o_req = 0, o_gnt = 0, o_gdep = 0, bytes = 0;
+    };
+    WaveLayout wv;
+    std::vector<uint32_t> wv_lfb, wv_lfx;
+    std::vector<int32_t> wv_feed, wv_nfeed, wv_sc, r_lf, pd_dix, blk_wave, blk_off;
+    constexpr int64_t kWaveBlockLds = 160 * 1024;  // LDS of a compute unit
+    constexpr int32_t kWaveBlocks = 256;           // compute units of the device
+    {
+        std::vector<std::vector<int32_t>> lflows(nl);
+        bool ok = nl >= 1 && nl <= 63 && T < (1ll << 25) - 1 && bm <= 8;
+        for (int32_t f = 0; ok && f < nflows; f++)
+            for (int64_t q = c->flow_path[f]; ok && c->path_link[q] >= 0; q++) {
+                auto &v = lflows[link_lane[c->path_link[q]]];
+                v.push_back(f);
+                if (v.size() > 4) ok = false;
+            }
+        int32_t maxfeed = 0;
+        for (int32_t i = 0; i < nl; i++) maxfeed = std::max(maxfeed, (int32_t)feeders[i].size());
+        const int32_t nfs = maxfeed + 1 <= 2 ? 2 : simgpu::kWaveMaxNF;
+        if (maxfeed + 1 > simgpu::kWaveMaxNF || nfs * bm > 32) ok = false;
+        for (int32_t l : fsrc)
+            if (nports_tail[l] > 255) ok = false;
+        if (ok) {
+            auto lf_index = [&](int32_t lane, int32_t f) {
+                const auto &v = lflows[lane];
+                return (int32_t)(std::find(v.begin(), v.end(), f) - v.begin());
+            };
+            // byte q of wv_lfb: local index at the next lane << 6 | next lane (63:
+            // the line leaves the network); byte q of wv_lfx: this lane's feeder
+            // index at the next lane.  A flow's delivered counter sits at
+            // (its last lane) * 4 + (its local index there).
+            wv_lfb.assign(nl, 0u);
+            wv_lfx.assign(nl, 0u);
+            std::vector<int32_t> flow_dix(nflows, 0);
+            for (int32_t f = 0; f < nflows; f++)
+                for (int64_t q = c->flow_path[f]; c->path_link[q] >= 0; q++) {
+                    const int32_t ln = link_lane[c->path_link[q]];
+                    const int32_t nx = c->path_link[q + 1];
+                    const uint32_t sh = 8u * (uint32_t)lf_index(ln, f);
+                    if (nx < 0) {
+                        wv_lfb[ln] |= 63u << sh;
+                        flow_dix[f] = ln * 4 + lf_index(ln, f);
+                    } else {
+                        const int32_t ln2 = link_lane[nx];
+                        const auto &fv = feeders[ln2];
+                        const int32_t fi = (int32_t)(std::find(fv.begin(), fv.end(), ln) - fv.begin());
+                        wv_lfb[ln] |= ((uint32_t)ln2 | ((uint32_t)lf_index(ln2, f) << 6)) << sh;
+                        wv_lfx[ln] |= (uint32_t)fi << sh;
+                    }
+                }
+            pd_dix.resize(pd_flow.size());
+            for (size_t q = 0; q < pd_flow.size(); q++) pd_dix[q] = flow_dix[pd_flow[q]];
+            wv_feed.assign((size_t)nl * 4, 0);
+            wv_nfeed.assign(nl, 0);
+            for (int32_t i = 0; i < nl; i++) {
+                wv_nfeed[i] = (int32_t)feeders[i].size();
+                for (size_t f = 0; f < feeders[i].size(); f++)
+                    wv_feed[(size_t)i * 4 + f] = feeders[i][f] | (port_at_head[fsrc[feeders[i][f]]] << 8);
+            }
+            r_lf.assign(nr, 0);
+            for (int64_t j = 0; j < nr; j++)
+                r_lf[j] = lf_index(link_lane[c->path_link[r_path[j]]], rflow[order[j]]);
+            const int32_t S = c->S;
+            const int32_t G = std::min(64 / nl, S);
+            std::vector<double> lcnt(nl, 0.0);
+            for (int64_t j = 0; j < nr; j++)
+                for (int64_t q = r_path[j]; c->path_link[q] >= 0; q++) lcnt[link_lane[c->path_link[q]]] += r_len[j];
+            // A wave runs the b = 1 loop only if all its scenarios can, and runs
+            // as long as its longest scenario: waves hold scenarios of one
+            // bandwidth bound only, in order of expected length (lines per unit
+            // of bandwidth on the busiest link, then smaller buffers first).
+            std::vector<double> est(S, 0.0);
+            std::vector<int32_t> mincap(S, SIM_MAX_CAP), sbmax(S, 1), ord(S);
+            for (int32_t s = 0; s < S; s++) {
+                for (int32_t i = 0; i < nl; i++) {
+                    const size_t pi = (size_t)s * m + fsrc[i];
+                    est[s] = std::max(est[s], lcnt[i] / c->bw[pi]);
+                    mincap[s] = std::min(mincap[s], c->cap[pi]);
+                    sbmax[s] = std::max(sbmax[s], c->bw[pi]);
+                }
+                ord[s] = s;
+            }
+            std::stable_sort(ord.begin(), ord.end(), [&](int32_t a, int32_t b2) {
+                if (sbmax[a] != sbmax[b2]) return sbmax[a] < sbmax[b2];
+                return est[a] != est[b2] ? est[a] > est[b2] : mincap[a] < mincap[b2];
+            });
+            wv_sc.clear();
+            for (int32_t k = 0; k < S; k++) {
+                const bool new_wave = wv_sc.size() % G == 0 || sbmax[ord[k]] != sbmax[ord[k - 1]];
+                if (new_wave)
+                    while (wv_sc.size() % G) wv_sc.push_back(-1);
+                wv_sc.push_back(ord[k]);
+            }
+            while (wv_sc.size() % G) wv_sc.push_back(-1);
+            const int32_t W = (int32_t)(wv_sc.size() / G);
+            // A wave's LDS region: its rings (+ one trash entry per lane), then
+            // words (64 + 64 trash) | reduction slots (64 + 64 trash) | delivered counters |
+            // for the general loop: request slots, grants, void flags (each +
+            // 64 trash).  Offsets below are relative to the end of the rings.
+            const bool general = bm > 1 || c->arb == SIM_ARB_ROUND_ROBIN;
+            int64_t off = 0;
+            wv.o_word = off;
+            off += 128 * 4;
+            wv.o_red = off;
+            off += 128 * 4;
+            wv.o_deliv = off;
+            off = align16(off + (int64_t)G * nl * 4 * 4);
+            const int64_t tail_fast = off;
+            wv.o_req = off;
+            // the general loop's slots, grants and void flags for a wave whose
+            // bandwidth bound rounds up to wb
+            auto tail_gen = [&](int64_t wb) {
+                return tail_fast + align16(((int64_t)64 * nfs * wb + 64) * 8) + align16(((int64_t)64 * wb + 64) * 8) +
+                       align16(((int64_t)64 * wb + 64) * 4);
+            };
+            std::vector<int64_t> wbytes(W);
+            bool fits = true;
+            for (int32_t q = 0; q < W; q++) {
+                int64_t ringn = 0;
+                int32_t wbmax = 1;
+                for (int32_t g = 0; g < G; g++) {
+                    const int32_t s = wv_sc[(size_t)q * G + g];
+                    if (s < 0) continue;
+                    for (int32_t i = 0; i < nl; i++) {
+                        ringn += c->cap[(size_t)s * m + fsrc[i]];
+                        wbmax = std::max(wbmax, c->bw[(size_t)s * m + fsrc[i]]);
+                    }
+                }
+                int64_t wb = 1;
+                while (wb < wbmax) wb <<= 1;
+                const bool fast = c->arb == SIM_ARB_LOWEST_ID && wbmax == 1;
+                wbytes[q] = align16((ringn + 64) * 8) + ((general && !fast) ? tail_gen(wb) : tail_fast);
+                if (wbytes[q] > kWaveBlockLds) fits = false;
+            }
+            // Pack the waves into workgroups of up to kWaveMaxWpb independent waves and
+            // at most kWaveBlockLds bytes, aiming at one workgroup per compute
+            // unit so that every wave is resident at once: largest first, each
+            // into the workgroup with the fewest waves that has room.
+            std::vector<int32_t> qord(W);
+            for (int32_t q = 0; q < W; q++) qord[q] = q;
+            std::stable_sort(qord.begin(), qord.end(), [&](int32_t a, int32_t b2) { return wbytes[a] > wbytes[b2]; });
+            std::vector<std::vector<int32_t>> blk(std::min<int32_t>(kWaveBlocks, W));
+            std::vector<int64_t> bbytes(blk.size(), 0);
+            for (int32_t q : qord) {
+                if (!fits) break;
+                int32_t best = -1;
+                for (int32_t k = 0; k < (int32_t)blk.size(); k++) {
+                    if ((int32_t)blk[k].size() >= simgpu::kWaveMaxWpb || bbytes[k] + wbytes[q] > kWaveBlockLds) continue;
+                    if (best < 0 || blk[k].size() < blk[best].size() ||
+                        (blk[k].size() == blk[best].size() && bbytes[k] < bbytes[best]))
+                        best = k;
+                }
+                if (best < 0) {
+                    blk.emplace_back();
+                    bbytes.push_back(0);
+                    best = (int32_t)blk.size() - 1;
+                }
+                blk[best].push_back(q);
+                bbytes[best] += wbytes[q];
+            }
+            // waves of a workgroup in scenario order (longest expected first);
+            // workgroups ordered by their first wave
+            for (auto &v : blk) std::sort(v.begin(), v.end());
+            std::stable_sort(blk.begin(), blk.end(), [](const std::vector<int32_t> &a, const std::vector<int32_t> &b2) {
+                return (a.empty() ? INT32_MAX : a[0]) < (b2.empty() ? INT32_MAX : b2[0]);
+            });
+            int32_t wpb = 1;
+            int64_t lmax = 16;
+            for (auto &v : blk) wpb = std::max(wpb, (int32_t)v.size());
+            blk_wave.assign(blk.size() * wpb, -1);
+            blk_off.assign(blk.size() * wpb, 0);
+            for (size_t k = 0; k < blk.size(); k++) {
+                int64_t o2 = 0;
+                for (size_t j = 0; j < blk[k].size(); j++) {
+                    blk_wave[k * wpb + j] = blk[k][j];
+                    blk_off[k * wpb + j] = (int32_t)o2;
+                    o2 += wbytes[blk[k][j]];
+                }
+                lmax = std::max(lmax, o2);
+            }
+            wv.bytes = lmax;
+            wv.G = G;
+            wv.W = W;
+            wv.nblk = (int32_t)blk.size();
+            wv.wpb = wpb;
+            wv.nfs = nfs;
+            wv.ok = fits && wv.bytes <= kWaveBlockLds;
+        }
+    }
     const int64_t path_bytes = (int64_t)c->path_link.size() * 4;
     struct LaneLayout { int64_t o_path, o_deliv, o_reqcnt, o_reqb, o_req, o_glist, o_grant, o_gdep, o_red, bytes; bool path_lds; };
     auto lane_layout = [&](bool fifo_lds) {
@@ -479,7 +677,8 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     const bool b1_ok = bmax == 1 && (int64_t)s_link.size() <= 1024 && nl <= 8 * 1024 && nl < 65536 && b1_bytes <= kLds &&
                        (c->arb == SIM_ARB_LOWEST_ID || rr_ports_fit);
     int engine = simgpu::kEngineWorkgroup;
-    if (nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds) engine = simgpu::kEngineLane;
+    if (wv.ok) engine = simgpu::kEngineWave;
+    else if (nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds) engine = simgpu::kEngineLane;
     else if (nl >= 1 && b1_ok) engine = simgpu::kEngineB1;
     else if (nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds) engine = simgpu::kEngineLaneHbm;
     if (const char *ev = std::getenv("SIMGPU_ENGINE")) {
@@ -488,8 +687,10 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         if (!std::strcmp(ev, "lane")) want = simgpu::kEngineLane;
         if (!std::strcmp(ev, "lanehbm")) want = simgpu::kEngineLaneHbm;
         if (!std::strcmp(ev, "b1")) want = simgpu::kEngineB1;
+        if (!std::strcmp(ev, "wave")) want = simgpu::kEngineWave;
         const bool ok = want == simgpu::kEngineWorkgroup ||
-                        (want == simgpu::kEngineLane && engine == simgpu::kEngineLane) ||
+                        (want == simgpu::kEngineWave && wv.ok) ||
+                        (want == simgpu::kEngineLane && nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds) ||
                         (want == simgpu::kEngineLaneHbm && nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds) ||
                         (want == simgpu::kEngineB1 && nl >= 1 && b1_ok);
         if (want < 0 || !ok) return fail(c, SIM_ERR_INVALID_ARG, std::string("SIMGPU_ENGINE=") + ev + " is not usable here");
@@ -539,7 +740,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     for (int32_t i = 0; i < nl; i++) ln_inoff[i] = node_inoff[c->tail[lane_link[i]]];
     const LaneLayout &lay = engine == simgpu::kEngineLane ? lay_lds : lay_hbm;
     const bool path_in_lds = lay.path_lds;
-    const int64_t lds_bytes = engine == simgpu::kEngineB1 ? b1_bytes : lay.bytes;
+    const int64_t lds_bytes = engine == simgpu::kEngineB1 ? b1_bytes : engine == simgpu::kEngineWave ? wv.bytes : lay.bytes;
 
     // everything below touches the device
     int dev = -1;
@@ -589,6 +790,17 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     d.o_grant = (int32_t)lay.o_grant;
     d.o_gdep = (int32_t)lay.o_gdep;
     d.o_red = (int32_t)lay.o_red;
+    d.wv_G = wv.G;
+    d.wv_W = wv.W;
+    d.wv_nblk = wv.nblk;
+    d.wv_wpb = wv.wpb;
+    d.wv_nfs = wv.nfs;
+    d.o_wword = (int32_t)wv.o_word;
+    d.o_wred = (int32_t)wv.o_red;
+    d.o_wdeliv = (int32_t)wv.o_deliv;
+    d.o_wreq = (int32_t)wv.o_req;
+    d.o_wgnt = (int32_t)wv.o_gnt;
+    d.o_wgdep = (int32_t)wv.o_gdep;
     d.path_len = (int32_t)path_lane.size();
     d.path_in_lds = path_in_lds ? 1 : 0;
     d.req_slots = (int32_t)lr;
@@ -638,6 +850,20 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     UP(lane_link, ln_link);
     UP(in_lane, in_lane);
     UP(ln_inoff, ln_inoff);
+    if (engine == simgpu::kEngineWave) {
+        uint32_t *tmp_wv_lfb, *tmp_wv_lfx;
+        int32_t *tmp_wv_feed, *tmp_wv_nfeed, *tmp_wv_sc, *tmp_r_lf, *tmp_pd_dix;
+        UP(wv_lfb, wv_lfb);
+        UP(wv_lfx, wv_lfx);
+        UP(pd_dix, pd_dix);
+        UP(wv_feed, wv_feed);
+        UP(wv_nfeed, wv_nfeed);
+        UP(wv_sc, wv_sc);
+        int32_t *tmp_blk_wave, *tmp_blk_off;
+        UP(blk_wave, blk_wave);
+        UP(blk_off, blk_off);
+        UP(r_lf, r_lf);
+    }
 #undef UP
     const size_t S = (size_t)c->S;
     const size_t nsrc = (size_t)m + (size_t)d.ns;
@@ -794,7 +1020,7 @@ sim_status sim_status_after_sync(sim_ctx *c, int32_t *status, uint64_t *cycles) 
         if (st[s] == simgpu::kRunMaxCycles)
             return fail(c, SIM_ERR_MAX_CYCLES, "scenario " + std::to_string(s) + " exceeded max_cycles");
         if (st[s] == simgpu::kRunInternal)
-            return fail(c, SIM_ERR_DEVICE, "scenario " + std::to_string(s) + ": request slot overflow (internal)");
+            return fail(c, SIM_ERR_DEVICE, "scenario " + std::to_string(s) + ": internal engine error (request slot overflow or line id out of range)");
         if (st[s] == simgpu::kRunWatchdog)
             return fail(c, SIM_ERR_DEVICE, "scenario " + std::to_string(s) + ": engine watchdog fired");
         if (st[s] != simgpu::kRunOk) return fail(c, SIM_ERR_DEVICE, "scenario " + std::to_string(s) + " did not finish");

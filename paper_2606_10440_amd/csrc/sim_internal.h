@@ -117,6 +117,24 @@ struct DevNet {
     const int32_t *ln_inoff;  // [nl] offset of the lane's tail node in in_lane
     uint32_t *gdeliv;         // [S*nflows] delivered counters in HBM
 
+    // wave engine: G scenarios per wavefront, lane = (scenario slot, traffic link)
+    int32_t wv_G;             // scenarios per wave (G * nl <= 64)
+    int32_t wv_W;             // waves
+    int32_t wv_nblk;          // workgroups: up to 16 independent waves each
+    int32_t wv_wpb;           // wave slots per workgroup
+    int32_t wv_nfs;           // request-slot groups per target lane: feeders + the lane's own stream
+    int32_t o_wword, o_wred, o_wdeliv, o_wreq, o_wgnt, o_wgdep;  // LDS byte offsets after a wave's rings
+    const int32_t *blk_wave;  // [wv_nblk*wv_wpb] wave of each slot, -1 if empty
+    const int32_t *blk_off;   // [wv_nblk*wv_wpb] LDS byte offset of the slot's region
+    const int32_t *wv_sc;     // [wv_W*G] scenario of each slot, -1 if empty; longest expected runs first
+    const uint32_t *wv_lfb;   // [nl] byte q: local flow q's next lane (63: leaves the network)
+                              //   | its local index at the next lane << 6
+    const uint32_t *wv_lfx;   // [nl] byte q: this lane's feeder index at local flow q's next lane
+    const int32_t *pd_dix;    // [#descriptors] delivered-counter index of pd_flow: last lane * 4 + local index
+    const int32_t *wv_feed;   // [nl*4] feeder lanes of a lane as a target: lane | port << 8
+    const int32_t *wv_nfeed;  // [nl]
+    const int32_t *r_lf;      // [nr] local flow index of a range's flow at its first lane
+
     // outputs
     uint32_t *completion; // [S*T]
     uint64_t *tx_lines;   // [S*m]
@@ -126,7 +144,16 @@ struct DevNet {
     uint64_t *cycles;     // [S] processed cycles
 };
 
-enum : int32_t { kEngineWorkgroup = 0, kEngineLane = 1, kEngineLaneHbm = 2, kEngineB1 = 3 };
+enum : int32_t { kEngineWorkgroup = 0, kEngineLane = 1, kEngineLaneHbm = 2, kEngineB1 = 3, kEngineWave = 4 };
+// Wave engine entry words: line id << kWaveXShift | local-flow index (0..3)
+// << 5, the low five bits free for a request slot number (so line ids must
+// be below 2^25 - 1).
+constexpr int kWaveXShift = 7;
+// Request-slot groups per target lane of the wave engine's general loop:
+// feeders plus the lane's own stream, 2 or kWaveMaxNF.
+constexpr int kWaveMaxNF = 4;
+// Waves per wave-engine workgroup (two per SIMD: 256 registers each).
+constexpr int kWaveMaxWpb = 8;
 // Registers cache up to this many predecessor descriptors of a stream's range.
 constexpr int kPredCache = 8;
 
@@ -142,5 +169,6 @@ namespace simgpu {
 hipError_t launch_workgroup(const DevNet &d, hipStream_t st);
 hipError_t launch_lane_any(const DevNet &d, hipStream_t st);
 hipError_t launch_b1_any(const DevNet &d, hipStream_t st);
+hipError_t launch_wave_any(const DevNet &d, hipStream_t st);
 
 }  // namespace simgpu
