@@ -567,10 +567,16 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                     const int32_t s = wv_sc[(size_t)q * G + g];
                     if (s < 0) continue;
                     for (int32_t i = 0; i < nl; i++) {
-                        ringn += c->cap[(size_t)s * m + fsrc[i]];
+                        const int64_t cp = c->cap[(size_t)s * m + fsrc[i]];
+                        ringn += cp + ((1 - cp) & 15);  // padded as the kernel does
                         wbmax = std::max(wbmax, c->bw[(size_t)s * m + fsrc[i]]);
                     }
                 }
+                // lanes without a link still take one padding entry each
+                int32_t on_lanes = 0;
+                for (int32_t g = 0; g < G; g++)
+                    if (wv_sc[(size_t)q * G + g] >= 0) on_lanes += nl;
+                ringn += 64 - on_lanes;
                 int64_t wb = 1;
                 while (wb < wbmax) wb <<= 1;
                 const bool fast = c->arb == SIM_ARB_LOWEST_ID && wbmax == 1;

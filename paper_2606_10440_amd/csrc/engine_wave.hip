@@ -212,14 +212,17 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
         rend = d.ln_srend[i];
         if (R < rend) load_wrange(d, R, cur);
     }
-    // this lane's ring: exclusive prefix sum of the capacities over the wave
-    uint32_t incl = on ? cap : 0u;
+    // this lane's ring: exclusive prefix sum over the wave of the capacities,
+    // each padded so that lane w's ring starts at an entry = w (mod 16): ring
+    // heads that advance in step then fall in different LDS banks
+    const uint32_t ralloc = (on ? cap : 0u) + ((1u - (on ? cap : 0u)) & 15u);
+    uint32_t incl = ralloc;
 #pragma unroll
     for (int sh = 1; sh < 64; sh <<= 1) {
         const uint32_t u = (uint32_t)__shfl_up((int)incl, sh);
         if (w >= sh) incl += u;
     }
-    const uint32_t rbase = incl - (on ? cap : 0u);
+    const uint32_t rbase = incl - ralloc;
     const uint32_t rtotal = (uint32_t)__shfl((int)incl, 63);
     unsigned char *tailp = base + (((rtotal + 64u) * 8u + 15u) & ~15u);
     uint32_t *word = reinterpret_cast<uint32_t *>(tailp + d.o_wword);        // [128]
@@ -384,11 +387,11 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
     // target (BMW >= the wave's largest bandwidth).
     auto general = [&](auto bmw_tag) {
         constexpr int BMW = decltype(bmw_tag)::value;
-        uint2 *wreq = reinterpret_cast<uint2 *>(tailp + d.o_wreq);  // [64*NF*BMW + 64] {entry word, tag}
+        uint2 *wreq = reinterpret_cast<uint2 *>(tailp + d.o_wreq);  // [(NF*BMW + 1) * 64] slot-major {entry word, tag}
         constexpr uint32_t kReqSlots = 64u * NF * BMW;
         uint2 *wgnt = reinterpret_cast<uint2 *>(tailp + d.o_wreq + ((kReqSlots + 64u) * 8u + 15u) / 16u * 16u);
         uint32_t *wvoid = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(wgnt) +
-                                                       ((64u * BMW + 64u) * 8u + 15u) / 16u * 16u);  // [64*BMW + 64] tag
+                                                       ((64u * BMW + 64u) * 8u + 15u) / 16u * 16u);  // [(BMW + 1) * 64] rank-major tag
         const uint32_t req_trash = kReqSlots + (uint32_t)w;
         const uint32_t gnt_trash = 64u * BMW + (uint32_t)w;
         for (int j = w; j < (int)kReqSlots + 64; j += 64) wreq[j] = make_uint2(0u, 0u);
@@ -404,7 +407,6 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
         uint2 e[BMW];  // first FIFO entries (meaningful for k < min(occ, b))
 #pragma unroll
         for (int k = 0; k < BMW; k++) e[k] = make_uint2(0u, 0u);
-        const uint32_t myreq = (uint32_t)w * NF * BMW;
         while (__ballot(live) != 0ull) {
             const uint32_t tag = processed + 1u;
             // ---------------------------------------------------------- R
@@ -421,7 +423,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                 const uint32_t tg = (uint32_t)gl0 + (lb & 63u);
                 tgk[k] = tg;
                 const bool rq = offk & !sk;
-                const uint32_t slot = rq ? (tg * NF + byte_of(lfx, q)) * BMW + k : req_trash;
+                const uint32_t slot = rq ? (byte_of(lfx, q) * BMW + k) * 64u + tg : req_trash;
                 wreq[slot] = make_uint2((ek.x & ~0x7Fu) | ((lb >> 6) << 5), tag);
                 ejm |= (offk & sk) ? 1u << k : 0u;
                 nf += offk ? 1u : 0u;
@@ -434,7 +436,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                                                 : 0u;
 #pragma unroll
             for (int k = 0; k < BMW; k++)
-                wreq[(uint32_t)k < nsr ? myreq + (NF - 1) * BMW + k : req_trash] =
+                wreq[(uint32_t)k < nsr ? ((NF - 1) * BMW + k) * 64u + (uint32_t)w : req_trash] =
                     make_uint2(((cur.start + o + k) << kXs) | (cur.lf << 5), tag);
             if ((nsr == cur.len - o) & (nsr < (uint32_t)b) & (R + 1 < rend) & live) {
                 int sR = R + 1;
@@ -443,7 +445,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                     load_wrange(d, sR, sr);
                     const uint32_t n = released_direct(d, sr, min((uint32_t)b - nsr, sr.len), deliv);
                     for (uint32_t q = 0; q < n; q++)
-                        wreq[myreq + (NF - 1) * BMW + nsr + q] = make_uint2(((sr.start + q) << kXs) | (sr.lf << 5), tag);
+                        wreq[((NF - 1) * BMW + nsr + q) * 64u + (uint32_t)w] = make_uint2(((sr.start + q) << kXs) | (sr.lf << 5), tag);
                     nsr += n;
                     if (n < sr.len) break;
                     sR++;
@@ -455,7 +457,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             {
                 uint2 qv[NF * BMW];
 #pragma unroll
-                for (int c = 0; c < NF * BMW; c++) qv[c] = wreq[myreq + c];
+                for (int c = 0; c < NF * BMW; c++) qv[c] = wreq[c * 64 + w];
                 K lists[NF][BMW];
 #pragma unroll
                 for (int f = 0; f < NF; f++) {
@@ -493,7 +495,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                 const uint32_t f = c / BMW, k = c % BMW;
                 const bool fs = f == NF - 1;
                 const uint32_t src = byte_of(fl, f);
-                wgnt[(gr & !fs) ? src * BMW + k : gnt_trash] = make_uint2(tag, (uint32_t)r);
+                wgnt[(gr & !fs) ? k * 64u + src : gnt_trash] = make_uint2(tag, (uint32_t)r);
                 sgr += (gr & fs) ? 1u : 0u;
                 ring[gr ? rbase + wrap_add(tail, (uint32_t)r, cap) : ring_trash] = make_uint2(lo & ~0x1Fu, ready);
                 if (ARB == 1) lastport = gr ? (fs ? P - 1u : byte_of(fp, f)) : lastport;
@@ -502,7 +504,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             // ---------------------------------------------------------- D
             uint2 gv[BMW];
 #pragma unroll
-            for (int k = 0; k < BMW; k++) gv[k] = wgnt[w * BMW + k];
+            for (int k = 0; k < BMW; k++) gv[k] = wgnt[k * 64 + w];
             uint32_t depf = 0, ejd = 0, vdm = 0;
             {
                 bool op = true;
@@ -539,13 +541,13 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                 cbar();
 #pragma unroll
                 for (int k = 0; k < BMW; k++)
-                    wvoid[((vdm >> k) & 1u) ? tgk[k] * BMW + gv[k].y : gnt_trash] = tag;
+                    wvoid[((vdm >> k) & 1u) ? gv[k].y * 64u + tgk[k] : gnt_trash] = tag;
                 cbar();
                 uint32_t j = 0;
 #pragma unroll
                 for (int r = 0; r < BMW; r++) {
                     const uint32_t lo = (uint32_t)lst[r];
-                    const bool keep = ((uint32_t)r < gcnt) & (wvoid[w * BMW + r] != tag);
+                    const bool keep = ((uint32_t)r < gcnt) & (wvoid[r * 64 + w] != tag);
                     ring[keep ? rbase + wrap_add(tail, j, cap) : ring_trash] = make_uint2(lo & ~0x1Fu, ready);
                     if (ARB == 1) {
                         const uint32_t f = (lo & 31u) / BMW;
