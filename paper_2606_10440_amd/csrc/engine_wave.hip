@@ -432,20 +432,22 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             const uint32_t nxt = (live & (occ != 0u) & (e[0].y > t)) ? e[0].y : kNever;
             // stream offers: the released lines of the current range, then (rarely)
             // of the ranges after it
+            // (the lane is their source and their target: they stay in registers)
             uint32_t nsr = (live & (R < rend)) ? released_count(d, cur, o, min((uint32_t)b, cur.len - o), dv0, dv1, deliv)
                                                 : 0u;
+            uint32_t sword[BMW];
 #pragma unroll
-            for (int k = 0; k < BMW; k++)
-                wreq[(uint32_t)k < nsr ? ((NF - 1) * BMW + k) * 64u + (uint32_t)w : req_trash] =
-                    make_uint2(((cur.start + o + k) << kXs) | (cur.lf << 5), tag);
+            for (int k = 0; k < BMW; k++) sword[k] = ((cur.start + o + k) << kXs) | (cur.lf << 5);
             if ((nsr == cur.len - o) & (nsr < (uint32_t)b) & (R + 1 < rend) & live) {
                 int sR = R + 1;
                 WRange sr;
                 while (sR < rend && nsr < (uint32_t)b) {
                     load_wrange(d, sR, sr);
                     const uint32_t n = released_direct(d, sr, min((uint32_t)b - nsr, sr.len), deliv);
-                    for (uint32_t q = 0; q < n; q++)
-                        wreq[((NF - 1) * BMW + nsr + q) * 64u + (uint32_t)w] = make_uint2(((sr.start + q) << kXs) | (sr.lf << 5), tag);
+#pragma unroll
+                    for (int k = 0; k < BMW; k++)
+                        if (((uint32_t)k >= nsr) & ((uint32_t)k < nsr + n))
+                            sword[k] = ((sr.start + (uint32_t)k - nsr) << kXs) | (sr.lf << 5);
                     nsr += n;
                     if (n < sr.len) break;
                     sR++;
@@ -455,22 +457,24 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             // ---------------------------------------------------------- G
             K lst[BMW];
             {
-                uint2 qv[NF * BMW];
+                uint2 qv[(NF - 1) * BMW];
 #pragma unroll
-                for (int c = 0; c < NF * BMW; c++) qv[c] = wreq[c * 64 + w];
+                for (int c = 0; c < (NF - 1) * BMW; c++) qv[c] = wreq[c * 64 + w];
                 K lists[NF][BMW];
 #pragma unroll
                 for (int f = 0; f < NF; f++) {
-                    const uint32_t port = f == NF - 1 ? P - 1u : (fp >> (8 * f)) & 0xFFu;
+                    const bool fs = f == NF - 1;  // the lane's own stream
+                    const uint32_t port = fs ? P - 1u : (fp >> (8 * f)) & 0xFFu;
                     const uint32_t rot = port >= rr ? port - rr : port + P - rr;
 #pragma unroll
                     for (int k = 0; k < BMW; k++) {
-                        const uint2 v = qv[f * BMW + k];
-                        const uint32_t lo = v.x | (uint32_t)(f * BMW + k);
+                        const uint32_t wx = fs ? sword[k] : qv[f * BMW + k].x;
+                        const bool valid = fs ? (uint32_t)k < nsr : qv[f * BMW + k].y == tag;
+                        const uint32_t lo = wx | (uint32_t)(f * BMW + k);
                         K key;
                         if constexpr (ARB == 0) key = lo;
                         else key = ((unsigned long long)((uint32_t)k * P + rot) << 32) | lo;
-                        lists[f][k] = (v.y == tag) ? key : kMax;
+                        lists[f][k] = valid ? key : kMax;
                     }
                 }
 #pragma unroll
