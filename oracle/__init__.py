@@ -52,11 +52,11 @@ def lib():
         L.oracle_fmix32.restype = C.c_uint32
         L.oracle_paths.argtypes = [C.c_int32, C.c_int32, P, P, P, P, C.c_int64]
         L.oracle_paths.restype = C.c_int
-        L.oracle_txn.argtypes = [C.c_int, C.c_uint64, C.c_int32, C.c_int32, P, C.c_int64,
+        L.oracle_txn.argtypes = [C.c_int, C.c_uint64, C.c_int32, C.c_int32, P, C.c_int32, C.c_int64,
                                  P, P, P, P, P]
         L.oracle_txn.restype = C.c_int
         L.oracle_simulate.argtypes = [C.c_int32, C.c_int32, P, P, P, P, P, C.c_int32,
-                                      C.c_int32, C.c_uint64, C.c_int32, P,
+                                      C.c_int32, C.c_uint64, C.c_int32, P, C.c_int32,
                                       C.c_int64, P, P, P, P,
                                       C.c_uint64, C.c_int32, P, P, P, P, P]
         L.oracle_simulate.restype = C.c_int
@@ -87,15 +87,16 @@ def paths(n, E, row_ptr, col_idx):
     return rc, pp, pl[:int(pp[-1])] if rc == 0 else pl
 
 
-def txn(coll, nbytes, group, E, x, order=None):
-    """Decode one transaction: (status, src, dst, preds list, T)."""
+def txn(coll, nbytes, group, E, x, order=None, dep=0):
+    """Decode one transaction: (status, src, dst, preds list, T).  With
+    dep=1 (chunk dependencies) a predecessor -1-c stands for whole chunk c."""
     src = np.zeros(1, np.int32)
     dst = np.zeros(1, np.int32)
     npred = np.zeros(1, np.int32)
     preds = np.zeros(4096, np.int64)
     T = np.zeros(1, np.int64)
     o = None if order is None else np.ascontiguousarray(order, np.int32)
-    rc = lib().oracle_txn(coll, nbytes, group, E, _p(o), x, _p(src), _p(dst), _p(npred),
+    rc = lib().oracle_txn(coll, nbytes, group, E, _p(o), dep, x, _p(src), _p(dst), _p(npred),
                           _p(preds), _p(T))
     return rc, int(src[0]), int(dst[0]), [int(v) for v in preds[:npred[0]]], int(T[0])
 
@@ -117,7 +118,7 @@ class Result:
 
 
 def simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, *, coll=-1, nbytes=0, group=0,
-             order=None, txns=None, max_cycles=0, check=False) -> Result:
+             order=None, dep=0, txns=None, max_cycles=0, check=False) -> Result:
     """Run one scenario.  ``txns`` = (src, dst, pred_ptr, pred_idx) for a custom
     transaction list (coll = -1); otherwise ``coll``/``nbytes``/``group``."""
     row_ptr = np.ascontiguousarray(row_ptr, np.int32)
@@ -138,7 +139,7 @@ def simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, *, coll=-1, nbytes=0, gr
         T = len(src)
     else:
         src = dst = pptr = pidx = None
-        rc, _, _, _, T = txn(coll, nbytes, group, E, 0, order)
+        rc, _, _, _, T = txn(coll, nbytes, group, E, 0, order, dep)
         if rc:
             return Result(rc, np.zeros(0, np.uint32), np.zeros(m, np.uint64),
                           np.zeros(m, np.uint64), 0, 0, 0, 0.0)
@@ -148,7 +149,7 @@ def simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, *, coll=-1, nbytes=0, gr
     mk = np.zeros(1, np.uint32)
     st = _Stats()
     rc = lib().oracle_simulate(n, E, _p(row_ptr), _p(col_idx), _p(bw), _p(lat), _p(cap), arb,
-                               coll, nbytes, group, _p(o), T, _p(src), _p(dst), _p(pptr),
+                               coll, nbytes, group, _p(o), dep, T, _p(src), _p(dst), _p(pptr),
                                _p(pidx), max_cycles, 1 if check else 0, _p(comp), _p(tx),
                                _p(busy), _p(mk), C.byref(st))
     return Result(rc, comp[:T], tx, busy, int(mk[0]), int(st.processed_cycles),
@@ -161,4 +162,4 @@ def simulate_workload(w, scenario: int = 0, *, max_cycles=0, check=False) -> Res
     sl = slice(scenario * m, (scenario + 1) * m)
     return simulate(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw[sl], w.lat[sl],
                     w.cap[sl], w.arb, coll=w.coll, nbytes=w.bytes, group=w.group_size,
-                    order=w.order, max_cycles=max_cycles, check=check)
+                    order=w.order, dep=w.dep, max_cycles=max_cycles, check=check)

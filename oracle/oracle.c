@@ -172,8 +172,15 @@ int oracle_paths(int32_t n, int32_t E, const int32_t *row_ptr,
 
 enum { COLL_RING = 0, COLL_DIRECT = 1, COLL_HIER = 2, COLL_A2A = 3, COLL_CUSTOM = -1 };
 
+/* Dependency granularity of a collective step (Sec. 4.2, 5.2): per line (a
+ * line may leave once the same line of the previous step has arrived, the
+ * get-style overlap), or per chunk (put + signal: a step's lines wait for the
+ * whole chunk of the previous step). */
+enum { DEP_LINE = 0, DEP_CHUNK = 1 };
+
 typedef struct {
     int coll;
+    int dep;                /* DEP_LINE or DEP_CHUNK */
     int32_t E;              /* endpoints */
     int32_t p;              /* participants (ring/direct: all endpoints) */
     const int32_t *rho;     /* ring order (NULL = rank order) */
@@ -191,10 +198,12 @@ static int32_t rho_of(const work_t *w, int64_t i) { return w->rho ? w->rho[i] : 
  * mixed-radix number whose most significant digit is the algorithm step, so
  * that lowest-id arbitration favours earlier steps. */
 static int setup_work(work_t *w, int coll, uint64_t bytes, int32_t group, int32_t E,
-                      const int32_t *order)
+                      const int32_t *order, int dep)
 {
     memset(w, 0, sizeof(*w));
-    w->coll = coll; w->E = E; w->p = E; w->rho = order;
+    w->coll = coll; w->E = E; w->p = E; w->rho = order; w->dep = dep;
+    if (dep != DEP_LINE && dep != DEP_CHUNK) return OR_ERR_INVALID_ARG;
+    if (dep == DEP_CHUNK && coll == COLL_HIER) return OR_ERR_INVALID_ARG;  /* not defined here */
     if (bytes == 0 || bytes % 128 != 0) return OR_ERR_SIZE;
     int64_t N = (int64_t)(bytes / 128);  /* lines */
     if (E < 2) return OR_ERR_INVALID_ARG;
@@ -235,7 +244,9 @@ static int64_t pmod(int64_t a, int64_t m) { int64_t r = a % m; return r < 0 ? r 
 
 /* Decode transaction x into (src, dst) and its predecessor list.
  * Returns the number of predecessors written to preds (at most 64 for the
- * collectives; custom lists are bounded by the caller's array). */
+ * collectives; custom lists are bounded by the caller's array).  A
+ * predecessor p >= 0 is a line; in chunk mode a predecessor is a whole chunk,
+ * written -1 - c for chunk c = the C lines [c*C, (c+1)*C). */
 static int32_t decode(const work_t *w, int64_t x, int32_t *src, int32_t *dst, int64_t *preds)
 {
     int32_t np = 0;
@@ -250,7 +261,10 @@ static int32_t decode(const work_t *w, int64_t x, int32_t *src, int32_t *dst, in
         int64_t p = w->p, C = w->C;
         int64_t j = x % C, q = x / C, i = q % p, s = q / p;
         *src = rho_of(w, i); *dst = rho_of(w, (i + 1) % p);
-        if (s >= 1) preds[np++] = ((s - 1) * p + pmod(i - 1, p)) * C + j;
+        if (s >= 1) {
+            int64_t prev = (s - 1) * p + pmod(i - 1, p);
+            preds[np++] = w->dep == DEP_CHUNK ? -1 - prev : prev * C + j;
+        }
         return np;
     }
     if (w->coll == COLL_DIRECT) {
@@ -266,7 +280,8 @@ static int32_t decode(const work_t *w, int64_t x, int32_t *src, int32_t *dst, in
             for (int64_t i2 = 0; i2 < p; i2++) {
                 if (i2 == i) continue;
                 int64_t k2 = pmod(i - i2, p);
-                preds[np++] = ((0 * (p - 1) + (k2 - 1)) * p + i2) * C + j;
+                int64_t rs = (0 * (p - 1) + (k2 - 1)) * p + i2;  /* reduce-scatter chunk into i */
+                preds[np++] = w->dep == DEP_CHUNK ? -1 - rs : rs * C + j;
             }
         return np;
     }
@@ -336,12 +351,12 @@ static int32_t decode(const work_t *w, int64_t x, int32_t *src, int32_t *dst, in
 }
 
 /* Public decoder (tests use it to pin the expansion). */
-int oracle_txn(int coll, uint64_t bytes, int32_t group, int32_t E, const int32_t *order,
+int oracle_txn(int coll, uint64_t bytes, int32_t group, int32_t E, const int32_t *order, int32_t dep,
                int64_t x, int32_t *src, int32_t *dst, int32_t *npred, int64_t *preds,
                int64_t *T_out)
 {
     work_t w;
-    int rc = setup_work(&w, coll, bytes, group, E, order);
+    int rc = setup_work(&w, coll, bytes, group, E, order, dep);
     if (rc) return rc;
     if (T_out) *T_out = w.T;
     if (x < 0 || x >= w.T) return OR_ERR_INVALID_ARG;
@@ -404,13 +419,24 @@ static const hcache_t *head_info(hcache_t *c, int64_t *slot, const work_t *w, ui
     return c;
 }
 
-/* rel(x) = max completion over predecessors; "never" while any is pending. */
-static uint64_t release_of(const hcache_t *c, const uint32_t *completion)
+/* rel(x) = max completion over predecessors; "never" while any is pending.
+ * A whole-chunk predecessor is complete once all C of its lines are; its
+ * completion is the latest of theirs (counted in chunk_done / chunk_max as
+ * lines complete). */
+static uint64_t release_of(const hcache_t *c, const uint32_t *completion, const int64_t *chunk_done,
+                           const uint32_t *chunk_max, int64_t C)
 {
     uint64_t rel = 0;
     for (int32_t q = 0; q < c->np; q++) {
-        uint32_t v = completion[c->preds[q]];
-        if (v == NEVER) return UINT64_MAX;
+        int64_t p = c->preds[q];
+        uint32_t v;
+        if (p >= 0) {
+            v = completion[p];
+            if (v == NEVER) return UINT64_MAX;
+        } else {
+            if (chunk_done[-1 - p] < C) return UINT64_MAX;
+            v = chunk_max[-1 - p];
+        }
         if (v > rel) rel = v;
     }
     return rel;
@@ -434,7 +460,7 @@ static int key_less(const req_t *a, const req_t *b, int arb, int32_t rr, int32_t
  */
 int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t *col_idx,
                     const int32_t *bw, const int32_t *lat, const int32_t *cap, int32_t arb,
-                    int32_t coll, uint64_t bytes, int32_t group, const int32_t *order,
+                    int32_t coll, uint64_t bytes, int32_t group, const int32_t *order, int32_t dep,
                     int64_t n_txn, const int32_t *csrc, const int32_t *cdst,
                     const int64_t *pred_ptr, const int64_t *pred_idx,
                     uint64_t max_cycles, int32_t check,
@@ -465,10 +491,14 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                 if (pred_idx[q] < 0 || pred_idx[q] >= n_txn) return OR_ERR_INVALID_ARG;
         }
     } else {
-        rc = setup_work(&w, coll, bytes, group, E, order);
+        rc = setup_work(&w, coll, bytes, group, E, order, dep);
         if (rc) return rc;
     }
     int64_t T = w.T;
+    /* chunk mode: lines completed per chunk and the latest completion */
+    int64_t nchunks = (w.dep == DEP_CHUNK && w.C > 0) ? T / w.C : 0;
+    int64_t *chunk_done = nchunks ? calloc((size_t)nchunks, sizeof(int64_t)) : NULL;
+    uint32_t *chunk_max = nchunks ? calloc((size_t)nchunks, sizeof(uint32_t)) : NULL;
 
     /* routes */
     int64_t *path_ptr = malloc(sizeof(int64_t) * ((size_t)E * E + 1));
@@ -512,7 +542,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     }
     if (rc) {
         free(path_ptr); free(path_link); free(port_of); free(nports); free(tail_of);
-        free(s_ptr); free(s_list); free(s_cur); free(preds);
+        free(s_ptr); free(s_list); free(s_cur); free(preds); free(chunk_done); free(chunk_max);
         return rc;
     }
     for (int32_t l = 0; l < m; l++) s_ptr[l + 1] += s_ptr[l];
@@ -602,7 +632,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                 uint32_t x = s_list[s_ptr[f] + s_cur[f] + k];
                 const hcache_t *hc = head_info(&hcache[(size_t)f * bmax + k], hpred + ((size_t)f * bmax + k) * maxp,
                                                &w, x, path_ptr, E);
-                uint64_t rel = release_of(hc, completion);
+                uint64_t rel = release_of(hc, completion, chunk_done, chunk_max, w.C);
                 if (rel > t) break;
                 req_t *r = &reqs[nr++];
                 r->src = sid; r->k = k; r->x = x;
@@ -689,6 +719,11 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                     if (check && completion[r->x] != NEVER) rc = OR_ERR_INVARIANT;  /* once */
                     completion[r->x] = (uint32_t)(t + 1);
                     remaining--;
+                    if (chunk_done) {
+                        int64_t ch = (int64_t)r->x / w.C;
+                        chunk_done[ch]++;
+                        if ((uint32_t)(t + 1) > chunk_max[ch]) chunk_max[ch] = (uint32_t)(t + 1);
+                    }
                 }
             }
             if (!dep) continue;
@@ -729,7 +764,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                 uint32_t x = s_list[s_ptr[f] + s_cur[f] + k];
                 const hcache_t *hc = head_info(&hcache[(size_t)f * bmax + k], hpred + ((size_t)f * bmax + k) * maxp,
                                                &w, x, path_ptr, E);
-                uint64_t rel = release_of(hc, completion);
+                uint64_t rel = release_of(hc, completion, chunk_done, chunk_max, w.C);
                 if (rel > t) { if (rel < next) next = rel; break; }
             }
         }
@@ -756,8 +791,13 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
             int32_t s, d;
             int32_t np = decode(&w, x, &s, &d, preds);
             uint64_t rel = 0;
-            for (int32_t q = 0; q < np; q++)
-                if (completion[preds[q]] > rel) rel = completion[preds[q]];
+            for (int32_t q = 0; q < np; q++) {
+                /* a whole-chunk predecessor: the latest of its C lines */
+                int64_t lo = preds[q] >= 0 ? preds[q] : (-1 - preds[q]) * w.C;
+                int64_t hi = preds[q] >= 0 ? preds[q] + 1 : lo + w.C;
+                for (int64_t y = lo; y < hi; y++)
+                    if (completion[y] > rel) rel = completion[y];
+            }
             uint64_t lsum = 0;
             for (int64_t q = path_ptr[(int64_t)s * E + d]; q < path_ptr[(int64_t)s * E + d + 1]; q++)
                 lsum += (uint64_t)lat[path_link[q]];
@@ -777,5 +817,6 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     free(bucket); free(touched); free(active);
     for (size_t i = 0; w.coll == COLL_CUSTOM && i < (size_t)m * bmax; i++) free(hcache[i].preds);
     free(hcache); free(hpred); free(src_first); free(src_cnt); free(admit0); free(adm_cnt);
+    free(chunk_done); free(chunk_max);
     return rc;
 }

@@ -32,6 +32,9 @@ COLL_DIRECT_ALLREDUCE = 1
 COLL_HIER_ALLREDUCE = 2
 COLL_ALLTOALL = 3
 
+DEP_LINE = 0   # a step's line waits for the matching line of the step before
+DEP_CHUNK = 1  # a step's line waits for the whole chunk of the step before
+
 MASK64 = (1 << 64) - 1
 
 
@@ -66,6 +69,7 @@ class Workload:
     group_size: int = 0          # hierarchical: endpoints per domain
     order: Optional[np.ndarray] = None
     meta: dict = field(default_factory=dict)
+    dep: int = 0                 # 0: per-line step dependencies, 1: per-chunk
 
     @property
     def n_links(self) -> int:
