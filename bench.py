@@ -5,7 +5,9 @@ every line of every scenario advanced hop by hop to completion, inputs and
 state resident in HBM.  The default workload is the batched design sweep
 (4096 scenarios of a 4x4 torus, ring all-reduce of 4 MiB per endpoint,
 seeded bandwidth/latency/depth per scenario), the largest workload by
-line-hop events; ``--workload C1..C4`` selects the others.
+line-hop events; ``--workload C1..C4`` selects the others, and a
+``_chunk`` suffix (C1, C2, C5) the same workload with per-chunk step
+dependencies.
 
 Prints one JSON line with the metric, a roofline entry for the engine
 kernel (algorithmic bytes per launch / measured launch time vs the 8 TB/s
@@ -36,6 +38,8 @@ DESCR = {
     "C4": "k=16 fat-tree (1024 hosts, 320 switches), all-to-all 64 KiB per pair, L in [100,300], cap 32",
     "C5": "4096 scenarios x 4x4 torus, ring all-reduce 4 MiB, seeded b in {1,2,4}, L in [20,200], depth in {16,32,64}",
 }
+for _k in ("C1", "C2", "C5"):
+    DESCR[_k + "_chunk"] = DESCR[_k] + "; per-chunk (put + signal) step dependencies"
 
 
 def algorithmic_bytes(T: int, S: int, m: int) -> int:

@@ -25,7 +25,8 @@
  *   - cycles in which nothing can change are skipped;
  *   - routes are minimal-hop paths; ties between next hops are broken by the
  *     MurmurHash3 32-bit finalizer of (src << 16 | dst) (hash ECMP);
- *   - a line is injected once all its predecessor lines have completed.
+ *   - a line is injected once all its predecessor lines have completed
+ *     (per line, or per whole chunk: sim_dep).
  *
  * Threading: a context is used by one host thread at a time; there is no
  * global mutable state, so distinct contexts may be used concurrently.
@@ -66,6 +67,15 @@ typedef enum {
     SIM_COLL_ALLTOALL = 3          /* linear-shift all-to-all                        */
 } sim_coll;
 
+/* Granularity of the step-to-step dependencies of a collective (Sec. 4.2
+ * and 5.2 contrast get-style transfers, which overlap steps line by line,
+ * with put + signal, where a step waits for the signal that the whole chunk
+ * of the step before has arrived). */
+typedef enum {
+    SIM_DEP_LINE = 0,  /* line j of a step waits for line j of each predecessor chunk */
+    SIM_DEP_CHUNK = 1  /* every line of a step waits for all lines of each predecessor chunk */
+} sim_dep;
+
 /* Limits checked by sim_create. */
 #define SIM_MAX_BW 64           /* lines per cycle */
 #define SIM_MAX_LAT (1 << 20)   /* cycles          */
@@ -104,11 +114,15 @@ sim_status sim_create(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_p
  *                0 otherwise.
  *   order      : ring/direct: participant order, a permutation of the
  *                endpoints (NULL = rank order); must be NULL otherwise.
+ *   dep        : sim_dep.  SIM_DEP_CHUNK is defined for ring and direct
+ *                all-reduce (and is a no-op for all-to-all, which has no
+ *                dependencies); hierarchical all-reduce takes SIM_DEP_LINE
+ *                only (SIM_ERR_INVALID_ARG otherwise).
  * Builds the routes of every flow used (SIM_ERR_UNREACHABLE if one has no
  * path), the injection streams and the predecessor tables, and uploads them.
  */
 sim_status sim_load_collective(sim_ctx *ctx, int32_t coll, uint64_t bytes, int32_t group_size,
-                               const int32_t *order);
+                               const int32_t *order, int32_t dep);
 
 /*
  * Load a custom transaction list: line x (0 <= x < n) goes src[x] -> dst[x]

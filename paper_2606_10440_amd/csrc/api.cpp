@@ -165,6 +165,7 @@ struct Ranges {
     std::vector<int64_t> pref_beg;   // [nr+1] into pref_rng/pref_delta
     std::vector<int64_t> pref_rng;   // predecessor range
     std::vector<uint32_t> pref_delta;  // line start+o waits for line pref_start+delta+o
+    bool whole = false;  // per-chunk: every line waits for the whole predecessor range
     void add(uint64_t s, uint64_t l, int32_t a, int32_t b) {
         start.push_back((uint32_t)s);
         len.push_back((uint32_t)l);
@@ -182,8 +183,12 @@ struct Ranges {
 inline int64_t wrap(int64_t a, int64_t m) { return ((a % m) + m) % m; }
 
 sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t group,
-                             const int32_t *order, Ranges &R) {
+                             const int32_t *order, int32_t dep, Ranges &R) {
     const int64_t E = c->E;
+    if (dep != SIM_DEP_LINE && dep != SIM_DEP_CHUNK) return fail(c, SIM_ERR_INVALID_ARG, "unknown dep");
+    if (dep == SIM_DEP_CHUNK && coll == SIM_COLL_HIER_ALLREDUCE)
+        return fail(c, SIM_ERR_INVALID_ARG, "per-chunk dependencies are not defined for the hierarchical all-reduce");
+    R.whole = dep == SIM_DEP_CHUNK;
     if (bytes == 0 || bytes % SIM_LINE_BYTES) return fail(c, SIM_ERR_SIZE, "bytes must be a positive multiple of 128");
     const int64_t N = (int64_t)(bytes / SIM_LINE_BYTES);
     if (E < 2) return fail(c, SIM_ERR_INVALID_ARG, "a collective needs at least 2 endpoints");
@@ -363,10 +368,10 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         r_pd[j] = (int32_t)pd_flow.size();
         for (int64_t q = R.pref_beg[i]; q < R.pref_beg[i + 1]; q++) {
             int64_t pr = R.pref_rng[q];
-            if ((uint64_t)R.pref_delta[q] + R.len[i] > R.len[pr])
+            if (!R.whole && (uint64_t)R.pref_delta[q] + R.len[i] > R.len[pr])
                 return fail(c, SIM_ERR_INVALID_ARG, "internal: predecessor range too short");
             pd_flow.push_back(rflow[pr]);
-            pd_base.push_back(seq0[pr] + R.pref_delta[q]);
+            pd_base.push_back(R.whole ? seq0[pr] + R.len[pr] - 1 : seq0[pr] + R.pref_delta[q]);
         }
     }
     r_pd[nr] = (int32_t)pd_flow.size();
@@ -768,6 +773,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     d.engine = engine;
     d.nl = nl;
     d.has_preds = any_preds ? 1 : 0;
+    d.pd_omask = R.whole ? 0u : 0xFFFFFFFFu;
     d.b1_ns = (int32_t)s_link.size();
     d.b1_lpt = (nl + 1023) / 1024;
     d.b1_deliv_lds = b1_deliv_lds ? 1 : 0;
@@ -945,12 +951,13 @@ sim_status sim_create(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_p
     return SIM_OK;
 }
 
-sim_status sim_load_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t group_size, const int32_t *order) {
+sim_status sim_load_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t group_size, const int32_t *order,
+                               int32_t dep) {
     if (!c) return SIM_ERR_INVALID_ARG;
     if (coll != SIM_COLL_HIER_ALLREDUCE && group_size != 0)
         return fail(c, SIM_ERR_INVALID_ARG, "group_size applies to the hierarchical all-reduce only");
     Ranges R;
-    sim_status st = expand_collective(c, coll, bytes, group_size, order, R);
+    sim_status st = expand_collective(c, coll, bytes, group_size, order, dep, R);
     if (st != SIM_OK) return st;
     return finish_load(c, R);
 }

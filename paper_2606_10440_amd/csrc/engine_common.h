@@ -37,14 +37,16 @@ __device__ __forceinline__ void load_range(const DevNet &d, int R, RangeReg<PC> 
 }
 
 // Line start+o of range r may be injected: every predecessor flow has
-// delivered more than base+o lines (values as of the start of the cycle).
+// delivered more than base+o lines, or more than base for per-chunk
+// dependencies (values as of the start of the cycle).
 template <int PC>
 __device__ __forceinline__ bool released(const DevNet &d, const RangeReg<PC> &r, uint32_t o, const uint32_t *deliv) {
     bool ok = true;
 #pragma unroll
     for (int q = 0; q < PC; q++)
-        if (r.pd0 + q < r.pd1) ok = ok && deliv[r.pf[q]] > r.pb[q] + o;
-    for (int idx = r.pd0 + PC; ok && idx < r.pd1; idx++) ok = deliv[d.pd_flow[idx]] > d.pd_base[idx] + o;
+        if (r.pd0 + q < r.pd1) ok = ok && deliv[r.pf[q]] > r.pb[q] + (o & d.pd_omask);
+    for (int idx = r.pd0 + PC; ok && idx < r.pd1; idx++)
+        ok = deliv[d.pd_flow[idx]] > d.pd_base[idx] + (o & d.pd_omask);
     return ok;
 }
 

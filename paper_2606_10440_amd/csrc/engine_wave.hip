@@ -96,32 +96,53 @@ __device__ __forceinline__ void load_wrange(const DevNet &d, int R, WRange &r) {
     vm_drain();
 }
 
+// Lines released by one predecessor whose flow has delivered v lines, from
+// a line that waits for more than bb: v - bb per line (each further line
+// waits for one more), all of them per chunk (CH).
+template <bool CH>
+__device__ __forceinline__ uint32_t pred_allows(uint32_t v, uint32_t bb) {
+    return v > bb ? (CH ? 0xFFFFFFFFu : v - bb) : 0u;
+}
+
 // Lines of range r from offset o on whose predecessors have all been
 // delivered (a prefix: the counts only grow with o), capped at n.  dv0/dv1
 // hold the first two predecessors' delivered counts as of the cycle start.
+// CH: per-chunk dependencies (every base is the whole chunk's; no offset).
+template <bool CH>
 __device__ __forceinline__ uint32_t released_count(const DevNet &d, const WRange &r, uint32_t o, uint32_t n,
                                                    uint32_t dv0, uint32_t dv1, const uint32_t *deliv) {
-    const uint32_t b0 = r.pb0 + o, b1 = r.pb1 + o;
-    n = r.np > 0 ? min(n, dv0 > b0 ? dv0 - b0 : 0u) : n;
-    n = r.np > 1 ? min(n, dv1 > b1 ? dv1 - b1 : 0u) : n;
+    const uint32_t oo = CH ? 0u : o;
+    n = r.np > 0 ? min(n, pred_allows<CH>(dv0, r.pb0 + oo)) : n;
+    n = r.np > 1 ? min(n, pred_allows<CH>(dv1, r.pb1 + oo)) : n;
     if ((n != 0u) & (r.np > 2)) {
-        for (int idx = r.pd0 + 2; idx < r.pd0 + (int)r.np; idx++) {
-            const uint32_t v = deliv[d.pd_dix[idx]], bb = d.pd_base[idx] + o;
-            n = min(n, v > bb ? v - bb : 0u);
-        }
+        for (int idx = r.pd0 + 2; idx < r.pd0 + (int)r.np; idx++)
+            n = min(n, pred_allows<CH>(deliv[d.pd_dix[idx]], d.pd_base[idx] + oo));
         vm_drain();
     }
     return n;
 }
 
+// Whether line o of range r is released (released_count for one line).
+template <bool CH>
+__device__ __forceinline__ bool released_one(const DevNet &d, const WRange &r, uint32_t o, uint32_t dv0, uint32_t dv1,
+                                             const uint32_t *deliv) {
+    const uint32_t oo = CH ? 0u : o;
+    bool ok = ((r.np < 1u) | (dv0 > r.pb0 + oo)) & ((r.np < 2u) | (dv1 > r.pb1 + oo));
+    if (ok & (r.np > 2u)) {
+        for (int idx = r.pd0 + 2; idx < r.pd0 + (int)r.np; idx++)
+            ok = ok & (deliv[d.pd_dix[idx]] > d.pd_base[idx] + oo);
+        vm_drain();
+    }
+    return ok;
+}
+
 // Same from offset 0, with the delivered counts read from LDS (a range
 // entered in the middle of a cycle).
+template <bool CH>
 __device__ __forceinline__ uint32_t released_direct(const DevNet &d, const WRange &r, uint32_t n,
                                                     const uint32_t *deliv) {
-    for (int idx = r.pd0; idx < r.pd0 + (int)r.np; idx++) {
-        const uint32_t v = deliv[d.pd_dix[idx]], bb = d.pd_base[idx];
-        n = min(n, v > bb ? v - bb : 0u);
-    }
+    for (int idx = r.pd0; idx < r.pd0 + (int)r.np; idx++)
+        n = min(n, pred_allows<CH>(deliv[d.pd_dix[idx]], d.pd_base[idx]));
     vm_drain();
     return n;
 }
@@ -163,8 +184,8 @@ __device__ __forceinline__ void merge_low(K (&a)[N], const K (&b)[N]) {
 }
 
 // NF: request-slot groups per target lane (feeders, then the lane's own
-// stream in group NF - 1).
-template <int BM, int ARB, int NF>
+// stream in group NF - 1).  CH: per-chunk step dependencies.
+template <int BM, int ARB, int NF, bool CH>
 __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
     extern __shared__ __align__(16) unsigned char smem[];
     // the workgroup's waves are independent: each has its own LDS region and
@@ -346,7 +367,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             const uint32_t tgw = fw ? (uint32_t)gl0 + (lb & 63u) : 64u + (uint32_t)w;
             const uint32_t fkey = (hx & ~0x7Fu) | ((lb >> 6) << 5) | 1u;
             atomicMin(&word[tgw], fkey);
-            const bool sw = live & (R < rend) & (released_count(d, cur, o, 1u, dv0, dv1, deliv) != 0u);
+            const bool sw = live & (R < rend) & released_one<CH>(d, cur, o, dv0, dv1, deliv);
             const uint32_t skey = ((cur.start + o) << kXs) | (cur.lf << 5) | 1u;
             atomicMin(&word[sw ? (uint32_t)w : 64u + (uint32_t)w], skey);
             const uint32_t nxt = (live & (occ != 0u) & (hr > t)) ? hr : kNever;
@@ -433,7 +454,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             // stream offers: the released lines of the current range, then (rarely)
             // of the ranges after it
             // (the lane is their source and their target: they stay in registers)
-            uint32_t nsr = (live & (R < rend)) ? released_count(d, cur, o, min((uint32_t)b, cur.len - o), dv0, dv1, deliv)
+            uint32_t nsr = (live & (R < rend)) ? released_count<CH>(d, cur, o, min((uint32_t)b, cur.len - o), dv0, dv1, deliv)
                                                 : 0u;
             uint32_t sword[BMW];
 #pragma unroll
@@ -443,7 +464,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                 WRange sr;
                 while (sR < rend && nsr < (uint32_t)b) {
                     load_wrange(d, sR, sr);
-                    const uint32_t n = released_direct(d, sr, min((uint32_t)b - nsr, sr.len), deliv);
+                    const uint32_t n = released_direct<CH>(d, sr, min((uint32_t)b - nsr, sr.len), deliv);
 #pragma unroll
                     for (int k = 0; k < BMW; k++)
                         if (((uint32_t)k >= nsr) & ((uint32_t)k < nsr + n))
@@ -601,7 +622,9 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
 
 template <int BM, int ARB, int NF>
 hipError_t launch_wave3(const DevNet &d, hipStream_t st) {
-    auto k = engine_wave<BM, ARB, NF>;
+    // per-chunk dependencies get their own instantiation: the per-line
+    // release test then carries no mask
+    auto k = d.pd_omask == 0u ? engine_wave<BM, ARB, NF, true> : engine_wave<BM, ARB, NF, false>;
     if (d.lds_bytes > 65536)
         (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
     hipLaunchKernelGGL(k, dim3((unsigned)d.wv_nblk), dim3(64 * d.wv_wpb), (unsigned)d.lds_bytes, st, d);

@@ -141,7 +141,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                 for (int k = 0; k < b && R < rend; k++) {
                     bool ok = true;
                     for (int q = d.r_pd[R]; q < d.r_pd[R + 1]; q++)
-                        if (delivered[d.pd_flow[q]] <= d.pd_base[q] + o) {
+                        if (delivered[d.pd_flow[q]] <= d.pd_base[q] + (o & d.pd_omask)) {
                             ok = false;
                             break;
                         }

@@ -51,9 +51,12 @@ struct DevNet {
     const int32_t *r_path;        // [nr] index of the range's first hop in path_link
     const int32_t *r_pd;          // [nr+1] predecessor descriptors of the range
     // predecessor descriptor: line start+o may be injected once flow pd_flow has
-    // delivered more than pd_base + o lines (flows deliver in id order)
+    // delivered more than pd_base + (o & pd_omask) lines (flows deliver in id
+    // order).  pd_omask is all ones for per-line dependencies; 0 for per-chunk
+    // ones, where pd_base is the last line of the predecessor chunk.
     const int32_t *pd_flow;
     const uint32_t *pd_base;
+    uint32_t pd_omask;
     // paths: hop link ids, each path terminated by -(1 + flow slot)
     const int32_t *path_link;
 

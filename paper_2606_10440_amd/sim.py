@@ -45,7 +45,7 @@ def lib():
         L = C.CDLL(LIB_PATH)
         P, i32, i64, u64 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64
         L.sim_create.argtypes = [i32, i32, P, P, i32, P, P, P, i32, C.POINTER(P)]
-        L.sim_load_collective.argtypes = [P, i32, u64, i32, P]
+        L.sim_load_collective.argtypes = [P, i32, u64, i32, P, i32]
         L.sim_load_transactions.argtypes = [P, i64, P, P, P, P]
         L.sim_sizes.argtypes = [P, P, P, P, P]
         L.sim_run.argtypes = [P, P, P, P, P, P, u64]
@@ -82,9 +82,9 @@ def sim_create(n_nodes, n_endpoints, row_ptr, col_idx, n_scenarios, bw, lat, cap
     return ctx
 
 
-def sim_load_collective(ctx, coll, nbytes, group_size=0, order=None):
+def sim_load_collective(ctx, coll, nbytes, group_size=0, order=None, dep=0):
     o = None if order is None else np.ascontiguousarray(order, np.int32)
-    _check(ctx, lib().sim_load_collective(ctx, coll, nbytes, group_size, _ptr(o)))
+    _check(ctx, lib().sim_load_collective(ctx, coll, nbytes, group_size, _ptr(o), dep))
 
 
 def sim_load_transactions(ctx, src, dst, pred_ptr, pred_idx):
@@ -157,11 +157,11 @@ class Simulator:
         sim = cls(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw, w.lat, w.cap, w.arb,
                   w.n_scenarios)
         if w.coll >= 0:
-            sim.load_collective(w.coll, w.bytes, w.group_size, w.order)
+            sim.load_collective(w.coll, w.bytes, w.group_size, w.order, w.dep)
         return sim
 
-    def load_collective(self, coll, nbytes, group_size=0, order=None):
-        sim_load_collective(self.ctx, coll, nbytes, group_size, order)
+    def load_collective(self, coll, nbytes, group_size=0, order=None, dep=0):
+        sim_load_collective(self.ctx, coll, nbytes, group_size, order, dep)
 
     def load_transactions(self, src, dst, pred_ptr, pred_idx):
         sim_load_transactions(self.ctx, src, dst, pred_ptr, pred_idx)

@@ -246,7 +246,13 @@ def config(name: str) -> Workload:
         of 64 MiB, round-robin arbitration.
     C4  k=16 fat-tree (1024 hosts, 320 switches), all-to-all 64 KiB per pair.
     C5  4096 scenarios of a 4x4 torus, ring all-reduce of 4 MiB, seeded params.
+    A "_chunk" suffix (C1, C2, C5) gives the same workload with per-chunk
+    step dependencies.
     """
+    if name.endswith("_chunk"):
+        # the same workload with per-chunk (put + signal) step dependencies
+        w = config(name[:-len("_chunk")])
+        return replace(w, dep=DEP_CHUNK, name=w.name + "_chunkdep")
     if name == "C1":
         return full_mesh(4, b=1, L=10, cap=16, coll=COLL_DIRECT_ALLREDUCE,
                          nbytes=64 * 1024, name="C1_mesh4_direct_ar_64KiB")

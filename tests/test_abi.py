@@ -119,6 +119,12 @@ def test_load_errors_before_device(simlib):
             simlib.sim_load_collective(ctx, si.COLL_RING_ALLREDUCE, 1024, order=[0, 1, 2, 3, 4, 5, 6, 6])
         assert e.value.status == simlib.SIM_ERR_INVALID_ARG
         with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_collective(ctx, si.COLL_RING_ALLREDUCE, 1024, dep=7)              # unknown dep
+        assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_collective(ctx, si.COLL_HIER_ALLREDUCE, 1024, 4, dep=si.DEP_CHUNK)  # not defined
+        assert e.value.status == simlib.SIM_ERR_INVALID_ARG and "hierarchical" in str(e.value)
+        with pytest.raises(simlib.SimError) as e:
             simlib.sim_run(ctx, 0, 0, 0, 0, 0)
         assert e.value.status == simlib.SIM_ERR_STATE
     finally:

@@ -48,7 +48,7 @@ def run_gpu(simmod, w, max_cycles=0, txns=None):
     if txns is not None:
         s.load_transactions(*txns)
     else:
-        s.load_collective(w.coll, w.bytes, w.group_size, w.order)
+        s.load_collective(w.coll, w.bytes, w.group_size, w.order, w.dep)
     r = s.run(max_cycles=max_cycles)
     s.close()
     return r
@@ -237,7 +237,7 @@ def _golden(name):
         return json.load(f)
 
 
-@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4"])
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C1_chunk", "C2_chunk"])
 def test_full_size_digest(simmod, torch_cuda, name):
     g = _golden(name)
     w = si.config(name)
@@ -253,10 +253,11 @@ def test_full_size_digest(simmod, torch_cuda, name):
     assert _digest(r.busy_cycles[0].cpu().numpy().astype("<u8")) == g["busy_cycles_sha256"][0]
 
 
-def test_full_size_batched_digest(simmod, torch_cuda):
-    g = _golden("C5")
-    w = si.config("C5")
-    say("full-size C5: running 4096 scenarios on GPU")
+@pytest.mark.parametrize("name", ["C5", "C5_chunk"])
+def test_full_size_batched_digest(simmod, torch_cuda, name):
+    g = _golden(name)
+    w = si.config(name)
+    say(f"full-size {name}: running 4096 scenarios on GPU")
     r = run_gpu(simmod, w)
     assert r.status == 0
     mk = r.makespan.cpu().numpy()
@@ -386,3 +387,49 @@ def test_wave_random_dags(simmod, oracle_lib, seed):
     src, dst, pptr, pidx = si.random_dag(rng, n_end, int(rng.integers(1, 250)), max_preds=3)
     w = si.Workload("rand_wave", n, n_end, rp, ci, 3, bw, lat, cap, seed % 2, -1, 0)
     check_engine(simmod, oracle_lib, w, "wave", txns=(src, dst, pptr, pidx))
+
+
+# ----------------------------------------------------- per-chunk dependencies
+# Every line of a step waits for the whole chunk of the step before (put +
+# signal); the oracle releases them through per-chunk join counters, the
+# engines through one delivered-count threshold per predecessor chunk.
+
+@pytest.mark.parametrize("engine", ENGINES)
+@pytest.mark.parametrize("p,C,b,L,coll", [(3, 5, 1, 4, 0), (4, 8, 2, 3, 0), (5, 10, 1, 7, 1), (4, 6, 3, 2, 1),
+                                          (2, 9, 1, 1, 0), (6, 12, 2, 20, 1), (5, 7, 1, 3, 3)])
+def test_chunk_mesh(simmod, oracle_lib, engine, p, C, b, L, coll):
+    w = si.full_mesh(p, b=b, L=L, cap=max(1, b * (L + 1) // 2), coll=coll, nbytes=128 * C * p)
+    w.dep = si.DEP_CHUNK
+    assert check_engine(simmod, oracle_lib, w, engine) == 1
+
+
+@pytest.mark.parametrize("engine", ENGINES)
+@pytest.mark.parametrize("arb", [0, 1])
+@pytest.mark.parametrize("coll", [si.COLL_RING_ALLREDUCE, si.COLL_DIRECT_ALLREDUCE])
+def test_chunk_torus(simmod, oracle_lib, engine, arb, coll):
+    X = 4 if coll == si.COLL_RING_ALLREDUCE else 2
+    bws = (1,) if engine == "b1" else (1, 2, 4)
+    w = si.torus2d(X, X, n_scenarios=9, seed=80 + arb + 2 * coll, bws=bws, lat_lo=1, lat_hi=25,
+                   depths=(1, 2, 3, 7, 32), nbytes=128 * X * X * 6, arb=arb, coll=coll)
+    w.dep = si.DEP_CHUNK
+    check_engine(simmod, oracle_lib, w, engine)
+
+
+@pytest.mark.parametrize("engine", ENGINES)
+def test_chunk_fat_tree(simmod, oracle_lib, engine):
+    w = si.fat_tree(4, nbytes=128 * 16 * 3, cap=5, lat_lo=2, lat_hi=9, arb=1, coll=si.COLL_RING_ALLREDUCE)
+    w.dep = si.DEP_CHUNK
+    assert check_engine(simmod, oracle_lib, w, engine) == 1
+
+
+def test_chunk_rejected_for_hierarchical(simmod):
+    w = si.scaled(si.config("C3"), bytes=128 * 64 * 8)
+    s = simmod.Simulator(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw, w.lat, w.cap, w.arb, 1)
+    try:
+        with pytest.raises(simmod.SimError) as e:
+            s.load_collective(w.coll, w.bytes, w.group_size, None, si.DEP_CHUNK)
+        assert e.value.status == simmod.SIM_ERR_INVALID_ARG
+        with pytest.raises(simmod.SimError):
+            s.load_collective(si.COLL_RING_ALLREDUCE, 128 * 64, 0, None, 2)
+    finally:
+        s.close()

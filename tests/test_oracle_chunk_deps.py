@@ -115,3 +115,15 @@ def test_chunk_mode_equals_explicit_dag(oracle_lib, seed):
 def test_chunk_mode_not_defined_for_hierarchical(oracle_lib):
     rc, *_ = oracle_lib.txn(si.COLL_HIER_ALLREDUCE, 128 * 8 * 4, 2, 4, 0, None, DEP_CHUNK)
     assert rc == 1  # invalid argument
+
+
+def test_c2_chunk_closed_form(oracle_lib):
+    # 8-endpoint mesh ring, C = 16384 lines, b = 1, L = 50, cap 64 >= b(L+1):
+    # D = 16383 + 51 and the makespan is 14 D.
+    w = si.config("C2_chunk")
+    assert w.dep == si.DEP_CHUNK
+    r = oracle_lib.simulate_workload(w, check=True)
+    D = 16383 + 51
+    assert r.makespan == 14 * D
+    ids = np.arange(len(r.completion))
+    assert np.array_equal(r.completion, (ids // (16384 * 8)) * D + ids % 16384 + 51)
