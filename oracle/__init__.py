@@ -89,7 +89,8 @@ def paths(n, E, row_ptr, col_idx):
 
 def txn(coll, nbytes, group, E, x, order=None, dep=0):
     """Decode one transaction: (status, src, dst, preds list, T).  With
-    dep=1 (chunk dependencies) a predecessor -1-c stands for whole chunk c."""
+    dep=1 (chunk dependencies) a predecessor -1-m stands for whole message m
+    (one step's transfer between two participants)."""
     src = np.zeros(1, np.int32)
     dst = np.zeros(1, np.int32)
     npred = np.zeros(1, np.int32)

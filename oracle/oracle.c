@@ -170,12 +170,17 @@ int oracle_paths(int32_t n, int32_t E, const int32_t *row_ptr,
 
 /* ------------------------------------------------------ workload expansion */
 
-enum { COLL_RING = 0, COLL_DIRECT = 1, COLL_HIER = 2, COLL_A2A = 3, COLL_CUSTOM = -1 };
+enum {
+    COLL_RING = 0, COLL_DIRECT = 1, COLL_HIER = 2, COLL_A2A = 3,
+    COLL_RING_AG = 4, COLL_RING_RS = 5, COLL_DIRECT_AG = 6, COLL_DIRECT_RS = 7,
+    COLL_RHD = 8, COLL_DBT = 9, COLL_CUSTOM = -1
+};
 
 /* Dependency granularity of a collective step (Sec. 4.2, 5.2): per line (a
  * line may leave once the same line of the previous step has arrived, the
- * get-style overlap), or per chunk (put + signal: a step's lines wait for the
- * whole chunk of the previous step). */
+ * get-style overlap), or per chunk (put + signal: a message -- one step's
+ * transfer from one participant to another -- starts once every message
+ * that delivers any of its inputs has arrived whole). */
 enum { DEP_LINE = 0, DEP_CHUNK = 1 };
 
 typedef struct {
@@ -184,7 +189,10 @@ typedef struct {
     int32_t E;              /* endpoints */
     int32_t p;              /* participants (ring/direct: all endpoints) */
     const int32_t *rho;     /* ring order (NULL = rank order) */
-    int64_t C;              /* ring/direct/a2a chunk lines */
+    int64_t C;              /* ring/direct/a2a/rhd chunk lines */
+    int64_t N;              /* rhd: buffer lines */
+    int32_t K;              /* rhd: log2 p */
+    int64_t H;              /* dbt: lines per tree (half the buffer) */
     int64_t G, M, C1, C2, B2, B3;  /* hierarchical */
     int64_t T;
     /* custom */
@@ -204,6 +212,7 @@ static int setup_work(work_t *w, int coll, uint64_t bytes, int32_t group, int32_
     w->coll = coll; w->E = E; w->p = E; w->rho = order; w->dep = dep;
     if (dep != DEP_LINE && dep != DEP_CHUNK) return OR_ERR_INVALID_ARG;
     if (dep == DEP_CHUNK && coll == COLL_HIER) return OR_ERR_INVALID_ARG;  /* not defined here */
+    if (order && (coll == COLL_HIER || coll == COLL_A2A)) return OR_ERR_INVALID_ARG;
     if (bytes == 0 || bytes % 128 != 0) return OR_ERR_SIZE;
     int64_t N = (int64_t)(bytes / 128);  /* lines */
     if (E < 2) return OR_ERR_INVALID_ARG;
@@ -233,6 +242,24 @@ static int setup_work(work_t *w, int coll, uint64_t bytes, int32_t group, int32_
         w->C = N;
         w->T = (int64_t)(E - 1) * E * w->C;
         break;
+    case COLL_RING_AG: case COLL_RING_RS: case COLL_DIRECT_AG: case COLL_DIRECT_RS:
+        if (N % E) return OR_ERR_SIZE;
+        w->C = N / E;
+        w->T = (int64_t)(E - 1) * E * w->C;
+        break;
+    case COLL_RHD:
+        if (E & (E - 1)) return OR_ERR_INVALID_ARG;   /* power of two participants */
+        if (N % E) return OR_ERR_SIZE;
+        while ((1 << w->K) < E) w->K++;
+        w->N = N;
+        w->C = N / E;
+        w->T = 2 * N * (int64_t)(E - 1);
+        break;
+    case COLL_DBT:
+        if (N % 2) return OR_ERR_SIZE;
+        w->H = N / 2;
+        w->T = 4 * (int64_t)(E - 1) * w->H;
+        break;
     default:
         return OR_ERR_INVALID_ARG;
     }
@@ -241,6 +268,118 @@ static int setup_work(work_t *w, int coll, uint64_t bytes, int32_t group, int32_
 }
 
 static int64_t pmod(int64_t a, int64_t m) { int64_t r = a % m; return r < 0 ? r + m : r; }
+
+/* ---- recursive halving-doubling all-reduce (Thakur et al., cited in Sec. 1)
+ * p = 2^K participants, N lines per buffer, chunk C = N/p.
+ * Reduce-scatter step j (0 <= j < K): partner at distance p >> (j+1).
+ *   Before the step participant i holds the block of 2 S_j lines (S_j =
+ *   N >> (j+1)) starting at (i >> (K-j)) * 2 S_j; it keeps the half chosen by
+ *   bit (K-1-j) of i and sends the other half to the partner.  After K steps
+ *   i holds chunk i reduced.
+ *   ids: p (N - 2 S_j) + i S_j + o.
+ * All-gather step j: partner at distance 1 << j; i sends its block of 2^j
+ *   chunks, which starts at chunk (i >> j) << j.
+ *   ids: N (p-1) + N (2^j - 1) + i 2^j C + o.
+ * A sent line at buffer position q waits, per line, for every earlier
+ * arrival of position q at its sender: in reduce-scatter the partial sums of
+ * all earlier steps; in all-gather, for the sender's own chunk, all K
+ * reduce-scatter arrivals, else the all-gather step that brought q. */
+static int64_t rhd_rs_len(const work_t *w, int32_t j) { return w->N >> (j + 1); }
+static int64_t rhd_rs_base(const work_t *w, int32_t j) { return (int64_t)w->p * (w->N - 2 * rhd_rs_len(w, j)); }
+static int64_t rhd_ag_len(const work_t *w, int32_t j) { return w->C << j; }
+static int64_t rhd_ag_base(const work_t *w, int32_t j)
+{
+    return w->N * (int64_t)(w->p - 1) + w->N * (((int64_t)1 << j) - 1);
+}
+/* first buffer position of the half participant i sends at reduce-scatter step j */
+static int64_t rhd_rs_send_start(const work_t *w, int64_t i, int32_t j)
+{
+    int64_t S = rhd_rs_len(w, j);
+    int64_t block = (i >> (w->K - j)) * 2 * S;
+    int64_t keep_upper = (i >> (w->K - 1 - j)) & 1;
+    return block + (keep_upper ? 0 : S);
+}
+/* id of the line that brought position q to participant i at reduce-scatter step j */
+static int64_t rhd_rs_arrival(const work_t *w, int64_t i, int32_t j, int64_t q)
+{
+    int64_t from = i ^ ((int64_t)w->p >> (j + 1));
+    return rhd_rs_base(w, j) + from * rhd_rs_len(w, j) + (q - rhd_rs_send_start(w, from, j));
+}
+/* id of the line that brought position q to participant i at all-gather step h */
+static int64_t rhd_ag_arrival(const work_t *w, int64_t i, int32_t h, int64_t q)
+{
+    int64_t from = i ^ ((int64_t)1 << h);
+    return rhd_ag_base(w, h) + from * rhd_ag_len(w, h) + (q - ((from >> h) << h) * w->C);
+}
+
+/* ---- double binary tree all-reduce (Jeaugey, cited in Sec. 1)
+ * Half t of the buffer (H lines) is reduced up tree t to its root and then
+ * broadcast down it.  Both trees have one shape over positions 0..p-1:
+ * position 0 is the root; any other position u with lowest set bit b hangs
+ * below u with bit b cleared and bit 2b set, when that is a position, else
+ * below u with bit b cleared (the in-order binary tree).  Tree 0
+ * puts participant i at position i, tree 1 at position p-1-i, so the leaves
+ * of one are inner nodes of the other.
+ * Edge e of tree t joins its non-root participant c (e = c-1 in tree 0, c in
+ * tree 1) to the parent.  ids: ((phase*2 + t)(p-1) + e) H + j, phase 0 =
+ * reduce (c -> parent), 1 = broadcast (parent -> c).
+ * A reduce line waits for the same line from each child; a broadcast line
+ * from the root waits for the same line from each child of the root, from
+ * any other node for the same line broadcast to it. */
+static int64_t dbt_parent_pos(int64_t u, int64_t p)
+{
+    if (u == 0) return -1;
+    int64_t b = u & -u;
+    int64_t up = (u - b) | (2 * b);
+    return up < p ? up : u - b;
+}
+static int64_t dbt_pos(int64_t i, int t, int64_t p) { return t == 0 ? i : p - 1 - i; }  /* its own inverse */
+static int64_t dbt_edge(int64_t c, int t) { return t == 0 ? c - 1 : c; }
+static int64_t dbt_edge_part(int64_t e, int t) { return t == 0 ? e + 1 : e; }
+
+/* Message of a line (chunk mode): one step's transfer between two
+ * participants, a contiguous id range. */
+static int64_t msg_of(const work_t *w, int64_t x)
+{
+    if (w->coll == COLL_DBT) return x / w->H;
+    if (w->coll == COLL_RHD) {
+        if (x < rhd_ag_base(w, 0)) {
+            int32_t j = 0;
+            while (j + 1 < w->K && x >= rhd_rs_base(w, j + 1)) j++;
+            return (int64_t)j * w->p + (x - rhd_rs_base(w, j)) / rhd_rs_len(w, j);
+        }
+        int32_t j = 0;
+        while (j + 1 < w->K && x >= rhd_ag_base(w, j + 1)) j++;
+        return (int64_t)(w->K + j) * w->p + (x - rhd_ag_base(w, j)) / rhd_ag_len(w, j);
+    }
+    return x / w->C;
+}
+static int64_t msg_count(const work_t *w)
+{
+    if (w->coll == COLL_DBT) return w->T / w->H;
+    if (w->coll == COLL_RHD) return 2 * (int64_t)w->K * w->p;
+    return w->T / w->C;
+}
+static int64_t msg_first(const work_t *w, int64_t m)
+{
+    if (w->coll == COLL_DBT) return m * w->H;
+    if (w->coll == COLL_RHD) {
+        int32_t j = (int32_t)(m / w->p);
+        int64_t i = m % w->p;
+        if (j < w->K) return rhd_rs_base(w, j) + i * rhd_rs_len(w, j);
+        return rhd_ag_base(w, j - w->K) + i * rhd_ag_len(w, j - w->K);
+    }
+    return m * w->C;
+}
+static int64_t msg_len(const work_t *w, int64_t m)
+{
+    if (w->coll == COLL_DBT) return w->H;
+    if (w->coll == COLL_RHD) {
+        int32_t j = (int32_t)(m / w->p);
+        return j < w->K ? rhd_rs_len(w, j) : rhd_ag_len(w, j - w->K);
+    }
+    return w->C;
+}
 
 /* Decode transaction x into (src, dst) and its predecessor list.
  * Returns the number of predecessors written to preds (at most 64 for the
@@ -255,9 +394,11 @@ static int32_t decode(const work_t *w, int64_t x, int32_t *src, int32_t *dst, in
         for (int64_t q = w->pptr[x]; q < w->pptr[x + 1]; q++) preds[np++] = w->pidx[q];
         return np;
     }
-    if (w->coll == COLL_RING) {
+    if (w->coll == COLL_RING || w->coll == COLL_RING_AG || w->coll == COLL_RING_RS) {
         /* id = (s*p + i)*C + j; sends rho(i) -> rho(i+1); waits for the same
-         * line of the previous step received from rho(i-1). */
+         * line of the previous step received from rho(i-1).  All-reduce runs
+         * 2(p-1) steps; reduce-scatter and all-gather p-1, whose dependency
+         * structure is the same (the reduction itself costs no time). */
         int64_t p = w->p, C = w->C;
         int64_t j = x % C, q = x / C, i = q % p, s = q / p;
         *src = rho_of(w, i); *dst = rho_of(w, (i + 1) % p);
@@ -340,6 +481,73 @@ static int32_t decode(const work_t *w, int64_t x, int32_t *src, int32_t *dst, in
         preds[np++] = w->B2 + ((s * M + r) * G + dm) * C2 + jj;
         return np;
     }
+    if (w->coll == COLL_DIRECT_AG || w->coll == COLL_DIRECT_RS) {
+        /* id = ((k-1)*p + i)*C + j; rho(i) -> rho(i+k), no predecessors: in
+         * reduce-scatter i sends its part of chunk i+k to that chunk's owner,
+         * in all-gather its own chunk to every peer. */
+        int64_t p = w->p, C = w->C;
+        int64_t q = x / C, i = q % p, k = q / p + 1;
+        *src = rho_of(w, i); *dst = rho_of(w, (i + k) % p);
+        return 0;
+    }
+    if (w->coll == COLL_RHD) {
+        int64_t p = w->p, C = w->C;
+        int32_t K = w->K;
+        if (x < rhd_ag_base(w, 0)) {
+            int32_t j = 0;
+            while (j + 1 < K && x >= rhd_rs_base(w, j + 1)) j++;
+            int64_t y = x - rhd_rs_base(w, j), S = rhd_rs_len(w, j);
+            int64_t i = y / S, q = rhd_rs_send_start(w, i, j) + y % S;
+            *src = rho_of(w, i); *dst = rho_of(w, i ^ (p >> (j + 1)));
+            for (int32_t j2 = 0; j2 < j; j2++)
+                preds[np++] = w->dep == DEP_CHUNK ? -1 - ((int64_t)j2 * p + (i ^ (p >> (j2 + 1))))
+                                                  : rhd_rs_arrival(w, i, j2, q);
+            return np;
+        }
+        int32_t j = 0;
+        while (j + 1 < K && x >= rhd_ag_base(w, j + 1)) j++;
+        int64_t y = x - rhd_ag_base(w, j), A = rhd_ag_len(w, j);
+        int64_t i = y / A, q = ((i >> j) << j) * C + y % A;
+        *src = rho_of(w, i); *dst = rho_of(w, i ^ ((int64_t)1 << j));
+        if (w->dep == DEP_CHUNK) {
+            for (int32_t j2 = 0; j2 < K; j2++) preds[np++] = -1 - ((int64_t)j2 * p + (i ^ (p >> (j2 + 1))));
+            for (int32_t h = 0; h < j; h++) preds[np++] = -1 - ((int64_t)(K + h) * p + (i ^ ((int64_t)1 << h)));
+            return np;
+        }
+        int64_t c = q / C;
+        if (c == i) {
+            for (int32_t j2 = 0; j2 < K; j2++) preds[np++] = rhd_rs_arrival(w, i, j2, q);
+        } else {
+            int32_t h = 0;
+            while ((c ^ i) >> (h + 1)) h++;   /* highest differing bit */
+            preds[np++] = rhd_ag_arrival(w, i, h, q);
+        }
+        return np;
+    }
+    if (w->coll == COLL_DBT) {
+        int64_t p = w->p, H = w->H;
+        int64_t j = x % H, q = x / H, e = q % (p - 1);
+        q /= p - 1;
+        int t = (int)(q % 2), ph = (int)(q / 2);
+        int64_t c = dbt_edge_part(e, t);
+        int64_t vpos = dbt_parent_pos(dbt_pos(c, t, p), p);
+        int64_t v = dbt_pos(vpos, t, p);
+        *src = rho_of(w, ph == 0 ? c : v);
+        *dst = rho_of(w, ph == 0 ? v : c);
+        /* reduce: children of c; broadcast from the root: children of the root */
+        int64_t gather = ph == 0 ? dbt_pos(c, t, p) : (vpos == 0 ? 0 : -1);
+        if (gather >= 0) {
+            for (int64_t u = 1; u < p; u++)
+                if (dbt_parent_pos(u, p) == gather) {
+                    int64_t mm = (int64_t)t * (p - 1) + dbt_edge(dbt_pos(u, t, p), t);
+                    preds[np++] = w->dep == DEP_CHUNK ? -1 - mm : mm * H + j;
+                }
+        } else {
+            int64_t mm = ((int64_t)2 + t) * (p - 1) + dbt_edge(v, t);
+            preds[np++] = w->dep == DEP_CHUNK ? -1 - mm : mm * H + j;
+        }
+        return np;
+    }
     /* all-to-all, linear shift: id = ((k-1)*E + i)*C + j; i -> i+k */
     {
         int64_t E = w->E, C = w->C;
@@ -420,11 +628,11 @@ static const hcache_t *head_info(hcache_t *c, int64_t *slot, const work_t *w, ui
 }
 
 /* rel(x) = max completion over predecessors; "never" while any is pending.
- * A whole-chunk predecessor is complete once all C of its lines are; its
+ * A whole-message predecessor is complete once all its lines are; its
  * completion is the latest of theirs (counted in chunk_done / chunk_max as
  * lines complete). */
 static uint64_t release_of(const hcache_t *c, const uint32_t *completion, const int64_t *chunk_done,
-                           const uint32_t *chunk_max, int64_t C)
+                           const uint32_t *chunk_max, const work_t *w)
 {
     uint64_t rel = 0;
     for (int32_t q = 0; q < c->np; q++) {
@@ -434,7 +642,7 @@ static uint64_t release_of(const hcache_t *c, const uint32_t *completion, const 
             v = completion[p];
             if (v == NEVER) return UINT64_MAX;
         } else {
-            if (chunk_done[-1 - p] < C) return UINT64_MAX;
+            if (chunk_done[-1 - p] < msg_len(w, -1 - p)) return UINT64_MAX;
             v = chunk_max[-1 - p];
         }
         if (v > rel) rel = v;
@@ -495,8 +703,8 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
         if (rc) return rc;
     }
     int64_t T = w.T;
-    /* chunk mode: lines completed per chunk and the latest completion */
-    int64_t nchunks = (w.dep == DEP_CHUNK && w.C > 0) ? T / w.C : 0;
+    /* chunk mode: lines completed per message and the latest completion */
+    int64_t nchunks = (w.dep == DEP_CHUNK && T > 0) ? msg_count(&w) : 0;
     int64_t *chunk_done = nchunks ? calloc((size_t)nchunks, sizeof(int64_t)) : NULL;
     uint32_t *chunk_max = nchunks ? calloc((size_t)nchunks, sizeof(uint32_t)) : NULL;
 
@@ -529,9 +737,11 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     int64_t *s_cur = calloc((size_t)m, sizeof(int64_t));
     int64_t *preds = malloc(sizeof(int64_t) * 4096);
     int64_t line_hops = 0;
+    int32_t maxp = 1;   /* most predecessors of any line (sizes the head cache) */
     for (int64_t x = 0; x < T; x++) {
         int32_t s, d;
-        decode(&w, x, &s, &d, preds);
+        int32_t np = decode(&w, x, &s, &d, preds);
+        if (np > maxp) maxp = np;
         int64_t f0 = path_ptr[(int64_t)s * E + d];
         if (path_ptr[(int64_t)s * E + d + 1] == f0) {   /* needed pair without a path */
             rc = OR_ERR_UNREACHABLE;
@@ -578,9 +788,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     int32_t *src_first = malloc(sizeof(int32_t) * (size_t)2 * m);
     int32_t *src_cnt = calloc((size_t)2 * m, sizeof(int32_t));
     /* decoded stream heads (re-used while a head waits) */
-    int32_t maxp = (w.coll == COLL_RING) ? 1 : (w.coll == COLL_DIRECT) ? w.p - 1
-                 : (w.coll == COLL_HIER) ? (int32_t)w.M : 0;  /* custom heads allocate their own */
-    if (maxp < 1) maxp = 1;
+    if (w.coll == COLL_CUSTOM) maxp = 1;  /* custom heads allocate their own */
     hcache_t *hcache = malloc(sizeof(hcache_t) * (size_t)m * bmax);
     int64_t *hpred = malloc(sizeof(int64_t) * (size_t)m * bmax * maxp);
     for (size_t i = 0; i < (size_t)m * bmax; i++) { hcache[i].x = NEVER; hcache[i].preds = NULL; }
@@ -632,7 +840,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                 uint32_t x = s_list[s_ptr[f] + s_cur[f] + k];
                 const hcache_t *hc = head_info(&hcache[(size_t)f * bmax + k], hpred + ((size_t)f * bmax + k) * maxp,
                                                &w, x, path_ptr, E);
-                uint64_t rel = release_of(hc, completion, chunk_done, chunk_max, w.C);
+                uint64_t rel = release_of(hc, completion, chunk_done, chunk_max, &w);
                 if (rel > t) break;
                 req_t *r = &reqs[nr++];
                 r->src = sid; r->k = k; r->x = x;
@@ -720,7 +928,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                     completion[r->x] = (uint32_t)(t + 1);
                     remaining--;
                     if (chunk_done) {
-                        int64_t ch = (int64_t)r->x / w.C;
+                        int64_t ch = msg_of(&w, (int64_t)r->x);
                         chunk_done[ch]++;
                         if ((uint32_t)(t + 1) > chunk_max[ch]) chunk_max[ch] = (uint32_t)(t + 1);
                     }
@@ -764,7 +972,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                 uint32_t x = s_list[s_ptr[f] + s_cur[f] + k];
                 const hcache_t *hc = head_info(&hcache[(size_t)f * bmax + k], hpred + ((size_t)f * bmax + k) * maxp,
                                                &w, x, path_ptr, E);
-                uint64_t rel = release_of(hc, completion, chunk_done, chunk_max, w.C);
+                uint64_t rel = release_of(hc, completion, chunk_done, chunk_max, &w);
                 if (rel > t) { if (rel < next) next = rel; break; }
             }
         }
@@ -792,9 +1000,9 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
             int32_t np = decode(&w, x, &s, &d, preds);
             uint64_t rel = 0;
             for (int32_t q = 0; q < np; q++) {
-                /* a whole-chunk predecessor: the latest of its C lines */
-                int64_t lo = preds[q] >= 0 ? preds[q] : (-1 - preds[q]) * w.C;
-                int64_t hi = preds[q] >= 0 ? preds[q] + 1 : lo + w.C;
+                /* a whole-message predecessor: the latest of its lines */
+                int64_t lo = preds[q] >= 0 ? preds[q] : msg_first(&w, -1 - preds[q]);
+                int64_t hi = preds[q] >= 0 ? preds[q] + 1 : lo + msg_len(&w, -1 - preds[q]);
                 for (int64_t y = lo; y < hi; y++)
                     if (completion[y] > rel) rel = completion[y];
             }

@@ -31,6 +31,12 @@ COLL_RING_ALLREDUCE = 0
 COLL_DIRECT_ALLREDUCE = 1
 COLL_HIER_ALLREDUCE = 2
 COLL_ALLTOALL = 3
+COLL_RING_ALLGATHER = 4
+COLL_RING_REDUCESCATTER = 5
+COLL_DIRECT_ALLGATHER = 6
+COLL_DIRECT_REDUCESCATTER = 7
+COLL_RHD_ALLREDUCE = 8      # recursive halving-doubling, power-of-two participants
+COLL_DBT_ALLREDUCE = 9      # double binary tree
 
 DEP_LINE = 0   # a step's line waits for the matching line of the step before
 DEP_CHUNK = 1  # a step's line waits for the whole chunk of the step before
