@@ -57,23 +57,67 @@ typedef enum {
 
 typedef enum { SIM_ARB_LOWEST_ID = 0, SIM_ARB_ROUND_ROBIN = 1 } sim_arb;
 
-/* Collectives (the paper's textbook algorithms, Sec. 1; the hierarchical
- * form composes direct and ring steps over scale-up domains).  Transaction
- * ids are step-major so that lowest-id arbitration favours earlier steps. */
+/* Collectives (the paper's textbook algorithms, Sec. 1 and 2.2: ring,
+ * all-pairs (direct), double binary tree and recursive halving-doubling; the
+ * hierarchical form composes direct and ring steps over scale-up domains).
+ * p = participants = all endpoints; participant i is endpoint order[i].
+ * Transaction ids are step-major (a mixed-radix number whose leading digit
+ * is the step), so that lowest-id arbitration favours earlier steps; a
+ * message is one step's transfer between two participants.
+ *
+ *   RING_*          step s, participant i sends C = N/p lines to i+1; id
+ *                   (s p + i) C + j.  Line j of step s >= 1 waits for line j
+ *                   that i received at step s-1.  All-reduce: 2(p-1) steps;
+ *                   reduce-scatter and all-gather: p-1 steps (the same DAG:
+ *                   a reduction costs no time).
+ *   DIRECT_ALLREDUCE  reduce-scatter: i sends chunk i+k to i+k (k = 1..p-1),
+ *                   then all-gather: i sends its reduced chunk i to i+k, line
+ *                   j waiting for line j of every reduce-scatter chunk into i;
+ *                   id ((phase (p-1) + k-1) p + i) C + j.
+ *   DIRECT_ALLGATHER / _REDUCESCATTER  one all-pairs exchange, id
+ *                   ((k-1) p + i) C + j, no waits.
+ *   RHD_ALLREDUCE   p = 2^K.  Halving step j = 0..K-1: partner i ^ (p >>
+ *                   (j+1)); i keeps the half of its block chosen by that bit
+ *                   of i and sends the other N >> (j+1) lines, id p(N - 2S) +
+ *                   i S + o.  Doubling step j: partner i ^ (1 << j); i sends
+ *                   its block of 2^j chunks (starting at chunk (i >> j) << j),
+ *                   id N(p-1) + N(2^j - 1) + i 2^j C + o.  A sent position
+ *                   waits for every earlier arrival of it at the sender.
+ *   DBT_ALLREDUCE   half t of the buffer (H = N/2 lines) is reduced up and
+ *                   broadcast down tree t.  Tree shape over positions: 0 is
+ *                   the root; position u with lowest set bit b hangs below u
+ *                   with bit b cleared and bit 2b set if that is < p, else
+ *                   below u with bit b cleared.  Tree 0 puts participant i at
+ *                   position i, tree 1 at p-1-i.  Edge e joins non-root
+ *                   participant c (e = c-1 in tree 0, c in tree 1) to its
+ *                   parent; id ((phase 2 + t)(p-1) + e) H + j, phase 0 = reduce
+ *                   (c -> parent, waits for line j from each child), 1 =
+ *                   broadcast (parent -> c, waits for line j from each child
+ *                   of the root if the parent is the root, else for line j
+ *                   broadcast to the parent).
+ *   HIER_ALLREDUCE  see sim_load_collective.
+ *   ALLTOALL        i sends N lines to i+k (k = 1..p-1), id ((k-1) p + i) N + j.
+ */
 typedef enum {
-    SIM_COLL_RING_ALLREDUCE = 0,   /* reduce-scatter + all-gather ring, 2(p-1) steps */
-    SIM_COLL_DIRECT_ALLREDUCE = 1, /* all-pairs reduce-scatter then all-gather       */
-    SIM_COLL_HIER_ALLREDUCE = 2,   /* direct RS in domain, ring per rail, direct AG  */
-    SIM_COLL_ALLTOALL = 3          /* linear-shift all-to-all                        */
+    SIM_COLL_RING_ALLREDUCE = 0,       /* reduce-scatter + all-gather ring, 2(p-1) steps */
+    SIM_COLL_DIRECT_ALLREDUCE = 1,     /* all-pairs reduce-scatter then all-gather       */
+    SIM_COLL_HIER_ALLREDUCE = 2,       /* direct RS in domain, ring per rail, direct AG  */
+    SIM_COLL_ALLTOALL = 3,             /* linear-shift all-to-all                        */
+    SIM_COLL_RING_ALLGATHER = 4,       /* p-1 ring steps                                 */
+    SIM_COLL_RING_REDUCESCATTER = 5,   /* p-1 ring steps                                 */
+    SIM_COLL_DIRECT_ALLGATHER = 6,     /* one all-pairs exchange                         */
+    SIM_COLL_DIRECT_REDUCESCATTER = 7, /* one all-pairs exchange                         */
+    SIM_COLL_RHD_ALLREDUCE = 8,        /* recursive halving-doubling, p a power of two   */
+    SIM_COLL_DBT_ALLREDUCE = 9         /* double binary tree                             */
 } sim_coll;
 
 /* Granularity of the step-to-step dependencies of a collective (Sec. 4.2
  * and 5.2 contrast get-style transfers, which overlap steps line by line,
- * with put + signal, where a step waits for the signal that the whole chunk
- * of the step before has arrived). */
+ * with put + signal, where a step waits for the signal that the whole
+ * message of the step before has arrived). */
 typedef enum {
-    SIM_DEP_LINE = 0,  /* line j of a step waits for line j of each predecessor chunk */
-    SIM_DEP_CHUNK = 1  /* every line of a step waits for all lines of each predecessor chunk */
+    SIM_DEP_LINE = 0,  /* a line waits for the lines that brought its data to the sender */
+    SIM_DEP_CHUNK = 1  /* a message waits for every message that delivers any of its data */
 } sim_dep;
 
 /* Limits checked by sim_create. */
@@ -106,18 +150,19 @@ sim_status sim_create(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_p
 /*
  * Load a collective (replaces any previous workload).
  *   coll       : sim_coll.
- *   bytes      : per endpoint (all-reduce) or per ordered pair (all-to-all);
- *                must be a multiple of 128 B times the collective's chunk
- *                divisor (p for ring/direct, M*G for hierarchical), else
- *                SIM_ERR_SIZE.
+ *   bytes      : N * 128: the buffer per endpoint (all-reduce; the input of
+ *                reduce-scatter; the output of all-gather) or per ordered
+ *                pair (all-to-all).  N must divide by the collective's chunk
+ *                divisor (p for ring/direct/RHD, 2 for DBT, M*G for
+ *                hierarchical), else SIM_ERR_SIZE.
  *   group_size : hierarchical only: endpoints per domain M (endpoint d*M + r);
  *                0 otherwise.
- *   order      : ring/direct: participant order, a permutation of the
- *                endpoints (NULL = rank order); must be NULL otherwise.
- *   dep        : sim_dep.  SIM_DEP_CHUNK is defined for ring and direct
- *                all-reduce (and is a no-op for all-to-all, which has no
- *                dependencies); hierarchical all-reduce takes SIM_DEP_LINE
- *                only (SIM_ERR_INVALID_ARG otherwise).
+ *   order      : participant order, a permutation of the endpoints (NULL =
+ *                rank order); must be NULL for hierarchical and all-to-all.
+ *                RHD needs a power-of-two endpoint count (SIM_ERR_INVALID_ARG).
+ *   dep        : sim_dep.  Hierarchical all-reduce takes SIM_DEP_LINE only
+ *                (SIM_ERR_INVALID_ARG otherwise); for collectives without
+ *                waits the two are the same.
  * Builds the routes of every flow used (SIM_ERR_UNREACHABLE if one has no
  * path), the injection streams and the predecessor tables, and uploads them.
  */

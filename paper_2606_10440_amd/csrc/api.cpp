@@ -182,6 +182,97 @@ struct Ranges {
 
 inline int64_t wrap(int64_t a, int64_t m) { return ((a % m) + m) % m; }
 
+// Recursive halving-doubling all-reduce over p = 2^K participants.  Range
+// layout: halving step j, participant i -> range j p + i (one message);
+// doubling step j, participant i -> one range per chunk of its block, so that
+// each range's data arrived in one piece (every range has single-range
+// predecessors).  In per-message mode every range of a message waits for the
+// last range of each message that feeds the message.
+sim_status expand_rhd(sim_ctx *c, int64_t N, const std::vector<int32_t> &rho, Ranges &R) {
+    const int64_t p = (int64_t)rho.size();
+    if (p & (p - 1)) return fail(c, SIM_ERR_INVALID_ARG, "recursive halving-doubling needs a power-of-two endpoint count");
+    if (N % p) return fail(c, SIM_ERR_SIZE, "recursive halving-doubling: lines not divisible by participants");
+    int K = 0;
+    while ((int64_t(1) << K) < p) K++;
+    const int64_t C = N / p;
+    auto half = [&](int j) { return N >> (j + 1); };
+    // first position of the half participant i sends at halving step j
+    auto send_start = [&](int64_t i, int j) {
+        const int64_t S = half(j);
+        return (i >> (K - j)) * 2 * S + (((i >> (K - 1 - j)) & 1) ? 0 : S);
+    };
+    auto rs_range = [&](int j, int64_t i) { return (int64_t)j * p + i; };
+    // range of doubling step j, participant i, chunk ch (within i's block)
+    auto ag_range = [&](int j, int64_t i, int64_t ch) {
+        return (int64_t)K * p + p * ((int64_t(1) << j) - 1) + (i << j) + (ch - ((i >> j) << j));
+    };
+    auto ag_last = [&](int j, int64_t i) { return ag_range(j, i, ((i >> j) << j) + (int64_t(1) << j) - 1); };
+    for (int j = 0; j < K; j++) {
+        const int64_t S = half(j);
+        for (int64_t i = 0; i < p; i++) {
+            R.add(p * (N - 2 * S) + i * S, S, rho[i], rho[i ^ (p >> (j + 1))]);
+            for (int j2 = 0; j2 < j; j2++) {
+                const int64_t from = i ^ (p >> (j2 + 1));
+                R.pred(rs_range(j2, from), R.whole ? 0 : send_start(i, j) - send_start(from, j2));
+            }
+        }
+    }
+    const int64_t TRS = N * (p - 1);
+    for (int j = 0; j < K; j++) {
+        for (int64_t i = 0; i < p; i++) {
+            const int64_t b0 = (i >> j) << j;
+            for (int64_t ch = b0; ch < b0 + (int64_t(1) << j); ch++) {
+                R.add(TRS + N * ((int64_t(1) << j) - 1) + (i << j) * C + (ch - b0) * C, C, rho[i], rho[i ^ (int64_t(1) << j)]);
+                if (R.whole) {
+                    for (int j2 = 0; j2 < K; j2++) R.pred(rs_range(j2, i ^ (p >> (j2 + 1))), 0);
+                    for (int h = 0; h < j; h++) R.pred(ag_last(h, i ^ (int64_t(1) << h)), 0);
+                } else if (ch == i) {
+                    // the reduced chunk: every halving-step arrival of it
+                    for (int j2 = 0; j2 < K; j2++) {
+                        const int64_t from = i ^ (p >> (j2 + 1));
+                        R.pred(rs_range(j2, from), ch * C - send_start(from, j2));
+                    }
+                } else {
+                    // arrived at the doubling step of the highest bit where ch and i differ
+                    int h = 0;
+                    while ((ch ^ i) >> (h + 1)) h++;
+                    R.pred(ag_range(h, i ^ (int64_t(1) << h), ch), 0);
+                }
+            }
+        }
+    }
+    return SIM_OK;
+}
+
+// Double binary tree all-reduce: one range per message, range index =
+// (phase 2 + tree)(p - 1) + edge.
+void expand_dbt(int64_t p, int64_t H, const std::vector<int32_t> &rho, Ranges &R) {
+    auto parent = [&](int64_t u) -> int64_t {
+        const int64_t b = u & -u;
+        const int64_t up = (u - b) | (2 * b);
+        return up < p ? up : u - b;
+    };
+    std::vector<std::vector<int64_t>> kids(p);
+    for (int64_t u = 1; u < p; u++) kids[parent(u)].push_back(u);
+    auto part = [&](int64_t pos, int t) { return t == 0 ? pos : p - 1 - pos; };  // position <-> participant
+    auto edge = [&](int64_t part_c, int t) { return t == 0 ? part_c - 1 : part_c; };
+    auto msg = [&](int ph, int t, int64_t e) { return ((int64_t)ph * 2 + t) * (p - 1) + e; };
+    for (int ph = 0; ph < 2; ph++)
+        for (int t = 0; t < 2; t++)
+            for (int64_t e = 0; e < p - 1; e++) {
+                const int64_t cpart = t == 0 ? e + 1 : e;
+                const int64_t cpos = part(cpart, t);
+                const int64_t vpos = parent(cpos), vpart = part(vpos, t);
+                R.add(msg(ph, t, e) * H, H, rho[ph == 0 ? cpart : vpart], rho[ph == 0 ? vpart : cpart]);
+                if (ph == 0 || vpos == 0) {
+                    // reduce: the children of c; broadcast from the root: the root's children
+                    for (int64_t u : kids[ph == 0 ? cpos : 0]) R.pred(msg(0, t, edge(part(u, t), t)), 0);
+                } else {
+                    R.pred(msg(1, t, edge(vpart, t)), 0);
+                }
+            }
+}
+
 sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t group,
                              const int32_t *order, int32_t dep, Ranges &R) {
     const int64_t E = c->E;
@@ -195,8 +286,8 @@ sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t g
     std::vector<int32_t> rho(E);
     for (int64_t i = 0; i < E; i++) rho[i] = (int32_t)i;
     if (order) {
-        if (coll != SIM_COLL_RING_ALLREDUCE && coll != SIM_COLL_DIRECT_ALLREDUCE)
-            return fail(c, SIM_ERR_INVALID_ARG, "order applies to ring/direct only");
+        if (coll == SIM_COLL_HIER_ALLREDUCE || coll == SIM_COLL_ALLTOALL)
+            return fail(c, SIM_ERR_INVALID_ARG, "order does not apply to the hierarchical all-reduce or all-to-all");
         std::vector<char> seen(E, 0);
         for (int64_t i = 0; i < E; i++) {
             if (order[i] < 0 || order[i] >= E || seen[order[i]])
@@ -275,6 +366,27 @@ sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t g
         const int64_t C = N;
         for (int64_t k = 1; k < E; k++)
             for (int64_t i = 0; i < E; i++) R.add(((k - 1) * E + i) * C, C, (int32_t)i, (int32_t)((i + k) % E));
+    } else if (coll == SIM_COLL_RING_ALLGATHER || coll == SIM_COLL_RING_REDUCESCATTER) {
+        const int64_t p = E;
+        if (N % p) return fail(c, SIM_ERR_SIZE, "ring: lines not divisible by participants");
+        const int64_t C = N / p;
+        for (int64_t s = 0; s < p - 1; s++)
+            for (int64_t i = 0; i < p; i++) {
+                R.add((s * p + i) * C, C, rho[i], rho[(i + 1) % p]);
+                if (s > 0) R.pred((s - 1) * p + wrap(i - 1, p), 0);
+            }
+    } else if (coll == SIM_COLL_DIRECT_ALLGATHER || coll == SIM_COLL_DIRECT_REDUCESCATTER) {
+        const int64_t p = E;
+        if (N % p) return fail(c, SIM_ERR_SIZE, "direct: lines not divisible by participants");
+        const int64_t C = N / p;
+        for (int64_t k = 1; k < p; k++)
+            for (int64_t i = 0; i < p; i++) R.add(((k - 1) * p + i) * C, C, rho[i], rho[(i + k) % p]);
+    } else if (coll == SIM_COLL_RHD_ALLREDUCE) {
+        const sim_status st = expand_rhd(c, N, rho, R);
+        if (st != SIM_OK) return st;
+    } else if (coll == SIM_COLL_DBT_ALLREDUCE) {
+        if (N % 2) return fail(c, SIM_ERR_SIZE, "double binary tree: lines not divisible by 2");
+        expand_dbt(E, N / 2, rho, R);
     } else {
         return fail(c, SIM_ERR_INVALID_ARG, "unknown collective");
     }

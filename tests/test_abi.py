@@ -113,7 +113,7 @@ def test_load_errors_before_device(simlib):
                 simlib.sim_load_collective(ctx, si.COLL_RING_ALLREDUCE, nbytes)
             assert e.value.status == simlib.SIM_ERR_SIZE
         with pytest.raises(simlib.SimError) as e:
-            simlib.sim_load_collective(ctx, 9, 1024)
+            simlib.sim_load_collective(ctx, 42, 1024)
         assert e.value.status == simlib.SIM_ERR_INVALID_ARG
         with pytest.raises(simlib.SimError) as e:
             simlib.sim_load_collective(ctx, si.COLL_RING_ALLREDUCE, 1024, order=[0, 1, 2, 3, 4, 5, 6, 6])
@@ -124,6 +124,18 @@ def test_load_errors_before_device(simlib):
         with pytest.raises(simlib.SimError) as e:
             simlib.sim_load_collective(ctx, si.COLL_HIER_ALLREDUCE, 1024, 4, dep=si.DEP_CHUNK)  # not defined
         assert e.value.status == simlib.SIM_ERR_INVALID_ARG and "hierarchical" in str(e.value)
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_collective(ctx, si.COLL_DBT_ALLREDUCE, 128 * 7)                     # odd buffer
+        assert e.value.status == simlib.SIM_ERR_SIZE
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_collective(ctx, si.COLL_RHD_ALLREDUCE, 128 * 12)                    # 12 over 8
+        assert e.value.status == simlib.SIM_ERR_SIZE
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_collective(ctx, si.COLL_ALLTOALL, 128, order=list(range(8)))        # no order
+        assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_collective(ctx, 10, 1024)                                            # unknown
+        assert e.value.status == simlib.SIM_ERR_INVALID_ARG
         with pytest.raises(simlib.SimError) as e:
             simlib.sim_run(ctx, 0, 0, 0, 0, 0)
         assert e.value.status == simlib.SIM_ERR_STATE
@@ -140,5 +152,16 @@ def test_load_errors_before_device(simlib):
         with pytest.raises(simlib.SimError) as e:
             simlib.sim_load_transactions(ctx, [0], [0], [0, 0], [])
         assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+    finally:
+        simlib.sim_destroy(ctx)
+
+
+def test_rhd_needs_power_of_two(simlib):
+    w = si.full_mesh(6, coll=si.COLL_RHD_ALLREDUCE, nbytes=128 * 12)
+    ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, w.arb)
+    try:
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_collective(ctx, si.COLL_RHD_ALLREDUCE, 128 * 12)
+        assert e.value.status == simlib.SIM_ERR_INVALID_ARG and "power-of-two" in str(e.value)
     finally:
         simlib.sim_destroy(ctx)

@@ -433,3 +433,39 @@ def test_chunk_rejected_for_hierarchical(simmod):
             s.load_collective(si.COLL_RING_ALLREDUCE, 128 * 64, 0, None, 2)
     finally:
         s.close()
+
+
+# ------------------------------------------------------- further collectives
+# Ring and direct all-gather / reduce-scatter, recursive halving-doubling and
+# double binary tree all-reduce, per line and per message.
+
+MORE = [si.COLL_RING_ALLGATHER, si.COLL_RING_REDUCESCATTER, si.COLL_DIRECT_ALLGATHER,
+        si.COLL_DIRECT_REDUCESCATTER, si.COLL_RHD_ALLREDUCE, si.COLL_DBT_ALLREDUCE]
+
+
+@pytest.mark.parametrize("engine", ENGINES)
+@pytest.mark.parametrize("coll", MORE)
+@pytest.mark.parametrize("dep", [0, 1])
+def test_more_collectives_mesh(simmod, oracle_lib, engine, coll, dep):
+    b = 1 if engine == "b1" else 2
+    w = si.full_mesh(4, b=b, L=5, cap=b * 3, coll=coll, nbytes=128 * 4 * 6)
+    w.dep = dep
+    assert check_engine(simmod, oracle_lib, w, engine) == 1
+
+
+@pytest.mark.parametrize("engine", ENGINES)
+@pytest.mark.parametrize("coll", MORE)
+@pytest.mark.parametrize("dep", [0, 1])
+def test_more_collectives_torus(simmod, oracle_lib, engine, coll, dep):
+    bws = (1,) if engine == "b1" else (1, 2, 4)
+    w = si.torus2d(4, 4, n_scenarios=5, seed=90 + coll + 16 * dep, bws=bws, lat_lo=1, lat_hi=25,
+                   depths=(1, 2, 3, 7, 32), nbytes=128 * 16 * 4, arb=(coll + dep) % 2, coll=coll)
+    w.dep = dep
+    check_engine(simmod, oracle_lib, w, engine)
+
+
+@pytest.mark.parametrize("coll", MORE)
+def test_more_collectives_fat_tree_ordered(simmod, oracle_lib, coll):
+    w = si.fat_tree(4, nbytes=128 * 16 * 2, cap=5, lat_lo=2, lat_hi=9, arb=1, coll=coll)
+    w.order = np.random.default_rng(coll).permutation(16).astype(np.int32)
+    check_vs_oracle(simmod, oracle_lib, w)
