@@ -5,9 +5,9 @@ every line of every scenario advanced hop by hop to completion, inputs and
 state resident in HBM.  The default workload is the batched design sweep
 (4096 scenarios of a 4x4 torus, ring all-reduce of 4 MiB per endpoint,
 seeded bandwidth/latency/depth per scenario), the largest workload by
-line-hop events; ``--workload C1..C4`` selects the others, and a
-``_chunk`` suffix (C1, C2, C5) the same workload with per-chunk step
-dependencies.
+line-hop events; ``--workload C1..C4`` selects the others, a ``_chunk``
+suffix (C1, C2, C5) the same workload with per-chunk step dependencies, and
+C5_rhd / C5_dbt / C5_ag the batched sweep with another collective.
 
 Prints one JSON line with the metric, a roofline entry for the engine
 kernel (algorithmic bytes per launch / measured launch time vs the 8 TB/s
@@ -40,6 +40,9 @@ DESCR = {
 }
 for _k in ("C1", "C2", "C5"):
     DESCR[_k + "_chunk"] = DESCR[_k] + "; per-chunk (put + signal) step dependencies"
+for _k, _c in (("rhd", "recursive halving-doubling all-reduce"), ("dbt", "double binary tree all-reduce"),
+               ("ag", "ring all-gather")):
+    DESCR["C5_" + _k] = DESCR["C5"].replace("ring all-reduce", _c)
 
 
 def algorithmic_bytes(T: int, S: int, m: int) -> int:

@@ -569,12 +569,13 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     constexpr int32_t kWaveBlocks = 256;           // compute units of the device
     {
         std::vector<std::vector<int32_t>> lflows(nl);
-        bool ok = nl >= 1 && nl <= 63 && T < (1ll << 25) - 1 && bm <= 8;
+        bool ok = nl >= 1 && nl <= 64 && T < (1ll << 25) - 1 && bm <= 8;
         for (int32_t f = 0; ok && f < nflows; f++)
             for (int64_t q = c->flow_path[f]; ok && c->path_link[q] >= 0; q++) {
                 auto &v = lflows[link_lane[c->path_link[q]]];
                 v.push_back(f);
                 if (v.size() > 4) ok = false;
+                if (c->path_link[q + 1] == c->path_link[q]) ok = false;  // the sink encoding needs this
             }
         int32_t maxfeed = 0;
         for (int32_t i = 0; i < nl; i++) maxfeed = std::max(maxfeed, (int32_t)feeders[i].size());
@@ -587,8 +588,9 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                 const auto &v = lflows[lane];
                 return (int32_t)(std::find(v.begin(), v.end(), f) - v.begin());
             };
-            // byte q of wv_lfb: local index at the next lane << 6 | next lane (63:
-            // the line leaves the network); byte q of wv_lfx: this lane's feeder
+            // byte q of wv_lfb: local index at the next lane << 6 | next lane (the
+            // lane itself: the line leaves the network, as a minimal path never
+            // takes a link twice); byte q of wv_lfx: this lane's feeder
             // index at the next lane.  A flow's delivered counter sits at
             // (its last lane) * 4 + (its local index there).
             wv_lfb.assign(nl, 0u);
@@ -600,7 +602,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                     const int32_t nx = c->path_link[q + 1];
                     const uint32_t sh = 8u * (uint32_t)lf_index(ln, f);
                     if (nx < 0) {
-                        wv_lfb[ln] |= 63u << sh;
+                        wv_lfb[ln] |= (uint32_t)ln << sh;
                         flow_dix[f] = ln * 4 + lf_index(ln, f);
                     } else {
                         const int32_t ln2 = link_lane[nx];

@@ -10,8 +10,9 @@
 // LDS (8-byte entries {line << 7 | local flow << 5, ready cycle}) and its
 // head entries, injection stream, round-robin pointer and counters in
 // registers.  At most four flows cross a link; a lane's local-flow table is
-// one register of four bytes (next lane, and the flow's local index there),
-// so no path table is read inside the cycle loop.  A flow's delivered
+// one register of four bytes (next lane, and the flow's local index there;
+// a flow's last link names its own lane), so no path table is read inside
+// the cycle loop.  A flow's delivered
 // counter is kept by the lane of its last link, at (lane, local index).
 //
 // The LDS operations of one wavefront are performed in issue order, so a
@@ -59,7 +60,6 @@ using namespace dev;
 constexpr uint32_t kWordEmpty = 0xFFFFFFFFu;
 constexpr uint32_t kWordFull = 0u;
 constexpr uint32_t kXs = kWaveXShift;  // line id position in an entry word
-constexpr uint32_t kSinkLane = 63u;    // next-lane value of a flow's last link
 
 // Compiler-only barrier between the phases of a cycle: a wavefront-scope
 // fence emits no instruction and no wait, but keeps LDS accesses in order.
@@ -361,7 +361,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             const bool hrdy = live & (occ != 0u) & (hr <= t);
             const uint32_t q = (hx >> 5) & 3u;
             const uint32_t lb = byte_of(lfb, q);
-            const bool sink = (lb & 63u) == kSinkLane;
+            const bool sink = (lb & 63u) == (uint32_t)i;  // a last link names itself
             const bool ej = hrdy & sink;
             const bool fw = hrdy & !sink;
             const uint32_t tgw = fw ? (uint32_t)gl0 + (lb & 63u) : 64u + (uint32_t)w;
@@ -440,7 +440,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                 const bool offk = open & (k < b) & ((uint32_t)k < occ) & (ek.y <= t);
                 const uint32_t q = (ek.x >> 5) & 3u;
                 const uint32_t lb = byte_of(lfb, q);
-                const bool sk = (lb & 63u) == kSinkLane;
+                const bool sk = (lb & 63u) == (uint32_t)i;
                 const uint32_t tg = (uint32_t)gl0 + (lb & 63u);
                 tgk[k] = tg;
                 const bool rq = offk & !sk;

@@ -130,7 +130,7 @@ struct DevNet {
     const int32_t *blk_wave;  // [wv_nblk*wv_wpb] wave of each slot, -1 if empty
     const int32_t *blk_off;   // [wv_nblk*wv_wpb] LDS byte offset of the slot's region
     const int32_t *wv_sc;     // [wv_W*G] scenario of each slot, -1 if empty; longest expected runs first
-    const uint32_t *wv_lfb;   // [nl] byte q: local flow q's next lane (63: leaves the network)
+    const uint32_t *wv_lfb;   // [nl] byte q: local flow q's next lane (the lane itself: leaves the network)
                               //   | its local index at the next lane << 6
     const uint32_t *wv_lfx;   // [nl] byte q: this lane's feeder index at local flow q's next lane
     const int32_t *pd_dix;    // [#descriptors] delivered-counter index of pd_flow: last lane * 4 + local index

@@ -240,7 +240,7 @@ def torus2d(X=4, Y=4, *, n_scenarios=4096, seed=5, bws=(1, 2, 4), lat_lo=20,
         lat[s * m:(s + 1) * m] = lat_lo + next(rng) % span
         cp[s * m:(s + 1) * m] = depths[next(rng) % len(depths)]
     return Workload(name, n, n, row_ptr, col_idx, n_scenarios, bw, lat, cp, arb,
-                    coll, nbytes)
+                    coll, nbytes, meta={"torus": (X, Y)})
 
 
 def config(name: str) -> Workload:
@@ -252,13 +252,27 @@ def config(name: str) -> Workload:
         of 64 MiB, round-robin arbitration.
     C4  k=16 fat-tree (1024 hosts, 320 switches), all-to-all 64 KiB per pair.
     C5  4096 scenarios of a 4x4 torus, ring all-reduce of 4 MiB, seeded params.
-    A "_chunk" suffix (C1, C2, C5) gives the same workload with per-chunk
-    step dependencies.
+    Suffixes change one thing of the workload: "_rhd", "_dbt" and "_ag" the
+    collective (recursive halving-doubling or double binary tree all-reduce,
+    ring all-gather; same buffer), "_chunk" the dependencies (per chunk, put
+    + signal); e.g. "C5_dbt_chunk".
     """
-    if name.endswith("_chunk"):
-        # the same workload with per-chunk (put + signal) step dependencies
-        w = config(name[:-len("_chunk")])
-        return replace(w, dep=DEP_CHUNK, name=w.name + "_chunkdep")
+    if "_" in name:
+        base, mod = name.rsplit("_", 1)
+        w = config(base)
+        if mod == "chunk":
+            return replace(w, dep=DEP_CHUNK, name=w.name + "_chunkdep")
+        colls = {"rhd": (COLL_RHD_ALLREDUCE, "rhd_ar"), "dbt": (COLL_DBT_ALLREDUCE, "dbt_ar"),
+                 "ag": (COLL_RING_ALLGATHER, "ring_ag")}
+        if mod in colls and w.coll in (COLL_RING_ALLREDUCE, COLL_DIRECT_ALLREDUCE):
+            coll, tag = colls[mod]
+            w = replace(w, coll=coll, name=w.name.replace("ring_ar", tag).replace("direct_ar", tag))
+            if mod == "rhd" and w.meta.get("torus"):
+                # halving-doubling partners differ in one bit: in Gray-code
+                # order each of them is a torus neighbour
+                w = replace(w, order=gray_torus_order(*w.meta["torus"]), name=w.name + "_gray")
+            return w
+        raise KeyError(name)
     if name == "C1":
         return full_mesh(4, b=1, L=10, cap=16, coll=COLL_DIRECT_ALLREDUCE,
                          nbytes=64 * 1024, name="C1_mesh4_direct_ar_64KiB")
@@ -272,6 +286,22 @@ def config(name: str) -> Workload:
     if name == "C5":
         return torus2d(name="C5_4096x_torus4x4_ring_ar_4MiB")
     raise KeyError(name)
+
+
+def gray_torus_order(X: int, Y: int) -> np.ndarray:
+    """Participant order for an X x Y torus (X, Y powers of two): participant
+    i = (high bits hy, low bits hx) sits at ring positions (gray(hx),
+    gray(hy)), gray(v) = v ^ (v >> 1), i.e. at rank X * y + x with x, y the
+    positions whose Gray codes are hx, hy.  Participants that differ in one
+    bit are then torus neighbours when X, Y <= 4."""
+    bx = X.bit_length() - 1
+    inv = lambda n: {v ^ (v >> 1): v for v in range(n)}  # Gray code -> position
+    ix, iy = inv(X), inv(Y)
+    order = np.zeros(X * Y, np.int32)
+    for i in range(X * Y):
+        hx, hy = i & (X - 1), i >> bx
+        order[i] = X * iy[hy] + ix[hx]
+    return order
 
 
 def scaled(w: Workload, **changes) -> Workload:

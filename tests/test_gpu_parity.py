@@ -253,7 +253,7 @@ def test_full_size_digest(simmod, torch_cuda, name):
     assert _digest(r.busy_cycles[0].cpu().numpy().astype("<u8")) == g["busy_cycles_sha256"][0]
 
 
-@pytest.mark.parametrize("name", ["C5", "C5_chunk"])
+@pytest.mark.parametrize("name", ["C5", "C5_chunk", "C5_rhd", "C5_dbt", "C5_ag"])
 def test_full_size_batched_digest(simmod, torch_cuda, name):
     g = _golden(name)
     w = si.config(name)
@@ -469,3 +469,26 @@ def test_more_collectives_fat_tree_ordered(simmod, oracle_lib, coll):
     w = si.fat_tree(4, nbytes=128 * 16 * 2, cap=5, lat_lo=2, lat_hi=9, arb=1, coll=coll)
     w.order = np.random.default_rng(coll).permutation(16).astype(np.int32)
     check_vs_oracle(simmod, oracle_lib, w)
+
+
+def test_rhd_rank_order_torus_deadlocks_like_oracle(simmod, oracle_lib):
+    """Full-size 4x4 torus sweep, RHD in rank order: two-hop partners close
+    cyclic buffer dependencies and every scenario deadlocks.  The engine must
+    stop where the oracle stops, with the same completed lines and counters."""
+    w = si.take_scenarios(si.config("C5"), [0, 1, 2, 3, 1000, 4095])
+    w.coll = si.COLL_RHD_ALLREDUCE
+    say("C5-sized RHD in rank order: 6 scenarios")
+    r, n_ok = check_vs_oracle(simmod, oracle_lib, w, expect_ok=False)
+    assert n_ok == 0 and r.status == simmod.SIM_ERR_DEADLOCK
+
+
+@pytest.mark.parametrize("dep", [0, 1])
+@pytest.mark.parametrize("arb", [0, 1])
+def test_wave_all_64_links(simmod, oracle_lib, dep, arb):
+    """RHD on the 4x4 torus in Gray-code order uses all 64 links: one
+    scenario per wavefront, every lane busy."""
+    w = si.torus2d(4, 4, n_scenarios=7, seed=123 + arb + 2 * dep, bws=(1, 2, 4), lat_lo=1, lat_hi=30,
+                   depths=(1, 2, 5, 16), nbytes=128 * 16 * 8, arb=arb, coll=si.COLL_RHD_ALLREDUCE)
+    w.order = si.gray_torus_order(4, 4)
+    w.dep = dep
+    check_engine(simmod, oracle_lib, w, "wave")

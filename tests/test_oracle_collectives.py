@@ -428,3 +428,22 @@ def test_order_permutes_participants(oracle_lib):
         T, dec = decode_all(oracle_lib, coll, p, N, order)
         assert [d[0] for d in dec] == [order[s] for s in src]
         assert [d[1] for d in dec] == [order[d] for d in dst]
+
+
+def test_gray_order_makes_rhd_partners_neighbours(oracle_lib):
+    # The 4x4 torus is the 4-cube: in Gray-code participant order every
+    # halving-doubling partner (one bit apart) is one hop away, so no route
+    # has a second hop and no cyclic buffer dependency can form.
+    w = si.config("C5_rhd")
+    rc, pp, _ = oracle_lib.paths(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx)
+    assert rc == 0
+    E = w.n_endpoints
+    for i in range(E):
+        for b in range(4):
+            s, d = int(w.order[i]), int(w.order[i ^ (1 << b)])
+            assert pp[s * E + d + 1] - pp[s * E + d] == 1
+    # in rank order some partners are two hops apart, and the same sweep
+    # deadlocks (cyclic buffer dependencies around the torus rings)
+    w2 = si.take_scenarios(si.config("C5"), [0])
+    w2.coll = si.COLL_RHD_ALLREDUCE
+    assert oracle_lib.simulate_workload(w2).status_name == "DEADLOCK"
