@@ -60,6 +60,10 @@ def lib():
                                       C.c_int64, P, P, P, P,
                                       C.c_uint64, C.c_int32, P, P, P, P, P]
         L.oracle_simulate.restype = C.c_int
+        i32, i64 = C.c_int32, C.c_int64
+        L.oracle_memcpy.argtypes = [i64, P, P, P, P, P, P, i32, i32, P, i32, i32, i64, i64,
+                                    P, P, P, P, P, P]
+        L.oracle_memcpy.restype = C.c_int
         _lib = L
     return _lib
 
@@ -100,6 +104,34 @@ def txn(coll, nbytes, group, E, x, order=None, dep=0):
     rc = lib().oracle_txn(coll, nbytes, group, E, _p(o), dep, x, _p(src), _p(dst), _p(npred),
                           _p(preds), _p(T))
     return rc, int(src[0]), int(dst[0]), [int(v) for v in preds[:npred[0]]], int(T[0])
+
+
+def memcpy_txns(mc):
+    """Expand memcpy programs (``sim_inputs.noc.Memcpy``) into the line list
+    (src, dst, pred_ptr, pred_idx)."""
+    n_ops = len(mc.cu)
+    cu = np.ascontiguousarray(mc.cu, np.int32)
+    ssp = np.ascontiguousarray(mc.src_space, np.int32)
+    dsp = np.ascontiguousarray(mc.dst_space, np.int32)
+    sl = np.ascontiguousarray(mc.src_line, np.int64)
+    dl = np.ascontiguousarray(mc.dst_line, np.int64)
+    nl = np.ascontiguousarray(mc.n_lines, np.int64)
+    ch = np.ascontiguousarray(mc.space_channels, np.int32)
+    n_spaces = len(ch) // mc.n_ch
+    T = np.zeros(1, np.int64)
+    P = np.zeros(1, np.int64)
+    args = (n_ops, _p(cu), _p(ssp), _p(dsp), _p(sl), _p(dl), _p(nl), n_spaces, mc.n_ch, _p(ch), mc.unroll, mc.window)
+    rc = lib().oracle_memcpy(*args, 0, 0, None, None, None, None, _p(T), _p(P))
+    if rc:
+        raise ValueError(f"oracle_memcpy: status {rc}")
+    src = np.zeros(max(int(T[0]), 1), np.int32)
+    dst = np.zeros(max(int(T[0]), 1), np.int32)
+    pptr = np.zeros(int(T[0]) + 1, np.int64)
+    pidx = np.zeros(max(int(P[0]), 1), np.int64)
+    rc = lib().oracle_memcpy(*args, int(T[0]), int(P[0]), _p(src), _p(dst), _p(pptr), _p(pidx), _p(T), _p(P))
+    assert rc == 0
+    t = int(T[0])
+    return src[:t], dst[:t], pptr, pidx[:int(P[0])]
 
 
 @dataclass
@@ -161,6 +193,9 @@ def simulate_workload(w, scenario: int = 0, *, max_cycles=0, check=False) -> Res
     """Run scenario ``scenario`` of a ``sim_inputs.Workload``."""
     m = w.n_links
     sl = slice(scenario * m, (scenario + 1) * m)
+    txns = None
+    if w.meta.get("memcpy") is not None:
+        txns = memcpy_txns(w.meta["memcpy"])
     return simulate(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw[sl], w.lat[sl],
                     w.cap[sl], w.arb, coll=w.coll, nbytes=w.bytes, group=w.group_size,
-                    order=w.order, dep=w.dep, max_cycles=max_cycles, check=check)
+                    order=w.order, dep=w.dep, txns=txns, max_cycles=max_cycles, check=check)

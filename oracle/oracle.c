@@ -572,6 +572,119 @@ int oracle_txn(int coll, uint64_t bytes, int32_t group, int32_t E, const int32_t
     return OR_OK;
 }
 
+/* ------------------------------------------------------- memcpy programs
+ * The injection side of the GPU model (Sec. 4.4.3 wavefront requests, 4.4.4
+ * loop unrolling; the outstanding-request limit of Sec. 5.3).  A CU runs its
+ * memcpy operations in list order.  Each copied line is a load and a store;
+ * unrolled by U, the loop issues U loads, waits for their data, then issues
+ * the U stores (the last group of an operation may be shorter).
+ *   load  = a request line (CU -> the channel of the source line) and a data
+ *           line (that channel -> CU) that may leave once the request has
+ *           arrived;
+ *   store = one line (CU -> the channel of the destination line) that may
+ *           leave once the data of every load of its group has arrived.
+ * The CU's requests (load requests and stores) are its issued wavefront
+ * requests, in program order; request k may be issued only once request
+ * k - W is done (its data arrived / the store arrived): at most W
+ * outstanding, retired in order.  Program order itself comes from the
+ * network: all of a CU's requests leave through its one link, in id order.
+ * Line a of space s lives on channel space_ch[s * n_ch + a mod n_ch].
+ * Ids are step-major: for issue index k = 0, 1, ... and the CUs in ascending
+ * endpoint order, a load takes two ids (request, then data), a store one. */
+typedef struct { int kind; int32_t chan; int64_t g0, gn; } minstr_t;   /* kind 0 load, 1 store */
+
+int oracle_memcpy(int64_t n_ops, const int32_t *cu, const int32_t *ssp, const int32_t *dsp,
+                  const int64_t *sline, const int64_t *dline, const int64_t *nlines,
+                  int32_t n_spaces, int32_t n_ch, const int32_t *space_ch, int32_t U, int32_t W,
+                  int64_t cap_txn, int64_t cap_pred, int32_t *src, int32_t *dst,
+                  int64_t *pred_ptr, int64_t *pred_idx, int64_t *T_out, int64_t *P_out)
+{
+    if (n_ops < 0 || n_ch < 1 || n_spaces < 1 || U < 1 || W < 1) return OR_ERR_INVALID_ARG;
+    /* the CUs, ascending */
+    int32_t *cus = malloc(sizeof(int32_t) * (size_t)(n_ops > 0 ? n_ops : 1));
+    int32_t ncu = 0;
+    for (int64_t o = 0; o < n_ops; o++) {
+        if (ssp[o] < 0 || ssp[o] >= n_spaces || dsp[o] < 0 || dsp[o] >= n_spaces || nlines[o] < 0 ||
+            sline[o] < 0 || dline[o] < 0) { free(cus); return OR_ERR_INVALID_ARG; }
+        int found = 0;
+        for (int32_t q = 0; q < ncu; q++) found |= cus[q] == cu[o];
+        if (!found) cus[ncu++] = cu[o];
+    }
+    for (int32_t a = 1; a < ncu; a++)          /* insertion sort */
+        for (int32_t b = a; b > 0 && cus[b - 1] > cus[b]; b--) { int32_t t = cus[b]; cus[b] = cus[b - 1]; cus[b - 1] = t; }
+    /* each CU's program */
+    minstr_t **prog = calloc((size_t)(ncu > 0 ? ncu : 1), sizeof(minstr_t *));
+    int64_t *plen = calloc((size_t)(ncu > 0 ? ncu : 1), sizeof(int64_t));
+    int64_t kmax = 0;
+    for (int32_t q = 0; q < ncu; q++) {
+        int64_t len = 0;
+        for (int64_t o = 0; o < n_ops; o++) if (cu[o] == cus[q]) len += 2 * nlines[o];
+        prog[q] = malloc(sizeof(minstr_t) * (size_t)(len > 0 ? len : 1));
+        int64_t k = 0;
+        for (int64_t o = 0; o < n_ops; o++) {
+            if (cu[o] != cus[q]) continue;
+            for (int64_t j0 = 0; j0 < nlines[o]; j0 += U) {
+                int64_t gn = nlines[o] - j0 < U ? nlines[o] - j0 : U;
+                int64_t g0 = k;                       /* first load of the group */
+                for (int64_t j = j0; j < j0 + gn; j++) {
+                    int64_t a = sline[o] + j;
+                    prog[q][k++] = (minstr_t){0, space_ch[(int64_t)ssp[o] * n_ch + a % n_ch], g0, gn};
+                }
+                for (int64_t j = j0; j < j0 + gn; j++) {
+                    int64_t a = dline[o] + j;
+                    prog[q][k++] = (minstr_t){1, space_ch[(int64_t)dsp[o] * n_ch + a % n_ch], g0, gn};
+                }
+            }
+        }
+        plen[q] = k;
+        if (k > kmax) kmax = k;
+    }
+    /* ids: first id of every instruction */
+    int64_t **id = calloc((size_t)(ncu > 0 ? ncu : 1), sizeof(int64_t *));
+    for (int32_t q = 0; q < ncu; q++) id[q] = malloc(sizeof(int64_t) * (size_t)(plen[q] > 0 ? plen[q] : 1));
+    int64_t T = 0;
+    for (int64_t k = 0; k < kmax; k++)
+        for (int32_t q = 0; q < ncu; q++)
+            if (k < plen[q]) { id[q][k] = T; T += prog[q][k].kind == 0 ? 2 : 1; }
+    /* the line that marks instruction k of CU q done */
+    #define DONE(q, k) (prog[q][k].kind == 0 ? id[q][k] + 1 : id[q][k])
+    int64_t P = 0;
+    int rc = OR_OK;
+    if (T >= (int64_t)0xFFFFFFFF) rc = OR_ERR_SIZE;
+    for (int64_t k = 0; k < kmax && rc == OR_OK; k++)
+        for (int32_t q = 0; q < ncu; q++) {
+            if (k >= plen[q]) continue;
+            const minstr_t *in = &prog[q][k];
+            int64_t x = id[q][k];
+            /* the issued line: request (load) or store */
+            int64_t np = (k >= W ? 1 : 0) + (in->kind == 1 ? in->gn : 0);
+            int64_t need = np + (in->kind == 0 ? 1 : 0);
+            if (cap_txn >= T && cap_pred >= P + need) {
+                src[x] = cus[q];
+                dst[x] = in->chan;
+                pred_ptr[x] = P;
+                int64_t w = P;
+                if (k >= W) pred_idx[w++] = DONE(q, k - W);
+                if (in->kind == 1)
+                    for (int64_t g = in->g0; g < in->g0 + in->gn; g++) pred_idx[w++] = id[q][g] + 1;
+                pred_ptr[x + 1] = w;
+                if (in->kind == 0) {       /* the data line: waits for its request */
+                    src[x + 1] = in->chan;
+                    dst[x + 1] = cus[q];
+                    pred_idx[w++] = x;
+                    pred_ptr[x + 2] = w;
+                }
+            }
+            P += need;
+        }
+    #undef DONE
+    if (T_out) *T_out = T;
+    if (P_out) *P_out = P;
+    for (int32_t q = 0; q < ncu; q++) { free(prog[q]); free(id[q]); }
+    free(prog); free(id); free(plen); free(cus);
+    return rc;
+}
+
 /* ------------------------------------------------------------- simulation */
 
 /* FIFO entry: line id, first cycle it may leave, hop index of this link on
