@@ -179,6 +179,38 @@ sim_status sim_load_collective(sim_ctx *ctx, int32_t coll, uint64_t bytes, int32
 sim_status sim_load_transactions(sim_ctx *ctx, int64_t n, const int32_t *src, const int32_t *dst,
                                  const int64_t *pred_ptr, const int64_t *pred_idx);
 
+/*
+ * Load memcpy programs run by compute units: the injection side of the GPU
+ * model (Sec. 4.4.3 wavefront requests, Sec. 4.4.4 loop unrolling, the
+ * outstanding-request limit of Sec. 5.3).  Replaces any previous workload.
+ *   n_ops, cu[], src_space[], dst_space[], src_line[], dst_line[], n_lines[]:
+ *       operation o copies n_lines[o] lines from line address src_line[o] of
+ *       address space src_space[o] to dst_line[o] of dst_space[o]; it runs on
+ *       endpoint cu[o].  A CU runs its operations in array order.
+ *   n_spaces, n_ch, space_ch[n_spaces * n_ch]: line a of space s lives on the
+ *       memory-channel endpoint space_ch[s * n_ch + a mod n_ch].
+ *   unroll U >= 1: the copy loop issues U loads, waits for their data, then
+ *       issues the U stores (an operation's last group may be shorter).
+ *   window W >= 1: a CU's wavefront requests (load requests and stores) are
+ *       issued in program order with at most W outstanding, retired in order:
+ *       request k waits until request k - W is done.
+ * Lines: a load is a request (CU -> source channel) and a data line
+ * (channel -> CU) that may leave once the request has arrived; a store
+ * (CU -> destination channel) may leave once the data of every load of its
+ * group has arrived; a load is done when its data has arrived, a store when
+ * it has.  Program order is kept by the network: all of a CU's requests
+ * leave through the CU's first link in id order.  Ids are step-major: for
+ * issue index k = 0, 1, ... and the CUs in ascending endpoint order, a load
+ * takes two ids (request, data), a store one.  Arrays are copied.
+ * SIM_ERR_INVALID_ARG for an endpoint out of range, a CU that is also the
+ * channel of one of its lines, a space out of range, negative sizes or
+ * addresses, U or W < 1; SIM_ERR_SIZE beyond 2^32 - 2 lines.
+ */
+sim_status sim_load_memcpy(sim_ctx *ctx, int64_t n_ops, const int32_t *cu, const int32_t *src_space,
+                           const int32_t *dst_space, const int64_t *src_line, const int64_t *dst_line,
+                           const int64_t *n_lines, int32_t n_spaces, int32_t n_ch, const int32_t *space_ch,
+                           int32_t unroll, int32_t window);
+
 /* Sizes of the loaded problem: transactions T, links m, scenarios S and
  * line-hops per scenario (sum of path lengths).  Any pointer may be NULL. */
 sim_status sim_sizes(const sim_ctx *ctx, int64_t *n_txn, int32_t *n_links, int32_t *n_scenarios,

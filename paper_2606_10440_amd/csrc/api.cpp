@@ -12,6 +12,7 @@
 #include <cstdlib>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <new>
 #include <string>
 #include <unordered_map>
@@ -1022,9 +1023,11 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
 
 }  // namespace
 
-extern "C" {
+namespace {
 
-sim_status sim_create(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_ptr, const int32_t *col_idx,
+// Entry points; their extern "C" wrappers follow.
+
+sim_status create_impl(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_ptr, const int32_t *col_idx,
                       int32_t n_scenarios, const int32_t *bw, const int32_t *lat, const int32_t *cap,
                       int32_t arb, sim_ctx **out) {
     if (!out || !row_ptr || !col_idx || !bw || !lat || !cap) return SIM_ERR_INVALID_ARG;
@@ -1065,7 +1068,7 @@ sim_status sim_create(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_p
     return SIM_OK;
 }
 
-sim_status sim_load_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t group_size, const int32_t *order,
+sim_status load_collective_impl(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t group_size, const int32_t *order,
                                int32_t dep) {
     if (!c) return SIM_ERR_INVALID_ARG;
     if (coll != SIM_COLL_HIER_ALLREDUCE && group_size != 0)
@@ -1076,7 +1079,7 @@ sim_status sim_load_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t
     return finish_load(c, R);
 }
 
-sim_status sim_load_transactions(sim_ctx *c, int64_t n, const int32_t *src, const int32_t *dst,
+sim_status load_transactions_impl(sim_ctx *c, int64_t n, const int32_t *src, const int32_t *dst,
                                  const int64_t *pred_ptr, const int64_t *pred_idx) {
     if (!c || n < 0 || (n > 0 && (!src || !dst || !pred_ptr))) return SIM_ERR_INVALID_ARG;
     if (n >= (int64_t)0xFFFFFFFFll) return fail(c, SIM_ERR_SIZE, "more than 2^32-2 transactions");
@@ -1097,17 +1100,92 @@ sim_status sim_load_transactions(sim_ctx *c, int64_t n, const int32_t *src, cons
     return finish_load(c, R);
 }
 
-sim_status sim_sizes(const sim_ctx *c, int64_t *n_txn, int32_t *n_links, int32_t *n_scenarios, uint64_t *line_hops) {
-    if (!c) return SIM_ERR_INVALID_ARG;
-    if (n_links) *n_links = c->m;
-    if (n_scenarios) *n_scenarios = c->S;
-    if (!c->loaded) return SIM_ERR_STATE;
-    if (n_txn) *n_txn = c->T;
-    if (line_hops) *line_hops = c->line_hops;
-    return SIM_OK;
+sim_status load_memcpy_impl(sim_ctx *c, int64_t n_ops, const int32_t *cu, const int32_t *src_space,
+                           const int32_t *dst_space, const int64_t *src_line, const int64_t *dst_line,
+                           const int64_t *n_lines, int32_t n_spaces, int32_t n_ch, const int32_t *space_ch,
+                           int32_t unroll, int32_t window) {
+    if (!c || n_ops < 0 || n_spaces < 1 || n_ch < 1 || !space_ch || unroll < 1 || window < 1 ||
+        (n_ops > 0 && (!cu || !src_space || !dst_space || !src_line || !dst_line || !n_lines)))
+        return c ? fail(c, SIM_ERR_INVALID_ARG, "memcpy: null array or bad n_spaces/n_ch/unroll/window")
+                 : SIM_ERR_INVALID_ARG;
+    for (int64_t q = 0; q < (int64_t)n_spaces * n_ch; q++)
+        if (space_ch[q] < 0 || space_ch[q] >= c->E) return fail(c, SIM_ERR_INVALID_ARG, "memcpy: channel is not an endpoint");
+    // One wavefront request of a CU's program: a load (request + data) or a
+    // store waiting for the data of loads [g0, g0 + gn) of the same program.
+    struct Req {
+        bool store;
+        int32_t chan;
+        int64_t g0;
+        int32_t gn;
+    };
+    std::map<int32_t, std::vector<Req>> prog;  // by CU, ascending
+    uint64_t lines = 0;
+    for (int64_t o = 0; o < n_ops; o++) {
+        if (cu[o] < 0 || cu[o] >= c->E) return fail(c, SIM_ERR_INVALID_ARG, "memcpy: CU is not an endpoint");
+        if (src_space[o] < 0 || src_space[o] >= n_spaces || dst_space[o] < 0 || dst_space[o] >= n_spaces ||
+            n_lines[o] < 0 || src_line[o] < 0 || dst_line[o] < 0)
+            return fail(c, SIM_ERR_INVALID_ARG, "memcpy: operation " + std::to_string(o) + " out of range");
+        lines += 3 * (uint64_t)n_lines[o];
+        if (lines >= 0xFFFFFFFFull) return fail(c, SIM_ERR_SIZE, "more than 2^32-2 transactions");
+        auto &pr = prog[cu[o]];
+        const int64_t first = (int64_t)pr.size();
+        const int32_t *sch = space_ch + (int64_t)src_space[o] * n_ch;
+        const int32_t *dch = space_ch + (int64_t)dst_space[o] * n_ch;
+        for (int64_t j0 = 0; j0 < n_lines[o]; j0 += unroll) {
+            const int32_t gn = (int32_t)std::min<int64_t>(unroll, n_lines[o] - j0);
+            const int64_t g0 = (int64_t)pr.size();
+            for (int32_t u = 0; u < gn; u++) pr.push_back({false, sch[(src_line[o] + j0 + u) % n_ch], g0, gn});
+            for (int32_t u = 0; u < gn; u++) pr.push_back({true, dch[(dst_line[o] + j0 + u) % n_ch], g0, gn});
+        }
+        for (int64_t q = first; q < (int64_t)pr.size(); q++)
+            if (pr[q].chan == cu[o]) return fail(c, SIM_ERR_INVALID_ARG, "memcpy: a CU is the channel of its own line");
+    }
+    // ids, step-major over the CUs
+    std::vector<std::pair<int32_t, std::vector<Req> *>> cus;
+    for (auto &kv : prog) cus.push_back({kv.first, &kv.second});
+    std::vector<std::vector<int64_t>> id(cus.size());
+    size_t kmax = 0;
+    for (size_t q = 0; q < cus.size(); q++) {
+        id[q].resize(cus[q].second->size());
+        kmax = std::max(kmax, cus[q].second->size());
+    }
+    int64_t T = 0;
+    for (size_t k = 0; k < kmax; k++)
+        for (size_t q = 0; q < cus.size(); q++)
+            if (k < cus[q].second->size()) {
+                id[q][k] = T;
+                T += (*cus[q].second)[k].store ? 1 : 2;
+            }
+    // one range per line (consecutive ids belong to different CUs)
+    Ranges R;
+    int64_t next = 0;
+    for (size_t k = 0; k < kmax; k++)
+        for (size_t q = 0; q < cus.size(); q++) {
+            const auto &pr = *cus[q].second;
+            if (k >= pr.size()) continue;
+            const Req &r = pr[k];
+            const int64_t x = id[q][k];
+            if (x != next) return fail(c, SIM_ERR_INVALID_ARG, "internal: memcpy ids not dense");
+            R.add((uint64_t)x, 1, cus[q].first, r.chan);
+            if (k >= (size_t)window) {
+                const size_t kd = k - (size_t)window;  // retired before this request is issued
+                R.pred(id[q][kd] + (pr[kd].store ? 0 : 1), 0);
+            }
+            if (r.store)
+                for (int64_t g = r.g0; g < r.g0 + r.gn; g++) R.pred(id[q][g] + 1, 0);
+            next = x + 1;
+            if (!r.store) {  // the data line
+                R.add((uint64_t)x + 1, 1, r.chan, cus[q].first);
+                R.pred(x, 0);
+                next = x + 2;
+            }
+        }
+    R.close();
+    return finish_load(c, R);
 }
 
-sim_status sim_run(sim_ctx *c, void *stream, uint32_t *d_completion, uint64_t *d_tx_lines,
+
+sim_status run_impl(sim_ctx *c, void *stream, uint32_t *d_completion, uint64_t *d_tx_lines,
                    uint64_t *d_busy_cycles, uint32_t *d_makespan, uint64_t max_cycles) {
     if (!c) return SIM_ERR_INVALID_ARG;
     if (!c->loaded) return fail(c, SIM_ERR_STATE, "sim_run before a workload was loaded");
@@ -1132,7 +1210,7 @@ sim_status sim_run(sim_ctx *c, void *stream, uint32_t *d_completion, uint64_t *d
     return SIM_OK;
 }
 
-sim_status sim_status_after_sync(sim_ctx *c, int32_t *status, uint64_t *cycles) {
+sim_status status_after_sync_impl(sim_ctx *c, int32_t *status, uint64_t *cycles) {
     if (!c) return SIM_ERR_INVALID_ARG;
     if (!c->loaded || !c->ran) return fail(c, SIM_ERR_STATE, "no run to report on");
     std::vector<int32_t> st(c->S);
@@ -1155,7 +1233,7 @@ sim_status sim_status_after_sync(sim_ctx *c, int32_t *status, uint64_t *cycles) 
     return SIM_OK;
 }
 
-sim_status sim_route(const sim_ctx *c, int32_t src, int32_t dst, int32_t *links, int32_t cap, int32_t *len) {
+sim_status route_impl(const sim_ctx *c, int32_t src, int32_t dst, int32_t *links, int32_t cap, int32_t *len) {
     if (!c || !len || src < 0 || dst < 0 || src >= c->E || dst >= c->E) return SIM_ERR_INVALID_ARG;
     std::vector<int32_t> hops;
     if (src == dst) {
@@ -1166,6 +1244,73 @@ sim_status sim_route(const sim_ctx *c, int32_t src, int32_t dst, int32_t *links,
     *len = (int32_t)hops.size();
     if ((int32_t)hops.size() > cap || (!links && !hops.empty())) return SIM_ERR_SIZE;
     std::copy(hops.begin(), hops.end(), links);
+    return SIM_OK;
+}
+
+
+
+}  // namespace
+
+// No C++ exception crosses the C ABI: allocation failures become
+// SIM_ERR_OOM, anything else SIM_ERR_DEVICE.
+template <typename F>
+sim_status guarded(sim_ctx *c, F &&f) {
+    try {
+        return f();
+    } catch (const std::bad_alloc &) {
+        if (c) c->err = "host allocation failed";
+        return SIM_ERR_OOM;
+    } catch (...) {
+        if (c) c->err = "unexpected host error";
+        return SIM_ERR_DEVICE;
+    }
+}
+
+extern "C" {
+
+sim_status sim_create(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_ptr, const int32_t *col_idx,
+                      int32_t n_scenarios, const int32_t *bw, const int32_t *lat, const int32_t *cap,
+                      int32_t arb, sim_ctx **out) {
+    return guarded(nullptr, [&] { return create_impl(n_nodes, n_endpoints, row_ptr, col_idx, n_scenarios, bw, lat, cap, arb, out); });
+}
+
+sim_status sim_load_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t group_size, const int32_t *order,
+                               int32_t dep) {
+    return guarded(c, [&] { return load_collective_impl(c, coll, bytes, group_size, order, dep); });
+}
+
+sim_status sim_load_transactions(sim_ctx *c, int64_t n, const int32_t *src, const int32_t *dst,
+                                 const int64_t *pred_ptr, const int64_t *pred_idx) {
+    return guarded(c, [&] { return load_transactions_impl(c, n, src, dst, pred_ptr, pred_idx); });
+}
+
+sim_status sim_load_memcpy(sim_ctx *c, int64_t n_ops, const int32_t *cu, const int32_t *src_space,
+                           const int32_t *dst_space, const int64_t *src_line, const int64_t *dst_line,
+                           const int64_t *n_lines, int32_t n_spaces, int32_t n_ch, const int32_t *space_ch,
+                           int32_t unroll, int32_t window) {
+    return guarded(c, [&] { return load_memcpy_impl(c, n_ops, cu, src_space, dst_space, src_line, dst_line, n_lines, n_spaces, n_ch, space_ch, unroll, window); });
+}
+
+sim_status sim_run(sim_ctx *c, void *stream, uint32_t *d_completion, uint64_t *d_tx_lines,
+                   uint64_t *d_busy_cycles, uint32_t *d_makespan, uint64_t max_cycles) {
+    return guarded(c, [&] { return run_impl(c, stream, d_completion, d_tx_lines, d_busy_cycles, d_makespan, max_cycles); });
+}
+
+sim_status sim_status_after_sync(sim_ctx *c, int32_t *status, uint64_t *cycles) {
+    return guarded(c, [&] { return status_after_sync_impl(c, status, cycles); });
+}
+
+sim_status sim_route(const sim_ctx *c, int32_t src, int32_t dst, int32_t *links, int32_t cap, int32_t *len) {
+    return guarded(const_cast<sim_ctx *>(c), [&] { return route_impl(c, src, dst, links, cap, len); });
+}
+
+sim_status sim_sizes(const sim_ctx *c, int64_t *n_txn, int32_t *n_links, int32_t *n_scenarios, uint64_t *line_hops) {
+    if (!c) return SIM_ERR_INVALID_ARG;
+    if (n_links) *n_links = c->m;
+    if (n_scenarios) *n_scenarios = c->S;
+    if (!c->loaded) return SIM_ERR_STATE;
+    if (n_txn) *n_txn = c->T;
+    if (line_hops) *line_hops = c->line_hops;
     return SIM_OK;
 }
 

@@ -1,7 +1,7 @@
 """Thin ctypes binding of libsimgpu (argument marshalling only).
 
 Functions keep the C ABI's names (``sim_create``, ``sim_load_collective``,
-``sim_load_transactions``, ``sim_sizes``, ``sim_run``,
+``sim_load_transactions``, ``sim_load_memcpy``, ``sim_sizes``, ``sim_run``,
 ``sim_status_after_sync``, ``sim_route``, ``sim_last_error``,
 ``sim_destroy``); ``Simulator`` bundles them with torch device buffers and
 the current HIP stream.  Every step of the simulation runs in the library's
@@ -24,7 +24,7 @@ SIM_OK, SIM_ERR_INVALID_ARG, SIM_ERR_TOPOLOGY, SIM_ERR_UNREACHABLE, SIM_ERR_SIZE
 SIM_ERR_OOM, SIM_ERR_DEVICE, SIM_ERR_DEADLOCK, SIM_ERR_MAX_CYCLES, SIM_ERR_STATE = 5, 6, 7, 8, 9
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "TOPOLOGY", 3: "UNREACHABLE", 4: "SIZE", 5: "OOM",
                 6: "DEVICE", 7: "DEADLOCK", 8: "MAX_CYCLES", 9: "STATE"}
-EXPORTS = ("sim_create", "sim_load_collective", "sim_load_transactions", "sim_sizes", "sim_run",
+EXPORTS = ("sim_create", "sim_load_collective", "sim_load_transactions", "sim_load_memcpy", "sim_sizes", "sim_run",
            "sim_status_after_sync", "sim_route", "sim_last_error", "sim_destroy")
 
 _lib = None
@@ -47,6 +47,7 @@ def lib():
         L.sim_create.argtypes = [i32, i32, P, P, i32, P, P, P, i32, C.POINTER(P)]
         L.sim_load_collective.argtypes = [P, i32, u64, i32, P, i32]
         L.sim_load_transactions.argtypes = [P, i64, P, P, P, P]
+        L.sim_load_memcpy.argtypes = [P, i64, P, P, P, P, P, P, C.c_int32, C.c_int32, P, C.c_int32, C.c_int32]
         L.sim_sizes.argtypes = [P, P, P, P, P]
         L.sim_run.argtypes = [P, P, P, P, P, P, u64]
         L.sim_status_after_sync.argtypes = [P, P, P]
@@ -95,6 +96,16 @@ def sim_load_transactions(ctx, src, dst, pred_ptr, pred_idx):
     if pidx.size == 0:
         pidx = np.zeros(1, np.int64)
     _check(ctx, lib().sim_load_transactions(ctx, len(src), _ptr(src), _ptr(dst), _ptr(pptr), _ptr(pidx)))
+
+
+def sim_load_memcpy(ctx, cu, src_space, dst_space, src_line, dst_line, n_lines, space_channels, n_ch,
+                    unroll, window):
+    a32 = [np.ascontiguousarray(v, np.int32) for v in (cu, src_space, dst_space)]
+    a64 = [np.ascontiguousarray(v, np.int64) for v in (src_line, dst_line, n_lines)]
+    ch = np.ascontiguousarray(space_channels, np.int32)
+    n_spaces = len(ch) // n_ch if n_ch > 0 else 0
+    _check(ctx, lib().sim_load_memcpy(ctx, len(a32[0]), *(_ptr(v) for v in a32), *(_ptr(v) for v in a64),
+                                      n_spaces, n_ch, _ptr(ch), unroll, window))
 
 
 def sim_sizes(ctx):
@@ -156,7 +167,9 @@ class Simulator:
     def from_workload(cls, w):
         sim = cls(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw, w.lat, w.cap, w.arb,
                   w.n_scenarios)
-        if w.coll >= 0:
+        if w.meta.get("memcpy") is not None:
+            sim.load_memcpy(w.meta["memcpy"])
+        elif w.coll >= 0:
             sim.load_collective(w.coll, w.bytes, w.group_size, w.order, w.dep)
         return sim
 
@@ -165,6 +178,11 @@ class Simulator:
 
     def load_transactions(self, src, dst, pred_ptr, pred_idx):
         sim_load_transactions(self.ctx, src, dst, pred_ptr, pred_idx)
+
+    def load_memcpy(self, mc):
+        """Memcpy programs (fields of ``sim_inputs.noc.Memcpy``)."""
+        sim_load_memcpy(self.ctx, mc.cu, mc.src_space, mc.dst_space, mc.src_line, mc.dst_line, mc.n_lines,
+                        mc.space_channels, mc.n_ch, mc.unroll, mc.window)
 
     def sizes(self):
         return sim_sizes(self.ctx)

@@ -165,3 +165,23 @@ def test_rhd_needs_power_of_two(simlib):
         assert e.value.status == simlib.SIM_ERR_INVALID_ARG and "power-of-two" in str(e.value)
     finally:
         simlib.sim_destroy(ctx)
+
+
+def test_memcpy_argument_errors(simlib):
+    from sim_inputs import noc
+    w, lay = noc.gpu_noc(1, mesh=(2, 2), cus_per_router=1, ch_per_router=2, ports_per_router=1)
+    ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, w.arb)
+    cu = int(lay.cus[0][0])
+    ch = lay.channels.reshape(-1)
+    good = dict(cu=[cu], src_space=[0], dst_space=[0], src_line=[0], dst_line=[8], n_lines=[4],
+                space_channels=ch, n_ch=len(ch), unroll=2, window=4)
+    bad = [dict(unroll=0), dict(window=0), dict(cu=[w.n_endpoints]), dict(src_space=[1]), dict(n_lines=[-1]),
+           dict(dst_line=[-3]), dict(space_channels=np.where(ch == ch[0], cu, ch)),
+           dict(space_channels=np.full_like(ch, w.n_endpoints))]
+    try:
+        for b in bad:
+            with pytest.raises(simlib.SimError) as e:
+                simlib.sim_load_memcpy(ctx, **{**good, **b})
+            assert e.value.status == simlib.SIM_ERR_INVALID_ARG, b
+    finally:
+        simlib.sim_destroy(ctx)

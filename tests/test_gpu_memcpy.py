@@ -1,0 +1,61 @@
+"""GPU parity of memcpy programs on the generic GPU NoC (the injection side
+of the GPU model) against the CPU oracle, line for line, through the C ABI.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from sim_inputs import noc
+from tests.test_gpu_parity import (ENGINES, check_engine, check_vs_oracle, simmod, torch_cuda,  # noqa: F401
+                                   say)
+
+pytestmark = pytest.mark.gpu
+
+
+def tiny_noc(seed, n_ops=6, max_lines=9):
+    w, lay = noc.gpu_noc(1, mesh=(2, 2), cus_per_router=2, ch_per_router=2, ports_per_router=1,
+                         noc=(4, 1, 8), cu_out=(2, 1, 4), mem=(1, 2, 3))
+    rng = np.random.default_rng(seed)
+    rows = [(int(rng.choice(lay.cus[0])), 0, 0, int(rng.integers(0, 20)), 40 + int(rng.integers(0, 20)),
+             int(rng.integers(0, max_lines))) for _ in range(n_ops)]
+    mc = noc._ops(rows, lay, int(rng.integers(1, 5)), int(rng.integers(1, 9)))
+    wm = noc.memcpy_workload(w, mc, name=f"tiny_noc_{seed}")
+    wm.arb = seed % 2
+    return wm
+
+
+@pytest.mark.parametrize("engine", ENGINES)
+@pytest.mark.parametrize("seed", range(6))
+def test_memcpy_tiny_noc(simmod, oracle_lib, engine, seed):
+    w = tiny_noc(seed)
+    if engine == "b1":
+        w.bw[:] = 1
+        w.cap[:] = np.maximum(w.cap, 2 * (w.lat + 1))
+    check_engine(simmod, oracle_lib, w, engine)
+
+
+@pytest.mark.parametrize("U,W", [(1, 1), (4, 16), (8, 64)])
+def test_memcpy_generic_gpu_local_copy(simmod, oracle_lib, U, W):
+    w, lay = noc.gpu_noc(1)
+    wm = noc.memcpy_workload(w, noc.local_copy_ops(lay, 128 * 6, n_wg=128, unroll=U, window=W),
+                             name=f"gpu_local_copy_U{U}_W{W}")
+    say(f"{wm.name}")
+    check_vs_oracle(simmod, oracle_lib, wm)
+
+
+@pytest.mark.parametrize("engine", ["workgroup", "lane", "lanehbm"])
+def test_memcpy_generic_gpu_sweep(simmod, oracle_lib, engine):
+    w, lay = noc.gpu_noc(1)
+    wm = noc.memcpy_workload(w, noc.local_copy_ops(lay, 32 * 8, n_wg=32, unroll=4, window=8), name="gpu_sweep")
+    wm = noc.with_scenarios(wm, 5, seed=7)
+    check_engine(simmod, oracle_lib, wm, engine)
+
+
+@pytest.mark.parametrize("kind", ["allgather", "alltoall"])
+def test_memcpy_two_gpus(simmod, oracle_lib, kind):
+    w, lay = noc.gpu_noc(2)
+    mc = noc.allgather_ops(lay, 2 * 32 * 2, n_wg=32) if kind == "allgather" else noc.alltoall_ops(lay, 64, n_wg=32)
+    wm = noc.memcpy_workload(w, mc, name=f"two_gpu_{kind}")
+    say(wm.name)
+    check_vs_oracle(simmod, oracle_lib, wm)

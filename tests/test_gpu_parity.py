@@ -47,6 +47,8 @@ def run_gpu(simmod, w, max_cycles=0, txns=None):
                          w.n_scenarios)
     if txns is not None:
         s.load_transactions(*txns)
+    elif w.meta.get("memcpy") is not None:
+        s.load_memcpy(w.meta["memcpy"])
     else:
         s.load_collective(w.coll, w.bytes, w.group_size, w.order, w.dep)
     r = s.run(max_cycles=max_cycles)
