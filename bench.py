@@ -7,7 +7,8 @@ state resident in HBM.  The default workload is the batched design sweep
 seeded bandwidth/latency/depth per scenario), the largest workload by
 line-hop events; ``--workload C1..C4`` selects the others, a ``_chunk``
 suffix (C1, C2, C5) the same workload with per-chunk step dependencies, and
-C5_rhd / C5_dbt / C5_ag the batched sweep with another collective.
+C5_rhd / C5_dbt / C5_ag the batched sweep with another collective; NOC2_ag
+is the GPU-as-NoC memcpy sweep.
 
 Prints one JSON line with the metric, a roofline entry for the engine
 kernel (algorithmic bytes per launch / measured launch time vs the 8 TB/s
@@ -43,6 +44,9 @@ for _k in ("C1", "C2", "C5"):
 for _k, _c in (("rhd", "recursive halving-doubling all-reduce"), ("dbt", "double binary tree all-reduce"),
                ("ag", "ring all-gather")):
     DESCR["C5_" + _k] = DESCR["C5"].replace("ring all-reduce", _c)
+DESCR["NOC2_ag"] = ("1024 scenarios x 2 generic GPUs as NoCs (448 nodes each) + 32 scale-up switches, "
+                    "put-based all-gather 2 MiB out per GPU as memcpy programs (32 WGs/GPU, unroll 4, "
+                    "64 outstanding), channel latency in {1,2,4,8}, scale-up cable latency in {40,67,134}")
 
 
 def algorithmic_bytes(T: int, S: int, m: int) -> int:

@@ -252,11 +252,22 @@ def config(name: str) -> Workload:
         of 64 MiB, round-robin arbitration.
     C4  k=16 fat-tree (1024 hosts, 320 switches), all-to-all 64 KiB per pair.
     C5  4096 scenarios of a 4x4 torus, ring all-reduce of 4 MiB, seeded params.
+    NOC2_ag is the GPU-as-NoC sweep (see sim_inputs.noc).
     Suffixes change one thing of the workload: "_rhd", "_dbt" and "_ag" the
     collective (recursive halving-doubling or double binary tree all-reduce,
     ring all-gather; same buffer), "_chunk" the dependencies (per chunk, put
     + signal); e.g. "C5_dbt_chunk".
     """
+    if name == "NOC2_ag":
+        # two generic GPUs (448 nodes each) joined by 32 scale-up switches;
+        # put-based all-gather of 2 MiB of output per GPU by 32 workgroups
+        # per GPU (unroll 4, 64 outstanding); 1024 scenarios sweep the
+        # channel and scale-up cable latencies
+        from . import noc
+        w, lay = noc.gpu_noc(2)
+        w = noc.memcpy_workload(w, noc.allgather_ops(lay, 16384, n_wg=32, unroll=4, window=64),
+                                name="NOC2_2gpu_noc_allgather_2MiB_x1024")
+        return noc.with_scenarios(w, 1024, seed=2)
     if "_" in name:
         base, mod = name.rsplit("_", 1)
         w = config(base)
