@@ -55,7 +55,7 @@ def lib():
         L.oracle_txn.argtypes = [C.c_int, C.c_uint64, C.c_int32, C.c_int32, P, C.c_int32, C.c_int64,
                                  P, P, P, P, P]
         L.oracle_txn.restype = C.c_int
-        L.oracle_simulate.argtypes = [C.c_int32, C.c_int32, P, P, P, P, P, C.c_int32,
+        L.oracle_simulate.argtypes = [C.c_int32, C.c_int32, P, P, P, P, P, P, C.c_int32,
                                       C.c_int32, C.c_uint64, C.c_int32, P, C.c_int32,
                                       C.c_int64, P, P, P, P,
                                       C.c_uint64, C.c_int32, P, P, P, P, P]
@@ -151,7 +151,7 @@ class Result:
 
 
 def simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, *, coll=-1, nbytes=0, group=0,
-             order=None, dep=0, txns=None, max_cycles=0, check=False) -> Result:
+             order=None, dep=0, txns=None, max_cycles=0, check=False, credit=None) -> Result:
     """Run one scenario.  ``txns`` = (src, dst, pred_ptr, pred_idx) for a custom
     transaction list (coll = -1); otherwise ``coll``/``nbytes``/``group``."""
     row_ptr = np.ascontiguousarray(row_ptr, np.int32)
@@ -160,6 +160,7 @@ def simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, *, coll=-1, nbytes=0, gr
     bw = np.ascontiguousarray(bw, np.int32)[:m]
     lat = np.ascontiguousarray(lat, np.int32)[:m]
     cap = np.ascontiguousarray(cap, np.int32)[:m]
+    cr = None if credit is None else np.ascontiguousarray(credit, np.int32)[:m]
     o = None if order is None else np.ascontiguousarray(order, np.int32)
     if txns is not None:
         coll = -1
@@ -181,7 +182,7 @@ def simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, *, coll=-1, nbytes=0, gr
     busy = np.zeros(m, np.uint64)
     mk = np.zeros(1, np.uint32)
     st = _Stats()
-    rc = lib().oracle_simulate(n, E, _p(row_ptr), _p(col_idx), _p(bw), _p(lat), _p(cap), arb,
+    rc = lib().oracle_simulate(n, E, _p(row_ptr), _p(col_idx), _p(bw), _p(lat), _p(cap), _p(cr), arb,
                                coll, nbytes, group, _p(o), dep, T, _p(src), _p(dst), _p(pptr),
                                _p(pidx), max_cycles, 1 if check else 0, _p(comp), _p(tx),
                                _p(busy), _p(mk), C.byref(st))
@@ -196,6 +197,8 @@ def simulate_workload(w, scenario: int = 0, *, max_cycles=0, check=False) -> Res
     txns = None
     if w.meta.get("memcpy") is not None:
         txns = memcpy_txns(w.meta["memcpy"])
+    credit = None if getattr(w, "credit", None) is None else w.credit[sl]
     return simulate(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw[sl], w.lat[sl],
                     w.cap[sl], w.arb, coll=w.coll, nbytes=w.bytes, group=w.group_size,
-                    order=w.order, dep=w.dep, txns=txns, max_cycles=max_cycles, check=check)
+                    order=w.order, dep=w.dep, txns=txns, max_cycles=max_cycles, check=check,
+                    credit=credit)

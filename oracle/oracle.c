@@ -778,9 +778,14 @@ static int key_less(const req_t *a, const req_t *b, int arb, int32_t rr, int32_t
  * completion[T] (cycle, NEVER if not delivered), tx_lines[m], busy[m],
  * makespan.  max_cycles bounds the processed cycle (0 = 2^32 - 2).
  * check != 0 verifies the per-cycle and end-of-run invariants.
+ * credit (NULL = all 1): per-link credit return delay D >= 1.  A slot that a
+ * line frees by leaving link l at cycle t is seen free by l's arbiter from
+ * cycle t + D on; D = 1 is the start-of-cycle snapshot of the base model.
+ * (A flow-control variant: credits that travel back over the link take
+ * time, which also gives a parallel simulation D cycles of lookahead.)
  */
 int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t *col_idx,
-                    const int32_t *bw, const int32_t *lat, const int32_t *cap, int32_t arb,
+                    const int32_t *bw, const int32_t *lat, const int32_t *cap, const int32_t *credit, int32_t arb,
                     int32_t coll, uint64_t bytes, int32_t group, const int32_t *order, int32_t dep,
                     int64_t n_txn, const int32_t *csrc, const int32_t *cdst,
                     const int64_t *pred_ptr, const int64_t *pred_idx,
@@ -791,7 +796,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     if (n < 1 || E < 1 || E > n || !row_ptr || !col_idx) return OR_ERR_INVALID_ARG;
     int32_t m = row_ptr[n];
     for (int32_t l = 0; l < m; l++) {
-        if (bw[l] < 1 || lat[l] < 1 || cap[l] < 1) return OR_ERR_TOPOLOGY;
+        if (bw[l] < 1 || lat[l] < 1 || cap[l] < 1 || (credit && credit[l] < 1)) return OR_ERR_TOPOLOGY;
         if (col_idx[l] < 0 || col_idx[l] >= n) return OR_ERR_TOPOLOGY;
     }
     for (int32_t u = 0; u < n; u++)
@@ -884,6 +889,13 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     entry_t *qbuf = malloc(sizeof(entry_t) * (size_t)(q_off[m] > 0 ? q_off[m] : 1));
     int32_t *qhead = calloc((size_t)m, sizeof(int32_t));
     int32_t *qocc = calloc((size_t)m, sizeof(int32_t));
+    /* credits not yet returned: per link a queue (at most cap entries) of
+     * (return cycle, count), and the total owed */
+    uint64_t *owe_t = malloc(sizeof(uint64_t) * (size_t)(q_off[m] > 0 ? q_off[m] : 1));
+    int32_t *owe_n = malloc(sizeof(int32_t) * (size_t)(q_off[m] > 0 ? q_off[m] : 1));
+    int32_t *owe_h = calloc((size_t)m, sizeof(int32_t));    /* queue head */
+    int32_t *owe_c = calloc((size_t)m, sizeof(int32_t));    /* queue length */
+    int32_t *owed = calloc((size_t)m, sizeof(int32_t));     /* credits owed */
     int32_t *rr = calloc((size_t)m, sizeof(int32_t));
 
     int32_t bmax = 1;
@@ -923,6 +935,13 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
         processed++;
         size_t nr = 0;
         int32_t ntouched = 0, nactive = 0;
+        /* --- credits that are back by this cycle */
+        for (int32_t l = 0; l < m; l++)
+            while (owe_c[l] && owe_t[q_off[l] + owe_h[l]] <= t) {
+                owed[l] -= owe_n[q_off[l] + owe_h[l]];
+                owe_h[l] = (owe_h[l] + 1) % cap[l];
+                owe_c[l]--;
+            }
         /* --- requests from FIFOs */
         for (int32_t l = 0; l < m; l++) {
             if (qocc[l] == 0) continue;
@@ -986,7 +1005,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                 bk[b + 1] = v;
             }
             int32_t g = bw[f];
-            if (cap[f] - qocc[f] < g) g = cap[f] - qocc[f];
+            if (cap[f] - qocc[f] - owed[f] < g) g = cap[f] - qocc[f] - owed[f];
             if (cnt < g) g = cnt;
             for (int32_t a = 0; a < g; a++) reqs[bk[a]].granted = 1;
         }
@@ -1053,6 +1072,14 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                 if (check && dep > bw[sid]) rc = OR_ERR_INVARIANT;       /* departures <= b */
                 qhead[sid] = (qhead[sid] + dep) % cap[sid];
                 qocc[sid] -= dep;
+                if (credit && credit[sid] > 1) {   /* the freed slots come back later */
+                    int32_t at = (owe_h[sid] + owe_c[sid]) % cap[sid];
+                    owe_t[q_off[sid] + at] = t + (uint64_t)credit[sid];
+                    owe_n[q_off[sid] + at] = (int32_t)dep;
+                    owe_c[sid]++;
+                    owed[sid] += (int32_t)dep;
+                    if (check && qocc[sid] + owed[sid] > cap[sid]) rc = OR_ERR_INVARIANT;
+                }
             } else {
                 s_cur[sid - m] += dep;
             }
@@ -1089,6 +1116,8 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                 if (rel > t) { if (rel < next) next = rel; break; }
             }
         }
+        for (int32_t l = 0; l < m; l++)   /* the next credit to come back */
+            if (owe_c[l] && owe_t[q_off[l] + owe_h[l]] < next) next = owe_t[q_off[l] + owe_h[l]];
         if (next == UINT64_MAX) { rc = OR_ERR_DEADLOCK; break; }
         t = next;
     }
@@ -1134,7 +1163,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     }
     free(path_ptr); free(path_link); free(port_of); free(nports); free(tail_of);
     free(s_ptr); free(s_list); free(s_cur); free(preds); free(q_off); free(qbuf);
-    free(qhead); free(qocc); free(rr); free(reqs); free(bucket_n); free(bucket_off);
+    free(qhead); free(qocc); free(owe_t); free(owe_n); free(owe_h); free(owe_c); free(owed); free(rr); free(reqs); free(bucket_n); free(bucket_off);
     free(bucket); free(touched); free(active);
     for (size_t i = 0; w.coll == COLL_CUSTOM && i < (size_t)m * bmax; i++) free(hcache[i].preds);
     free(hcache); free(hpred); free(src_first); free(src_cnt); free(admit0); free(adm_cnt);

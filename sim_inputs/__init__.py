@@ -76,6 +76,7 @@ class Workload:
     order: Optional[np.ndarray] = None
     meta: dict = field(default_factory=dict)
     dep: int = 0                 # 0: per-line step dependencies, 1: per-chunk
+    credit: Optional[np.ndarray] = None  # int32 [S*m] credit return delay (None: 1)
 
     @property
     def n_links(self) -> int:
@@ -326,7 +327,8 @@ def take_scenarios(w: Workload, idx) -> Workload:
     m = w.n_links
     sel = (idx[:, None] * m + np.arange(m)[None, :]).reshape(-1)
     return replace(w, n_scenarios=len(idx), bw=w.bw[sel].copy(),
-                   lat=w.lat[sel].copy(), cap=w.cap[sel].copy())
+                   lat=w.lat[sel].copy(), cap=w.cap[sel].copy(),
+                   credit=None if w.credit is None else w.credit[sel].copy())
 
 
 def random_graph(rng: np.random.Generator, n_end: int, n_sw: int, extra: int,

@@ -66,14 +66,18 @@ def route(n, row_ptr, col_idx, s, d, dist):
     return path
 
 
-def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, max_cycles=10 ** 6):
-    """Returns (status, completion list, tx_lines, busy, makespan)."""
+def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, max_cycles=10 ** 6, credit=None):
+    """Returns (status, completion list, tx_lines, busy, makespan).  credit:
+    per-link credit delay D (default 1): the slot a line frees by leaving
+    link l at cycle t can be granted again from cycle t + D on."""
     row_ptr = [int(v) for v in row_ptr]
     col_idx = [int(v) for v in col_idx]
     m = row_ptr[-1]
     bw = [int(v) for v in bw[:m]]
     lat = [int(v) for v in lat[:m]]
     cap = [int(v) for v in cap[:m]]
+    credit = [1] * m if credit is None else [int(v) for v in credit[:m]]
+    owed = [[] for _ in range(m)]   # [cycle the credits come back, how many]
     tail = [u for u in range(n) for _ in range(row_ptr[u], row_ptr[u + 1])]
     ports = {v: sorted(l for l in range(m) if col_idx[l] == v) for v in range(n)}
     port_of = {l: ports[col_idx[l]].index(l) for l in range(m)}
@@ -102,6 +106,8 @@ def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, ma
     while any(c is None for c in comp):
         if t > max_cycles:
             return "MAX_CYCLES", comp, tx, busy, None
+        for l in range(m):
+            owed[l] = [c for c in owed[l] if c[0] > t]
         reqs = []   # dict(source, k, x, target, port, hop)
         for l in range(m):
             for k, (x, ready, hop) in enumerate(list(fifo[l])[:bw[l]]):
@@ -129,7 +135,7 @@ def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, ma
                 rs.sort(key=lambda r: r["x"])
             else:
                 rs.sort(key=lambda r: (r["k"], (r["port"] - rr[f]) % P))
-            g = min(bw[f], cap[f] - len(fifo[f]), len(rs))
+            g = min(bw[f], cap[f] - len(fifo[f]) - sum(c[1] for c in owed[f]), len(rs))
             for r in rs[:g]:
                 r["granted"] = True
             order_of[f] = rs
@@ -160,9 +166,12 @@ def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, ma
             if kind == "fifo":
                 for _ in range(ndep):
                     fifo[idx].popleft()
+                if ndep and credit[idx] > 1:
+                    owed[idx].append([t + credit[idx], ndep])
             else:
                 cursor[idx] += ndep
-        if departed == 0 and not any(e[1] > t for q in fifo for e in q) and any(c is None for c in comp):
+        if departed == 0 and not any(e[1] > t for q in fifo for e in q) and not any(owed) and \
+                any(c is None for c in comp):
             return "DEADLOCK", comp, tx, busy, None
         t += 1
     return "OK", comp, tx, busy, max(comp) if comp else 0
