@@ -23,6 +23,8 @@
  *     target FIFO in grant order and may leave at t + L; a line leaving its
  *     last link completes at t + 1;
  *   - cycles in which nothing can change are skipped;
+ *   - optionally (sim_set_credit) a freed slot returns to its link's
+ *     arbiter only some cycles after the line left;
  *   - routes are minimal-hop paths; ties between next hops are broken by the
  *     MurmurHash3 32-bit finalizer of (src << 16 | dst) (hash ECMP);
  *   - a line is injected once all its predecessor lines have completed
@@ -146,6 +148,20 @@ typedef enum {
 sim_status sim_create(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_ptr,
                       const int32_t *col_idx, int32_t n_scenarios, const int32_t *bw,
                       const int32_t *lat, const int32_t *cap, int32_t arb, sim_ctx **out);
+
+/*
+ * Credit-delay flow control (a flow-control variant of the model).
+ *   credit : [S*m] int32, scenario-major like bw/lat/cap; 1 <= credit <=
+ *            SIM_MAX_LAT; NULL = every delay 1.
+ * A slot that a line frees by leaving link l at cycle t is seen free by l's
+ * arbiter from cycle t + credit[l] on (1 = the start-of-cycle snapshot of
+ * the base model): credits that travel back to the sender take time, which
+ * also bounds how soon a link's state can affect its upstream neighbours.
+ * Returns of owed credits are events of the time advance.  Delays above 1
+ * are simulated by the workgroup engine.  Any loaded workload is dropped:
+ * call sim_load_* again before sim_run.  The array is copied.
+ */
+sim_status sim_set_credit(sim_ctx *ctx, const int32_t *credit);
 
 /*
  * Load a collective (replaces any previous workload).

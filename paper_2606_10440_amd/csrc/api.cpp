@@ -43,6 +43,7 @@ struct sim_ctx {
     int device = 0;
     std::vector<int32_t> row_ptr, col_idx, tail;
     std::vector<int32_t> bw, lat, cap;
+    std::vector<int32_t> credit;  // [S*m] credit return delays; empty = all 1
     std::vector<int32_t> hops;  // [E*n]: hop count from node v to endpoint d (-1 none)
 
     // loaded workload
@@ -802,11 +803,17 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     const int64_t b1_bytes = align16(align16(b1_words) + (b1_deliv_lds ? (int64_t)nflows * 4 : 0)) + 64;
     const bool b1_ok = bmax == 1 && (int64_t)s_link.size() <= 1024 && nl <= 8 * 1024 && nl < 65536 && b1_bytes <= kLds &&
                        (c->arb == SIM_ARB_LOWEST_ID || rr_ports_fit);
+    // credit delays above 1 are simulated by the workgroup engine only
+    const bool credits = !c->credit.empty();
+    if (credits) wv.ok = false;
+    const bool lane_ok = !credits && nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds;
+    const bool lanehbm_ok = !credits && nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds;
+    const bool b1_usable = !credits && nl >= 1 && b1_ok;
     int engine = simgpu::kEngineWorkgroup;
     if (wv.ok) engine = simgpu::kEngineWave;
-    else if (nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds) engine = simgpu::kEngineLane;
-    else if (nl >= 1 && b1_ok) engine = simgpu::kEngineB1;
-    else if (nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds) engine = simgpu::kEngineLaneHbm;
+    else if (lane_ok) engine = simgpu::kEngineLane;
+    else if (b1_usable) engine = simgpu::kEngineB1;
+    else if (lanehbm_ok) engine = simgpu::kEngineLaneHbm;
     if (const char *ev = std::getenv("SIMGPU_ENGINE")) {
         int want = -1;
         if (!std::strcmp(ev, "workgroup")) want = simgpu::kEngineWorkgroup;
@@ -814,11 +821,9 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         if (!std::strcmp(ev, "lanehbm")) want = simgpu::kEngineLaneHbm;
         if (!std::strcmp(ev, "b1")) want = simgpu::kEngineB1;
         if (!std::strcmp(ev, "wave")) want = simgpu::kEngineWave;
-        const bool ok = want == simgpu::kEngineWorkgroup ||
-                        (want == simgpu::kEngineWave && wv.ok) ||
-                        (want == simgpu::kEngineLane && nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds) ||
-                        (want == simgpu::kEngineLaneHbm && nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds) ||
-                        (want == simgpu::kEngineB1 && nl >= 1 && b1_ok);
+        const bool ok = want == simgpu::kEngineWorkgroup || (want == simgpu::kEngineWave && wv.ok) ||
+                        (want == simgpu::kEngineLane && lane_ok) || (want == simgpu::kEngineLaneHbm && lanehbm_ok) ||
+                        (want == simgpu::kEngineB1 && b1_usable);
         if (want < 0 || !ok) return fail(c, SIM_ERR_INVALID_ARG, std::string("SIMGPU_ENGINE=") + ev + " is not usable here");
         engine = want;
     }
@@ -961,6 +966,10 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     UP(c->bw, bw);
     UP(c->lat, lat);
     UP(c->cap, cap);
+    if (credits) {
+        int32_t *tmp_credit;
+        UP(c->credit, credit);
+    }
     int32_t *tmp_ln_P, *tmp_ln_port, *tmp_ln_fifo, *tmp_ln_mask, *tmp_ln_req, *tmp_ln_reqcap, *tmp_ln_srbeg,
         *tmp_ln_srend, *tmp_link_lane, *tmp_path_lane;
     UP(ln_P, ln_P);
@@ -1007,6 +1016,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     if (engine == simgpu::kEngineWorkgroup &&
         ((st = alloc(c, ost, S * ftot, &d.fifo_x)) || (st = alloc(c, ost, S * ftot, &d.fifo_rdy)) ||
         (st = alloc(c, ost, S * ftot, &d.fifo_pp)) || (st = alloc(c, ost, S * m, &d.qhead)) ||
+        (st = alloc(c, ost, S * m, &d.qcred)) ||
         (st = alloc(c, ost, S * m, &d.qtail)) || (st = alloc(c, ost, S * m, &d.rr)) ||
         (st = alloc(c, ost, S * d.ns, &d.cur_rng)) || (st = alloc(c, ost, S * d.ns, &d.cur_off)) ||
         (st = alloc(c, ost, S * nflows, &d.delivered)) || (st = alloc(c, ost, S * m, &d.req_cnt)) ||
@@ -1249,6 +1259,24 @@ sim_status route_impl(const sim_ctx *c, int32_t src, int32_t dst, int32_t *links
 
 
 
+sim_status set_credit_impl(sim_ctx *c, const int32_t *credit) {
+    if (!c) return SIM_ERR_INVALID_ARG;
+    const size_t pm = (size_t)c->S * (size_t)c->m;
+    bool any = false;
+    for (size_t i = 0; credit && i < pm; i++) {
+        if (credit[i] < 1 || credit[i] > SIM_MAX_LAT) return fail(c, SIM_ERR_INVALID_ARG, "credit delay out of range");
+        any |= credit[i] > 1;
+    }
+    if (any) c->credit.assign(credit, credit + pm);
+    else c->credit.clear();
+    // the engine and its tables depend on the delays: the workload is loaded again
+    free_list(c->dev_static);
+    free_list(c->dev_state);
+    c->loaded = false;
+    c->ran = false;
+    return SIM_OK;
+}
+
 }  // namespace
 
 // No C++ exception crosses the C ABI: allocation failures become
@@ -1272,6 +1300,10 @@ sim_status sim_create(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_p
                       int32_t n_scenarios, const int32_t *bw, const int32_t *lat, const int32_t *cap,
                       int32_t arb, sim_ctx **out) {
     return guarded(nullptr, [&] { return create_impl(n_nodes, n_endpoints, row_ptr, col_idx, n_scenarios, bw, lat, cap, arb, out); });
+}
+
+sim_status sim_set_credit(sim_ctx *c, const int32_t *credit) {
+    return guarded(c, [&] { return set_credit_impl(c, credit); });
 }
 
 sim_status sim_load_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t group_size, const int32_t *order,

@@ -10,7 +10,11 @@
 //      last hop complete (cycle + 1) and bump their flow's delivered count;
 //   E  targets append the departing lines in grant order (ready = t + L).
 // Then the next cycle is t + 1 if anything departed, otherwise the earliest
-// FIFO-head ready time (no such time = deadlock).
+// FIFO-head ready time or credit return (no such time = deadlock).
+//
+// With credit delays a line that leaves a FIFO keeps its slot until the
+// credit is back: the entry stays between qcred and qhead with the cycle it
+// left in place of its ready time.
 //
 // Predecessor release uses per-flow delivered counters: lines of one flow
 // (same source, destination and hence path) are injected in id order and
@@ -35,12 +39,14 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
     const int32_t *__restrict__ bw = d.bw + sm;
     const int32_t *__restrict__ lat = d.lat + sm;
     const int32_t *__restrict__ cap = d.cap + sm;
+    const int32_t *__restrict__ cred = d.credit ? d.credit + sm : nullptr;
     const size_t fo = (size_t)s * d.fifo_total;
     uint32_t *fx = d.fifo_x + fo;
     uint32_t *frdy = d.fifo_rdy + fo;
     int32_t *fpp = d.fifo_pp + fo;
     uint32_t *qhead = d.qhead + sm;
     uint32_t *qtail = d.qtail + sm;
+    uint32_t *qcred = d.qcred ? d.qcred + sm : nullptr;
     uint32_t *rr = d.rr + sm;
     int32_t *cur_rng = d.cur_rng + (size_t)s * d.ns;
     uint32_t *cur_off = d.cur_off + (size_t)s * d.ns;
@@ -66,6 +72,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
     for (int l = tid; l < m; l += kThreads) {
         qhead[l] = 0;
         qtail[l] = 0;
+        if (qcred) qcred[l] = 0;
         rr[l] = 0;
         req_cnt[l] = 0;
         gcount[l] = 0;
@@ -101,6 +108,15 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                 const uint32_t occ = qtail[l] - h;
                 const int b = bw[l];
                 const int base = d.fifo_off[l], mask = d.fifo_mask[l];
+                if (cred) {
+                    // slots of lines that left at least credit cycles ago are free
+                    // again; the next return is an event of the time advance
+                    const uint32_t D = (uint32_t)cred[l];
+                    uint32_t qc = qcred[l];
+                    while (qc != h && frdy[base + (int)(qc & (uint32_t)mask)] + D <= t) qc++;
+                    qcred[l] = qc;
+                    if (qc != h) atomicMin(&sh_next, frdy[base + (int)(qc & (uint32_t)mask)] + D);
+                }
                 int nr = 0;
                 for (int k = 0; k < b && (uint32_t)k < occ; k++) {
                     const int e = base + (int)((h + k) & (uint32_t)mask);
@@ -169,7 +185,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
             const uint32_t c = req_cnt[f];
             if (c == 0) continue;
             req_cnt[f] = 0;
-            const int occ = (int)(qtail[f] - qhead[f]);
+            const int occ = (int)(qtail[f] - (cred ? qcred[f] : qhead[f]));
             int g = bw[f];
             if (cap[f] - occ < g) g = cap[f] - occ;
             if ((int)c < g) g = (int)c;
@@ -217,6 +233,10 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
             if (dep) {
                 sh_anydep = 1;
                 if (src < m) {
+                    if (cred) {  // a left entry keeps its slot until its credit is back
+                        const int base = d.fifo_off[src], mask = d.fifo_mask[src];
+                        for (int k = 0; k < dep; k++) frdy[base + (int)((qhead[src] + (uint32_t)k) & (uint32_t)mask)] = t;
+                    }
                     qhead[src] += (uint32_t)dep;
                 } else {
                     const int j = src - m;

@@ -62,6 +62,7 @@ struct DevNet {
 
     // per-scenario parameters [S*m]
     const int32_t *bw, *lat, *cap;
+    const int32_t *credit;  // [S*m] credit return delay, or null when every delay is 1
 
     // per-scenario state
     uint32_t *fifo_x;     // [S*fifo_total] line id
@@ -69,6 +70,8 @@ struct DevNet {
     int32_t *fifo_pp;     // [S*fifo_total] path index of the link the entry is on
     uint32_t *qhead;      // [S*m] popped count
     uint32_t *qtail;      // [S*m] pushed count
+    uint32_t *qcred;      // [S*m] popped entries whose slot is free again (credit returned);
+                          // a popped entry's fifo_rdy then holds the cycle it left
     uint32_t *rr;         // [S*m] round-robin pointer
     int32_t *cur_rng;     // [S*ns] stream cursor: range
     uint32_t *cur_off;    // [S*ns] stream cursor: offset in range

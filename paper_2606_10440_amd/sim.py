@@ -1,6 +1,6 @@
 """Thin ctypes binding of libsimgpu (argument marshalling only).
 
-Functions keep the C ABI's names (``sim_create``, ``sim_load_collective``,
+Functions keep the C ABI's names (``sim_create``, ``sim_set_credit``, ``sim_load_collective``,
 ``sim_load_transactions``, ``sim_load_memcpy``, ``sim_sizes``, ``sim_run``,
 ``sim_status_after_sync``, ``sim_route``, ``sim_last_error``,
 ``sim_destroy``); ``Simulator`` bundles them with torch device buffers and
@@ -24,7 +24,8 @@ SIM_OK, SIM_ERR_INVALID_ARG, SIM_ERR_TOPOLOGY, SIM_ERR_UNREACHABLE, SIM_ERR_SIZE
 SIM_ERR_OOM, SIM_ERR_DEVICE, SIM_ERR_DEADLOCK, SIM_ERR_MAX_CYCLES, SIM_ERR_STATE = 5, 6, 7, 8, 9
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "TOPOLOGY", 3: "UNREACHABLE", 4: "SIZE", 5: "OOM",
                 6: "DEVICE", 7: "DEADLOCK", 8: "MAX_CYCLES", 9: "STATE"}
-EXPORTS = ("sim_create", "sim_load_collective", "sim_load_transactions", "sim_load_memcpy", "sim_sizes", "sim_run",
+EXPORTS = ("sim_create", "sim_set_credit", "sim_load_collective", "sim_load_transactions", "sim_load_memcpy",
+           "sim_sizes", "sim_run",
            "sim_status_after_sync", "sim_route", "sim_last_error", "sim_destroy")
 
 _lib = None
@@ -45,6 +46,7 @@ def lib():
         L = C.CDLL(LIB_PATH)
         P, i32, i64, u64 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64
         L.sim_create.argtypes = [i32, i32, P, P, i32, P, P, P, i32, C.POINTER(P)]
+        L.sim_set_credit.argtypes = [P, P]
         L.sim_load_collective.argtypes = [P, i32, u64, i32, P, i32]
         L.sim_load_transactions.argtypes = [P, i64, P, P, P, P]
         L.sim_load_memcpy.argtypes = [P, i64, P, P, P, P, P, P, C.c_int32, C.c_int32, P, C.c_int32, C.c_int32]
@@ -81,6 +83,11 @@ def sim_create(n_nodes, n_endpoints, row_ptr, col_idx, n_scenarios, bw, lat, cap
                           _ptr(arrs[2]), _ptr(arrs[3]), _ptr(arrs[4]), arb, C.byref(ctx))
     _check(None, st)
     return ctx
+
+
+def sim_set_credit(ctx, credit=None):
+    c = None if credit is None else np.ascontiguousarray(credit, np.int32)
+    _check(ctx, lib().sim_set_credit(ctx, _ptr(c)))
 
 
 def sim_load_collective(ctx, coll, nbytes, group_size=0, order=None, dep=0):
@@ -167,6 +174,8 @@ class Simulator:
     def from_workload(cls, w):
         sim = cls(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw, w.lat, w.cap, w.arb,
                   w.n_scenarios)
+        if w.credit is not None:
+            sim.set_credit(w.credit)
         if w.meta.get("memcpy") is not None:
             sim.load_memcpy(w.meta["memcpy"])
         elif w.coll >= 0:
@@ -175,6 +184,10 @@ class Simulator:
 
     def load_collective(self, coll, nbytes, group_size=0, order=None, dep=0):
         sim_load_collective(self.ctx, coll, nbytes, group_size, order, dep)
+
+    def set_credit(self, credit=None):
+        """Per-link credit return delays [S*m] (None: all 1); load again after."""
+        sim_set_credit(self.ctx, credit)
 
     def load_transactions(self, src, dst, pred_ptr, pred_idx):
         sim_load_transactions(self.ctx, src, dst, pred_ptr, pred_idx)

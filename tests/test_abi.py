@@ -185,3 +185,22 @@ def test_memcpy_argument_errors(simlib):
             assert e.value.status == simlib.SIM_ERR_INVALID_ARG, b
     finally:
         simlib.sim_destroy(ctx)
+
+
+def test_set_credit_errors(simlib):
+    w = si.config("C1")
+    ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, w.arb)
+    try:
+        for bad in (0, -1, (1 << 20) + 1):
+            v = np.ones(w.n_links, np.int32)
+            v[3] = bad
+            with pytest.raises(simlib.SimError) as e:
+                simlib.sim_set_credit(ctx, v)
+            assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+        simlib.sim_set_credit(ctx, np.full(w.n_links, 5, np.int32))
+        simlib.sim_set_credit(ctx, None)
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_run(ctx, 0, 0, 0, 0, 0)
+        assert e.value.status == simlib.SIM_ERR_STATE
+    finally:
+        simlib.sim_destroy(ctx)

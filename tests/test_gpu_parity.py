@@ -45,6 +45,8 @@ def say(*a):
 def run_gpu(simmod, w, max_cycles=0, txns=None):
     s = simmod.Simulator(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw, w.lat, w.cap, w.arb,
                          w.n_scenarios)
+    if w.credit is not None:
+        s.set_credit(w.credit)
     if txns is not None:
         s.load_transactions(*txns)
     elif w.meta.get("memcpy") is not None:
@@ -317,7 +319,8 @@ def check_engine(simmod, oracle_lib, w, engine, txns=None):
             want = oracle_lib.simulate_workload(w, s)
         else:
             want = oracle_lib.simulate(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw[sl], w.lat[sl],
-                                       w.cap[sl], w.arb, txns=txns)
+                                       w.cap[sl], w.arb, txns=txns,
+                                       credit=None if w.credit is None else w.credit[sl])
         if want.status_name == "DEADLOCK":
             compare_deadlocked(r, s, want)
         else:
