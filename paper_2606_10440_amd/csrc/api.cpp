@@ -803,9 +803,10 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     const int64_t b1_bytes = align16(align16(b1_words) + (b1_deliv_lds ? (int64_t)nflows * 4 : 0)) + 64;
     const bool b1_ok = bmax == 1 && (int64_t)s_link.size() <= 1024 && nl <= 8 * 1024 && nl < 65536 && b1_bytes <= kLds &&
                        (c->arb == SIM_ARB_LOWEST_ID || rr_ports_fit);
-    // credit delays above 1 are simulated by the workgroup engine only
+    // credit delays above 1 are simulated by the wave engine (not together
+    // with per-chunk dependencies) and the workgroup engine
     const bool credits = !c->credit.empty();
-    if (credits) wv.ok = false;
+    if (credits && R.whole) wv.ok = false;
     const bool lane_ok = !credits && nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds;
     const bool lanehbm_ok = !credits && nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds;
     const bool b1_usable = !credits && nl >= 1 && b1_ok;

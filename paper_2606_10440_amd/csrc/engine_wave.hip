@@ -184,8 +184,10 @@ __device__ __forceinline__ void merge_low(K (&a)[N], const K (&b)[N]) {
 }
 
 // NF: request-slot groups per target lane (feeders, then the lane's own
-// stream in group NF - 1).  CH: per-chunk step dependencies.
-template <int BM, int ARB, int NF, bool CH>
+// stream in group NF - 1).  CH: per-chunk step dependencies.  CR: credit
+// delays -- a line that leaves keeps its ring slot, with the cycle it left
+// in place of its ready time, until its credit is back.
+template <int BM, int ARB, int NF, bool CH, bool CR>
 __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
     extern __shared__ __align__(16) unsigned char smem[];
     // the workgroup's waves are independent: each has its own LDS region and
@@ -209,6 +211,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
     // lane registers
     int link = 0, b = 1;
     uint32_t L = 1, cap = 1, P = 1;
+    uint32_t D = 1;  // credit delay (CR)
     uint32_t lfb = 0, lfx = 0;  // local-flow tables (one byte per local flow)
     uint32_t fl = 0, fp = 0;    // feeder wave lanes and their ports, one byte each
     int R = 0, rend = 0;
@@ -220,6 +223,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
         b = d.bw[pi];
         L = (uint32_t)d.lat[pi];
         cap = (uint32_t)d.cap[pi];
+        if constexpr (CR) D = (uint32_t)d.credit[pi];
         P = (uint32_t)d.ln_P[i];
         lfb = d.wv_lfb[i];
         lfx = d.wv_lfx[i];
@@ -287,6 +291,9 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
     bool live = on && d.T > 0;
     int32_t state = live ? kRunRunning : kRunOk;
     uint32_t occ = 0, head = 0, tail = 0, rr = 0;
+    // CR: owed credits are the ring entries ch .. head-1; crt = cycle the
+    // oldest comes back (credits come back in the order the lines left)
+    uint32_t owed = 0, ch = 0, crt = kNever;
     uint64_t tx = 0, busy = 0;
     uint32_t dv0 = 0, dv1 = 0;
     // a line id outside [0, T) can only come from an engine fault: the store
@@ -309,6 +316,18 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
     auto refresh_dv = [&]() {
         if (__ballot(cur.np > 0u) != 0ull) dv0 = deliv[cur.ix0];
         if (__ballot(cur.np > 1u) != 0ull) dv1 = deliv[cur.ix1];
+    };
+    // CR: slots whose credit is back by the (new) cycle t are free again
+    auto credits_back = [&]() {
+        bool pop = live & (owed != 0u) & (crt <= t);
+        while (__ballot(pop) != 0ull) {
+            if (pop) {
+                ch = wrap_add(ch, 1u, cap);
+                owed -= 1u;
+                crt = owed != 0u ? ring[rbase + ch].y + D : kNever;
+            }
+            pop = live & (owed != 0u) & (crt <= t);
+        }
     };
     // End of cycle: clock and status of every scenario of the wave.  nxt is
     // the lane's FIFO-head ready time if still in the future at the start of
@@ -370,7 +389,8 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             const bool sw = live & (R < rend) & released_one<CH>(d, cur, o, dv0, dv1, deliv);
             const uint32_t skey = ((cur.start + o) << kXs) | (cur.lf << 5) | 1u;
             atomicMin(&word[sw ? (uint32_t)w : 64u + (uint32_t)w], skey);
-            const uint32_t nxt = (live & (occ != 0u) & (hr > t)) ? hr : kNever;
+            uint32_t nxt = (live & (occ != 0u) & (hr > t)) ? hr : kNever;
+            if constexpr (CR) nxt = min(nxt, (live & (owed != 0u)) ? crt : kNever);
             atomicMin(&red[nxt != kNever ? (uint32_t)g : 64u + (uint32_t)w], nxt);
             cbar();
             const uint32_t wt = word[tgw];
@@ -388,6 +408,11 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                 atomicAdd(&deliv[mydx + q], 1u);
             }
             ring[app ? rbase + tail : ring_trash] = make_uint2(wm & ~0x1Fu, t + L);
+            if constexpr (CR) {  // the slot stays owed until the credit is back
+                ring[fwon ? rbase + head : ring_trash] = make_uint2(hx, t);
+                crt = (fwon & (owed == 0u)) ? t + D : crt;
+                owed += fwon ? 1u : 0u;
+            }
             head = fwon ? wrap_add(head, 1u, cap) : head;
             tail = app ? wrap_add(tail, 1u, cap) : tail;
             occ = occ - (fwon ? 1u : 0u) + (app ? 1u : 0u);
@@ -395,11 +420,16 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             o += swon ? 1u : 0u;
             if (o >= cur.len) next_range();
             cbar();
-            word[w] = occ < cap ? kWordEmpty : kWordFull;
+            if constexpr (!CR) word[w] = occ < cap ? kWordEmpty : kWordFull;
             red[i == 0 ? (uint32_t)g : 64u + (uint32_t)w] = kNever;
             he = ring[rbase + head];
             refresh_dv();
             time_phase(fwon | swon, nxt, rv, false);
+            if constexpr (CR) {  // fullness at the next processed cycle
+                credits_back();
+                word[w] = occ + owed < cap ? kWordEmpty : kWordFull;
+                cbar();
+            }
         }
         busy = tx;  // one line per cycle at most
       }
@@ -450,7 +480,8 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                 nf += offk ? 1u : 0u;
                 open = offk;
             }
-            const uint32_t nxt = (live & (occ != 0u) & (e[0].y > t)) ? e[0].y : kNever;
+            uint32_t nxt = (live & (occ != 0u) & (e[0].y > t)) ? e[0].y : kNever;
+            if constexpr (CR) nxt = min(nxt, (live & (owed != 0u)) ? crt : kNever);
             // stream offers: the released lines of the current range, then (rarely)
             // of the ranges after it
             // (the lane is their source and their target: they stay in registers)
@@ -509,7 +540,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             uint32_t nval = 0;
 #pragma unroll
             for (int r = 0; r < BMW; r++) nval += lst[r] != kMax ? 1u : 0u;
-            const uint32_t gcnt = live ? min(min((uint32_t)b, cap - occ), nval) : 0u;
+            const uint32_t gcnt = live ? min(min((uint32_t)b, cap - occ - (CR ? owed : 0u)), nval) : 0u;
             uint32_t sgr = 0, lastport = 0;
             const uint32_t ready = t + L;
 #pragma unroll
@@ -556,6 +587,14 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                     }
                 }
             }
+            if constexpr (CR) {  // left slots stay owed until their credits are back
+#pragma unroll
+                for (int k = 0; k < BMW; k++)
+                    ring[(uint32_t)k < depf ? rbase + wrap_add(head, (uint32_t)k, cap) : ring_trash] =
+                        make_uint2(e[k].x, t);
+                crt = ((depf != 0u) & (owed == 0u)) ? t + D : crt;
+                owed += depf;
+            }
             head = wrap_add(head, depf, cap);
             occ -= depf;
             o += sgr;
@@ -592,6 +631,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             for (int k = 0; k < BMW; k++) e[k] = ring[rbase + wrap_add(head, min((uint32_t)k, cap - 1u), cap)];
             refresh_dv();
             time_phase((depf | sgr) != 0u, nxt, kNever, true);
+            if constexpr (CR) credits_back();
         }
     };
     if constexpr (kGeneral) {
@@ -622,9 +662,12 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
 
 template <int BM, int ARB, int NF>
 hipError_t launch_wave3(const DevNet &d, hipStream_t st) {
-    // per-chunk dependencies get their own instantiation: the per-line
-    // release test then carries no mask
-    auto k = d.pd_omask == 0u ? engine_wave<BM, ARB, NF, true> : engine_wave<BM, ARB, NF, false>;
+    // per-chunk dependencies and credit delays get their own instantiations,
+    // so that the base loops carry neither; the host does not pick this
+    // engine for the two together
+    if (d.credit && d.pd_omask == 0u) return hipErrorInvalidValue;
+    auto k = d.credit ? engine_wave<BM, ARB, NF, false, true>
+                      : d.pd_omask == 0u ? engine_wave<BM, ARB, NF, true, false> : engine_wave<BM, ARB, NF, false, false>;
     if (d.lds_bytes > 65536)
         (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
     hipLaunchKernelGGL(k, dim3((unsigned)d.wv_nblk), dim3(64 * d.wv_wpb), (unsigned)d.lds_bytes, st, d);

@@ -68,3 +68,30 @@ def test_credit_reset_restores_base_model(simmod, oracle_lib):
         comp = b.completion[k, :len(base.completion)].cpu().numpy().view(np.uint32)
         assert np.array_equal(comp, base.completion)
     assert a.status == 0
+
+
+@pytest.mark.parametrize("arb", [0, 1])
+@pytest.mark.parametrize("bws", [(1,), (1, 2, 4), (8,), (2, 8)])
+def test_credit_wave_torus(simmod, oracle_lib, arb, bws):
+    """The wave engine's b = 1 loop and its general loop with delays."""
+    w = si.torus2d(4, 4, n_scenarios=13, seed=170 + arb + len(bws), bws=bws, lat_lo=1, lat_hi=25,
+                   depths=(1, 2, 3, 7, 32), nbytes=128 * 16 * 6, arb=arb)
+    w.credit = np.random.default_rng(arb + 7 * len(bws)).integers(1, 14, size=len(w.bw)).astype(np.int32)
+    check_engine(simmod, oracle_lib, w, "wave")
+
+
+@pytest.mark.parametrize("engine", ["wave", "workgroup"])
+def test_credit_wave_full_size_sample(simmod, oracle_lib, engine):
+    w = si.take_scenarios(si.config("C5"), [3, 7, 2048, 4000])
+    w.credit = w.lat.copy()
+    check_engine(simmod, oracle_lib, w, engine)
+
+
+def test_credit_with_chunk_dependencies_not_on_wave(simmod, oracle_lib):
+    # the wave engine has no instantiation for both: the workgroup engine runs it
+    w = si.torus2d(4, 4, n_scenarios=3, seed=5, bws=(1, 2), lat_lo=1, lat_hi=9, depths=(2, 5), nbytes=128 * 16 * 2)
+    w.dep = si.DEP_CHUNK
+    w.credit = np.full(len(w.bw), 4, np.int32)
+    check_vs_oracle(simmod, oracle_lib, w)
+    with pytest.raises(pytest.skip.Exception):
+        check_engine(simmod, oracle_lib, w, "wave")
