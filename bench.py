@@ -44,6 +44,7 @@ for _k in ("C1", "C2", "C5"):
 for _k, _c in (("rhd", "recursive halving-doubling all-reduce"), ("dbt", "double binary tree all-reduce"),
                ("ag", "ring all-gather")):
     DESCR["C5_" + _k] = DESCR["C5"].replace("ring all-reduce", _c)
+DESCR["C5_credit"] = DESCR["C5"] + "; credit delay = link latency"
 DESCR["NOC2_ag"] = ("1024 scenarios x 2 generic GPUs as NoCs (448 nodes each) + 32 scale-up switches, "
                     "put-based all-gather 2 MiB out per GPU as memcpy programs (32 WGs/GPU, unroll 4, "
                     "64 outstanding), channel latency in {1,2,4,8}, scale-up cable latency in {40,67,134}")

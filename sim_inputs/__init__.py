@@ -257,7 +257,8 @@ def config(name: str) -> Workload:
     Suffixes change one thing of the workload: "_rhd", "_dbt" and "_ag" the
     collective (recursive halving-doubling or double binary tree all-reduce,
     ring all-gather; same buffer), "_chunk" the dependencies (per chunk, put
-    + signal); e.g. "C5_dbt_chunk".
+    + signal), "_credit" the flow control (credit delay = link latency);
+    e.g. "C5_dbt_chunk".
     """
     if name == "NOC2_ag":
         # two generic GPUs (448 nodes each) joined by 32 scale-up switches;
@@ -274,6 +275,9 @@ def config(name: str) -> Workload:
         w = config(base)
         if mod == "chunk":
             return replace(w, dep=DEP_CHUNK, name=w.name + "_chunkdep")
+        if mod == "credit":
+            # credits travel back over the link: credit delay = link latency
+            return replace(w, credit=w.lat.copy(), name=w.name + "_creditlat")
         colls = {"rhd": (COLL_RHD_ALLREDUCE, "rhd_ar"), "dbt": (COLL_DBT_ALLREDUCE, "dbt_ar"),
                  "ag": (COLL_RING_ALLGATHER, "ring_ag")}
         if mod in colls and w.coll in (COLL_RING_ALLREDUCE, COLL_DIRECT_ALLREDUCE):

@@ -257,7 +257,7 @@ def test_full_size_digest(simmod, torch_cuda, name):
     assert _digest(r.busy_cycles[0].cpu().numpy().astype("<u8")) == g["busy_cycles_sha256"][0]
 
 
-@pytest.mark.parametrize("name", ["C5", "C5_chunk", "C5_rhd", "C5_dbt", "C5_ag", "NOC2_ag"])
+@pytest.mark.parametrize("name", ["C5", "C5_chunk", "C5_rhd", "C5_dbt", "C5_ag", "C5_credit", "NOC2_ag"])
 def test_full_size_batched_digest(simmod, torch_cuda, name):
     g = _golden(name)
     w = si.config(name)
