@@ -57,12 +57,12 @@ def lib():
         L.oracle_txn.restype = C.c_int
         L.oracle_simulate.argtypes = [C.c_int32, C.c_int32, P, P, P, P, P, P, C.c_int32,
                                       C.c_int32, C.c_uint64, C.c_int32, P, C.c_int32,
-                                      C.c_int64, P, P, P, P,
+                                      C.c_int64, P, P, P, P, P,
                                       C.c_uint64, C.c_int32, P, P, P, P, P]
         L.oracle_simulate.restype = C.c_int
         i32, i64 = C.c_int32, C.c_int64
         L.oracle_memcpy.argtypes = [i64, P, P, P, P, P, P, i32, i32, P, i32, i32, i64, i64,
-                                    P, P, P, P, P, P]
+                                    P, P, P, P, P, P, P]
         L.oracle_memcpy.restype = C.c_int
         _lib = L
     return _lib
@@ -106,9 +106,9 @@ def txn(coll, nbytes, group, E, x, order=None, dep=0):
     return rc, int(src[0]), int(dst[0]), [int(v) for v in preds[:npred[0]]], int(T[0])
 
 
-def memcpy_txns(mc):
+def memcpy_txns(mc, with_class=False):
     """Expand memcpy programs (``sim_inputs.noc.Memcpy``) into the line list
-    (src, dst, pred_ptr, pred_idx)."""
+    (src, dst, pred_ptr, pred_idx) [+ per-line class: 1 = load request]."""
     n_ops = len(mc.cu)
     cu = np.ascontiguousarray(mc.cu, np.int32)
     ssp = np.ascontiguousarray(mc.src_space, np.int32)
@@ -121,16 +121,20 @@ def memcpy_txns(mc):
     T = np.zeros(1, np.int64)
     P = np.zeros(1, np.int64)
     args = (n_ops, _p(cu), _p(ssp), _p(dsp), _p(sl), _p(dl), _p(nl), n_spaces, mc.n_ch, _p(ch), mc.unroll, mc.window)
-    rc = lib().oracle_memcpy(*args, 0, 0, None, None, None, None, _p(T), _p(P))
+    rc = lib().oracle_memcpy(*args, 0, 0, None, None, None, None, None, _p(T), _p(P))
     if rc:
         raise ValueError(f"oracle_memcpy: status {rc}")
     src = np.zeros(max(int(T[0]), 1), np.int32)
     dst = np.zeros(max(int(T[0]), 1), np.int32)
     pptr = np.zeros(int(T[0]) + 1, np.int64)
     pidx = np.zeros(max(int(P[0]), 1), np.int64)
-    rc = lib().oracle_memcpy(*args, int(T[0]), int(P[0]), _p(src), _p(dst), _p(pptr), _p(pidx), _p(T), _p(P))
+    cls = np.zeros(max(int(T[0]), 1), np.uint8)
+    rc = lib().oracle_memcpy(*args, int(T[0]), int(P[0]), _p(src), _p(dst), _p(pptr), _p(pidx), _p(cls),
+                             _p(T), _p(P))
     assert rc == 0
     t = int(T[0])
+    if with_class:
+        return src[:t], dst[:t], pptr, pidx[:int(P[0])], cls[:t]
     return src[:t], dst[:t], pptr, pidx[:int(P[0])]
 
 
@@ -151,7 +155,7 @@ class Result:
 
 
 def simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, *, coll=-1, nbytes=0, group=0,
-             order=None, dep=0, txns=None, max_cycles=0, check=False, credit=None) -> Result:
+             order=None, dep=0, txns=None, max_cycles=0, check=False, credit=None, cls=None) -> Result:
     """Run one scenario.  ``txns`` = (src, dst, pred_ptr, pred_idx) for a custom
     transaction list (coll = -1); otherwise ``coll``/``nbytes``/``group``."""
     row_ptr = np.ascontiguousarray(row_ptr, np.int32)
@@ -171,7 +175,9 @@ def simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, *, coll=-1, nbytes=0, gr
         if len(pidx) == 0:
             pidx = np.zeros(1, np.int64)
         T = len(src)
+        cls = None if cls is None else np.ascontiguousarray(cls, np.uint8)
     else:
+        cls = None
         src = dst = pptr = pidx = None
         rc, _, _, _, T = txn(coll, nbytes, group, E, 0, order, dep)
         if rc:
@@ -183,7 +189,7 @@ def simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, *, coll=-1, nbytes=0, gr
     mk = np.zeros(1, np.uint32)
     st = _Stats()
     rc = lib().oracle_simulate(n, E, _p(row_ptr), _p(col_idx), _p(bw), _p(lat), _p(cap), _p(cr), arb,
-                               coll, nbytes, group, _p(o), dep, T, _p(src), _p(dst), _p(pptr),
+                               coll, nbytes, group, _p(o), dep, T, _p(src), _p(dst), _p(cls), _p(pptr),
                                _p(pidx), max_cycles, 1 if check else 0, _p(comp), _p(tx),
                                _p(busy), _p(mk), C.byref(st))
     return Result(rc, comp[:T], tx, busy, int(mk[0]), int(st.processed_cycles),
@@ -194,11 +200,11 @@ def simulate_workload(w, scenario: int = 0, *, max_cycles=0, check=False) -> Res
     """Run scenario ``scenario`` of a ``sim_inputs.Workload``."""
     m = w.n_links
     sl = slice(scenario * m, (scenario + 1) * m)
-    txns = None
+    txns = cls = None
     if w.meta.get("memcpy") is not None:
-        txns = memcpy_txns(w.meta["memcpy"])
+        *txns, cls = memcpy_txns(w.meta["memcpy"], with_class=True)
     credit = None if getattr(w, "credit", None) is None else w.credit[sl]
     return simulate(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw[sl], w.lat[sl],
                     w.cap[sl], w.arb, coll=w.coll, nbytes=w.bytes, group=w.group_size,
                     order=w.order, dep=w.dep, txns=txns, max_cycles=max_cycles, check=check,
-                    credit=credit)
+                    credit=credit, cls=cls)

@@ -590,14 +590,16 @@ int oracle_txn(int coll, uint64_t bytes, int32_t group, int32_t E, const int32_t
  * network: all of a CU's requests leave through its one link, in id order.
  * Line a of space s lives on channel space_ch[s * n_ch + a mod n_ch].
  * Ids are step-major: for issue index k = 0, 1, ... and the CUs in ascending
- * endpoint order, a load takes two ids (request, then data), a store one. */
+ * endpoint order, a load takes two ids (request, then data), a store one.
+ * A load request is a control message (class 1); data lines and stores are
+ * data (class 0). */
 typedef struct { int kind; int32_t chan; int64_t g0, gn; } minstr_t;   /* kind 0 load, 1 store */
 
 int oracle_memcpy(int64_t n_ops, const int32_t *cu, const int32_t *ssp, const int32_t *dsp,
                   const int64_t *sline, const int64_t *dline, const int64_t *nlines,
                   int32_t n_spaces, int32_t n_ch, const int32_t *space_ch, int32_t U, int32_t W,
                   int64_t cap_txn, int64_t cap_pred, int32_t *src, int32_t *dst,
-                  int64_t *pred_ptr, int64_t *pred_idx, int64_t *T_out, int64_t *P_out)
+                  int64_t *pred_ptr, int64_t *pred_idx, uint8_t *cls, int64_t *T_out, int64_t *P_out)
 {
     if (n_ops < 0 || n_ch < 1 || n_spaces < 1 || U < 1 || W < 1) return OR_ERR_INVALID_ARG;
     /* the CUs, ascending */
@@ -662,6 +664,7 @@ int oracle_memcpy(int64_t n_ops, const int32_t *cu, const int32_t *ssp, const in
             if (cap_txn >= T && cap_pred >= P + need) {
                 src[x] = cus[q];
                 dst[x] = in->chan;
+                if (cls) cls[x] = in->kind == 0 ? 1 : 0;   /* a load request is a control message */
                 pred_ptr[x] = P;
                 int64_t w = P;
                 if (k >= W) pred_idx[w++] = DONE(q, k - W);
@@ -671,6 +674,7 @@ int oracle_memcpy(int64_t n_ops, const int32_t *cu, const int32_t *ssp, const in
                 if (in->kind == 0) {       /* the data line: waits for its request */
                     src[x + 1] = in->chan;
                     dst[x + 1] = cus[q];
+                    if (cls) cls[x + 1] = 0;
                     pred_idx[w++] = x;
                     pred_ptr[x + 2] = w;
                 }
@@ -765,14 +769,15 @@ static uint64_t release_of(const hcache_t *c, const uint32_t *completion, const 
 
 static int key_less(const req_t *a, const req_t *b, int arb, int32_t rr, int32_t P)
 {
-    if (arb == 0) return a->x < b->x;
+    if ((arb & 1) == 0) return a->x < b->x;
     if (a->k != b->k) return a->k < b->k;
     return pmod(a->port - rr, P) < pmod(b->port - rr, P);
 }
 
 /*
  * Run one scenario.  Inputs: CSR topology (endpoints are nodes 0..E-1), the
- * per-link bw/lat/cap, the arbitration policy (0 lowest id, 1 round-robin),
+ * per-link bw/lat/cap, the arbitration policy (0 lowest id, 1 round-robin,
+ * plus 2 for class-fair arbitration, see below),
  * and either a collective (coll >= 0) or a custom transaction list
  * (coll == -1: n_txn lines with src/dst and predecessor CSR).  Outputs:
  * completion[T] (cycle, NEVER if not delivered), tx_lines[m], busy[m],
@@ -783,11 +788,17 @@ static int key_less(const req_t *a, const req_t *b, int arb, int32_t rr, int32_t
  * cycle t + D on; D = 1 is the start-of-cycle snapshot of the base model.
  * (A flow-control variant: credits that travel back over the link take
  * time, which also gives a parallel simulation D cycles of lookahead.)
+ * cls (NULL = all 0): class of every line of a custom list, 0 data, 1
+ * control.  With arb & 2 (the fair arbitration of control and data messages
+ * of Sec. 5.2) a link orders each class's requests by the usual key and
+ * interleaves the two classes, starting with the class its pointer names;
+ * after a cycle in which it appended lines, the pointer names the class
+ * other than that of the last line appended.  Pointers start at data.
  */
 int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t *col_idx,
                     const int32_t *bw, const int32_t *lat, const int32_t *cap, const int32_t *credit, int32_t arb,
                     int32_t coll, uint64_t bytes, int32_t group, const int32_t *order, int32_t dep,
-                    int64_t n_txn, const int32_t *csrc, const int32_t *cdst,
+                    int64_t n_txn, const int32_t *csrc, const int32_t *cdst, const uint8_t *cls,
                     const int64_t *pred_ptr, const int64_t *pred_idx,
                     uint64_t max_cycles, int32_t check,
                     uint32_t *completion, uint64_t *tx_lines, uint64_t *busy,
@@ -896,12 +907,14 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     int32_t *owe_h = calloc((size_t)m, sizeof(int32_t));    /* queue head */
     int32_t *owe_c = calloc((size_t)m, sizeof(int32_t));    /* queue length */
     int32_t *owed = calloc((size_t)m, sizeof(int32_t));     /* credits owed */
+    int32_t *cptr = calloc((size_t)m, sizeof(int32_t));     /* class-fair pointer */
     int32_t *rr = calloc((size_t)m, sizeof(int32_t));
 
     int32_t bmax = 1;
     for (int32_t l = 0; l < m; l++) if (bw[l] > bmax) bmax = bw[l];
     size_t rcap = (size_t)2 * m * bmax + 1;
     req_t *reqs = malloc(sizeof(req_t) * rcap);
+    int32_t *fair_a = malloc(sizeof(int32_t) * rcap), *fair_b = malloc(sizeof(int32_t) * rcap);
     /* per-target request slots: at most (input ports of its tail) * bmax */
     int32_t *bucket_n = calloc((size_t)m, sizeof(int32_t));
     int64_t *bucket_off = malloc(sizeof(int64_t) * ((size_t)m + 1));
@@ -1004,6 +1017,16 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                 }
                 bk[b + 1] = v;
             }
+            if (arb & 2) {   /* the classes interleaved, each in key order */
+                int32_t na = 0, nb = 0;
+                for (int32_t a = 0; a < cnt; a++) {
+                    int c = cls ? cls[reqs[bk[a]].x] : 0;
+                    if (c == cptr[f]) fair_a[na++] = bk[a]; else fair_b[nb++] = bk[a];
+                }
+                int32_t ia = 0, ib = 0;
+                for (int32_t a = 0; a < cnt; a++)
+                    bk[a] = (ia < na && (ib >= nb || ia <= ib)) ? fair_a[ia++] : fair_b[ib++];
+            }
             int32_t g = bw[f];
             if (cap[f] - qocc[f] - owed[f] < g) g = cap[f] - qocc[f] - owed[f];
             if (cnt < g) g = cnt;
@@ -1025,7 +1048,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
             int32_t cnt = bucket_n[f];
             bucket_n[f] = 0;
             int32_t *bk = bucket + bucket_off[f];
-            int32_t entered = 0, last_port = -1;
+            int32_t entered = 0, last_port = -1, last_cls = 0;
             for (int32_t a = 0; a < cnt; a++) {
                 req_t *r = &reqs[bk[a]];
                 if (!r->departs) continue;
@@ -1035,12 +1058,14 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                 qocc[f]++;
                 entered++;
                 last_port = r->port;
+                last_cls = cls ? cls[r->x] : 0;
                 if (admit0 && r->hop == 0) admit0[r->x] = (uint32_t)t;
             }
             if (entered) {
                 tx_lines[f] += (uint64_t)entered;
                 busy[f] += 1;
-                if (arb == 1) rr[f] = (last_port + 1) % nports[tail_of[f]];
+                if (arb & 1) rr[f] = (last_port + 1) % nports[tail_of[f]];
+                if (arb & 2) cptr[f] = 1 - last_cls;
                 if (check) {
                     if (entered > bw[f]) rc = OR_ERR_INVARIANT;         /* admissions <= b */
                     if (qocc[f] > cap[f]) rc = OR_ERR_INVARIANT;         /* occupancy <= cap */
@@ -1163,7 +1188,8 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     }
     free(path_ptr); free(path_link); free(port_of); free(nports); free(tail_of);
     free(s_ptr); free(s_list); free(s_cur); free(preds); free(q_off); free(qbuf);
-    free(qhead); free(qocc); free(owe_t); free(owe_n); free(owe_h); free(owe_c); free(owed); free(rr); free(reqs); free(bucket_n); free(bucket_off);
+    free(qhead); free(qocc); free(owe_t); free(owe_n); free(owe_h); free(owe_c); free(owed); free(cptr); free(rr);
+    free(fair_a); free(fair_b); free(reqs); free(bucket_n); free(bucket_off);
     free(bucket); free(touched); free(active);
     for (size_t i = 0; w.coll == COLL_CUSTOM && i < (size_t)m * bmax; i++) free(hcache[i].preds);
     free(hcache); free(hpred); free(src_first); free(src_cnt); free(admit0); free(adm_cnt);

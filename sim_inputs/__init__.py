@@ -26,6 +26,7 @@ LINE_BYTES = 128  # one cache line = one transaction (the paper's wavefront requ
 
 ARB_LOWEST_ID = 0
 ARB_ROUND_ROBIN = 1
+ARB_FAIR_CLASSES = 2   # flag: control and data messages take turns at every link
 
 COLL_RING_ALLREDUCE = 0
 COLL_DIRECT_ALLREDUCE = 1

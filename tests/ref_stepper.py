@@ -66,10 +66,15 @@ def route(n, row_ptr, col_idx, s, d, dist):
     return path
 
 
-def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, max_cycles=10 ** 6, credit=None):
+def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, max_cycles=10 ** 6, credit=None,
+                  cls=None):
     """Returns (status, completion list, tx_lines, busy, makespan).  credit:
     per-link credit delay D (default 1): the slot a line frees by leaving
-    link l at cycle t can be granted again from cycle t + D on."""
+    link l at cycle t can be granted again from cycle t + D on.  arb: 0
+    lowest id, 1 round-robin, +2 class-fair: each class (cls[x], 0 data, 1
+    control) in key order, the two alternating from the class the link's
+    pointer names; after appending, the pointer names the class other than
+    the last appended line's."""
     row_ptr = [int(v) for v in row_ptr]
     col_idx = [int(v) for v in col_idx]
     m = row_ptr[-1]
@@ -99,6 +104,8 @@ def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, ma
     cursor = {f: 0 for f in streams}
     fifo = [deque() for _ in range(m)]   # [line, ready, hop]
     rr = [0] * m
+    cptr = [0] * m
+    cls = [0] * len(src) if cls is None else [int(v) for v in cls]
     comp = [None] * T
     tx = [0] * m
     busy = [0] * m
@@ -131,10 +138,19 @@ def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, ma
         for f in set(r["target"] for r in reqs if r["target"] is not SINK):
             rs = [r for r in reqs if r["target"] == f]
             P = nports[tail[f]]
-            if arb == 0:
+            if arb & 1 == 0:
                 rs.sort(key=lambda r: r["x"])
             else:
                 rs.sort(key=lambda r: (r["k"], (r["port"] - rr[f]) % P))
+            if arb & 2:
+                first = [r for r in rs if cls[r["x"]] == cptr[f]]
+                second = [r for r in rs if cls[r["x"]] != cptr[f]]
+                rs = []
+                while first or second:
+                    if first:
+                        rs.append(first.pop(0))
+                    if second:
+                        rs.append(second.pop(0))
             g = min(bw[f], cap[f] - len(fifo[f]) - sum(c[1] for c in owed[f]), len(rs))
             for r in rs[:g]:
                 r["granted"] = True
@@ -156,8 +172,10 @@ def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, ma
             if moved:
                 tx[f] += len(moved)
                 busy[f] += 1
-                if arb == 1:
+                if arb & 1:
                     rr[f] = (moved[-1]["port"] + 1) % nports[tail[f]]
+                if arb & 2:
+                    cptr[f] = 1 - cls[moved[-1]["x"]]
         for (kind, idx), rs in by_source.items():
             ndep = sum(1 for r in rs if r["departs"])
             for r in rs:
