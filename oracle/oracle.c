@@ -790,10 +790,14 @@ static int key_less(const req_t *a, const req_t *b, int arb, int32_t rr, int32_t
  * time, which also gives a parallel simulation D cycles of lookahead.)
  * cls (NULL = all 0): class of every line of a custom list, 0 data, 1
  * control.  With arb & 2 (the fair arbitration of control and data messages
- * of Sec. 5.2) a link orders each class's requests by the usual key and
- * interleaves the two classes, starting with the class its pointer names;
- * after a cycle in which it appended lines, the pointer names the class
- * other than that of the last line appended.  Pointers start at data.
+ * of Sec. 5.2) a link ranks its requests by class turns: starting with the
+ * class its pointer names, each pick takes the lowest-key request of the
+ * class whose turn it is among the sources' heads (requests with no earlier
+ * request of the same source left; a source's lines are never reordered),
+ * or of either class if that class has none, and the turn passes to the
+ * other class.  After a cycle in which it appended lines, the pointer names
+ * the class other than that of the last line appended.  Pointers start at
+ * data.
  */
 int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t *col_idx,
                     const int32_t *bw, const int32_t *lat, const int32_t *cap, const int32_t *credit, int32_t arb,
@@ -914,7 +918,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     for (int32_t l = 0; l < m; l++) if (bw[l] > bmax) bmax = bw[l];
     size_t rcap = (size_t)2 * m * bmax + 1;
     req_t *reqs = malloc(sizeof(req_t) * rcap);
-    int32_t *fair_a = malloc(sizeof(int32_t) * rcap), *fair_b = malloc(sizeof(int32_t) * rcap);
+    int32_t *fair_a = malloc(sizeof(int32_t) * rcap);
     /* per-target request slots: at most (input ports of its tail) * bmax */
     int32_t *bucket_n = calloc((size_t)m, sizeof(int32_t));
     int64_t *bucket_off = malloc(sizeof(int64_t) * ((size_t)m + 1));
@@ -1017,15 +1021,30 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                 }
                 bk[b + 1] = v;
             }
-            if (arb & 2) {   /* the classes interleaved, each in key order */
-                int32_t na = 0, nb = 0;
-                for (int32_t a = 0; a < cnt; a++) {
-                    int c = cls ? cls[reqs[bk[a]].x] : 0;
-                    if (c == cptr[f]) fair_a[na++] = bk[a]; else fair_b[nb++] = bk[a];
+            if (arb & 2) {
+                /* class turns over the sources' heads: each pick takes, among
+                 * the requests whose source has no earlier request left, the
+                 * lowest key of the class whose turn it is (of either class if
+                 * none), and hands the turn to the other class */
+                int32_t turn = cptr[f];
+                for (int32_t a = 0; a < cnt; a++) fair_a[a] = bk[a];   /* key order */
+                for (int32_t pos = 0; pos < cnt; pos++) {
+                    int32_t pick = -1, any = -1;
+                    for (int32_t a = 0; a < cnt; a++) {
+                        if (fair_a[a] < 0) continue;
+                        const req_t *ra = &reqs[fair_a[a]];
+                        int head = 1;
+                        for (int32_t b2 = 0; b2 < cnt && head; b2++)
+                            if (fair_a[b2] >= 0 && reqs[fair_a[b2]].src == ra->src && reqs[fair_a[b2]].k < ra->k) head = 0;
+                        if (!head) continue;
+                        if (any < 0) any = a;
+                        if (pick < 0 && (cls ? cls[ra->x] : 0) == turn) pick = a;
+                    }
+                    if (pick < 0) pick = any;
+                    bk[pos] = fair_a[pick];
+                    turn = 1 - (cls ? cls[reqs[fair_a[pick]].x] : 0);
+                    fair_a[pick] = -1;
                 }
-                int32_t ia = 0, ib = 0;
-                for (int32_t a = 0; a < cnt; a++)
-                    bk[a] = (ia < na && (ib >= nb || ia <= ib)) ? fair_a[ia++] : fair_b[ib++];
             }
             int32_t g = bw[f];
             if (cap[f] - qocc[f] - owed[f] < g) g = cap[f] - qocc[f] - owed[f];
@@ -1179,6 +1198,17 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
             if (admit0[x] < rel) rc = OR_ERR_INVARIANT;
             if ((uint64_t)completion[x] < rel + lsum + 1) rc = OR_ERR_INVARIANT;
         }
+        /* a flow (same source and destination, so the same path) delivers its
+         * lines in id order: no arbitration reorders a source's lines */
+        uint32_t *flow_last = calloc((size_t)E * E, sizeof(uint32_t));
+        for (int64_t x = 0; x < T && rc == OR_OK && flow_last; x++) {
+            int32_t s, d;
+            decode(&w, x, &s, &d, preds);
+            uint32_t *fl = &flow_last[(int64_t)s * E + d];
+            if (completion[x] < *fl) rc = OR_ERR_INVARIANT;
+            *fl = completion[x];
+        }
+        free(flow_last);
     }
 
     if (stats) {
@@ -1189,7 +1219,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     free(path_ptr); free(path_link); free(port_of); free(nports); free(tail_of);
     free(s_ptr); free(s_list); free(s_cur); free(preds); free(q_off); free(qbuf);
     free(qhead); free(qocc); free(owe_t); free(owe_n); free(owe_h); free(owe_c); free(owed); free(cptr); free(rr);
-    free(fair_a); free(fair_b); free(reqs); free(bucket_n); free(bucket_off);
+    free(fair_a); free(reqs); free(bucket_n); free(bucket_off);
     free(bucket); free(touched); free(active);
     for (size_t i = 0; w.coll == COLL_CUSTOM && i < (size_t)m * bmax; i++) free(hcache[i].preds);
     free(hcache); free(hpred); free(src_first); free(src_cnt); free(admit0); free(adm_cnt);

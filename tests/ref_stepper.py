@@ -71,10 +71,11 @@ def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, ma
     """Returns (status, completion list, tx_lines, busy, makespan).  credit:
     per-link credit delay D (default 1): the slot a line frees by leaving
     link l at cycle t can be granted again from cycle t + D on.  arb: 0
-    lowest id, 1 round-robin, +2 class-fair: each class (cls[x], 0 data, 1
-    control) in key order, the two alternating from the class the link's
-    pointer names; after appending, the pointer names the class other than
-    the last appended line's."""
+    lowest id, 1 round-robin, +2 class-fair: picks alternate between the
+    classes (cls[x], 0 data, 1 control) starting from the class the link's
+    pointer names, each the lowest key of that class among the sources' next
+    requests (or of any class); after appending, the pointer names the class
+    other than the last appended line's."""
     row_ptr = [int(v) for v in row_ptr]
     col_idx = [int(v) for v in col_idx]
     m = row_ptr[-1]
@@ -143,14 +144,16 @@ def step_simulate(n, E, row_ptr, col_idx, bw, lat, cap, arb, src, dst, preds, ma
             else:
                 rs.sort(key=lambda r: (r["k"], (r["port"] - rr[f]) % P))
             if arb & 2:
-                first = [r for r in rs if cls[r["x"]] == cptr[f]]
-                second = [r for r in rs if cls[r["x"]] != cptr[f]]
-                rs = []
-                while first or second:
-                    if first:
-                        rs.append(first.pop(0))
-                    if second:
-                        rs.append(second.pop(0))
+                # class turns, picking only among each source's next request
+                left, rs, turn = list(rs), [], cptr[f]
+                while left:
+                    heads = [r for r in left
+                             if not any(o["source"] == r["source"] and o["k"] < r["k"] for o in left)]
+                    mine = [r for r in heads if cls[r["x"]] == turn]
+                    r = (mine or heads)[0]
+                    rs.append(r)
+                    left.remove(r)
+                    turn = 1 - cls[r["x"]]
             g = min(bw[f], cap[f] - len(fifo[f]) - sum(c[1] for c in owed[f]), len(rs))
             for r in rs[:g]:
                 r["granted"] = True

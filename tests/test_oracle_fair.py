@@ -91,3 +91,23 @@ def test_memcpy_requests_are_control(oracle_lib, seed):
     req = [i for i in range(len(src)) if ocls[i] == 1]
     assert all(preds[x + 1] == [x] and src[x + 1] == dst[x] and dst[x + 1] == src[x] for x in req)
     assert len(req) == int(mc.n_lines.sum())
+
+
+@pytest.mark.parametrize("seed", [103, 105])
+def test_fair_never_reorders_a_flow(oracle_lib, seed):
+    """Regression: interleaving classes over all offered lines put a source's
+    later control line ahead of its earlier data line within one cycle, so a
+    flow delivered out of id order.  Picks are taken among heads only."""
+    from tests.test_gpu_memcpy import tiny_noc
+    w = tiny_noc(seed)
+    w.arb |= si.ARB_FAIR_CLASSES
+    r = oracle_lib.simulate_workload(w, check=True)   # check mode verifies per-flow order
+    assert r.status_name in ("OK", "DEADLOCK")
+    mc = w.meta["memcpy"]
+    src, dst, _ = model(mc)
+    last = {}
+    for x, c in enumerate(r.completion):
+        if c == 0xFFFFFFFF:
+            continue
+        assert c >= last.get((src[x], dst[x]), 0)
+        last[(src[x], dst[x])] = int(c)
