@@ -57,7 +57,18 @@ typedef enum {
     SIM_ERR_STATE = 9        /* call out of order (e.g. run before load)         */
 } sim_status;
 
-typedef enum { SIM_ARB_LOWEST_ID = 0, SIM_ARB_ROUND_ROBIN = 1 } sim_arb;
+/* Arbitration: lowest line id, or round-robin over input ports; either may
+ * add SIM_ARB_FAIR_CLASSES (Sec. 5.2: fair arbitration of control and data
+ * messages).  Then a link ranks its requests by class turns: starting with
+ * the class its pointer names (data at first), each pick takes the lowest
+ * base key of the class whose turn it is among the sources' heads (requests
+ * with no earlier request of the same source left at this link, so that no
+ * source's lines are reordered), or of either class if that class has none,
+ * and hands the turn to the other class.  After a cycle in which it appended
+ * lines, the pointer names the class other than that of the last line
+ * appended.  Load requests of sim_load_memcpy are control messages; every
+ * other line is data.  The workgroup engine simulates SIM_ARB_FAIR_CLASSES. */
+typedef enum { SIM_ARB_LOWEST_ID = 0, SIM_ARB_ROUND_ROBIN = 1, SIM_ARB_FAIR_CLASSES = 2 } sim_arb;
 
 /* Collectives (the paper's textbook algorithms, Sec. 1 and 2.2: ring,
  * all-pairs (direct), double binary tree and recursive halving-doubling; the
@@ -141,7 +152,8 @@ typedef enum {
  *                          routing and workload (batched design sweeps).
  *   bw, lat, cap         : [S*m] int32, scenario-major; 1 <= bw <= SIM_MAX_BW,
  *                          1 <= lat <= SIM_MAX_LAT, 1 <= cap <= SIM_MAX_CAP.
- *   arb                  : sim_arb.
+ *   arb                  : sim_arb: SIM_ARB_LOWEST_ID or SIM_ARB_ROUND_ROBIN,
+ *                          optionally | SIM_ARB_FAIR_CLASSES.
  * Host arrays are copied; the caller keeps ownership.  Routing distances are
  * built here.  Uses the current HIP device.  *out is set only on SIM_OK.
  */

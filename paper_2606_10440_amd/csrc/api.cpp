@@ -168,6 +168,7 @@ struct Ranges {
     std::vector<int64_t> pref_rng;   // predecessor range
     std::vector<uint32_t> pref_delta;  // line start+o waits for line pref_start+delta+o
     bool whole = false;  // per-chunk: every line waits for the whole predecessor range
+    std::vector<uint8_t> cls;  // [T] message class per line (empty: all data)
     void add(uint64_t s, uint64_t l, int32_t a, int32_t b) {
         start.push_back((uint32_t)s);
         len.push_back((uint32_t)l);
@@ -804,12 +805,14 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     const bool b1_ok = bmax == 1 && (int64_t)s_link.size() <= 1024 && nl <= 8 * 1024 && nl < 65536 && b1_bytes <= kLds &&
                        (c->arb == SIM_ARB_LOWEST_ID || rr_ports_fit);
     // credit delays above 1 are simulated by the wave engine (not together
-    // with per-chunk dependencies) and the workgroup engine
+    // with per-chunk dependencies) and the workgroup engine; class-fair
+    // arbitration by the workgroup engine
     const bool credits = !c->credit.empty();
-    if (credits && R.whole) wv.ok = false;
-    const bool lane_ok = !credits && nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds;
-    const bool lanehbm_ok = !credits && nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds;
-    const bool b1_usable = !credits && nl >= 1 && b1_ok;
+    const bool fair = (c->arb & SIM_ARB_FAIR_CLASSES) != 0;
+    if ((credits && R.whole) || fair) wv.ok = false;
+    const bool lane_ok = !credits && !fair && nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds;
+    const bool lanehbm_ok = !credits && !fair && nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds;
+    const bool b1_usable = !credits && !fair && nl >= 1 && b1_ok;
     int engine = simgpu::kEngineWorkgroup;
     if (wv.ok) engine = simgpu::kEngineWave;
     else if (lane_ok) engine = simgpu::kEngineLane;
@@ -971,6 +974,10 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         int32_t *tmp_credit;
         UP(c->credit, credit);
     }
+    if (fair && !R.cls.empty()) {
+        uint8_t *tmp_line_cls;
+        UP(R.cls, line_cls);
+    }
     int32_t *tmp_ln_P, *tmp_ln_port, *tmp_ln_fifo, *tmp_ln_mask, *tmp_ln_req, *tmp_ln_reqcap, *tmp_ln_srbeg,
         *tmp_ln_srend, *tmp_link_lane, *tmp_path_lane;
     UP(ln_P, ln_P);
@@ -1017,7 +1024,8 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     if (engine == simgpu::kEngineWorkgroup &&
         ((st = alloc(c, ost, S * ftot, &d.fifo_x)) || (st = alloc(c, ost, S * ftot, &d.fifo_rdy)) ||
         (st = alloc(c, ost, S * ftot, &d.fifo_pp)) || (st = alloc(c, ost, S * m, &d.qhead)) ||
-        (st = alloc(c, ost, S * m, &d.qcred)) ||
+        (st = alloc(c, ost, S * m, &d.qcred)) || (st = alloc(c, ost, S * m, &d.cptr)) ||
+        (fair && (st = alloc(c, ost, S * rtot, &d.req_aux))) ||
         (st = alloc(c, ost, S * m, &d.qtail)) || (st = alloc(c, ost, S * m, &d.rr)) ||
         (st = alloc(c, ost, S * d.ns, &d.cur_rng)) || (st = alloc(c, ost, S * d.ns, &d.cur_off)) ||
         (st = alloc(c, ost, S * nflows, &d.delivered)) || (st = alloc(c, ost, S * m, &d.req_cnt)) ||
@@ -1044,7 +1052,7 @@ sim_status create_impl(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_
     if (!out || !row_ptr || !col_idx || !bw || !lat || !cap) return SIM_ERR_INVALID_ARG;
     *out = nullptr;
     if (n_nodes < 1 || n_endpoints < 1 || n_endpoints > n_nodes || n_scenarios < 1) return SIM_ERR_INVALID_ARG;
-    if (arb != SIM_ARB_LOWEST_ID && arb != SIM_ARB_ROUND_ROBIN) return SIM_ERR_INVALID_ARG;
+    if (arb < 0 || arb > (SIM_ARB_ROUND_ROBIN | SIM_ARB_FAIR_CLASSES)) return SIM_ERR_INVALID_ARG;
     if (n_endpoints > 65536) return SIM_ERR_INVALID_ARG;  // (src << 16 | dst) hash key
     if (row_ptr[0] != 0) return SIM_ERR_TOPOLOGY;
     for (int32_t v = 0; v < n_nodes; v++)
@@ -1185,9 +1193,11 @@ sim_status load_memcpy_impl(sim_ctx *c, int64_t n_ops, const int32_t *cu, const 
             if (r.store)
                 for (int64_t g = r.g0; g < r.g0 + r.gn; g++) R.pred(id[q][g] + 1, 0);
             next = x + 1;
+            R.cls.push_back(r.store ? 0 : 1);  // a load request is a control message
             if (!r.store) {  // the data line
                 R.add((uint64_t)x + 1, 1, r.chan, cus[q].first);
                 R.pred(x, 0);
+                R.cls.push_back(0);
                 next = x + 2;
             }
         }

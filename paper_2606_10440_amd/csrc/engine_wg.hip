@@ -47,12 +47,16 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
     uint32_t *qhead = d.qhead + sm;
     uint32_t *qtail = d.qtail + sm;
     uint32_t *qcred = d.qcred ? d.qcred + sm : nullptr;
+    const bool fair = (d.arb & 2) != 0;
+    uint32_t *cptr = d.cptr + sm;
+    const uint8_t *lcls = d.line_cls;  // null: every line is data
     uint32_t *rr = d.rr + sm;
     int32_t *cur_rng = d.cur_rng + (size_t)s * d.ns;
     uint32_t *cur_off = d.cur_off + (size_t)s * d.ns;
     uint32_t *delivered = d.delivered + (size_t)s * d.nflows;
     uint32_t *req_cnt = d.req_cnt + sm;
     uint64_t *req_rec = d.req_rec + (size_t)s * d.req_total;
+    uint32_t *req_aux = d.req_aux ? d.req_aux + (size_t)s * d.req_total : nullptr;
     const size_t nsrc = (size_t)m + d.ns;
     uint32_t *sreq_x = d.sreq_x + (size_t)s * nsrc * bmax;
     int32_t *sreq_pp = d.sreq_pp + (size_t)s * nsrc * bmax;
@@ -73,6 +77,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
         qhead[l] = 0;
         qtail[l] = 0;
         if (qcred) qcred[l] = 0;
+        cptr[l] = 0;
         rr[l] = 0;
         req_cnt[l] = 0;
         gcount[l] = 0;
@@ -136,7 +141,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                     } else {
                         const uint32_t P = (uint32_t)d.nports_tail[tgt];
                         const uint32_t key =
-                            d.arb == 0 ? x
+                            (d.arb & 1) == 0 ? x
                                        : (uint32_t)k * P + ((uint32_t)d.port_at_head[l] + P - rr[tgt]) % P;
                         const uint32_t slot = atomicAdd(&req_cnt[tgt], 1u);
                         req_rec[d.req_off[tgt] + slot] = ((uint64_t)key << 32) | ((uint32_t)l << 8) | (uint32_t)k;
@@ -166,7 +171,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                     const size_t si = (size_t)src * bmax + k;
                     sreq_x[si] = x;
                     sreq_pp[si] = d.r_path[R];
-                    const uint32_t key = d.arb == 0 ? x : (uint32_t)k * P + ((P - 1) + P - rr[f]) % P;
+                    const uint32_t key = (d.arb & 1) == 0 ? x : (uint32_t)k * P + ((P - 1) + P - rr[f]) % P;
                     const uint32_t slot = atomicAdd(&req_cnt[f], 1u);
                     req_rec[d.req_off[f] + slot] = ((uint64_t)key << 32) | ((uint32_t)src << 8) | (uint32_t)k;
                     nr++;
@@ -190,15 +195,54 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
             if (cap[f] - occ < g) g = cap[f] - occ;
             if ((int)c < g) g = (int)c;
             const uint64_t *rec = req_rec + d.req_off[f];
-            for (uint32_t i = 0; i < c; i++) {
-                const uint64_t ri = rec[i];
-                const uint32_t ki = (uint32_t)(ri >> 32);
-                int rank = 0;
-                for (uint32_t jj = 0; jj < c; jj++) rank += ((uint32_t)(rec[jj] >> 32) < ki) ? 1 : 0;
-                if (rank < g) {
-                    const uint32_t sk = (uint32_t)ri;
-                    glist[(size_t)f * bmax + rank] = sk;
-                    grant[(size_t)(sk >> 8) * bmax + (sk & 255u)] = rank;
+            if (!fair) {
+                for (uint32_t i = 0; i < c; i++) {
+                    const uint64_t ri = rec[i];
+                    const uint32_t ki = (uint32_t)(ri >> 32);
+                    int rank = 0;
+                    for (uint32_t jj = 0; jj < c; jj++) rank += ((uint32_t)(rec[jj] >> 32) < ki) ? 1 : 0;
+                    if (rank < g) {
+                        const uint32_t sk = (uint32_t)ri;
+                        glist[(size_t)f * bmax + rank] = sk;
+                        grant[(size_t)(sk >> 8) * bmax + (sk & 255u)] = rank;
+                    }
+                }
+            } else {
+                // class turns over the sources' heads: each pick takes the lowest
+                // key of the class whose turn it is (of either class if none)
+                // among requests with no request of the same source ahead of them
+                // at this link, and hands the turn to the other class
+                uint32_t *aux = req_aux + d.req_off[f];
+                auto cls_of = [&](uint32_t sk) -> uint32_t {
+                    return lcls ? (uint32_t)lcls[sreq_x[(size_t)(sk >> 8) * bmax + (sk & 255u)]] : 0u;
+                };
+                for (uint32_t i = 0; i < c; i++) {
+                    const uint32_t si = (uint32_t)rec[i];
+                    uint32_t ahead = 0;
+                    for (uint32_t jj = 0; jj < c; jj++) {
+                        const uint32_t sj = (uint32_t)rec[jj];
+                        ahead += ((sj >> 8) == (si >> 8) && (sj & 255u) < (si & 255u)) ? 1u : 0u;
+                    }
+                    aux[i] = ahead;
+                }
+                uint32_t turn = cptr[f];
+                for (int pos = 0; pos < g; pos++) {
+                    int best = -1, any = -1;
+                    uint32_t kb = 0xFFFFFFFFu, ka = 0xFFFFFFFFu;
+                    for (uint32_t i = 0; i < c; i++) {
+                        if (aux[i] != 0u) continue;  // picked (all ones) or not yet its source's head
+                        const uint32_t ki = (uint32_t)(rec[i] >> 32);
+                        if (ki < ka) { ka = ki; any = (int)i; }
+                        if (ki < kb && cls_of((uint32_t)rec[i]) == turn) { kb = ki; best = (int)i; }
+                    }
+                    const int pi = best >= 0 ? best : any;
+                    const uint32_t sk = (uint32_t)rec[pi];
+                    aux[pi] = 0xFFFFFFFFu;
+                    for (uint32_t i = 0; i < c; i++)  // the source's next request moves up
+                        if (aux[i] != 0xFFFFFFFFu && ((uint32_t)rec[i] >> 8) == (sk >> 8)) aux[i] -= 1u;
+                    glist[(size_t)f * bmax + pos] = sk;
+                    grant[(size_t)(sk >> 8) * bmax + (sk & 255u)] = pos;
+                    turn = 1u - cls_of(sk);
                 }
             }
             gcount[f] = (uint32_t)(g > 0 ? g : 0);
@@ -264,7 +308,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
             const int base = d.fifo_off[f], mask = d.fifo_mask[f];
             const uint32_t ready = t + (uint32_t)lat[f];
             int cnt = 0;
-            uint32_t last_port = 0;
+            uint32_t last_port = 0, last_x = 0;
             for (int r = 0; r < g; r++) {
                 const size_t gi = (size_t)f * bmax + r;
                 if (!gdep[gi]) continue;
@@ -276,6 +320,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                 fx[e] = sreq_x[si];
                 frdy[e] = ready;
                 fpp[e] = sreq_pp[si];
+                last_x = sreq_x[si];
                 tl++;
                 cnt++;
                 last_port = src < m ? (uint32_t)d.port_at_head[src] : P - 1;
@@ -284,7 +329,8 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                 qtail[f] = tl;
                 tx[f] += (uint64_t)cnt;
                 busy[f] += 1;
-                if (d.arb == 1) rr[f] = (last_port + 1) % P;
+                if (d.arb & 1) rr[f] = (last_port + 1) % P;
+                if (fair) cptr[f] = 1u - (lcls ? (uint32_t)lcls[last_x] : 0u);
             }
         }
         __syncthreads();

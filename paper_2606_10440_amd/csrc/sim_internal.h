@@ -63,6 +63,7 @@ struct DevNet {
     // per-scenario parameters [S*m]
     const int32_t *bw, *lat, *cap;
     const int32_t *credit;  // [S*m] credit return delay, or null when every delay is 1
+    const uint8_t *line_cls;  // [T] message class (1 control, 0 data) or null (all data)
 
     // per-scenario state
     uint32_t *fifo_x;     // [S*fifo_total] line id
@@ -70,6 +71,7 @@ struct DevNet {
     int32_t *fifo_pp;     // [S*fifo_total] path index of the link the entry is on
     uint32_t *qhead;      // [S*m] popped count
     uint32_t *qtail;      // [S*m] pushed count
+    uint32_t *cptr;       // [S*m] class-fair arbitration: the class that goes first
     uint32_t *qcred;      // [S*m] popped entries whose slot is free again (credit returned);
                           // a popped entry's fifo_rdy then holds the cycle it left
     uint32_t *rr;         // [S*m] round-robin pointer
@@ -80,6 +82,7 @@ struct DevNet {
     // per-scenario scratch
     uint32_t *req_cnt;    // [S*m] requests received this cycle
     uint64_t *req_rec;    // [S*req_total] (key << 32) | (source << 8) | k
+    uint32_t *req_aux;    // [S*req_total] class-fair picks: requests of the same source ahead
     uint32_t *sreq_x;     // [S*(m+ns)*bmax] requested line
     int32_t *sreq_pp;     // [S*(m+ns)*bmax] path index of the requested hop
     int32_t *sreq_n;      // [S*(m+ns)] requests made this cycle

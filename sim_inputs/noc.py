@@ -152,12 +152,14 @@ def wg_cu(lay: NocLayout, g: int, wg: int, n_wg: int) -> int:
     return int(lay.cus[g][(wg % R) * per + (wg // R) % per])
 
 
-def allgather_ops(lay: NocLayout, out_lines: int, n_wg: int = 32, unroll=4, window=64) -> Memcpy:
-    """Put-based all-gather (the scalability workload of Sec. 5.4): GPU g's
-    input of out_lines / G lines (at address 0) is copied into every GPU's
-    output buffer (at address out_lines / G, slot g), split evenly over the
-    n_wg workgroups of GPU g; a workgroup writes the peers in the order
-    g, g+1, ..."""
+def allgather_ops(lay: NocLayout, out_lines: int, n_wg: int = 32, unroll=4, window=64, get=False) -> Memcpy:
+    """All-gather (the scalability workload of Sec. 5.4): GPU g's input of
+    out_lines / G lines (at address 0) is copied into every GPU's output
+    buffer (at address out_lines / G, slot g).  Put-based: the n_wg
+    workgroups of GPU g split g's input and write it to the peers g, g+1,
+    ... (remote stores).  Get-based (Sec. 5.2): the workgroups of GPU h split
+    each peer's input and read it into h's output, peers h, h+1, ... (remote
+    loads: their requests are control messages)."""
     G = lay.n_gpus
     chunk = out_lines // G
     assert chunk * G == out_lines and chunk % n_wg == 0
@@ -168,7 +170,10 @@ def allgather_ops(lay: NocLayout, out_lines: int, n_wg: int = 32, unroll=4, wind
             cu = wg_cu(lay, g, wg, n_wg)
             for d in range(G):
                 h = (g + d) % G
-                rows.append((cu, g, h, wg * c, chunk + g * chunk + wg * c, c))
+                if get:   # GPU g reads h's input into its own output slot h
+                    rows.append((cu, h, g, wg * c, chunk + h * chunk + wg * c, c))
+                else:
+                    rows.append((cu, g, h, wg * c, chunk + g * chunk + wg * c, c))
     return _ops(rows, lay, unroll, window)
 
 

@@ -204,3 +204,13 @@ def test_set_credit_errors(simlib):
         assert e.value.status == simlib.SIM_ERR_STATE
     finally:
         simlib.sim_destroy(ctx)
+
+
+def test_fair_arbitration_flag_accepted(simlib):
+    w = si.config("C1")
+    for arb in (2, 3):
+        ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, arb)
+        simlib.sim_destroy(ctx)
+    with pytest.raises(simlib.SimError) as e:
+        simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, 4)
+    assert e.value.status == simlib.SIM_ERR_INVALID_ARG
