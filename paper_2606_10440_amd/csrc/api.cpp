@@ -898,6 +898,14 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     d.nl = nl;
     d.has_preds = any_preds ? 1 : 0;
     d.pd_omask = R.whole ? 0u : 0xFFFFFFFFu;
+    {   // workgroup engine: 7 words per link, one per source, two per stream in LDS when they
+        // fit and every scenario's workgroup is resident at once (else fewer resident
+        // workgroups hide less HBM latency than the LDS saves)
+        const int64_t words = 7 * (int64_t)m + ((int64_t)m + (int64_t)s_link.size()) + 2 * (int64_t)s_link.size();
+        const int64_t bytes = words * 4, room = kLds - 1024;  // room for the static LDS
+        const int64_t per_cu = bytes <= room ? room / bytes : 0;
+        d.wg_lds = per_cu > 0 && (int64_t)c->S <= 256 * per_cu ? (int32_t)bytes : 0;
+    }
     d.b1_ns = (int32_t)s_link.size();
     d.b1_lpt = (nl + 1023) / 1024;
     d.b1_deliv_lds = b1_deliv_lds ? 1 : 0;

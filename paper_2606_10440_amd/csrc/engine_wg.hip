@@ -30,7 +30,13 @@ namespace {
 
 constexpr int kThreads = 256;
 
+// SM: the per-link and per-stream scalars (queue pointers, request and grant
+// counts, round-robin and class pointers, stream cursors) live in LDS, so
+// that the every-cycle scans over idle links cost LDS reads; FIFO entries and
+// request records stay in HBM.  Otherwise all state is in HBM.
+template <bool SM>
 __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
+    extern __shared__ __align__(16) uint32_t wg_lds[];
     const int s = blockIdx.x;
     const int tid = threadIdx.x;
     const int m = d.m;
@@ -44,25 +50,41 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
     uint32_t *fx = d.fifo_x + fo;
     uint32_t *frdy = d.fifo_rdy + fo;
     int32_t *fpp = d.fifo_pp + fo;
-    uint32_t *qhead = d.qhead + sm;
-    uint32_t *qtail = d.qtail + sm;
-    uint32_t *qcred = d.qcred ? d.qcred + sm : nullptr;
     const bool fair = (d.arb & 2) != 0;
-    uint32_t *cptr = d.cptr + sm;
     const uint8_t *lcls = d.line_cls;  // null: every line is data
-    uint32_t *rr = d.rr + sm;
-    int32_t *cur_rng = d.cur_rng + (size_t)s * d.ns;
-    uint32_t *cur_off = d.cur_off + (size_t)s * d.ns;
+    const size_t nsrc = (size_t)m + d.ns;
+    uint32_t *qhead, *qtail, *qcred, *cptr, *rr, *cur_off, *req_cnt, *gcount;
+    int32_t *cur_rng, *sreq_n;
+    if constexpr (SM) {
+        uint32_t *p = wg_lds;
+        qhead = p; p += m;
+        qtail = p; p += m;
+        qcred = p; p += m;
+        cptr = p; p += m;
+        rr = p; p += m;
+        req_cnt = p; p += m;
+        gcount = p; p += m;
+        sreq_n = reinterpret_cast<int32_t *>(p); p += nsrc;
+        cur_rng = reinterpret_cast<int32_t *>(p); p += d.ns;
+        cur_off = p;
+    } else {
+        qhead = d.qhead + sm;
+        qtail = d.qtail + sm;
+        qcred = d.qcred + sm;
+        cptr = d.cptr + sm;
+        rr = d.rr + sm;
+        req_cnt = d.req_cnt + sm;
+        gcount = d.gcount + sm;
+        sreq_n = d.sreq_n + (size_t)s * nsrc;
+        cur_rng = d.cur_rng + (size_t)s * d.ns;
+        cur_off = d.cur_off + (size_t)s * d.ns;
+    }
     uint32_t *delivered = d.delivered + (size_t)s * d.nflows;
-    uint32_t *req_cnt = d.req_cnt + sm;
     uint64_t *req_rec = d.req_rec + (size_t)s * d.req_total;
     uint32_t *req_aux = d.req_aux ? d.req_aux + (size_t)s * d.req_total : nullptr;
-    const size_t nsrc = (size_t)m + d.ns;
     uint32_t *sreq_x = d.sreq_x + (size_t)s * nsrc * bmax;
     int32_t *sreq_pp = d.sreq_pp + (size_t)s * nsrc * bmax;
-    int32_t *sreq_n = d.sreq_n + (size_t)s * nsrc;
     int32_t *grant = d.grant + (size_t)s * nsrc * bmax;
-    uint32_t *gcount = d.gcount + sm;
     uint32_t *glist = d.glist + sm * bmax;
     uint8_t *gdep = d.gdep + sm * bmax;
     uint32_t *comp = d.completion + (size_t)s * d.T;
@@ -76,7 +98,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
     for (int l = tid; l < m; l += kThreads) {
         qhead[l] = 0;
         qtail[l] = 0;
-        if (qcred) qcred[l] = 0;
+        qcred[l] = 0;
         cptr[l] = 0;
         rr[l] = 0;
         req_cnt[l] = 0;
@@ -370,7 +392,14 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
 }  // namespace
 
 hipError_t launch_workgroup(const DevNet &d, hipStream_t st) {
-    hipLaunchKernelGGL(engine_wg, dim3((unsigned)d.S), dim3(kThreads), 0, st, d);
+    if (d.wg_lds > 0) {
+        auto k = engine_wg<true>;
+        if (d.wg_lds > 65536)
+            (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, d.wg_lds);
+        hipLaunchKernelGGL(k, dim3((unsigned)d.S), dim3(kThreads), (unsigned)d.wg_lds, st, d);
+    } else {
+        hipLaunchKernelGGL(engine_wg<false>, dim3((unsigned)d.S), dim3(kThreads), 0, st, d);
+    }
     return hipGetLastError();
 }
 
