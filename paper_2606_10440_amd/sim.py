@@ -74,6 +74,24 @@ def _check(ctx, st: int):
         raise SimError(st, msg)
 
 
+# ------------------------------------------------------------------ reporting
+
+_BUS_FACTOR = {0: "ar", 1: "ar", 2: "ar", 8: "ar", 9: "ar", 4: "one", 5: "one", 6: "one", 7: "one", 3: "a2a"}
+
+
+def bus_bandwidth(coll, nbytes, p, seconds):
+    """Bus bandwidth in bits/s of a collective that took ``seconds`` (the
+    measure the paper reports next to the completion time): algorithm
+    bandwidth nbytes / seconds times 2(p-1)/p for all-reduce, (p-1)/p for
+    reduce-scatter and all-gather (nbytes = the full buffer per endpoint),
+    and (p-1)/p for all-to-all with nbytes per ordered pair (p * nbytes per
+    endpoint).  With seconds in cycles the result is in bits per cycle."""
+    kind = _BUS_FACTOR[int(coll)]
+    per_ep = nbytes * p if kind == "a2a" else nbytes
+    factor = 2.0 * (p - 1) / p if kind == "ar" else (p - 1) / p
+    return 8.0 * per_ep / seconds * factor
+
+
 # ---------------------------------------------------------------- C-ABI names
 
 def sim_create(n_nodes, n_endpoints, row_ptr, col_idx, n_scenarios, bw, lat, cap, arb):

@@ -80,6 +80,42 @@ def compare_deadlocked(r, s, want):
     assert np.array_equal(r.busy_cycles[s].cpu().numpy().astype(np.uint64), want.busy_cycles)
 
 
+def first_divergence(simmod, oracle_lib, w, s, txns=None):
+    """Locate a mismatch: the smallest max_cycles bound at which the GPU and
+    the oracle differ for scenario s (bisection), with the first lines and
+    links that differ there."""
+    m = w.n_links
+    sl = slice(s * m, (s + 1) * m)
+
+    def both(mc):
+        r = run_gpu(simmod, w, max_cycles=mc, txns=txns)
+        if txns is None:
+            o = oracle_lib.simulate_workload(w, s, max_cycles=mc)
+        else:
+            o = oracle_lib.simulate(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw[sl], w.lat[sl], w.cap[sl],
+                                    w.arb, txns=txns, max_cycles=mc,
+                                    credit=None if w.credit is None else w.credit[sl])
+        comp = r.completion[s, :len(o.completion)].cpu().numpy().view(np.uint32)
+        done = o.completion != 0xFFFFFFFF
+        lines = np.nonzero(done & (comp != o.completion))[0]
+        links = np.nonzero(r.tx_lines[s].cpu().numpy().astype(np.uint64) != o.tx_lines)[0]
+        return lines, links
+
+    full = oracle_lib.simulate_workload(w, s) if txns is None else None
+    lo, hi = 0, (full.makespan + 2) if full is not None and full.makespan else 1 << 20
+    lines, links = both(hi)
+    if not len(lines) and not len(links):
+        return "no divergence found below the makespan"
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        ln, lk = both(mid)
+        if len(ln) or len(lk):
+            hi, lines, links = mid, ln, lk
+        else:
+            lo = mid
+    return f"first divergence at max_cycles={hi}: lines {lines[:8].tolist()}, links {links[:8].tolist()}"
+
+
 def check_vs_oracle(simmod, oracle_lib, w, scenarios=None, expect_ok=True):
     r = run_gpu(simmod, w)
     if expect_ok:
@@ -87,11 +123,14 @@ def check_vs_oracle(simmod, oracle_lib, w, scenarios=None, expect_ok=True):
     n_ok = 0
     for s in (range(w.n_scenarios) if scenarios is None else scenarios):
         want = oracle_lib.simulate_workload(w, s)
-        if want.status_name == "DEADLOCK":
-            compare_deadlocked(r, s, want)
-        else:
-            compare_scenario(r, s, want, len(want.completion))
-            n_ok += 1
+        try:
+            if want.status_name == "DEADLOCK":
+                compare_deadlocked(r, s, want)
+            else:
+                compare_scenario(r, s, want, len(want.completion))
+                n_ok += 1
+        except AssertionError as e:
+            raise AssertionError(f"{e}\n{first_divergence(simmod, oracle_lib, w, s)}") from None
     return r, n_ok
 
 
@@ -321,11 +360,23 @@ def check_engine(simmod, oracle_lib, w, engine, txns=None):
             want = oracle_lib.simulate(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, w.bw[sl], w.lat[sl],
                                        w.cap[sl], w.arb, txns=txns,
                                        credit=None if w.credit is None else w.credit[sl])
-        if want.status_name == "DEADLOCK":
-            compare_deadlocked(r, s, want)
-        else:
-            compare_scenario(r, s, want, len(want.completion))
-            n_ok += 1
+        try:
+            if want.status_name == "DEADLOCK":
+                compare_deadlocked(r, s, want)
+            else:
+                compare_scenario(r, s, want, len(want.completion))
+                n_ok += 1
+        except AssertionError as e:
+            old = os.environ.get("SIMGPU_ENGINE")
+            os.environ["SIMGPU_ENGINE"] = engine
+            try:
+                report = first_divergence(simmod, oracle_lib, w, s, txns)
+            finally:
+                if old is None:
+                    del os.environ["SIMGPU_ENGINE"]
+                else:
+                    os.environ["SIMGPU_ENGINE"] = old
+            raise AssertionError(f"{e}\n{report}") from None
     return n_ok
 
 
