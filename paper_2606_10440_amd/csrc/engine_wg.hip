@@ -28,13 +28,13 @@ namespace simgpu {
 
 namespace {
 
-constexpr int kThreads = 256;
-
 // SM: the per-link and per-stream scalars (queue pointers, request and grant
 // counts, round-robin and class pointers, stream cursors) live in LDS, so
 // that the every-cycle scans over idle links cost LDS reads; FIFO entries and
 // request records stay in HBM.  Otherwise all state is in HBM.
-template <bool SM>
+// kThreads: 1024 when few scenarios run (more links and memory requests in
+// flight per scenario), 256 for large batches (more scenarios per CU).
+template <bool SM, int kThreads>
 __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
     extern __shared__ __align__(16) uint32_t wg_lds[];
     const int s = blockIdx.x;
@@ -391,16 +391,21 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
 
 }  // namespace
 
-hipError_t launch_workgroup(const DevNet &d, hipStream_t st) {
+template <int NT>
+hipError_t launch_wg(const DevNet &d, hipStream_t st) {
     if (d.wg_lds > 0) {
-        auto k = engine_wg<true>;
+        auto k = engine_wg<true, NT>;
         if (d.wg_lds > 65536)
             (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, d.wg_lds);
-        hipLaunchKernelGGL(k, dim3((unsigned)d.S), dim3(kThreads), (unsigned)d.wg_lds, st, d);
+        hipLaunchKernelGGL(k, dim3((unsigned)d.S), dim3(NT), (unsigned)d.wg_lds, st, d);
     } else {
-        hipLaunchKernelGGL(engine_wg<false>, dim3((unsigned)d.S), dim3(kThreads), 0, st, d);
+        hipLaunchKernelGGL((engine_wg<false, NT>), dim3((unsigned)d.S), dim3(NT), 0, st, d);
     }
     return hipGetLastError();
+}
+
+hipError_t launch_workgroup(const DevNet &d, hipStream_t st) {
+    return d.S <= 256 ? launch_wg<1024>(d, st) : launch_wg<256>(d, st);
 }
 
 }  // namespace simgpu
