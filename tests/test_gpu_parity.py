@@ -332,7 +332,10 @@ def run_engine(simmod, w, engine, txns=None):
     for this workload (the wave engine's limits: at most 64 traffic links,
     four flows per link, three feeders per link)."""
     old = os.environ.get("SIMGPU_ENGINE")
-    os.environ["SIMGPU_ENGINE"] = engine
+    if engine:
+        os.environ["SIMGPU_ENGINE"] = engine
+    else:  # the library's own choice
+        os.environ.pop("SIMGPU_ENGINE", None)
     try:
         try:
             return run_gpu(simmod, w, txns=txns)
@@ -342,7 +345,7 @@ def run_engine(simmod, w, engine, txns=None):
             raise
     finally:
         if old is None:
-            del os.environ["SIMGPU_ENGINE"]
+            os.environ.pop("SIMGPU_ENGINE", None)
         else:
             os.environ["SIMGPU_ENGINE"] = old
 
@@ -368,12 +371,15 @@ def check_engine(simmod, oracle_lib, w, engine, txns=None):
                 n_ok += 1
         except AssertionError as e:
             old = os.environ.get("SIMGPU_ENGINE")
-            os.environ["SIMGPU_ENGINE"] = engine
+            if engine:
+                os.environ["SIMGPU_ENGINE"] = engine
+            else:
+                os.environ.pop("SIMGPU_ENGINE", None)
             try:
                 report = first_divergence(simmod, oracle_lib, w, s, txns)
             finally:
                 if old is None:
-                    del os.environ["SIMGPU_ENGINE"]
+                    os.environ.pop("SIMGPU_ENGINE", None)
                 else:
                     os.environ["SIMGPU_ENGINE"] = old
             raise AssertionError(f"{e}\n{report}") from None
