@@ -128,7 +128,7 @@ def main():
     a = ap.parse_args()
 
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print(f"bench.py: this build runs on exactly one GPU (asked for {a.gpus}); "
+        print(f"bench.py: simgpu runs on exactly one GPU (asked for {a.gpus}); "
               "batched scenarios would shard across GPUs with no exchange, but no "
               "multi-GPU path is built", file=sys.stderr)
         sys.exit(2)
