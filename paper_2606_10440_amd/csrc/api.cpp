@@ -818,9 +818,14 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     else if (lane_ok) engine = simgpu::kEngineLane;
     else if (b1_usable) engine = simgpu::kEngineB1;
     else if (lanehbm_ok) engine = simgpu::kEngineLaneHbm;
+    bool wg_scan = false;  // workgroup engine without active sets (tests)
     if (const char *ev = std::getenv("SIMGPU_ENGINE")) {
         int want = -1;
         if (!std::strcmp(ev, "workgroup")) want = simgpu::kEngineWorkgroup;
+        if (!std::strcmp(ev, "workgroup_scan")) {
+            want = simgpu::kEngineWorkgroup;
+            wg_scan = true;
+        }
         if (!std::strcmp(ev, "lane")) want = simgpu::kEngineLane;
         if (!std::strcmp(ev, "lanehbm")) want = simgpu::kEngineLaneHbm;
         if (!std::strcmp(ev, "b1")) want = simgpu::kEngineB1;
@@ -898,13 +903,19 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     d.nl = nl;
     d.has_preds = any_preds ? 1 : 0;
     d.pd_omask = R.whole ? 0u : 0xFFFFFFFFu;
-    {   // workgroup engine: 7 words per link, one per source, two per stream in LDS when they
-        // fit and every scenario's workgroup is resident at once (else fewer resident
-        // workgroups hide less HBM latency than the LDS saves)
-        const int64_t words = 7 * (int64_t)m + ((int64_t)m + (int64_t)s_link.size()) + 2 * (int64_t)s_link.size();
-        const int64_t bytes = words * 4, room = kLds - 1024;  // room for the static LDS
+    {   // workgroup engine: the active sets (a bit and a list entry per source, a list
+        // entry per link) in LDS unless the graph is too large for them or the full
+        // scan is asked for; then 7 words per link, one per source, two per stream
+        // in LDS too when they fit and every scenario's workgroup is resident at once
+        // (else fewer resident workgroups hide less HBM latency than the LDS saves)
+        const int64_t nsrc_all = (int64_t)m + (int64_t)s_link.size();
+        const int64_t act = 4 * ((nsrc_all + 31) / 32 + nsrc_all + (int64_t)m);
+        const int64_t room = kLds - 1024;  // room for the static LDS
+        d.wg_act = (act <= room / 2 && !wg_scan) ? (int32_t)act : 0;
+        const int64_t words = 7 * (int64_t)m + nsrc_all + 2 * (int64_t)s_link.size();
+        const int64_t bytes = words * 4 + d.wg_act;
         const int64_t per_cu = bytes <= room ? room / bytes : 0;
-        d.wg_lds = per_cu > 0 && (int64_t)c->S <= 256 * per_cu ? (int32_t)bytes : 0;
+        d.wg_lds = per_cu > 0 && (int64_t)c->S <= 256 * per_cu ? (int32_t)(words * 4) : 0;
     }
     d.b1_ns = (int32_t)s_link.size();
     d.b1_lpt = (nl + 1023) / 1024;

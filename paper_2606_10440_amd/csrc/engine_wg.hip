@@ -12,6 +12,15 @@
 // Then the next cycle is t + 1 if anything departed, otherwise the earliest
 // FIFO-head ready time or credit return (no such time = deadlock).
 //
+// Active sets (ACT): a bitmap in LDS marks the sources that hold anything (a
+// link FIFO with entries, waiting or owed a credit; a stream with lines
+// left).  Each cycle starts by compacting it into a list, and R and D walk
+// that list; R appends each target that receives its first request of the
+// cycle to a target list, which G and E walk.  D clears the bit of a source
+// it empties, E sets the bit of a link it appends to, so a cycle costs in
+// proportion to the busy part of the graph rather than to the whole graph.
+// Without ACT every phase scans every source or target.
+//
 // With credit delays a line that leaves a FIFO keeps its slot until the
 // credit is back: the entry stays between qcred and qhead with the cycle it
 // left in place of its ready time.
@@ -34,7 +43,8 @@ namespace {
 // request records stay in HBM.  Otherwise all state is in HBM.
 // kThreads: 1024 when few scenarios run (more links and memory requests in
 // flight per scenario), 256 for large batches (more scenarios per CU).
-template <bool SM, int kThreads>
+// ACT: active sets in LDS, after the scalars (see above).
+template <bool SM, bool ACT, int kThreads>
 __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
     extern __shared__ __align__(16) uint32_t wg_lds[];
     const int s = blockIdx.x;
@@ -92,8 +102,15 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
     uint64_t *busy = d.busy + sm;
     const int32_t *__restrict__ path = d.path_link;
 
-    __shared__ uint32_t sh_t, sh_next, sh_anydep, sh_ndone;
+    __shared__ uint32_t sh_t, sh_next, sh_anydep, sh_ndone, sh_nalive, sh_ntgt;
     __shared__ int32_t sh_state;
+    // active sets: live-source bitmap [nw], live-source list [m + ns], target list [m]
+    const int nw = (int)((nsrc + 31) / 32);
+    uint32_t *livew = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(wg_lds) + (SM ? d.wg_lds : 0));
+    int32_t *alist = reinterpret_cast<int32_t *>(livew + nw);
+    int32_t *tlist = alist + nsrc;
+    auto set_live = [&](int src) { atomicOr(&livew[src >> 5], 1u << (src & 31)); };
+    auto clear_live = [&](int src) { atomicAnd(&livew[src >> 5], ~(1u << (src & 31))); };
 
     for (int l = tid; l < m; l += kThreads) {
         qhead[l] = 0;
@@ -114,23 +131,46 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
         cur_off[j] = 0;
     }
     for (int f = tid; f < d.nflows; f += kThreads) delivered[f] = 0;
+    if constexpr (ACT)
+        for (int j = tid; j < nw; j += kThreads) livew[j] = 0;
     if (tid == 0) {
         sh_t = 0;
         sh_state = d.T > 0 ? kRunRunning : kRunOk;
         sh_next = kNever;
         sh_anydep = 0;
         sh_ndone = 0;
+        sh_nalive = 0;
+        sh_ntgt = 0;
     }
     __syncthreads();
+    if constexpr (ACT) {  // streams with lines are live from the start; links start empty
+        for (int j = tid; j < d.ns; j += kThreads)
+            if (d.s_rbeg[j] < d.s_rend[j]) set_live(m + j);
+        __syncthreads();
+    }
 
     uint64_t done = 0, processed = 0;  // meaningful in thread 0
     const int nact = d.n_fsrc + d.ns;
     while (sh_state == kRunRunning) {
         const uint32_t t = sh_t;
+        if constexpr (ACT) {  // the live sources, in no particular order
+            for (int j = tid; j < nw; j += kThreads) {
+                uint32_t bits = livew[j];
+                if (bits == 0u) continue;
+                int pos = (int)atomicAdd(&sh_nalive, (uint32_t)__popc(bits));
+                while (bits) {
+                    alist[pos++] = j * 32 + __ffs(bits) - 1;
+                    bits &= bits - 1u;
+                }
+            }
+            __syncthreads();
+        }
+        const int nsrc_now = ACT ? (int)sh_nalive : nact;
         // ---------------------------------------------------------------- R
-        for (int a = tid; a < nact; a += kThreads) {
-            if (a < d.n_fsrc) {
-                const int l = d.fsrc_link[a];
+        for (int a = tid; a < nsrc_now; a += kThreads) {
+            const int sid = ACT ? alist[a] : (a < d.n_fsrc ? d.fsrc_link[a] : m + (a - d.n_fsrc));
+            if (sid < m) {
+                const int l = sid;
                 const uint32_t h = qhead[l];
                 const uint32_t occ = qtail[l] - h;
                 const int b = bw[l];
@@ -143,6 +183,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                     while (qc != h && frdy[base + (int)(qc & (uint32_t)mask)] + D <= t) qc++;
                     qcred[l] = qc;
                     if (qc != h) atomicMin(&sh_next, frdy[base + (int)(qc & (uint32_t)mask)] + D);
+                    if (ACT && qc == qtail[l]) clear_live(l);  // nothing held: every credit is back
                 }
                 int nr = 0;
                 for (int k = 0; k < b && (uint32_t)k < occ; k++) {
@@ -167,12 +208,13 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                                        : (uint32_t)k * P + ((uint32_t)d.port_at_head[l] + P - rr[tgt]) % P;
                         const uint32_t slot = atomicAdd(&req_cnt[tgt], 1u);
                         req_rec[d.req_off[tgt] + slot] = ((uint64_t)key << 32) | ((uint32_t)l << 8) | (uint32_t)k;
+                        if (ACT && slot == 0u) tlist[atomicAdd(&sh_ntgt, 1u)] = tgt;
                     }
                     nr++;
                 }
                 sreq_n[l] = nr;
             } else {
-                const int j = a - d.n_fsrc;
+                const int j = sid - m;
                 const int f = d.s_link[j];
                 const int src = m + j;
                 int R = cur_rng[j];
@@ -196,6 +238,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                     const uint32_t key = (d.arb & 1) == 0 ? x : (uint32_t)k * P + ((P - 1) + P - rr[f]) % P;
                     const uint32_t slot = atomicAdd(&req_cnt[f], 1u);
                     req_rec[d.req_off[f] + slot] = ((uint64_t)key << 32) | ((uint32_t)src << 8) | (uint32_t)k;
+                    if (ACT && slot == 0u) tlist[atomicAdd(&sh_ntgt, 1u)] = f;
                     nr++;
                     if (++o == d.r_len[R]) {
                         R++;
@@ -207,8 +250,9 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
         }
         __syncthreads();
         // ---------------------------------------------------------------- G
-        for (int a = tid; a < d.n_fsrc; a += kThreads) {
-            const int f = d.fsrc_link[a];
+        const int ntgt = ACT ? (int)sh_ntgt : d.n_fsrc;
+        for (int a = tid; a < ntgt; a += kThreads) {
+            const int f = ACT ? tlist[a] : d.fsrc_link[a];
             const uint32_t c = req_cnt[f];
             if (c == 0) continue;
             req_cnt[f] = 0;
@@ -271,8 +315,8 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
         }
         __syncthreads();
         // ---------------------------------------------------------------- D
-        for (int a = tid; a < nact; a += kThreads) {
-            const int src = a < d.n_fsrc ? d.fsrc_link[a] : m + (a - d.n_fsrc);
+        for (int a = tid; a < nsrc_now; a += kThreads) {
+            const int src = ACT ? alist[a] : (a < d.n_fsrc ? d.fsrc_link[a] : m + (a - d.n_fsrc));
             const int nr = sreq_n[src];
             if (nr == 0) continue;
             sreq_n[src] = 0;
@@ -304,6 +348,8 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                         for (int k = 0; k < dep; k++) frdy[base + (int)((qhead[src] + (uint32_t)k) & (uint32_t)mask)] = t;
                     }
                     qhead[src] += (uint32_t)dep;
+                    // emptied (left entries that still owe a credit keep it live)
+                    if (ACT && !cred && qhead[src] == qtail[src]) clear_live(src);
                 } else {
                     const int j = src - m;
                     int R = cur_rng[j];
@@ -314,14 +360,15 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                     }
                     cur_rng[j] = R;
                     cur_off[j] = o;
+                    if (ACT && R == d.s_rend[j]) clear_live(src);
                 }
                 if (sinks) atomicAdd(&sh_ndone, (uint32_t)sinks);
             }
         }
         __syncthreads();
         // ---------------------------------------------------------------- E
-        for (int a = tid; a < d.n_fsrc; a += kThreads) {
-            const int f = d.fsrc_link[a];
+        for (int a = tid; a < ntgt; a += kThreads) {
+            const int f = ACT ? tlist[a] : d.fsrc_link[a];
             const int g = (int)gcount[f];
             if (g == 0) continue;
             gcount[f] = 0;
@@ -348,6 +395,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                 last_port = src < m ? (uint32_t)d.port_at_head[src] : P - 1;
             }
             if (cnt) {
+                if (ACT) set_live(f);
                 qtail[f] = tl;
                 tx[f] += (uint64_t)cnt;
                 busy[f] += 1;
@@ -379,6 +427,8 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
             sh_next = kNever;
             sh_anydep = 0;
             sh_ndone = 0;
+            sh_nalive = 0;
+            sh_ntgt = 0;
         }
         __syncthreads();
     }
@@ -391,17 +441,18 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
 
 }  // namespace
 
+template <bool ACT, int NT>
+hipError_t launch_wg2(const DevNet &d, hipStream_t st) {
+    const int lds = d.wg_lds + (ACT ? d.wg_act : 0);
+    auto k = d.wg_lds > 0 ? engine_wg<true, ACT, NT> : engine_wg<false, ACT, NT>;
+    if (lds > 65536) (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    hipLaunchKernelGGL(k, dim3((unsigned)d.S), dim3(NT), (unsigned)lds, st, d);
+    return hipGetLastError();
+}
+
 template <int NT>
 hipError_t launch_wg(const DevNet &d, hipStream_t st) {
-    if (d.wg_lds > 0) {
-        auto k = engine_wg<true, NT>;
-        if (d.wg_lds > 65536)
-            (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, d.wg_lds);
-        hipLaunchKernelGGL(k, dim3((unsigned)d.S), dim3(NT), (unsigned)d.wg_lds, st, d);
-    } else {
-        hipLaunchKernelGGL((engine_wg<false, NT>), dim3((unsigned)d.S), dim3(NT), 0, st, d);
-    }
-    return hipGetLastError();
+    return d.wg_act > 0 ? launch_wg2<true, NT>(d, st) : launch_wg2<false, NT>(d, st);
 }
 
 hipError_t launch_workgroup(const DevNet &d, hipStream_t st) {

@@ -44,7 +44,7 @@ def test_memcpy_generic_gpu_local_copy(simmod, oracle_lib, U, W):
     check_vs_oracle(simmod, oracle_lib, wm)
 
 
-@pytest.mark.parametrize("engine", ["workgroup", "lane", "lanehbm"])
+@pytest.mark.parametrize("engine", ["workgroup", "workgroup_scan", "lane", "lanehbm"])
 def test_memcpy_generic_gpu_sweep(simmod, oracle_lib, engine):
     w, lay = noc.gpu_noc(1)
     wm = noc.memcpy_workload(w, noc.local_copy_ops(lay, 32 * 8, n_wg=32, unroll=4, window=8), name="gpu_sweep")
