@@ -909,9 +909,12 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         // in LDS too when they fit and every scenario's workgroup is resident at once
         // (else fewer resident workgroups hide less HBM latency than the LDS saves)
         const int64_t nsrc_all = (int64_t)m + (int64_t)s_link.size();
-        const int64_t act = 4 * ((nsrc_all + 31) / 32 + nsrc_all + (int64_t)m);
+        const int64_t rcap = std::min<int64_t>(2048, nsrc_all * bmax);  // request list (8 B each)
+        // (+ one word: the request list is 8-byte aligned)
+        const int64_t act = 4 * ((nsrc_all + 31) / 32 + nsrc_all + (int64_t)m + 1) + 8 * rcap;
         const int64_t room = kLds - 1024;  // room for the static LDS
         d.wg_act = (act <= room / 2 && !wg_scan) ? (int32_t)act : 0;
+        d.wg_rcap = (int32_t)rcap;
         const int64_t words = 7 * (int64_t)m + nsrc_all + 2 * (int64_t)s_link.size();
         const int64_t bytes = words * 4 + d.wg_act;
         const int64_t per_cu = bytes <= room ? room / bytes : 0;

@@ -19,6 +19,10 @@
 // cycle to a target list, which G and E walk.  D clears the bit of a source
 // it empties, E sets the bit of a link it appends to, so a cycle costs in
 // proportion to the busy part of the graph rather than to the whole graph.
+// R also lists every request (target, slot); when the cycle's requests fit
+// that list and arbitration is by key alone, G ranks one request per thread
+// (its rank = the number of smaller keys at its target) instead of one
+// target per thread, which spreads a busy router's many requests.
 // Without ACT every phase scans every source or target.
 //
 // With credit delays a line that leaves a FIFO keeps its slot until the
@@ -41,11 +45,15 @@ namespace {
 // counts, round-robin and class pointers, stream cursors) live in LDS, so
 // that the every-cycle scans over idle links cost LDS reads; FIFO entries and
 // request records stay in HBM.  Otherwise all state is in HBM.
-// kThreads: 1024 when few scenarios run (more links and memory requests in
-// flight per scenario), 256 for large batches (more scenarios per CU).
+// kThreads: as many as let every scenario's workgroup be resident at once
+// (32 waves per CU): 1024 up to 512 scenarios, 512 up to 1024, else 256;
+// more threads per scenario means fewer sources per thread, so fewer
+// dependent memory round trips per phase.
 // ACT: active sets in LDS, after the scalars (see above).
-template <bool SM, bool ACT, int kThreads>
-__global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
+// kMinWaves: waves per SIMD the registers must allow (8 when 32 waves share
+// a CU; the compiler then keeps some scalars in vector-register lanes).
+template <bool SM, bool ACT, int kThreads, int kMinWaves>
+__global__ void __launch_bounds__(kThreads, kMinWaves) engine_wg(DevNet d) {
     extern __shared__ __align__(16) uint32_t wg_lds[];
     const int s = blockIdx.x;
     const int tid = threadIdx.x;
@@ -102,13 +110,23 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
     uint64_t *busy = d.busy + sm;
     const int32_t *__restrict__ path = d.path_link;
 
-    __shared__ uint32_t sh_t, sh_next, sh_anydep, sh_ndone, sh_nalive, sh_ntgt;
+    __shared__ uint32_t sh_t, sh_next, sh_anydep, sh_ndone, sh_nalive, sh_ntgt, sh_nreq;
     __shared__ int32_t sh_state;
-    // active sets: live-source bitmap [nw], live-source list [m + ns], target list [m]
+    // active sets: live-source bitmap [nw], live-source list [m + ns], target list [m],
+    // request list [wg_rcap] of (target, slot)
     const int nw = (int)((nsrc + 31) / 32);
-    uint32_t *livew = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(wg_lds) + (SM ? d.wg_lds : 0));
+    const size_t aoff = SM ? (size_t)d.wg_lds : 0;
+    uint32_t *livew = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(wg_lds) + aoff);
     int32_t *alist = reinterpret_cast<int32_t *>(livew + nw);
     int32_t *tlist = alist + nsrc;
+    uint2 *rlist = reinterpret_cast<uint2 *>(reinterpret_cast<unsigned char *>(wg_lds) +
+                                             ((aoff + 4 * ((size_t)nw + nsrc + (size_t)m) + 7) & ~(size_t)7));
+    const uint32_t rcap = (uint32_t)d.wg_rcap;
+    auto post = [&](int tgt, uint32_t slot) {  // a request's place in the active sets
+        if (slot == 0u) tlist[atomicAdd(&sh_ntgt, 1u)] = tgt;
+        const uint32_t q = atomicAdd(&sh_nreq, 1u);
+        if (q < rcap) rlist[q] = make_uint2((uint32_t)tgt, slot);
+    };
     auto set_live = [&](int src) { atomicOr(&livew[src >> 5], 1u << (src & 31)); };
     auto clear_live = [&](int src) { atomicAnd(&livew[src >> 5], ~(1u << (src & 31))); };
 
@@ -141,6 +159,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
         sh_ndone = 0;
         sh_nalive = 0;
         sh_ntgt = 0;
+        sh_nreq = 0;
     }
     __syncthreads();
     if constexpr (ACT) {  // streams with lines are live from the start; links start empty
@@ -208,7 +227,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                                        : (uint32_t)k * P + ((uint32_t)d.port_at_head[l] + P - rr[tgt]) % P;
                         const uint32_t slot = atomicAdd(&req_cnt[tgt], 1u);
                         req_rec[d.req_off[tgt] + slot] = ((uint64_t)key << 32) | ((uint32_t)l << 8) | (uint32_t)k;
-                        if (ACT && slot == 0u) tlist[atomicAdd(&sh_ntgt, 1u)] = tgt;
+                        if (ACT) post(tgt, slot);
                     }
                     nr++;
                 }
@@ -238,7 +257,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
                     const uint32_t key = (d.arb & 1) == 0 ? x : (uint32_t)k * P + ((P - 1) + P - rr[f]) % P;
                     const uint32_t slot = atomicAdd(&req_cnt[f], 1u);
                     req_rec[d.req_off[f] + slot] = ((uint64_t)key << 32) | ((uint32_t)src << 8) | (uint32_t)k;
-                    if (ACT && slot == 0u) tlist[atomicAdd(&sh_ntgt, 1u)] = f;
+                    if (ACT) post(f, slot);
                     nr++;
                     if (++o == d.r_len[R]) {
                         R++;
@@ -251,7 +270,31 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
         __syncthreads();
         // ---------------------------------------------------------------- G
         const int ntgt = ACT ? (int)sh_ntgt : d.n_fsrc;
-        for (int a = tid; a < ntgt; a += kThreads) {
+        const uint32_t nreq = ACT ? sh_nreq : 0u;
+        const bool flat = ACT && !fair && nreq <= rcap;  // one request per thread
+        if (flat) {
+            for (uint32_t q = (uint32_t)tid; q < nreq; q += kThreads) {
+                const uint2 rq = rlist[q];
+                const int f = (int)rq.x;
+                const uint32_t c = req_cnt[f];
+                const uint64_t *rec = req_rec + d.req_off[f];
+                const uint64_t ri = rec[rq.y];
+                const uint32_t ki = (uint32_t)(ri >> 32);
+                int rank = 0;
+                for (uint32_t jj = 0; jj < c; jj++) rank += ((uint32_t)(rec[jj] >> 32) < ki) ? 1 : 0;
+                const int occ = (int)(qtail[f] - (cred ? qcred[f] : qhead[f]));
+                int g = bw[f];
+                if (cap[f] - occ < g) g = cap[f] - occ;
+                if ((int)c < g) g = (int)c;
+                if (rank < g) {
+                    const uint32_t sk = (uint32_t)ri;
+                    glist[(size_t)f * bmax + rank] = sk;
+                    grant[(size_t)(sk >> 8) * bmax + (sk & 255u)] = rank;
+                }
+                if (rq.y == 0u) gcount[f] = (uint32_t)(g > 0 ? g : 0);
+            }
+        }
+        for (int a = tid; a < (flat ? 0 : ntgt); a += kThreads) {
             const int f = ACT ? tlist[a] : d.fsrc_link[a];
             const uint32_t c = req_cnt[f];
             if (c == 0) continue;
@@ -369,6 +412,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
         // ---------------------------------------------------------------- E
         for (int a = tid; a < ntgt; a += kThreads) {
             const int f = ACT ? tlist[a] : d.fsrc_link[a];
+            if (flat) req_cnt[f] = 0;  // every request of the cycle has been ranked
             const int g = (int)gcount[f];
             if (g == 0) continue;
             gcount[f] = 0;
@@ -429,6 +473,7 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
             sh_ndone = 0;
             sh_nalive = 0;
             sh_ntgt = 0;
+            sh_nreq = 0;
         }
         __syncthreads();
     }
@@ -441,22 +486,26 @@ __global__ void __launch_bounds__(kThreads) engine_wg(DevNet d) {
 
 }  // namespace
 
-template <bool ACT, int NT>
+template <bool ACT, int NT, int MW>
 hipError_t launch_wg2(const DevNet &d, hipStream_t st) {
     const int lds = d.wg_lds + (ACT ? d.wg_act : 0);
-    auto k = d.wg_lds > 0 ? engine_wg<true, ACT, NT> : engine_wg<false, ACT, NT>;
+    auto k = d.wg_lds > 0 ? engine_wg<true, ACT, NT, MW> : engine_wg<false, ACT, NT, MW>;
     if (lds > 65536) (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     hipLaunchKernelGGL(k, dim3((unsigned)d.S), dim3(NT), (unsigned)lds, st, d);
     return hipGetLastError();
 }
 
-template <int NT>
+template <int NT, int MW>
 hipError_t launch_wg(const DevNet &d, hipStream_t st) {
-    return d.wg_act > 0 ? launch_wg2<true, NT>(d, st) : launch_wg2<false, NT>(d, st);
+    return d.wg_act > 0 ? launch_wg2<true, NT, MW>(d, st) : launch_wg2<false, NT, MW>(d, st);
 }
 
 hipError_t launch_workgroup(const DevNet &d, hipStream_t st) {
-    return d.S <= 256 ? launch_wg<1024>(d, st) : launch_wg<256>(d, st);
+    const int per_cu = (d.S + 255) / 256;  // workgroups per CU when all are resident
+    if (per_cu <= 1) return launch_wg<1024, 4>(d, st);
+    if (per_cu <= 2) return launch_wg<1024, 8>(d, st);
+    if (per_cu <= 4) return launch_wg<512, 8>(d, st);
+    return launch_wg<256, 4>(d, st);
 }
 
 }  // namespace simgpu

@@ -74,6 +74,7 @@ struct DevNet {
     uint32_t *cptr;       // [S*m] class-fair arbitration: the class that goes first
     int32_t wg_lds;       // workgroup engine: bytes of per-scenario scalars kept in LDS (0: in HBM)
     int32_t wg_act;       // workgroup engine: bytes of the active sets in LDS after them (0: full scans)
+    int32_t wg_rcap;      // workgroup engine: capacity of the active sets' request list
     uint32_t *qcred;      // [S*m] popped entries whose slot is free again (credit returned);
                           // a popped entry's fifo_rdy then holds the cycle it left
     uint32_t *rr;         // [S*m] round-robin pointer

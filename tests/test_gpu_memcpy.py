@@ -59,3 +59,13 @@ def test_memcpy_two_gpus(simmod, oracle_lib, kind):
     wm = noc.memcpy_workload(w, mc, name=f"two_gpu_{kind}")
     say(wm.name)
     check_vs_oracle(simmod, oracle_lib, wm)
+
+
+@pytest.mark.parametrize("S", [300, 700, 1100])
+def test_memcpy_workgroup_batch_sizes(simmod, oracle_lib, S):
+    """The workgroup engine's launch shape follows the batch size (threads per
+    workgroup and register budget chosen so that every scenario's workgroup
+    is resident at once); each shape against the oracle, scenario by
+    scenario."""
+    w = noc.with_scenarios(tiny_noc(3, n_ops=8, max_lines=24), S, seed=S)
+    check_engine(simmod, oracle_lib, w, "workgroup")
