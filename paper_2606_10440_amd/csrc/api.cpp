@@ -996,6 +996,26 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         int32_t *tmp_credit;
         UP(c->credit, credit);
     }
+    if (engine == simgpu::kEngineWorkgroup) {
+        // streams to wake when a flow delivers: every flow that a range of the
+        // stream waits on (flow-major CSR, each stream once per flow)
+        std::vector<std::pair<int32_t, int32_t>> fs;
+        for (size_t j = 0; j < s_link.size(); j++)
+            for (int32_t r = s_rbeg[j]; r < s_rend[j]; r++)
+                for (int32_t q = r_pd[r]; q < r_pd[r + 1]; q++) fs.emplace_back(pd_flow[q], (int32_t)j);
+        std::sort(fs.begin(), fs.end());
+        fs.erase(std::unique(fs.begin(), fs.end()), fs.end());
+        std::vector<int32_t> fw_ptr(nflows + 1, 0), fw_str(fs.size());
+        for (size_t q = 0; q < fs.size(); q++) {
+            fw_ptr[fs[q].first + 1]++;
+            fw_str[q] = fs[q].second;
+        }
+        for (int32_t f = 0; f < nflows; f++) fw_ptr[f + 1] += fw_ptr[f];
+        if (fw_str.empty()) fw_str.push_back(0);
+        int32_t *tmp_fw_ptr, *tmp_fw_str;
+        UP(fw_ptr, fw_ptr);
+        UP(fw_str, fw_str);
+    }
     if (fair && !R.cls.empty()) {
         uint8_t *tmp_line_cls;
         UP(R.cls, line_cls);

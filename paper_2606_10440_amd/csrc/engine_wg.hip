@@ -19,6 +19,9 @@
 // cycle to a target list, which G and E walk.  D clears the bit of a source
 // it empties, E sets the bit of a link it appends to, so a cycle costs in
 // proportion to the busy part of the graph rather than to the whole graph.
+// A stream whose next line waits on predecessors sleeps (its bit cleared in
+// R) until one of the flows it waits on delivers a line (D sets its bit):
+// only a delivery can release a line.
 // R also lists every request (target, slot); when the cycle's requests fit
 // that list and arbitration is by key alone, G ranks one request per thread
 // (its rank = the number of smaller keys at its target) instead of one
@@ -41,19 +44,21 @@ namespace simgpu {
 
 namespace {
 
+// FIFO heads, requests and grants of one source or target are handled kC at
+// a time, so that their memory loads are in flight together.
+constexpr int kC = 4;
+
 // SM: the per-link and per-stream scalars (queue pointers, request and grant
 // counts, round-robin and class pointers, stream cursors) live in LDS, so
 // that the every-cycle scans over idle links cost LDS reads; FIFO entries and
 // request records stay in HBM.  Otherwise all state is in HBM.
-// kThreads: as many as let every scenario's workgroup be resident at once
-// (32 waves per CU): 1024 up to 512 scenarios, 512 up to 1024, else 256;
-// more threads per scenario means fewer sources per thread, so fewer
-// dependent memory round trips per phase.
+// kThreads: 16 waves per CU in all, so that every scenario's workgroup is
+// resident at once when there are at most 1024 (1024 threads up to 256
+// scenarios, 512 up to 512, else 256) and each thread keeps up to 128
+// registers for the chunked loops below.
 // ACT: active sets in LDS, after the scalars (see above).
-// kMinWaves: waves per SIMD the registers must allow (8 when 32 waves share
-// a CU; the compiler then keeps some scalars in vector-register lanes).
-template <bool SM, bool ACT, int kThreads, int kMinWaves>
-__global__ void __launch_bounds__(kThreads, kMinWaves) engine_wg(DevNet d) {
+template <bool SM, bool ACT, int kThreads>
+__global__ void __launch_bounds__(kThreads, 4) engine_wg(DevNet d) {
     extern __shared__ __align__(16) uint32_t wg_lds[];
     const int s = blockIdx.x;
     const int tid = threadIdx.x;
@@ -204,32 +209,66 @@ __global__ void __launch_bounds__(kThreads, kMinWaves) engine_wg(DevNet d) {
                     if (qc != h) atomicMin(&sh_next, frdy[base + (int)(qc & (uint32_t)mask)] + D);
                     if (ACT && qc == qtail[l]) clear_live(l);  // nothing held: every credit is back
                 }
+                // the ready heads, kC at a time (their loads in flight together)
+                const int lim = b < (int)occ ? b : (int)occ;
                 int nr = 0;
-                for (int k = 0; k < b && (uint32_t)k < occ; k++) {
-                    const int e = base + (int)((h + k) & (uint32_t)mask);
-                    const uint32_t rdy = frdy[e];
-                    if (rdy > t) {
-                        atomicMin(&sh_next, rdy);
-                        break;
+                bool run = true;
+                for (int k0 = 0; run && k0 < lim; k0 += kC) {
+                    int e[kC];
+                    uint32_t rdy[kC];
+#pragma unroll
+                    for (int u = 0; u < kC; u++) {
+                        e[u] = base + (int)((h + (uint32_t)(k0 + u)) & (uint32_t)mask);
+                        rdy[u] = k0 + u < lim ? frdy[e[u]] : kNever;
                     }
-                    const uint32_t x = fx[e];
-                    const int pp = fpp[e] + 1;
-                    const int tgt = path[pp];
-                    const size_t si = (size_t)l * bmax + k;
-                    sreq_x[si] = x;
-                    sreq_pp[si] = pp;
-                    if (tgt < 0) {
-                        grant[si] = -2;  // the sink takes everything
-                    } else {
-                        const uint32_t P = (uint32_t)d.nports_tail[tgt];
-                        const uint32_t key =
-                            (d.arb & 1) == 0 ? x
-                                       : (uint32_t)k * P + ((uint32_t)d.port_at_head[l] + P - rr[tgt]) % P;
-                        const uint32_t slot = atomicAdd(&req_cnt[tgt], 1u);
-                        req_rec[d.req_off[tgt] + slot] = ((uint64_t)key << 32) | ((uint32_t)l << 8) | (uint32_t)k;
-                        if (ACT) post(tgt, slot);
+                    int nrd = 0;
+#pragma unroll
+                    for (int u = 0; u < kC; u++) {
+                        if (run && k0 + u < lim && rdy[u] > t) atomicMin(&sh_next, rdy[u]);  // first head not ready
+                        run = run && k0 + u < lim && rdy[u] <= t;
+                        nrd += run ? 1 : 0;
                     }
-                    nr++;
+                    uint32_t x[kC];
+                    int pp[kC], tg[kC];
+#pragma unroll
+                    for (int u = 0; u < kC; u++)
+                        if (u < nrd) {
+                            x[u] = fx[e[u]];
+                            pp[u] = fpp[e[u]] + 1;
+                        }
+#pragma unroll
+                    for (int u = 0; u < kC; u++)
+                        if (u < nrd) tg[u] = path[pp[u]];
+                    uint32_t P[kC], rot[kC];
+                    if (d.arb & 1) {
+                        const uint32_t ph = (uint32_t)d.port_at_head[l];
+#pragma unroll
+                        for (int u = 0; u < kC; u++)
+                            if (u < nrd && tg[u] >= 0) {
+                                P[u] = (uint32_t)d.nports_tail[tg[u]];
+                                rot[u] = rr[tg[u]];
+                            }
+#pragma unroll
+                        for (int u = 0; u < kC; u++)
+                            if (u < nrd && tg[u] >= 0) rot[u] = (ph + P[u] - rot[u]) % P[u];
+                    }
+#pragma unroll
+                    for (int u = 0; u < kC; u++) {
+                        if (u >= nrd) continue;
+                        const int k = k0 + u;
+                        const size_t si = (size_t)l * bmax + k;
+                        sreq_x[si] = x[u];
+                        sreq_pp[si] = pp[u];
+                        if (tg[u] < 0) {
+                            grant[si] = -2;  // the sink takes everything
+                        } else {
+                            const uint32_t key = (d.arb & 1) == 0 ? x[u] : (uint32_t)k * P[u] + rot[u];
+                            const uint32_t slot = atomicAdd(&req_cnt[tg[u]], 1u);
+                            req_rec[d.req_off[tg[u]] + slot] = ((uint64_t)key << 32) | ((uint32_t)l << 8) | (uint32_t)k;
+                            if (ACT) post(tg[u], slot);
+                        }
+                    }
+                    nr += nrd;
                 }
                 sreq_n[l] = nr;
             } else {
@@ -241,28 +280,61 @@ __global__ void __launch_bounds__(kThreads, kMinWaves) engine_wg(DevNet d) {
                 const int rend = d.s_rend[j];
                 const int b = bw[f];
                 const uint32_t P = (uint32_t)d.nports_tail[f];
+                if (ACT && R >= rend) clear_live(src);
+                // each range in turn: the lines from o on whose predecessors have all
+                // delivered (a prefix), all requested at once from the stream's link
+                const uint32_t rot = (d.arb & 1) ? ((P - 1) + P - rr[f]) % P : 0u;
                 int nr = 0;
-                for (int k = 0; k < b && R < rend; k++) {
-                    bool ok = true;
-                    for (int q = d.r_pd[R]; q < d.r_pd[R + 1]; q++)
-                        if (delivered[d.pd_flow[q]] <= d.pd_base[q] + (o & d.pd_omask)) {
-                            ok = false;
-                            break;
-                        }
-                    if (!ok) break;
-                    const uint32_t x = d.r_start[R] + o;
-                    const size_t si = (size_t)src * bmax + k;
-                    sreq_x[si] = x;
-                    sreq_pp[si] = d.r_path[R];
-                    const uint32_t key = (d.arb & 1) == 0 ? x : (uint32_t)k * P + ((P - 1) + P - rr[f]) % P;
-                    const uint32_t slot = atomicAdd(&req_cnt[f], 1u);
-                    req_rec[d.req_off[f] + slot] = ((uint64_t)key << 32) | ((uint32_t)src << 8) | (uint32_t)k;
-                    if (ACT) post(f, slot);
-                    nr++;
-                    if (++o == d.r_len[R]) {
-                        R++;
-                        o = 0;
+                while (nr < b && R < rend) {
+                    const int q0 = d.r_pd[R], q1 = d.r_pd[R + 1];
+                    const uint32_t len = d.r_len[R];
+                    uint32_t n = (uint32_t)(b - nr) < len - o ? (uint32_t)(b - nr) : len - o;
+                    for (int q = q0; q < q1 && n != 0u; q += kC) {
+                        int fl[kC];
+                        uint32_t bs[kC], dv[kC];
+#pragma unroll
+                        for (int u = 0; u < kC; u++)
+                            if (q + u < q1) {
+                                fl[u] = d.pd_flow[q + u];
+                                bs[u] = d.pd_base[q + u] + (o & d.pd_omask);
+                            }
+#pragma unroll
+                        for (int u = 0; u < kC; u++)
+                            if (q + u < q1) dv[u] = delivered[fl[u]];
+#pragma unroll
+                        for (int u = 0; u < kC; u++)
+                            if (q + u < q1) {
+                                // lines o + i with delivered > base + i (per line) or > base (per chunk)
+                                const uint32_t allow = dv[u] > bs[u] ? (d.pd_omask ? dv[u] - bs[u] : 0xFFFFFFFFu) : 0u;
+                                n = n < allow ? n : allow;
+                            }
                     }
+                    if (n == 0u) {
+                        if (ACT && nr == 0) clear_live(src);  // asleep until a flow it waits on delivers
+                        break;
+                    }
+                    const uint32_t x0 = d.r_start[R] + o;
+                    const int rp = d.r_path[R];
+                    const uint32_t slot0 = atomicAdd(&req_cnt[f], n);
+                    uint64_t *rec = req_rec + d.req_off[f] + slot0;
+                    for (uint32_t i = 0; i < n; i++) {
+                        const uint32_t k = (uint32_t)nr + i;
+                        const size_t si = (size_t)src * bmax + k;
+                        sreq_x[si] = x0 + i;
+                        sreq_pp[si] = rp;
+                        const uint32_t key = (d.arb & 1) == 0 ? x0 + i : k * P + rot;
+                        rec[i] = ((uint64_t)key << 32) | ((uint32_t)src << 8) | k;
+                    }
+                    if (ACT) {
+                        if (slot0 == 0u) tlist[atomicAdd(&sh_ntgt, 1u)] = f;
+                        const uint32_t q = atomicAdd(&sh_nreq, n);
+                        for (uint32_t i = 0; i < n && q + i < rcap; i++) rlist[q + i] = make_uint2((uint32_t)f, slot0 + i);
+                    }
+                    nr += (int)n;
+                    o += n;
+                    if (o < len) break;  // held back by a predecessor or by the bandwidth
+                    R++;
+                    o = 0;
                 }
                 sreq_n[src] = nr;
             }
@@ -363,24 +435,47 @@ __global__ void __launch_bounds__(kThreads, kMinWaves) engine_wg(DevNet d) {
             const int nr = sreq_n[src];
             if (nr == 0) continue;
             sreq_n[src] = 0;
+            // the longest granted prefix departs; every grant slot is reset
             int dep = 0, sinks = 0;
             bool open = true;
-            for (int k = 0; k < nr; k++) {
-                const size_t si = (size_t)src * bmax + k;
-                const int gr = grant[si];
-                grant[si] = -1;
-                if (!open || gr == -1) {
-                    open = false;
-                    continue;
+            for (int k0 = 0; k0 < nr; k0 += kC) {
+                const size_t s0 = (size_t)src * bmax + k0;
+                int gr[kC], pv[kC];
+                uint32_t xs[kC];
+#pragma unroll
+                for (int u = 0; u < kC; u++) gr[u] = k0 + u < nr ? grant[s0 + u] : -1;
+#pragma unroll
+                for (int u = 0; u < kC; u++) {
+                    if (k0 + u < nr) grant[s0 + u] = -1;
+                    open = open && gr[u] != -1;
+                    gr[u] = open ? gr[u] : -1;  // -1: stays
                 }
-                dep++;
-                const int pv = path[sreq_pp[si]];
-                if (gr == -2) {
-                    comp[sreq_x[si]] = t + 1;
-                    delivered[-pv - 1]++;
-                    sinks++;
-                } else {
-                    gdep[(size_t)pv * bmax + gr] = 1;
+#pragma unroll
+                for (int u = 0; u < kC; u++)
+                    if (gr[u] != -1) pv[u] = sreq_pp[s0 + u];
+#pragma unroll
+                for (int u = 0; u < kC; u++)
+                    if (gr[u] != -1) pv[u] = path[pv[u]];
+#pragma unroll
+                for (int u = 0; u < kC; u++)
+                    if (gr[u] == -2) xs[u] = sreq_x[s0 + u];
+#pragma unroll
+                for (int u = 0; u < kC; u++) {
+                    if (gr[u] == -1) continue;
+                    dep++;
+                    if (gr[u] == -2) {
+                        comp[xs[u]] = t + 1;
+                        atomicAdd(&delivered[-pv[u] - 1], 1u);
+                        sinks++;
+                        if constexpr (ACT)
+                            for (int q = d.fw_ptr[-pv[u] - 1]; q < d.fw_ptr[-pv[u]]; q++) set_live(m + d.fw_str[q]);
+                    } else {
+                        gdep[(size_t)pv[u] * bmax + gr[u]] = 1;
+                    }
+                }
+                if (!open) {  // the rest stays; reset its grant slots
+                    for (int k = k0 + kC; k < nr; k++) grant[(size_t)src * bmax + k] = -1;
+                    break;
                 }
             }
             if (dep) {
@@ -420,30 +515,51 @@ __global__ void __launch_bounds__(kThreads, kMinWaves) engine_wg(DevNet d) {
             uint32_t tl = qtail[f];
             const int base = d.fifo_off[f], mask = d.fifo_mask[f];
             const uint32_t ready = t + (uint32_t)lat[f];
-            int cnt = 0;
-            uint32_t last_port = 0, last_x = 0;
-            for (int r = 0; r < g; r++) {
-                const size_t gi = (size_t)f * bmax + r;
-                if (!gdep[gi]) continue;
-                gdep[gi] = 0;
-                const uint32_t sk = glist[gi];
-                const int src = (int)(sk >> 8);
-                const size_t si = (size_t)src * bmax + (sk & 255u);
-                const int e = base + (int)(tl & (uint32_t)mask);
-                fx[e] = sreq_x[si];
-                frdy[e] = ready;
-                fpp[e] = sreq_pp[si];
-                last_x = sreq_x[si];
-                tl++;
-                cnt++;
-                last_port = src < m ? (uint32_t)d.port_at_head[src] : P - 1;
+            // the departed grants in rank order, kC at a time
+            int cnt = 0, last_src = 0;
+            uint32_t last_x = 0;
+            for (int r0 = 0; r0 < g; r0 += kC) {
+                const size_t g0 = (size_t)f * bmax + r0;
+                bool gd[kC];
+                uint32_t sk[kC], sx[kC];
+                int sp[kC];
+#pragma unroll
+                for (int u = 0; u < kC; u++) gd[u] = r0 + u < g && gdep[g0 + u] != 0;
+#pragma unroll
+                for (int u = 0; u < kC; u++)
+                    if (gd[u]) {
+                        gdep[g0 + u] = 0;
+                        sk[u] = glist[g0 + u];
+                    }
+#pragma unroll
+                for (int u = 0; u < kC; u++)
+                    if (gd[u]) {
+                        const size_t si = (size_t)(sk[u] >> 8) * bmax + (sk[u] & 255u);
+                        sx[u] = sreq_x[si];
+                        sp[u] = sreq_pp[si];
+                    }
+#pragma unroll
+                for (int u = 0; u < kC; u++) {
+                    if (!gd[u]) continue;
+                    const int e = base + (int)(tl & (uint32_t)mask);
+                    fx[e] = sx[u];
+                    frdy[e] = ready;
+                    fpp[e] = sp[u];
+                    last_x = sx[u];
+                    last_src = (int)(sk[u] >> 8);
+                    tl++;
+                    cnt++;
+                }
             }
             if (cnt) {
                 if (ACT) set_live(f);
                 qtail[f] = tl;
                 tx[f] += (uint64_t)cnt;
                 busy[f] += 1;
-                if (d.arb & 1) rr[f] = (last_port + 1) % P;
+                if (d.arb & 1) {
+                    const uint32_t last_port = last_src < m ? (uint32_t)d.port_at_head[last_src] : P - 1;
+                    rr[f] = (last_port + 1) % P;
+                }
                 if (fair) cptr[f] = 1u - (lcls ? (uint32_t)lcls[last_x] : 0u);
             }
         }
@@ -486,26 +602,25 @@ __global__ void __launch_bounds__(kThreads, kMinWaves) engine_wg(DevNet d) {
 
 }  // namespace
 
-template <bool ACT, int NT, int MW>
+template <bool ACT, int NT>
 hipError_t launch_wg2(const DevNet &d, hipStream_t st) {
     const int lds = d.wg_lds + (ACT ? d.wg_act : 0);
-    auto k = d.wg_lds > 0 ? engine_wg<true, ACT, NT, MW> : engine_wg<false, ACT, NT, MW>;
+    auto k = d.wg_lds > 0 ? engine_wg<true, ACT, NT> : engine_wg<false, ACT, NT>;
     if (lds > 65536) (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     hipLaunchKernelGGL(k, dim3((unsigned)d.S), dim3(NT), (unsigned)lds, st, d);
     return hipGetLastError();
 }
 
-template <int NT, int MW>
+template <int NT>
 hipError_t launch_wg(const DevNet &d, hipStream_t st) {
-    return d.wg_act > 0 ? launch_wg2<true, NT, MW>(d, st) : launch_wg2<false, NT, MW>(d, st);
+    return d.wg_act > 0 ? launch_wg2<true, NT>(d, st) : launch_wg2<false, NT>(d, st);
 }
 
 hipError_t launch_workgroup(const DevNet &d, hipStream_t st) {
     const int per_cu = (d.S + 255) / 256;  // workgroups per CU when all are resident
-    if (per_cu <= 1) return launch_wg<1024, 4>(d, st);
-    if (per_cu <= 2) return launch_wg<1024, 8>(d, st);
-    if (per_cu <= 4) return launch_wg<512, 8>(d, st);
-    return launch_wg<256, 4>(d, st);
+    if (per_cu <= 1) return launch_wg<1024>(d, st);
+    if (per_cu <= 2) return launch_wg<512>(d, st);
+    return launch_wg<256>(d, st);
 }
 
 }  // namespace simgpu

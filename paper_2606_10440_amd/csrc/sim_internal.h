@@ -59,6 +59,9 @@ struct DevNet {
     uint32_t pd_omask;
     // paths: hop link ids, each path terminated by -(1 + flow slot)
     const int32_t *path_link;
+    // workgroup engine: streams that wait on a flow ([nflows+1] CSR), woken
+    // when the flow delivers
+    const int32_t *fw_ptr, *fw_str;
 
     // per-scenario parameters [S*m]
     const int32_t *bw, *lat, *cap;
