@@ -20,6 +20,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -57,16 +58,21 @@ def algorithmic_bytes(T: int, S: int, m: int) -> int:
     return S * (T * COMPLETION_BYTES + m * 16 + 4)
 
 
-def engine_source_hash() -> str:
-    """Digest of the device engine sources (counters taken on other sources
-    are not reported)."""
-    h = hashlib.sha256()
+def engine_source_hash(kernel: str = "") -> str:
+    """Digest of the device sources a kernel is built from: its engine's
+    .hip file (named after the kernel symbol, e.g. engine_wave) and the two
+    shared headers.  With no kernel name, every engine source.  Counters
+    taken on other sources are not reported."""
     csrc = os.path.join(ROOT, "paper_2606_10440_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".h")):
-            with open(os.path.join(csrc, f), "rb") as fh:
-                h.update(f.encode())
-                h.update(fh.read())
+    m = re.search(r"(engine_[a-z0-9]+)", kernel or "")
+    names = sorted(f for f in os.listdir(csrc) if f.endswith((".hip", ".h")))
+    if m and m.group(1) + ".hip" in names:
+        names = sorted({m.group(1) + ".hip", "engine_common.h", "sim_internal.h"} & set(names))
+    h = hashlib.sha256()
+    for f in names:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode())
+            h.update(fh.read())
     return h.hexdigest()[:16]
 
 
@@ -78,7 +84,7 @@ def load_traffic(workload: str, launch_s: float):
         return None
     with open(path) as f:
         c = json.load(f)
-    if c.get("engine_source_hash") != engine_source_hash():
+    if c.get("engine_source_hash") != engine_source_hash(c.get("kernel", "")):
         return None
     return c.get("traffic_bytes_per_launch")
 
