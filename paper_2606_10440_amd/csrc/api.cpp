@@ -705,38 +705,121 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                 wbytes[q] = align16((ringn + 64) * 8) + ((general && !fast) ? tail_gen(wb) : tail_fast);
                 if (wbytes[q] > kWaveBlockLds) fits = false;
             }
-            // Pack the waves into workgroups of up to kWaveMaxWpb independent waves and
-            // at most kWaveBlockLds bytes, aiming at one workgroup per compute
-            // unit so that every wave is resident at once: largest first, each
-            // into the workgroup with the fewest waves that has room.
-            std::vector<int32_t> qord(W);
-            for (int32_t q = 0; q < W; q++) qord[q] = q;
-            std::stable_sort(qord.begin(), qord.end(), [&](int32_t a, int32_t b2) { return wbytes[a] > wbytes[b2]; });
-            std::vector<std::vector<int32_t>> blk(std::min<int32_t>(kWaveBlocks, W));
-            std::vector<int64_t> bbytes(blk.size(), 0);
-            for (int32_t q : qord) {
-                if (!fits) break;
-                int32_t best = -1;
-                for (int32_t k = 0; k < (int32_t)blk.size(); k++) {
-                    if ((int32_t)blk[k].size() >= simgpu::kWaveMaxWpb || bbytes[k] + wbytes[q] > kWaveBlockLds) continue;
-                    if (best < 0 || blk[k].size() < blk[best].size() ||
-                        (blk[k].size() == blk[best].size() && bbytes[k] < bbytes[best]))
-                        best = k;
+            // Estimated run time of each wave, for placement only: its longest
+            // scenario's processed cycles (lines on the busiest link per cycle
+            // of bandwidth, plus a few fill/drain cycles per buffer's worth of
+            // lines) times the relative cost of a cycle of the loop it runs
+            // (the b = 1 loop, or the general loop unrolled to 1, 2, 4, 8).
+            std::vector<double> wtime(W, 0.0);
+            for (int32_t q = 0; q < W; q++) {
+                double cyc = 0.0;
+                int32_t wbmax = 1;
+                for (int32_t g = 0; g < G; g++) {
+                    const int32_t s = wv_sc[(size_t)q * G + g];
+                    if (s < 0) continue;
+                    for (int32_t i = 0; i < nl; i++) {
+                        const size_t pi = (size_t)s * m + fsrc[i];
+                        cyc = std::max(cyc, lcnt[i] / c->bw[pi] + 4.0 * lcnt[i] / c->cap[pi]);
+                        wbmax = std::max(wbmax, c->bw[pi]);
+                    }
                 }
-                if (best < 0) {
-                    blk.emplace_back();
-                    bbytes.push_back(0);
-                    best = (int32_t)blk.size() - 1;
-                }
-                blk[best].push_back(q);
-                bbytes[best] += wbytes[q];
+                const bool fast = c->arb == SIM_ARB_LOWEST_ID && wbmax == 1;
+                const double per = fast ? 1.0 : wbmax <= 1 ? 1.5 : wbmax <= 2 ? 1.8 : wbmax <= 4 ? 2.9 : 5.5;
+                wtime[q] = cyc * per;
             }
-            // waves of a workgroup in scenario order (longest expected first);
-            // workgroups ordered by their first wave
-            for (auto &v : blk) std::sort(v.begin(), v.end());
-            std::stable_sort(blk.begin(), blk.end(), [](const std::vector<int32_t> &a, const std::vector<int32_t> &b2) {
-                return (a.empty() ? INT32_MAX : a[0]) < (b2.empty() ? INT32_MAX : b2[0]);
-            });
+            std::vector<std::vector<int32_t>> blk;
+            int64_t lds_floor = 0;
+            // A compute unit has four SIMDs and runs the waves of one workgroup
+            // on them in turn (wave j on SIMD j mod 4).  When there are more
+            // waves than SIMDs, the shortest waves share a SIMD two by two
+            // (a pair sits at positions j and j + 4 of a workgroup) and the
+            // longest run alone; each workgroup takes four SIMD slots and
+            // reserves more than half of the LDS, so that it has a compute unit
+            // to itself.
+            const int32_t nsimd = 4 * kWaveBlocks;
+            if (fits && W > nsimd && W <= 2 * nsimd) {
+                const int32_t E = W - nsimd;  // SIMDs holding two waves
+                std::vector<int32_t> qs(W);
+                for (int32_t q = 0; q < W; q++) qs[q] = q;
+                std::stable_sort(qs.begin(), qs.end(), [&](int32_t a, int32_t b2) { return wtime[a] > wtime[b2]; });
+                // slots: the W - 2E longest alone; the 2E shortest paired,
+                // longest of them with shortest
+                struct Slot { int32_t a, b; int64_t bytes; };
+                std::vector<Slot> slots;
+                for (int32_t k = 0; k < W - 2 * E; k++) slots.push_back({qs[k], -1, wbytes[qs[k]]});
+                for (int32_t k = 0; k < E; k++) {
+                    const int32_t a = qs[W - 2 * E + k], b2 = qs[W - 1 - k];
+                    slots.push_back({a, b2, wbytes[a] + wbytes[b2]});
+                }
+                std::stable_sort(slots.begin(), slots.end(), [](const Slot &x, const Slot &y) { return x.bytes > y.bytes; });
+                std::vector<std::vector<Slot>> bs(kWaveBlocks);
+                std::vector<int64_t> bb(kWaveBlocks, 0);
+                bool ok2 = true;
+                for (const Slot &sl : slots) {
+                    int32_t best = -1;
+                    for (int32_t k = 0; k < kWaveBlocks; k++) {
+                        if (bs[k].size() >= 4 || bb[k] + sl.bytes > kWaveBlockLds) continue;
+                        if (best < 0 || bb[k] < bb[best]) best = k;
+                    }
+                    if (best < 0) {
+                        ok2 = false;
+                        break;
+                    }
+                    bs[best].push_back(sl);
+                    bb[best] += sl.bytes;
+                }
+                if (ok2) {
+                    // positions: pairs' first waves, lone waves, then the pairs'
+                    // second waves at position + 4 (-1 = no wave)
+                    blk.resize(kWaveBlocks);
+                    for (int32_t k = 0; k < kWaveBlocks; k++) {
+                        std::stable_sort(bs[k].begin(), bs[k].end(), [](const Slot &x, const Slot &y) {
+                            return (x.b >= 0) > (y.b >= 0);
+                        });
+                        auto &v = blk[k];
+                        for (const Slot &sl : bs[k]) v.push_back(sl.a);
+                        while (v.size() < 4) v.push_back(-1);
+                        for (const Slot &sl : bs[k])
+                            if (sl.b >= 0) v.push_back(sl.b);
+                    }
+                    lds_floor = kWaveBlockLds / 2 + 16;
+                }
+            }
+            if (blk.empty()) {
+                // Otherwise pack the waves into workgroups of up to kWaveMaxWpb
+                // independent waves and at most kWaveBlockLds bytes, aiming at one
+                // workgroup per compute unit so that every wave is resident at
+                // once: largest first, each into the workgroup with the fewest
+                // waves that has room.
+                std::vector<int32_t> qord(W);
+                for (int32_t q = 0; q < W; q++) qord[q] = q;
+                std::stable_sort(qord.begin(), qord.end(), [&](int32_t a, int32_t b2) { return wbytes[a] > wbytes[b2]; });
+                blk.resize(std::min<int32_t>(kWaveBlocks, W));
+                std::vector<int64_t> bbytes(blk.size(), 0);
+                for (int32_t q : qord) {
+                    if (!fits) break;
+                    int32_t best = -1;
+                    for (int32_t k = 0; k < (int32_t)blk.size(); k++) {
+                        if ((int32_t)blk[k].size() >= simgpu::kWaveMaxWpb || bbytes[k] + wbytes[q] > kWaveBlockLds) continue;
+                        if (best < 0 || blk[k].size() < blk[best].size() ||
+                            (blk[k].size() == blk[best].size() && bbytes[k] < bbytes[best]))
+                            best = k;
+                    }
+                    if (best < 0) {
+                        blk.emplace_back();
+                        bbytes.push_back(0);
+                        best = (int32_t)blk.size() - 1;
+                    }
+                    blk[best].push_back(q);
+                    bbytes[best] += wbytes[q];
+                }
+                // waves of a workgroup in scenario order (longest expected first);
+                // workgroups ordered by their first wave
+                for (auto &v : blk) std::sort(v.begin(), v.end());
+                std::stable_sort(blk.begin(), blk.end(), [](const std::vector<int32_t> &a, const std::vector<int32_t> &b2) {
+                    return (a.empty() ? INT32_MAX : a[0]) < (b2.empty() ? INT32_MAX : b2[0]);
+                });
+            }
             int32_t wpb = 1;
             int64_t lmax = 16;
             for (auto &v : blk) wpb = std::max(wpb, (int32_t)v.size());
@@ -745,12 +828,14 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
             for (size_t k = 0; k < blk.size(); k++) {
                 int64_t o2 = 0;
                 for (size_t j = 0; j < blk[k].size(); j++) {
-                    blk_wave[k * wpb + j] = blk[k][j];
+                    const int32_t q = blk[k][j];
+                    blk_wave[k * wpb + j] = q;
                     blk_off[k * wpb + j] = (int32_t)o2;
-                    o2 += wbytes[blk[k][j]];
+                    if (q >= 0) o2 += wbytes[q];
                 }
                 lmax = std::max(lmax, o2);
             }
+            lmax = std::max(lmax, lds_floor);
             wv.bytes = lmax;
             wv.G = G;
             wv.W = W;
