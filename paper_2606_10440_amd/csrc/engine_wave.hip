@@ -332,21 +332,12 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
     // End of cycle: clock and status of every scenario of the wave.  nxt is
     // the lane's FIFO-head ready time if still in the future at the start of
     // the cycle; a scenario in which nothing departed jumps to the minimum of
-    // its lanes' nxt.  That minimum is either taken during the cycle by the
-    // caller (rv) or, when lazy, through LDS only in cycles that need it.
-    auto time_phase = [&](bool dep, uint32_t nxt, uint32_t rv, bool lazy) {
+    // its lanes' nxt, rv, which the caller took during the cycle (an LDS
+    // atomic minimum issued with the requests).
+    auto time_phase = [&](bool dep, uint32_t rv) {
         const bool act = live & ((occ != 0u) | (R < rend));
         const bool sdep = (__ballot(dep) & smask) != 0ull;
         const bool sact = (__ballot(act) & smask) != 0ull;
-        const bool idle = live & !sdep;
-        if (lazy && __ballot(idle) != 0ull) {
-            cbar();
-            atomicMin(&red[idle ? (uint32_t)g : 64u + (uint32_t)w], nxt);
-            cbar();
-            rv = red[g];
-            cbar();
-            red[i == 0 ? (uint32_t)g : 64u + (uint32_t)w] = kNever;
-        }
         const uint32_t tn = sdep ? t + 1u : rv;
         processed += live ? 1u : 0u;
         const bool go = sact & (sdep | (rv != kNever)) & (tn <= maxc) & (processed <= wdog);
@@ -424,7 +415,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             red[i == 0 ? (uint32_t)g : 64u + (uint32_t)w] = kNever;
             he = ring[rbase + head];
             refresh_dv();
-            time_phase(fwon | swon, nxt, rv, false);
+            time_phase(fwon | swon, rv);
             if constexpr (CR) {  // fullness at the next processed cycle
                 credits_back();
                 word[w] = occ + owed < cap ? kWordEmpty : kWordFull;
@@ -482,6 +473,9 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             }
             uint32_t nxt = (live & (occ != 0u) & (e[0].y > t)) ? e[0].y : kNever;
             if constexpr (CR) nxt = min(nxt, (live & (owed != 0u)) ? crt : kNever);
+            // the scenario's earliest future event, taken with the requests so
+            // that an idle cycle needs no extra LDS round trip to jump
+            atomicMin(&red[nxt != kNever ? (uint32_t)g : 64u + (uint32_t)w], nxt);
             // stream offers: the released lines of the current range, then (rarely)
             // of the ranges after it
             // (the lane is their source and their target: they stay in registers)
@@ -507,11 +501,13 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             }
             cbar();
             // ---------------------------------------------------------- G
+            uint32_t rv;
             K lst[BMW];
             {
                 uint2 qv[(NF - 1) * BMW];
 #pragma unroll
                 for (int c = 0; c < (NF - 1) * BMW; c++) qv[c] = wreq[c * 64 + w];
+                rv = red[g];
                 K lists[NF][BMW];
 #pragma unroll
                 for (int f = 0; f < NF; f++) {
@@ -607,11 +603,15 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                 for (int k = 0; k < BMW; k++)
                     wvoid[((vdm >> k) & 1u) ? gv[k].y * 64u + tgk[k] : gnt_trash] = tag;
                 cbar();
+                uint32_t vt[BMW];  // read every void flag before the first ring write
+#pragma unroll
+                for (int r = 0; r < BMW; r++) vt[r] = wvoid[r * 64 + w];
+                cbar();
                 uint32_t j = 0;
 #pragma unroll
                 for (int r = 0; r < BMW; r++) {
                     const uint32_t lo = (uint32_t)lst[r];
-                    const bool keep = ((uint32_t)r < gcnt) & (wvoid[r * 64 + w] != tag);
+                    const bool keep = ((uint32_t)r < gcnt) & (vt[r] != tag);
                     ring[keep ? rbase + wrap_add(tail, j, cap) : ring_trash] = make_uint2(lo & ~0x1Fu, ready);
                     if (ARB == 1) {
                         const uint32_t f = (lo & 31u) / BMW;
@@ -627,10 +627,11 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             busy += cnt ? 1u : 0u;
             if (ARB == 1) rr = cnt ? (lastport + 1u == P ? 0u : lastport + 1u) : rr;
             cbar();
+            red[i == 0 ? (uint32_t)g : 64u + (uint32_t)w] = kNever;
 #pragma unroll
             for (int k = 0; k < BMW; k++) e[k] = ring[rbase + wrap_add(head, min((uint32_t)k, cap - 1u), cap)];
             refresh_dv();
-            time_phase((depf | sgr) != 0u, nxt, kNever, true);
+            time_phase((depf | sgr) != 0u, rv);
             if constexpr (CR) credits_back();
         }
     };
