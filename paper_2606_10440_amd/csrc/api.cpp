@@ -569,7 +569,14 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     std::vector<uint32_t> wv_lfb, wv_lfx;
     std::vector<int32_t> wv_feed, wv_nfeed, wv_sc, r_lf, pd_dix, blk_wave, blk_off;
     constexpr int64_t kWaveBlockLds = 160 * 1024;  // LDS of a compute unit
-    constexpr int32_t kWaveBlocks = 256;           // compute units of the device
+    // compute units of the current device (256 on MI355X)
+    int32_t wave_blocks = 256;
+    {
+        int cur = 0, ncu = 0;
+        if (hipGetDevice(&cur) == hipSuccess &&
+            hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, cur) == hipSuccess && ncu > 0)
+            wave_blocks = ncu;
+    }
     {
         std::vector<std::vector<int32_t>> lflows(nl);
         bool ok = nl >= 1 && nl <= 64 && T < (1ll << 25) - 1 && bm <= 8;
@@ -736,7 +743,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
             // longest run alone; each workgroup takes four SIMD slots and
             // reserves more than half of the LDS, so that it has a compute unit
             // to itself.
-            const int32_t nsimd = 4 * kWaveBlocks;
+            const int32_t nsimd = 4 * wave_blocks;
             if (fits && W > nsimd && W <= 2 * nsimd) {
                 const int32_t E = W - nsimd;  // SIMDs holding two waves
                 std::vector<int32_t> qs(W);
@@ -752,12 +759,12 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                     slots.push_back({a, b2, wbytes[a] + wbytes[b2]});
                 }
                 std::stable_sort(slots.begin(), slots.end(), [](const Slot &x, const Slot &y) { return x.bytes > y.bytes; });
-                std::vector<std::vector<Slot>> bs(kWaveBlocks);
-                std::vector<int64_t> bb(kWaveBlocks, 0);
+                std::vector<std::vector<Slot>> bs(wave_blocks);
+                std::vector<int64_t> bb(wave_blocks, 0);
                 bool ok2 = true;
                 for (const Slot &sl : slots) {
                     int32_t best = -1;
-                    for (int32_t k = 0; k < kWaveBlocks; k++) {
+                    for (int32_t k = 0; k < wave_blocks; k++) {
                         if (bs[k].size() >= 4 || bb[k] + sl.bytes > kWaveBlockLds) continue;
                         if (best < 0 || bb[k] < bb[best]) best = k;
                     }
@@ -771,8 +778,8 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                 if (ok2) {
                     // positions: pairs' first waves, lone waves, then the pairs'
                     // second waves at position + 4 (-1 = no wave)
-                    blk.resize(kWaveBlocks);
-                    for (int32_t k = 0; k < kWaveBlocks; k++) {
+                    blk.resize(wave_blocks);
+                    for (int32_t k = 0; k < wave_blocks; k++) {
                         std::stable_sort(bs[k].begin(), bs[k].end(), [](const Slot &x, const Slot &y) {
                             return (x.b >= 0) > (y.b >= 0);
                         });
@@ -794,7 +801,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                 std::vector<int32_t> qord(W);
                 for (int32_t q = 0; q < W; q++) qord[q] = q;
                 std::stable_sort(qord.begin(), qord.end(), [&](int32_t a, int32_t b2) { return wbytes[a] > wbytes[b2]; });
-                blk.resize(std::min<int32_t>(kWaveBlocks, W));
+                blk.resize(std::min<int32_t>(wave_blocks, W));
                 std::vector<int64_t> bbytes(blk.size(), 0);
                 for (int32_t q : qord) {
                     if (!fits) break;
