@@ -42,9 +42,13 @@ __device__ __forceinline__ void load_range(const DevNet &d, int R, RangeReg<PC> 
 template <int PC>
 __device__ __forceinline__ bool released(const DevNet &d, const RangeReg<PC> &r, uint32_t o, const uint32_t *deliv) {
     bool ok = true;
+    // the cached descriptors' counters are read together, without branches
+    // (an absent descriptor has flow 0, a valid index, and is ignored)
 #pragma unroll
-    for (int q = 0; q < PC; q++)
-        if (r.pd0 + q < r.pd1) ok = ok && deliv[r.pf[q]] > r.pb[q] + (o & d.pd_omask);
+    for (int q = 0; q < PC; q++) {
+        const uint32_t v = deliv[r.pf[q]];
+        ok = ok & ((r.pd0 + q >= r.pd1) | (v > r.pb[q] + (o & d.pd_omask)));
+    }
     for (int idx = r.pd0 + PC; ok && idx < r.pd1; idx++)
         ok = deliv[d.pd_flow[idx]] > d.pd_base[idx] + (o & d.pd_omask);
     return ok;

@@ -22,11 +22,15 @@ namespace {
 
 using namespace dev;
 
+
 // HBMFIFO: the FIFO rings live in HBM instead of LDS (a ring is only ever
 // touched by its own lane, so no extra ordering is needed).
 template <int BM, bool ONEWAVE, int ARB, bool HBMFIFO>
 __global__ void __launch_bounds__(1024) engine_lane(DevNet d) {
     extern __shared__ __align__(16) unsigned char smem[];
+    // requests per target ranked in registers (more: ranked from LDS); none
+    // for wide links, whose request records already fill the registers
+    constexpr int kRankRegs = BM <= 4 ? 8 : 0;
     uint4 *fifo = HBMFIFO ? d.gfifo + (size_t)blockIdx.x * d.fifo_total : reinterpret_cast<uint4 *>(smem);
     int32_t *lpath = reinterpret_cast<int32_t *>(smem + d.o_path);
     uint32_t *deliv = reinterpret_cast<uint32_t *>(smem + d.o_deliv);
@@ -96,6 +100,25 @@ __global__ void __launch_bounds__(1024) engine_lane(DevNet d) {
     uint64_t processed = 0;
     int32_t state = d.T > 0 ? kRunRunning : kRunOk;
     bool overflow = false;
+    // a request's arbitration key at this target: its line id, or its
+    // round-robin rank (k, port offset from the pointer); ports are < P
+    auto req_key = [&](const uint4 &r) -> uint32_t {
+        if (ARB == 0) return r.x;
+        const uint32_t off = r.w + P - rr;
+        return (r.z & 255u) * P + (off >= P ? off - P : off);
+    };
+
+    // The first FIFO entries a lane may offer are read at the end of the
+    // previous cycle, after its pops and appends, so that their load (from
+    // HBM with HBMFIFO) overlaps the time phase instead of opening the next
+    // cycle; for narrow links only, whose entries fit the registers.
+    constexpr int kPre = BM <= 4 ? BM : 0;
+    uint4 pre[kPre > 0 ? kPre : 1];
+    auto prefetch = [&]() {
+#pragma unroll
+        for (int k = 0; k < kPre; k++)
+            if (on && k < b && (uint32_t)k < tail - head) pre[k] = fifo[fbase + ((head + k) & fmask)];
+    };
 
     while (state == kRunRunning) {
         // -------------------------------------------------------------- R
@@ -110,7 +133,7 @@ __global__ void __launch_bounds__(1024) engine_lane(DevNet d) {
                 ftg[k] = 0;
                 fxv[k] = 0;
                 if (k < b && (uint32_t)k < occ && nf == k) {
-                    const uint4 e = fifo[fbase + ((head + k) & fmask)];
+                    const uint4 e = kPre > 0 ? pre[k < kPre ? k : 0] : fifo[fbase + ((head + k) & fmask)];
                     if (e.y > t) {
                         next = e.y;
                     } else {
@@ -156,37 +179,66 @@ __global__ void __launch_bounds__(1024) engine_lane(DevNet d) {
         phase_sync<ONEWAVE>();
         // -------------------------------------------------------------- G
         int g = 0;
+        uint32_t creq = 0;  // this target's request count
         if (on) {
             const uint32_t c = req_cnt[i];
+            creq = c;
             if (c) {
                 req_cnt[i] = 0;
                 if (c > (uint32_t)rcap) overflow = true;
                 g = cap - (int)(tail - head);
                 if (b < g) g = b;
                 if ((int)c < g) g = (int)c;
-                if (g > 0 && !overflow) {
-                    if (c == 1) {
-                        const uint4 r0 = req[rbase];
-                        grant[(r0.z >> 8) * BM + (r0.z & 255u)] = 0;
-                        glist[i * BM] = (uint32_t)rbase;
-                    } else {
-                        for (uint32_t a = 0; a < c; a++) {
-                            const uint4 ra = req[rbase + a];
-                            const uint32_t ka = ARB == 0 ? ra.x : (ra.z & 255u) * P + (ra.w + P - rr) % P;
-                            int rank = 0;
-                            for (uint32_t q = 0; q < c; q++) {
-                                const uint4 rq = req[rbase + q];
-                                const uint32_t kq = ARB == 0 ? rq.x : (rq.z & 255u) * P + (rq.w + P - rr) % P;
-                                rank += kq < ka ? 1 : 0;
-                            }
-                            if (rank < g) {
-                                grant[(ra.z >> 8) * BM + (ra.z & 255u)] = rank;
-                                glist[i * BM + rank] = (uint32_t)rbase + a;
-                            }
+                if (g > 0 && !overflow && c > (uint32_t)kRankRegs) {
+                    // many requests: rank each against all, reading them from LDS
+                    for (uint32_t a = 0; a < c; a++) {
+                        const uint4 ra = req[rbase + a];
+                        const uint32_t ka = req_key(ra);
+                        int rank = 0;
+                        for (uint32_t q = 0; q < c; q++) rank += req_key(req[rbase + q]) < ka ? 1 : 0;
+                        if (rank < g) {
+                            grant[(ra.z >> 8) * BM + (ra.z & 255u)] = rank;
+                            glist[i * BM + rank] = (uint32_t)rbase + a;
                         }
                     }
                 }
                 if (g < 0) g = 0;
+            }
+        }
+        if constexpr (kRankRegs > 0) {
+            // Up to kRankRegs requests per target: their keys are read once,
+            // all together, and ranked in registers; the loops run to the
+            // wave's largest request count (wave-uniform bounds, so the
+            // register arrays are indexed at compile time).
+            const uint32_t cq = (on && g > 0 && !overflow && creq <= (uint32_t)kRankRegs) ? creq : 0u;
+            uint32_t cmax = cq;
+#pragma unroll
+            for (int sh = 32; sh >= 1; sh >>= 1) cmax = max(cmax, (uint32_t)__shfl_xor((int)cmax, sh));
+            if (cmax > 0u) {
+                uint32_t key[kRankRegs], rz[kRankRegs];
+#pragma unroll
+                for (int q = 0; q < kRankRegs; q++) {
+                    key[q] = 0xFFFFFFFFu;
+                    rz[q] = 0u;
+                    if ((uint32_t)q < cmax) {
+                        const uint4 rq = req[rbase + ((uint32_t)q < cq ? q : 0)];
+                        key[q] = (uint32_t)q < cq ? req_key(rq) : 0xFFFFFFFFu;
+                        rz[q] = rq.z;
+                    }
+                }
+#pragma unroll
+                for (int a = 0; a < kRankRegs; a++) {
+                    if ((uint32_t)a < cmax) {
+                        int rank = 0;
+#pragma unroll
+                        for (int q = 0; q < kRankRegs; q++)
+                            if ((uint32_t)q < cmax) rank += key[q] < key[a] ? 1 : 0;
+                        if (((uint32_t)a < cq) & (rank < g)) {
+                            grant[(rz[a] >> 8) * BM + (rz[a] & 255u)] = rank;
+                            glist[i * BM + rank] = (uint32_t)rbase + (uint32_t)a;
+                        }
+                    }
+                }
             }
         }
         phase_sync<ONEWAVE>();
@@ -262,7 +314,7 @@ __global__ void __launch_bounds__(1024) engine_lane(DevNet d) {
             if (cnt) {
                 tx += (uint64_t)cnt;
                 busy += 1;
-                if (ARB == 1) rr = (last_port + 1) % P;
+                if (ARB == 1) rr = last_port + 1u == P ? 0u : last_port + 1u;
             }
         }
         // -------------------------------------------------------------- time
@@ -325,6 +377,7 @@ __global__ void __launch_bounds__(1024) engine_lane(DevNet d) {
         if (state == kRunRunning && (uint64_t)t > d.max_cycles) state = kRunMaxCycles;
         if (state == kRunRunning && processed > d.watchdog) state = kRunWatchdog;
         if (!ONEWAVE) lds_fence_block();
+        if constexpr (kPre > 0) prefetch();
     }
     if (on) {
         d.tx_lines[(size_t)s * m + link] = tx;
