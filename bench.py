@@ -60,14 +60,22 @@ def algorithmic_bytes(T: int, S: int, m: int) -> int:
 
 def engine_source_hash(kernel: str = "") -> str:
     """Digest of the device sources a kernel is built from: its engine's
-    .hip file (named after the kernel symbol, e.g. engine_wave) and the two
-    shared headers.  With no kernel name, every engine source.  Counters
-    taken on other sources are not reported."""
+    .hip file (named after the kernel symbol, e.g. engine_wave) and the
+    headers it includes, transitively.  With no kernel name, every engine
+    source.  Counters taken on other sources are not reported."""
     csrc = os.path.join(ROOT, "paper_2606_10440_amd", "csrc")
     m = re.search(r"(engine_[a-z0-9]+)", kernel or "")
     names = sorted(f for f in os.listdir(csrc) if f.endswith((".hip", ".h")))
     if m and m.group(1) + ".hip" in names:
-        names = sorted({m.group(1) + ".hip", "engine_common.h", "sim_internal.h"} & set(names))
+        todo, names = [m.group(1) + ".hip"], set()
+        while todo:
+            f = todo.pop()
+            if f in names or not os.path.exists(os.path.join(csrc, f)):
+                continue
+            names.add(f)
+            with open(os.path.join(csrc, f)) as fh:
+                todo += re.findall(r'^#include "([^"]+)"', fh.read(), re.M)
+        names = sorted(names)
     h = hashlib.sha256()
     for f in names:
         with open(os.path.join(csrc, f), "rb") as fh:
