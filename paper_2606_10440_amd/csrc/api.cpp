@@ -740,9 +740,8 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
             // on them in turn (wave j on SIMD j mod 4).  When there are more
             // waves than SIMDs, the shortest waves share a SIMD two by two
             // (a pair sits at positions j and j + 4 of a workgroup) and the
-            // longest run alone; each workgroup takes four SIMD slots and
-            // reserves more than half of the LDS, so that it has a compute unit
-            // to itself.
+            // longest run alone; each workgroup takes four SIMD slots and has a
+            // compute unit to itself (below).
             const int32_t nsimd = 4 * wave_blocks;
             if (fits && W > nsimd && W <= 2 * nsimd) {
                 const int32_t E = W - nsimd;  // SIMDs holding two waves
@@ -789,7 +788,6 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                         for (const Slot &sl : bs[k])
                             if (sl.b >= 0) v.push_back(sl.b);
                     }
-                    lds_floor = kWaveBlockLds / 2 + 16;
                 }
             }
             if (blk.empty()) {
@@ -842,6 +840,9 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                 }
                 lmax = std::max(lmax, o2);
             }
+            // no more workgroups than compute units: each reserves more than half
+            // of the LDS, so that no two share a compute unit while another idles
+            if ((int32_t)blk.size() <= wave_blocks) lds_floor = kWaveBlockLds / 2 + 16;
             lmax = std::max(lmax, lds_floor);
             wv.bytes = lmax;
             wv.G = G;
