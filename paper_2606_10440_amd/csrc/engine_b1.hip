@@ -114,9 +114,19 @@ __global__ void __launch_bounds__(1024) engine_b1(DevNet d) {
         unsigned long long *wcur = ARB == 0 ? word + (size_t)par * nl : word;
         // -------------------------------------------------------------- R
         uint32_t next = kNever;
+        // First every lane completes last cycle's appended entry and issues
+        // the head reloads it needs, then the heads are used.  The memory
+        // counter also counts stores, so one explicit wait here (for last
+        // cycle's next-hop loads, long complete) keeps the compiler from
+        // waiting on each lane's store before the next lane's; the reloads
+        // are then waited for once.
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
 #pragma unroll
         for (int q = 0; q < LPT; q++) {
             const int lane = tid + q * NT;
+            // the lane's constants are re-derived each cycle rather than kept
+            // (hoisted) in spilled registers
+            asm volatile("" : "+v"(pa[q]), "+v"(pb[q]));
             st8[q] &= 0x9FFu;
             if (st8[q] & 2048u) {
                 // complete the entry appended last cycle with its next hop
@@ -125,15 +135,19 @@ __global__ void __launch_bounds__(1024) engine_b1(DevNet d) {
                 if ((st8[q] & 256u) && head[q] == tail[q] - 1u) ctg[q] = ntg[q];
                 st8[q] &= ~2048u;
             }
+            if (lane < nl && tail[q] != head[q] && !(st8[q] & 256u)) {
+                const uint4 e = fifo[((size_t)lane << lg) + (head[q] & rmask)];
+                cx[q] = e.x;
+                cpp[q] = e.y;
+                crdy[q] = e.z;
+                ctg[q] = (int32_t)e.w;
+                st8[q] |= 256u;
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < LPT; q++) {
+            const int lane = tid + q * NT;
             if (lane < nl && tail[q] != head[q]) {
-                if (!(st8[q] & 256u)) {
-                    const uint4 e = fifo[((size_t)lane << lg) + (head[q] & rmask)];
-                    cx[q] = e.x;
-                    cpp[q] = e.y;
-                    crdy[q] = e.z;
-                    ctg[q] = (int32_t)e.w;
-                    st8[q] |= 256u;
-                }
                 if (crdy[q] > t) {
                     next = crdy[q] < next ? crdy[q] : next;
                 } else {
@@ -164,10 +178,15 @@ __global__ void __launch_bounds__(1024) engine_b1(DevNet d) {
         }
         lds_fence_block();
         // -------------------------------------------------------------- G
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): R's stores and reloads
         bool sdep = false;
+        // lane-derived addresses are recomputed here rather than kept
+        // (hoisted) in spilled registers
+        int tq = tid;
+        asm volatile("" : "+v"(tq));
 #pragma unroll
         for (int q = 0; q < LPT; q++) {
-            const int lane = tid + q * NT;
+            const int lane = tq + q * NT;
             if (lane >= nl) continue;
             if (ARB == 0) word[(size_t)(par ^ 1) * nl + lane] = kNone;  // buffer of the next cycle
             const unsigned long long w = wcur[lane];
@@ -216,7 +235,10 @@ __global__ void __launch_bounds__(1024) engine_b1(DevNet d) {
         }
         lds_fence_block();
         // -------------------------------------------------------------- D
+        // Departures first (completion stores included), then the next heads'
+        // loads, so that no lane's store waits behind another lane's load.
         int dep = 0;
+        uint32_t gmask = 0;
 #pragma unroll
         for (int q = 0; q < LPT; q++) {
             const int lane = tid + q * NT;
@@ -233,16 +255,21 @@ __global__ void __launch_bounds__(1024) engine_b1(DevNet d) {
                 head[q]++;
                 dep++;
                 st8[q] &= ~256u;
-                // fetch the next head now (used next cycle) unless it is the
-                // entry appended this cycle, which is completed next cycle
-                if (tail[q] != head[q] && !((st8[q] & 2048u) && head[q] == tail[q] - 1u)) {
-                    const uint4 e = fifo[((size_t)lane << lg) + (head[q] & rmask)];
-                    cx[q] = e.x;
-                    cpp[q] = e.y;
-                    crdy[q] = e.z;
-                    ctg[q] = (int32_t)e.w;
-                    st8[q] |= 256u;
-                }
+                gmask |= 1u << q;
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < LPT; q++) {
+            const int lane = tid + q * NT;
+            // fetch the next head now (used next cycle) unless it is the
+            // entry appended this cycle, which is completed next cycle
+            if (((gmask >> q) & 1u) && tail[q] != head[q] && !((st8[q] & 2048u) && head[q] == tail[q] - 1u)) {
+                const uint4 e = fifo[((size_t)lane << lg) + (head[q] & rmask)];
+                cx[q] = e.x;
+                cpp[q] = e.y;
+                crdy[q] = e.z;
+                ctg[q] = (int32_t)e.w;
+                st8[q] |= 256u;
             }
         }
         if (sreq) {
