@@ -85,16 +85,18 @@ def engine_source_hash(kernel: str = "") -> str:
 
 
 def load_traffic(workload: str, launch_s: float):
-    """HBM traffic per launch from the committed rocprofv3 counter summary,
-    only if it was taken on the current engine source."""
+    """HBM traffic per launch and kernel symbol from the committed rocprofv3
+    counter summary; the traffic only if it was taken on the current engine
+    source."""
     path = os.path.join(ROOT, "profiles", f"engine_{workload}_hbm_counters.json")
     if not os.path.exists(path):
-        return None
+        return None, KERNEL_NAME
     with open(path) as f:
         c = json.load(f)
-    if c.get("engine_source_hash") != engine_source_hash(c.get("kernel", "")):
-        return None
-    return c.get("traffic_bytes_per_launch")
+    kernel = c.get("kernel", KERNEL_NAME)
+    if c.get("engine_source_hash") != engine_source_hash(kernel):
+        return None, kernel
+    return c.get("traffic_bytes_per_launch"), kernel
 
 
 def cpu_baseline(w, sample_seconds: float):
@@ -266,7 +268,7 @@ def main():
     total_hops = line_hops * S
     value = total_hops * a.steps / (gpu_ms / 1e3)
     alg = algorithmic_bytes(T, S, m)
-    traffic = load_traffic(a.workload, launch_s)
+    traffic, kernel = load_traffic(a.workload, launch_s)
     achieved = alg / launch_s / 1e9
     out = {
         "metric": "simulated line-hop events/sec on 1 MI355X (bit-exact vs CPU oracle)",
@@ -288,7 +290,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "traffic_frac": None if traffic is None else traffic / launch_s / 1e9 / HBM_PEAK_GBS,
-                     "kernel": KERNEL_NAME, "algorithmic_bytes_per_launch": alg},
+                     "kernel": kernel, "algorithmic_bytes_per_launch": alg},
     }
     s.close()
     if not a.no_cpu_baseline:
