@@ -202,6 +202,20 @@ def test_batched_torus_subset(simmod, oracle_lib):
     check_vs_oracle(simmod, oracle_lib, w)
 
 
+def test_batched_more_waves_than_simds(simmod, oracle_lib):
+    # 6000 scenarios of a 3x3 torus need more wavefronts than the device has
+    # SIMDs, so the shortest share SIMDs in pairs; every bandwidth class and
+    # ring size mixes in the placement.  A spread sample is checked line by
+    # line, the rest by status.
+    w = si.torus2d(3, 3, n_scenarios=6000, seed=23, bws=(1, 2, 4), lat_lo=1, lat_hi=24,
+                   depths=(16, 32, 64), nbytes=128 * 9 * 6)
+    sample = sorted({0, 1, 2, 5999, 5998} | set(range(7, 6000, 251)))
+    say(f"6000-scenario torus: checking {len(sample)} scenarios against the oracle")
+    r, n_ok = check_vs_oracle(simmod, oracle_lib, w, scenarios=sample)
+    assert n_ok == len(sample)
+    assert (r.scenario_status == 0).all()
+
+
 @pytest.mark.parametrize("arb,coll,depths,nbytes", [(0, si.COLL_DIRECT_ALLREDUCE, (8, 13, 16, 32), 128 * 120),
                                                     (1, si.COLL_ALLTOALL, (8, 13, 16, 32), 128 * 3),
                                                     (1, si.COLL_ALLTOALL, (16, 32, 64), 128 * 8),
