@@ -69,3 +69,18 @@ def test_memcpy_workgroup_batch_sizes(simmod, oracle_lib, S):
     scenario."""
     w = noc.with_scenarios(tiny_noc(3, n_ops=8, max_lines=24), S, seed=S)
     check_engine(simmod, oracle_lib, w, "workgroup")
+
+
+@pytest.mark.parametrize("kind,size,U,W", [("alltoall", 4096, 1, 64), ("alltoall", 4096, 8, 64),
+                                           ("alltoall", 64, 16, 64), ("allgather", 16384, 16, 8),
+                                           ("allgather", 16384, 16, 256), ("allgather", 128, 16, 4)])
+def test_memcpy_exploration_points(simmod, oracle_lib, kind, size, U, W):
+    """Points of the unroll and outstanding-limit sweeps (Sec. 5.3) whose
+    trends tests/test_oracle_exploration.py checks on the oracle: the GPU
+    path gives the same completion cycle for every line."""
+    w, lay = noc.gpu_noc(2)
+    mc = (noc.alltoall_ops(lay, size, n_wg=32, unroll=U, window=W) if kind == "alltoall"
+          else noc.allgather_ops(lay, size, n_wg=32, unroll=U, window=W))
+    wm = noc.memcpy_workload(w, mc, name=f"two_gpu_{kind}_{size}_U{U}_W{W}")
+    say(wm.name)
+    check_vs_oracle(simmod, oracle_lib, wm)
