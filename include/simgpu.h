@@ -241,13 +241,20 @@ sim_status sim_load_memcpy(sim_ctx *ctx, int64_t n_ops, const int32_t *cu, const
                            int32_t unroll, int32_t window);
 
 /* Sizes of the loaded problem: transactions T, links m, scenarios S and
- * line-hops per scenario (sum of path lengths).  Any pointer may be NULL. */
+ * line-hops per scenario (sum of path lengths; a line-hop is one admission of
+ * a 128 B wavefront request onto a link, the per-line, per-hop unit of work
+ * of Sec. 4.4.3).  Any pointer may be NULL.  SIM_ERR_STATE before a load
+ * (n_links and n_scenarios are still written). */
 sim_status sim_sizes(const sim_ctx *ctx, int64_t *n_txn, int32_t *n_links, int32_t *n_scenarios,
                      uint64_t *line_hops);
 
 /*
  * Enqueue one full simulation of every scenario on hip_stream (a
- * hipStream_t; NULL = the null stream) and return.  Outputs are caller-owned
+ * hipStream_t; NULL = the null stream) and return.  This is the network
+ * side of the fine-grained simulation: every wavefront request (one 128 B
+ * cache line, Sec. 4.4.3) is advanced link by link through the graph of
+ * endpoints and switches with the routing of Sec. 4.5, under the queueing
+ * rules stated at the top of this header.  Outputs are caller-owned
  * device buffers that must stay valid until the stream reaches this work:
  *   d_completion  [S*T] u32 : completion cycle of every line (scenario-major)
  *   d_tx_lines    [S*m] u64 : lines admitted onto each link
@@ -262,20 +269,52 @@ sim_status sim_run(sim_ctx *ctx, void *hip_stream, uint32_t *d_completion, uint6
                    uint64_t *d_busy_cycles, uint32_t *d_makespan, uint64_t max_cycles);
 
 /* After the caller has synchronised the run's stream: SIM_OK, or the first
- * device-detected error (DEADLOCK / MAX_CYCLES) over the scenarios.  If
+ * device-detected error (DEADLOCK / MAX_CYCLES) over the scenarios.  (Error
+ * reporting of this library; the paper has no counterpart.)  If
  * status/cycles are non-NULL they receive per-scenario statuses ([S] int32)
  * and processed-cycle counts ([S] u64) on the host. */
 sim_status sim_status_after_sync(sim_ctx *ctx, int32_t *status, uint64_t *cycles);
 
-/* Route of flow src -> dst as link ids (host copy; *len = hop count).
- * SIM_ERR_SIZE if cap < hop count (then *len still holds the count). */
+/* Route of flow src -> dst as link ids (host copy; *len = hop count): the
+ * routing function of Sec. 4.5 over the graph of Sec. 4.6, here minimal-hop
+ * paths with MurmurHash3-finalizer ECMP tie-breaks (see the top of this
+ * header).  src == dst gives *len = 0.  SIM_ERR_INVALID_ARG for endpoints out
+ * of range or a NULL len; SIM_ERR_UNREACHABLE if dst cannot be reached;
+ * SIM_ERR_SIZE if cap < hop count or links is NULL for a non-empty route
+ * (then *len still holds the count).  links (cap entries) is caller-owned. */
 sim_status sim_route(const sim_ctx *ctx, int32_t src, int32_t dst, int32_t *links, int32_t cap,
                      int32_t *len);
 
-/* Last error message of this context (owned by the context; never NULL). */
+/*
+ * Decode line id of the loaded workload: the unit transfer of the network
+ * model is one 128 B wavefront request (Sec. 4.4.3); this names which
+ * transfer of the workload it is.
+ *   *src, *dst  : its source and destination endpoints;
+ *   *phase_step : the algorithm step of the line, the leading digit of the
+ *                 step-major id (see sim_coll): ring s; direct all-reduce
+ *                 phase (p-1) + k-1; direct all-gather / reduce-scatter and
+ *                 all-to-all k-1; hierarchical: phase 1 k-1, phase 2 (M-1) +
+ *                 s, phase 3 (M-1) + (2G-2) + k-1; RHD: halving step j,
+ *                 doubling step K + j; DBT: 2 phase + tree.  memcpy
+ *                 programs: the issue index of the request in its CU's
+ *                 program.  Custom transaction lists: -1;
+ *   *line       : the line's offset within its message (one step's transfer
+ *                 between two participants); memcpy: 0 for a load request or
+ *                 a store, 1 for a load's data line; custom lists: 0.
+ * Any output pointer may be NULL.  SIM_ERR_STATE before a load;
+ * SIM_ERR_INVALID_ARG if id is outside [0, T).  Host-only, no device work:
+ * it answers for the last load whose workload expansion succeeded, also when
+ * that load then failed to bind device memory (SIM_ERR_DEVICE / SIM_ERR_OOM).
+ */
+sim_status sim_txn_info(const sim_ctx *ctx, int64_t id, int32_t *src, int32_t *dst, int32_t *phase_step,
+                        int32_t *line);
+
+/* Last error message of this context (owned by the context; never NULL).
+ * Error reporting of this library; the paper has no counterpart. */
 const char *sim_last_error(const sim_ctx *ctx);
 
-/* Free the context and all its device memory.  NULL is allowed. */
+/* Free the context and all its device memory.  NULL is allowed.  (Resource
+ * management of this library; the paper has no counterpart.) */
 void sim_destroy(sim_ctx *ctx);
 
 #ifdef __cplusplus

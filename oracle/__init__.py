@@ -53,7 +53,7 @@ def lib():
         L.oracle_paths.argtypes = [C.c_int32, C.c_int32, P, P, P, P, C.c_int64]
         L.oracle_paths.restype = C.c_int
         L.oracle_txn.argtypes = [C.c_int, C.c_uint64, C.c_int32, C.c_int32, P, C.c_int32, C.c_int64,
-                                 P, P, P, P, P]
+                                 P, P, P, P, C.c_int32, P]
         L.oracle_txn.restype = C.c_int
         L.oracle_simulate.argtypes = [C.c_int32, C.c_int32, P, P, P, P, P, P, C.c_int32,
                                       C.c_int32, C.c_uint64, C.c_int32, P, C.c_int32,
@@ -98,11 +98,15 @@ def txn(coll, nbytes, group, E, x, order=None, dep=0):
     src = np.zeros(1, np.int32)
     dst = np.zeros(1, np.int32)
     npred = np.zeros(1, np.int32)
-    preds = np.zeros(4096, np.int64)
+    preds = np.zeros(64, np.int64)
     T = np.zeros(1, np.int64)
     o = None if order is None else np.ascontiguousarray(order, np.int32)
     rc = lib().oracle_txn(coll, nbytes, group, E, _p(o), dep, x, _p(src), _p(dst), _p(npred),
-                          _p(preds), _p(T))
+                          _p(preds), len(preds), _p(T))
+    if rc == 4 and npred[0] > len(preds):  # more predecessors than the first buffer holds
+        preds = np.zeros(int(npred[0]), np.int64)
+        rc = lib().oracle_txn(coll, nbytes, group, E, _p(o), dep, x, _p(src), _p(dst), _p(npred),
+                              _p(preds), len(preds), _p(T))
     return rc, int(src[0]), int(dst[0]), [int(v) for v in preds[:npred[0]]], int(T[0])
 
 

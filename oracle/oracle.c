@@ -101,14 +101,14 @@ static void bfs_to(int32_t n, const int32_t *in_ptr, const int32_t *in_tail,
  * out-links (ascending id) whose head is one hop closer to d; at the j-th
  * node with two or more candidates, the choice is byte (j mod 4) of the hash
  * modulo the candidate count, and the hash is re-mixed before every fourth
- * choice point after the first.  Returns the hop count. */
+ * choice point after the first.  cand has room for the largest out-degree.
+ * Returns the hop count. */
 static int32_t trace_path(const int32_t *row_ptr, const int32_t *col_idx,
                           const int32_t *dist, int32_t s, int32_t d,
-                          int32_t *out)
+                          int32_t *out, int32_t *cand)
 {
     uint32_t h = oracle_fmix32(((uint32_t)s << 16) | (uint32_t)d);
     int32_t v = s, len = 0, j = 0;
-    int32_t cand[4096];
     while (v != d) {
         int32_t nc = 0;
         for (int32_t l = row_ptr[v]; l < row_ptr[v + 1]; l++)
@@ -137,9 +137,13 @@ int oracle_paths(int32_t n, int32_t E, const int32_t *row_ptr,
     int32_t *dist = malloc(sizeof(int32_t) * (size_t)n * (size_t)E);
     int32_t *queue = malloc(sizeof(int32_t) * (size_t)n);
     int32_t *tmp = malloc(sizeof(int32_t) * (size_t)(n + 1));
-    if (!dist || !queue || !tmp) { free(dist); free(queue); free(tmp); return OR_ERR_OOM; }
-    int rc = OR_OK;
     int32_t m = row_ptr[n];
+    int32_t maxdeg = 1;
+    for (int32_t u = 0; u < n; u++)
+        if (row_ptr[u + 1] - row_ptr[u] > maxdeg) maxdeg = row_ptr[u + 1] - row_ptr[u];
+    int32_t *cand = malloc(sizeof(int32_t) * (size_t)maxdeg);
+    if (!dist || !queue || !tmp || !cand) { free(dist); free(queue); free(tmp); free(cand); return OR_ERR_OOM; }
+    int rc = OR_OK;
     int32_t *in_ptr = calloc((size_t)n + 1, sizeof(int32_t));
     int32_t *in_tail = malloc(sizeof(int32_t) * (size_t)(m + 1));
     int32_t *fill = calloc((size_t)n, sizeof(int32_t));
@@ -157,14 +161,14 @@ int oracle_paths(int32_t n, int32_t E, const int32_t *row_ptr,
             if (s == d) continue;
             const int32_t *dd = dist + (size_t)d * n;
             if (dd[s] < 0) continue;  /* unreachable: empty path */
-            int32_t len = trace_path(row_ptr, col_idx, dd, s, d, tmp);
+            int32_t len = trace_path(row_ptr, col_idx, dd, s, d, tmp, cand);
             if (pos + len <= path_cap) memcpy(path_link + pos, tmp, sizeof(int32_t) * (size_t)len);
             pos += len;
         }
     }
     path_ptr[(int64_t)E * E] = pos;
     if (rc == OR_OK && pos > path_cap) rc = OR_ERR_SIZE;
-    free(dist); free(queue); free(tmp);
+    free(dist); free(queue); free(tmp); free(cand);
     return rc;
 }
 
@@ -381,9 +385,24 @@ static int64_t msg_len(const work_t *w, int64_t m)
     return w->C;
 }
 
+/* Most predecessors decode() can write for one line of this workload: the
+ * longest list of a custom workload; for the collectives, the sender's
+ * arrivals of one position, which the endpoint count bounds (direct: p - 1;
+ * hierarchical: M; RHD: K + j < 2K; DBT: at most two children). */
+static int64_t pred_bound(const work_t *w)
+{
+    if (w->coll == COLL_CUSTOM) {
+        int64_t most = 1;
+        for (int64_t x = 0; x < w->T; x++)
+            if (w->pptr[x + 1] - w->pptr[x] > most) most = w->pptr[x + 1] - w->pptr[x];
+        return most;
+    }
+    return (int64_t)w->E + 2 * (int64_t)w->K + 8;
+}
+
 /* Decode transaction x into (src, dst) and its predecessor list.
- * Returns the number of predecessors written to preds (at most 64 for the
- * collectives; custom lists are bounded by the caller's array).  A
+ * Returns the number of predecessors written to preds, which must have room
+ * for pred_bound(w) entries.  A
  * predecessor p >= 0 is a line; in chunk mode a predecessor is a whole chunk,
  * written -1 - c for chunk c = the C lines [c*C, (c+1)*C). */
 static int32_t decode(const work_t *w, int64_t x, int32_t *src, int32_t *dst, int64_t *preds)
@@ -558,9 +577,11 @@ static int32_t decode(const work_t *w, int64_t x, int32_t *src, int32_t *dst, in
     }
 }
 
-/* Public decoder (tests use it to pin the expansion). */
+/* Public decoder (tests use it to pin the expansion).  preds has room for
+ * pred_cap entries; a line with more predecessors returns OR_ERR_SIZE with
+ * *npred set to the count needed. */
 int oracle_txn(int coll, uint64_t bytes, int32_t group, int32_t E, const int32_t *order, int32_t dep,
-               int64_t x, int32_t *src, int32_t *dst, int32_t *npred, int64_t *preds,
+               int64_t x, int32_t *src, int32_t *dst, int32_t *npred, int64_t *preds, int32_t pred_cap,
                int64_t *T_out)
 {
     work_t w;
@@ -568,8 +589,14 @@ int oracle_txn(int coll, uint64_t bytes, int32_t group, int32_t E, const int32_t
     if (rc) return rc;
     if (T_out) *T_out = w.T;
     if (x < 0 || x >= w.T) return OR_ERR_INVALID_ARG;
-    *npred = decode(&w, x, src, dst, preds);
-    return OR_OK;
+    int64_t *all = malloc(sizeof(int64_t) * (size_t)pred_bound(&w));
+    if (!all) return OR_ERR_OOM;
+    int32_t np = decode(&w, x, src, dst, all);
+    *npred = np;
+    if (np <= pred_cap) memcpy(preds, all, sizeof(int64_t) * (size_t)np);
+    else rc = OR_ERR_SIZE;
+    free(all);
+    return rc;
 }
 
 /* ------------------------------------------------------- memcpy programs
@@ -868,7 +895,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     int64_t *s_ptr = calloc((size_t)m + 1, sizeof(int64_t));
     uint32_t *s_list = malloc(sizeof(uint32_t) * (size_t)(T > 0 ? T : 1));
     int64_t *s_cur = calloc((size_t)m, sizeof(int64_t));
-    int64_t *preds = malloc(sizeof(int64_t) * 4096);
+    int64_t *preds = malloc(sizeof(int64_t) * (size_t)pred_bound(&w));
     int64_t line_hops = 0;
     int32_t maxp = 1;   /* most predecessors of any line (sizes the head cache) */
     for (int64_t x = 0; x < T; x++) {

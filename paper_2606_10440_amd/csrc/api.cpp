@@ -48,11 +48,15 @@ struct sim_ctx {
 
     // loaded workload
     bool loaded = false;
+    bool expanded = false;  // the host expansion of the last load succeeded (sim_txn_info)
     int64_t T = 0;
     uint64_t line_hops = 0;
     std::unordered_map<uint64_t, int32_t> flow_slot;  // (src << 32 | dst) -> slot
     std::vector<int32_t> flow_path;                   // [nflows] start in path_link
     std::vector<int32_t> path_link;
+    // the workload's id ranges in id order, for sim_txn_info
+    std::vector<uint32_t> h_start, h_moff;
+    std::vector<int32_t> h_src, h_dst, h_step;
 
     DevNet dn{};
     std::vector<void *> dev_static;  // freed on reload / destroy
@@ -164,16 +168,20 @@ bool trace_route(const sim_ctx *c, int32_t s, int32_t d, std::vector<int32_t> &o
 struct Ranges {
     std::vector<uint32_t> start, len;
     std::vector<int32_t> src, dst;
+    std::vector<int32_t> step;   // algorithm step of the range's lines (-1: none)
+    std::vector<uint32_t> moff;  // offset of the range's first line in its message
     std::vector<int64_t> pref_beg;   // [nr+1] into pref_rng/pref_delta
     std::vector<int64_t> pref_rng;   // predecessor range
     std::vector<uint32_t> pref_delta;  // line start+o waits for line pref_start+delta+o
     bool whole = false;  // per-chunk: every line waits for the whole predecessor range
     std::vector<uint8_t> cls;  // [T] message class per line (empty: all data)
-    void add(uint64_t s, uint64_t l, int32_t a, int32_t b) {
+    void add(uint64_t s, uint64_t l, int32_t a, int32_t b, int64_t st = -1, int64_t mo = 0) {
         start.push_back((uint32_t)s);
         len.push_back((uint32_t)l);
         src.push_back(a);
         dst.push_back(b);
+        step.push_back((int32_t)st);
+        moff.push_back((uint32_t)mo);
         pref_beg.push_back((int64_t)pref_rng.size());
     }
     void pred(int64_t r, uint64_t delta) {
@@ -213,7 +221,7 @@ sim_status expand_rhd(sim_ctx *c, int64_t N, const std::vector<int32_t> &rho, Ra
     for (int j = 0; j < K; j++) {
         const int64_t S = half(j);
         for (int64_t i = 0; i < p; i++) {
-            R.add(p * (N - 2 * S) + i * S, S, rho[i], rho[i ^ (p >> (j + 1))]);
+            R.add(p * (N - 2 * S) + i * S, S, rho[i], rho[i ^ (p >> (j + 1))], j);
             for (int j2 = 0; j2 < j; j2++) {
                 const int64_t from = i ^ (p >> (j2 + 1));
                 R.pred(rs_range(j2, from), R.whole ? 0 : send_start(i, j) - send_start(from, j2));
@@ -225,7 +233,8 @@ sim_status expand_rhd(sim_ctx *c, int64_t N, const std::vector<int32_t> &rho, Ra
         for (int64_t i = 0; i < p; i++) {
             const int64_t b0 = (i >> j) << j;
             for (int64_t ch = b0; ch < b0 + (int64_t(1) << j); ch++) {
-                R.add(TRS + N * ((int64_t(1) << j) - 1) + (i << j) * C + (ch - b0) * C, C, rho[i], rho[i ^ (int64_t(1) << j)]);
+                R.add(TRS + N * ((int64_t(1) << j) - 1) + (i << j) * C + (ch - b0) * C, C, rho[i], rho[i ^ (int64_t(1) << j)],
+                      K + j, (ch - b0) * C);
                 if (R.whole) {
                     for (int j2 = 0; j2 < K; j2++) R.pred(rs_range(j2, i ^ (p >> (j2 + 1))), 0);
                     for (int h = 0; h < j; h++) R.pred(ag_last(h, i ^ (int64_t(1) << h)), 0);
@@ -266,7 +275,7 @@ void expand_dbt(int64_t p, int64_t H, const std::vector<int32_t> &rho, Ranges &R
                 const int64_t cpart = t == 0 ? e + 1 : e;
                 const int64_t cpos = part(cpart, t);
                 const int64_t vpos = parent(cpos), vpart = part(vpos, t);
-                R.add(msg(ph, t, e) * H, H, rho[ph == 0 ? cpart : vpart], rho[ph == 0 ? vpart : cpart]);
+                R.add(msg(ph, t, e) * H, H, rho[ph == 0 ? cpart : vpart], rho[ph == 0 ? vpart : cpart], ph * 2 + t);
                 if (ph == 0 || vpos == 0) {
                     // reduce: the children of c; broadcast from the root: the root's children
                     for (int64_t u : kids[ph == 0 ? cpos : 0]) R.pred(msg(0, t, edge(part(u, t), t)), 0);
@@ -305,7 +314,7 @@ sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t g
         const int64_t C = N / p;
         for (int64_t s = 0; s < 2 * p - 2; s++)
             for (int64_t i = 0; i < p; i++) {
-                R.add((s * p + i) * C, C, rho[i], rho[(i + 1) % p]);
+                R.add((s * p + i) * C, C, rho[i], rho[(i + 1) % p], s);
                 if (s > 0) R.pred((s - 1) * p + wrap(i - 1, p), 0);
             }
     } else if (coll == SIM_COLL_DIRECT_ALLREDUCE) {
@@ -316,7 +325,7 @@ sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t g
             for (int64_t k = 1; k < p; k++)
                 for (int64_t i = 0; i < p; i++) {
                     int64_t idx = (ph * (p - 1) + (k - 1)) * p + i;
-                    R.add(idx * C, C, rho[i], rho[(i + k) % p]);
+                    R.add(idx * C, C, rho[i], rho[(i + k) % p], ph * (p - 1) + k - 1);
                     if (ph == 1)
                         for (int64_t i2 = 0; i2 < p; i2++)
                             if (i2 != i) R.pred(((wrap(i - i2, p) - 1) * p + i2), 0);
@@ -337,13 +346,13 @@ sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t g
             for (int64_t d = 0; d < G; d++)
                 for (int64_t r = 0; r < M; r++)
                     R.add((((k - 1) * G + d) * M + r) * C1, C1, (int32_t)(d * M + r),
-                          (int32_t)(d * M + (r + k) % M));
+                          (int32_t)(d * M + (r + k) % M), k - 1);
         // phase 2: ring over the domains on each rail r
         for (int64_t s = 0; s < 2 * G - 2; s++)
             for (int64_t r = 0; r < M; r++)
                 for (int64_t d = 0; d < G; d++) {
                     R.add(B2 + ((s * M + r) * G + d) * C2, C2, (int32_t)(d * M + r),
-                          (int32_t)(((d + 1) % G) * M + r));
+                          (int32_t)(((d + 1) % G) * M + r), (M - 1) + s);
                     // Up to the first all-gather step the sent sub-chunk (d - s) mod G
                     // includes this node's own copy, reduced inside the domain first.
                     if (s <= G - 1)
@@ -357,7 +366,7 @@ sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t g
                 for (int64_t r = 0; r < M; r++)
                     for (int64_t sub = 0; sub < G; sub++) {
                         R.add(B3 + (((k - 1) * G + d) * M + r) * C1 + sub * C2, C2, (int32_t)(d * M + r),
-                              (int32_t)(d * M + (r + k) % M));
+                              (int32_t)(d * M + (r + k) % M), (M - 1) + (2 * G - 2) + (k - 1), sub * C2);
                         const bool owned = sub == (d + 1) % G;  // fully reduced here by the ring
                         int64_t s = owned ? G - 2 : G - 1 + wrap(d - sub, G);
                         if (owned)
@@ -368,14 +377,14 @@ sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t g
     } else if (coll == SIM_COLL_ALLTOALL) {
         const int64_t C = N;
         for (int64_t k = 1; k < E; k++)
-            for (int64_t i = 0; i < E; i++) R.add(((k - 1) * E + i) * C, C, (int32_t)i, (int32_t)((i + k) % E));
+            for (int64_t i = 0; i < E; i++) R.add(((k - 1) * E + i) * C, C, (int32_t)i, (int32_t)((i + k) % E), k - 1);
     } else if (coll == SIM_COLL_RING_ALLGATHER || coll == SIM_COLL_RING_REDUCESCATTER) {
         const int64_t p = E;
         if (N % p) return fail(c, SIM_ERR_SIZE, "ring: lines not divisible by participants");
         const int64_t C = N / p;
         for (int64_t s = 0; s < p - 1; s++)
             for (int64_t i = 0; i < p; i++) {
-                R.add((s * p + i) * C, C, rho[i], rho[(i + 1) % p]);
+                R.add((s * p + i) * C, C, rho[i], rho[(i + 1) % p], s);
                 if (s > 0) R.pred((s - 1) * p + wrap(i - 1, p), 0);
             }
     } else if (coll == SIM_COLL_DIRECT_ALLGATHER || coll == SIM_COLL_DIRECT_REDUCESCATTER) {
@@ -383,7 +392,7 @@ sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t g
         if (N % p) return fail(c, SIM_ERR_SIZE, "direct: lines not divisible by participants");
         const int64_t C = N / p;
         for (int64_t k = 1; k < p; k++)
-            for (int64_t i = 0; i < p; i++) R.add(((k - 1) * p + i) * C, C, rho[i], rho[(i + k) % p]);
+            for (int64_t i = 0; i < p; i++) R.add(((k - 1) * p + i) * C, C, rho[i], rho[(i + k) % p], k - 1);
     } else if (coll == SIM_COLL_RHD_ALLREDUCE) {
         const sim_status st = expand_rhd(c, N, rho, R);
         if (st != SIM_OK) return st;
@@ -403,6 +412,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     free_list(c->dev_static);
     free_list(c->dev_state);
     c->loaded = false;
+    c->expanded = false;
     const int64_t nr = (int64_t)R.start.size();
     int64_t T = 0;
     for (int64_t i = 0; i < nr; i++) {
@@ -411,6 +421,11 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     }
     if (T >= (int64_t)0xFFFFFFFFll) return fail(c, SIM_ERR_SIZE, "more than 2^32-2 transactions");
     c->T = T;
+    c->h_start = R.start;
+    c->h_src = R.src;
+    c->h_dst = R.dst;
+    c->h_step = R.step;
+    c->h_moff = R.moff;
 
     // flow slots and paths
     c->flow_slot.clear();
@@ -895,8 +910,12 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     for (int32_t l : fsrc) b1_ring = std::max(b1_ring, fifo_mask[l] + 1);
     const bool b1_deliv_lds = any_preds && align16(b1_words) + (int64_t)nflows * 4 + 64 <= kLds;
     const int64_t b1_bytes = align16(align16(b1_words) + (b1_deliv_lds ? (int64_t)nflows * 4 : 0)) + 64;
-    const bool b1_ok = bmax == 1 && (int64_t)s_link.size() <= 1024 && nl <= 8 * 1024 && nl < 65536 && b1_bytes <= kLds &&
-                       (c->arb == SIM_ARB_LOWEST_ID || rr_ports_fit);
+    // the compact engine keeps delivered counters in LDS only (its phases wait
+    // on LDS, never on global memory), and round-robin keeps the in-link lane
+    // table and each lane's offset in it as 16-bit values
+    const bool b1_ok = bmax == 1 && (int64_t)s_link.size() <= 1024 && nl <= 8 * 1024 && b1_bytes <= kLds &&
+                       (!any_preds || b1_deliv_lds) &&
+                       (c->arb == SIM_ARB_LOWEST_ID || (rr_ports_fit && m < 65536));
     // credit delays above 1 are simulated by the wave engine (not together
     // with per-chunk dependencies) and the workgroup engine; class-fair
     // arbitration by the workgroup engine
@@ -976,6 +995,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     const int64_t lds_bytes = engine == simgpu::kEngineB1 ? b1_bytes : engine == simgpu::kEngineWave ? wv.bytes : lay.bytes;
 
     // everything below touches the device
+    c->expanded = true;
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess) return fail(c, SIM_ERR_DEVICE, "no HIP device");
     if (c->device >= 0 && dev != c->device)
@@ -1154,8 +1174,6 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         d.fifo_total = nl << d.b1_ring_lg;
         if ((st = alloc(c, ost, S * (size_t)d.fifo_total, &d.gfifo))) return st;
     }
-    if (engine == simgpu::kEngineB1 && any_preds && !b1_deliv_lds)
-        if ((st = alloc(c, ost, S * (size_t)nflows, &d.gdeliv))) return st;
     if (engine == simgpu::kEngineWorkgroup &&
         ((st = alloc(c, ost, S * ftot, &d.fifo_x)) || (st = alloc(c, ost, S * ftot, &d.fifo_rdy)) ||
         (st = alloc(c, ost, S * ftot, &d.fifo_pp)) || (st = alloc(c, ost, S * m, &d.qhead)) ||
@@ -1320,7 +1338,7 @@ sim_status load_memcpy_impl(sim_ctx *c, int64_t n_ops, const int32_t *cu, const 
             const Req &r = pr[k];
             const int64_t x = id[q][k];
             if (x != next) return fail(c, SIM_ERR_INVALID_ARG, "internal: memcpy ids not dense");
-            R.add((uint64_t)x, 1, cus[q].first, r.chan);
+            R.add((uint64_t)x, 1, cus[q].first, r.chan, (int64_t)k, 0);
             if (k >= (size_t)window) {
                 const size_t kd = k - (size_t)window;  // retired before this request is issued
                 R.pred(id[q][kd] + (pr[kd].store ? 0 : 1), 0);
@@ -1330,7 +1348,7 @@ sim_status load_memcpy_impl(sim_ctx *c, int64_t n_ops, const int32_t *cu, const 
             next = x + 1;
             R.cls.push_back(r.store ? 0 : 1);  // a load request is a control message
             if (!r.store) {  // the data line
-                R.add((uint64_t)x + 1, 1, r.chan, cus[q].first);
+                R.add((uint64_t)x + 1, 1, r.chan, cus[q].first, (int64_t)k, 1);
                 R.pred(x, 0);
                 R.cls.push_back(0);
                 next = x + 2;
@@ -1389,6 +1407,19 @@ sim_status status_after_sync_impl(sim_ctx *c, int32_t *status, uint64_t *cycles)
     return SIM_OK;
 }
 
+sim_status txn_info_impl(const sim_ctx *c, int64_t id, int32_t *src, int32_t *dst, int32_t *step, int32_t *line) {
+    if (!c) return SIM_ERR_INVALID_ARG;
+    if (!c->expanded) return SIM_ERR_STATE;
+    if (id < 0 || id >= c->T) return SIM_ERR_INVALID_ARG;
+    // the range holding id: the last one whose first id is <= id
+    const size_t r = (size_t)(std::upper_bound(c->h_start.begin(), c->h_start.end(), (uint32_t)id) - c->h_start.begin()) - 1;
+    if (src) *src = c->h_src[r];
+    if (dst) *dst = c->h_dst[r];
+    if (step) *step = c->h_step[r];
+    if (line) *line = c->h_step[r] < 0 ? 0 : (int32_t)(c->h_moff[r] + ((uint32_t)id - c->h_start[r]));
+    return SIM_OK;
+}
+
 sim_status route_impl(const sim_ctx *c, int32_t src, int32_t dst, int32_t *links, int32_t cap, int32_t *len) {
     if (!c || !len || src < 0 || dst < 0 || src >= c->E || dst >= c->E) return SIM_ERR_INVALID_ARG;
     std::vector<int32_t> hops;
@@ -1419,6 +1450,7 @@ sim_status set_credit_impl(sim_ctx *c, const int32_t *credit) {
     free_list(c->dev_static);
     free_list(c->dev_state);
     c->loaded = false;
+    c->expanded = false;
     c->ran = false;
     return SIM_OK;
 }
@@ -1480,6 +1512,10 @@ sim_status sim_status_after_sync(sim_ctx *c, int32_t *status, uint64_t *cycles) 
 
 sim_status sim_route(const sim_ctx *c, int32_t src, int32_t dst, int32_t *links, int32_t cap, int32_t *len) {
     return guarded(const_cast<sim_ctx *>(c), [&] { return route_impl(c, src, dst, links, cap, len); });
+}
+
+sim_status sim_txn_info(const sim_ctx *c, int64_t id, int32_t *src, int32_t *dst, int32_t *phase_step, int32_t *line) {
+    return guarded(const_cast<sim_ctx *>(c), [&] { return txn_info_impl(c, id, src, dst, phase_step, line); });
 }
 
 sim_status sim_sizes(const sim_ctx *c, int64_t *n_txn, int32_t *n_links, int32_t *n_scenarios, uint64_t *line_hops) {

@@ -43,8 +43,9 @@ __global__ void __launch_bounds__(1024) engine_b1(DevNet d) {
     const int nl = d.nl;
     const int m = d.m;
     uint4 *fifo = d.gfifo + (size_t)s * d.fifo_total;
-    uint32_t *deliv = d.b1_deliv_lds ? reinterpret_cast<uint32_t *>(smem + d.o_b1deliv)
-                                     : (d.gdeliv ? d.gdeliv + (size_t)s * d.nflows : nullptr);
+    // delivered counters: in LDS whenever lines have predecessors (the host
+    // declines this engine otherwise)
+    uint32_t *deliv = reinterpret_cast<uint32_t *>(smem + d.o_b1deliv);
     const int32_t *path = d.path_lane;
     constexpr unsigned long long kNone = ARB == 0 ? ~0ull : 0ull;
     constexpr unsigned long long kWon = ~0ull;

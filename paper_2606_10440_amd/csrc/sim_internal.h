@@ -125,12 +125,11 @@ struct DevNet {
     int32_t has_preds;        // some line has predecessors
     int32_t b1_ns;            // stream lanes (lanes 0..b1_ns-1 start a stream)
     int32_t b1_lpt;           // lanes per thread
-    int32_t b1_deliv_lds;     // delivered counters in LDS (else gdeliv)
+    int32_t b1_deliv_lds;     // delivered counters in LDS (required when lines have predecessors)
     int32_t o_word, o_gnt, o_inl, o_b1deliv, o_b1cnt, o_b1ino, o_b1red;  // LDS byte offsets
     int32_t b1_ring_lg;       // log2 of the (uniform) ring size
     const int32_t *in_lane;   // [m] lanes of each node's in-links in port order (-1: no traffic)
     const int32_t *ln_inoff;  // [nl] offset of the lane's tail node in in_lane
-    uint32_t *gdeliv;         // [S*nflows] delivered counters in HBM
 
     // wave engine: G scenarios per wavefront, lane = (scenario slot, traffic link)
     int32_t wv_G;             // scenarios per wave (G * nl <= 64)

@@ -2,7 +2,7 @@
 
 Functions keep the C ABI's names (``sim_create``, ``sim_set_credit``, ``sim_load_collective``,
 ``sim_load_transactions``, ``sim_load_memcpy``, ``sim_sizes``, ``sim_run``,
-``sim_status_after_sync``, ``sim_route``, ``sim_last_error``,
+``sim_status_after_sync``, ``sim_route``, ``sim_txn_info``, ``sim_last_error``,
 ``sim_destroy``); ``Simulator`` bundles them with torch device buffers and
 the current HIP stream.  Every step of the simulation runs in the library's
 HIP kernels; there is no host fallback: if the library is missing, loading
@@ -26,7 +26,7 @@ STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "TOPOLOGY", 3: "UNREACHABLE", 4: "
                 6: "DEVICE", 7: "DEADLOCK", 8: "MAX_CYCLES", 9: "STATE"}
 EXPORTS = ("sim_create", "sim_set_credit", "sim_load_collective", "sim_load_transactions", "sim_load_memcpy",
            "sim_sizes", "sim_run",
-           "sim_status_after_sync", "sim_route", "sim_last_error", "sim_destroy")
+           "sim_status_after_sync", "sim_route", "sim_txn_info", "sim_last_error", "sim_destroy")
 
 _lib = None
 
@@ -54,6 +54,7 @@ def lib():
         L.sim_run.argtypes = [P, P, P, P, P, P, u64]
         L.sim_status_after_sync.argtypes = [P, P, P]
         L.sim_route.argtypes = [P, i32, i32, P, i32, P]
+        L.sim_txn_info.argtypes = [P, i64, P, P, P, P]
         L.sim_last_error.argtypes = [P]
         L.sim_last_error.restype = C.c_char_p
         L.sim_destroy.argtypes = [P]
@@ -160,6 +161,13 @@ def sim_route(ctx, src, dst, cap=256):
     return out[:n.value].copy()
 
 
+def sim_txn_info(ctx, x):
+    """(src, dst, phase_step, line) of line id x of the loaded workload."""
+    v = [C.c_int32() for _ in range(4)]
+    _check(ctx, lib().sim_txn_info(ctx, x, *(C.byref(a) for a in v)))
+    return tuple(a.value for a in v)
+
+
 def sim_last_error(ctx) -> str:
     return lib().sim_last_error(ctx).decode()
 
@@ -220,6 +228,9 @@ class Simulator:
 
     def route(self, src, dst):
         return sim_route(self.ctx, src, dst)
+
+    def txn_info(self, x):
+        return sim_txn_info(self.ctx, x)
 
     def alloc_outputs(self, device="cuda"):
         import torch

@@ -13,7 +13,8 @@
 typedef struct { uint64_t processed_cycles, line_hops; double seconds; } oracle_stats;
 
 int oracle_txn(int coll, uint64_t bytes, int32_t group, int32_t E, const int32_t *order, int32_t dep,
-               int64_t x, int32_t *src, int32_t *dst, int32_t *npred, int64_t *preds, int64_t *T_out);
+               int64_t x, int32_t *src, int32_t *dst, int32_t *npred, int64_t *preds, int32_t pred_cap,
+               int64_t *T_out);
 int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t *col_idx,
                     const int32_t *bw, const int32_t *lat, const int32_t *cap, const int32_t *credit, int32_t arb,
                     int32_t coll, uint64_t bytes, int32_t group, const int32_t *order, int32_t dep,
@@ -45,7 +46,7 @@ static int run(int coll, int group, int dep, int arb, const int32_t *cr, uint64_
     int64_t T = 0;
     int32_t s, d, np;
     int64_t preds[64];
-    int rc = oracle_txn(coll, bytes, group, P, NULL, dep, 0, &s, &d, &np, preds, &T);
+    int rc = oracle_txn(coll, bytes, group, P, NULL, dep, 0, &s, &d, &np, preds, 64, &T);
     if (rc) return rc;
     uint32_t *comp = malloc(sizeof(uint32_t) * (size_t)T), mk;
     uint64_t tx[M_LINKS], busy[M_LINKS];
@@ -98,6 +99,41 @@ int main(void)
     expect(oracle_simulate(P, P, row_ptr, col_idx, bw, lat, cap, NULL, 0, -1, 0, 0, NULL, 0, 2, cs, cd, NULL, cp, ci,
                            0, 1, comp, tx, busy, &mk, &st), 7, "cyclic", 0, 0);
     free(src); free(dst); free(pptr); free(pidx); free(cls); free(comp);
+
+    /* a custom DAG whose last line waits for all 5000 lines before it */
+    {
+        enum { N = 5001 };
+        int32_t *s5 = malloc(sizeof(int32_t) * N), *d5 = malloc(sizeof(int32_t) * N);
+        int64_t *p5 = malloc(sizeof(int64_t) * (N + 1)), *i5 = malloc(sizeof(int64_t) * (N - 1));
+        uint32_t *c5 = malloc(sizeof(uint32_t) * N);
+        for (int x = 0; x < N; x++) { s5[x] = x % P; d5[x] = (x + 1 + x / P % (P - 1)) % P; p5[x] = 0; }
+        for (int x = 0; x < N - 1; x++) i5[x] = x;
+        p5[N] = N - 1;
+        for (int arb = 0; arb <= 1; arb++)
+            expect(oracle_simulate(P, P, row_ptr, col_idx, bw, lat, cap, NULL, arb, -1, 0, 0, NULL, 0, N, s5, d5, NULL,
+                                   p5, i5, 0, 1, c5, tx, busy, &mk, &st), 0, "fan-in 5000", arb, 0);
+        free(s5); free(d5); free(p5); free(i5); free(c5);
+    }
+    /* a node with 5000 parallel out-links to one neighbour (route choice
+     * among 5000 candidates) */
+    {
+        enum { K = 5000 };
+        int32_t rp[3] = {0, K, K + 1}, *ci5 = malloc(sizeof(int32_t) * (K + 1));
+        int32_t *b5 = malloc(sizeof(int32_t) * (K + 1)), *l5 = malloc(sizeof(int32_t) * (K + 1)),
+                *k5 = malloc(sizeof(int32_t) * (K + 1));
+        for (int l2 = 0; l2 <= K; l2++) { ci5[l2] = l2 < K ? 1 : 0; b5[l2] = 1; l5[l2] = 3; k5[l2] = 8; }
+        uint64_t *tx5 = malloc(sizeof(uint64_t) * (K + 1)), *bu5 = malloc(sizeof(uint64_t) * (K + 1));
+        uint32_t c5[2 * 64];
+        expect(oracle_simulate(2, 2, rp, ci5, b5, l5, k5, NULL, 1, 3, 128 * 64, 0, NULL, 0, 0, NULL, NULL, NULL,
+                               NULL, NULL, 0, 1, c5, tx5, bu5, &mk, &st), 0, "out-degree 5000", 0, 0);
+        int32_t s, d, np;
+        int64_t one[1], T5;
+        /* direct all-reduce over 4100 endpoints: an all-gather line has 4099 predecessors */
+        expect(oracle_txn(1, 128 * 4100, 0, 4100, NULL, 0, (int64_t)4099 * 4100, &s, &d, &np, one, 1, &T5), 4,
+               "txn needs more room", np, 0);
+        if (np != 4099) { fprintf(stderr, "txn predecessor count %d\n", np); failures++; }
+        free(ci5); free(b5); free(l5); free(k5); free(tx5); free(bu5);
+    }
     if (failures) return 1;
     printf("oracle sanitizer driver: ok\n");
     return 0;

@@ -214,3 +214,139 @@ def test_fair_arbitration_flag_accepted(simlib):
     with pytest.raises(simlib.SimError) as e:
         simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, 4)
     assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+
+
+# ------------------------------------------------------------- sim_txn_info
+# The library's decoder is checked line by line: src and dst against the
+# oracle's own decoder, the step and in-message offset against the step-major
+# id formulas of include/simgpu.h, re-derived here.
+
+def _load_host(simlib, ctx, *args, **kw):
+    """Load a workload; without a GPU the device binding fails after the host
+    expansion, which is all sim_txn_info needs."""
+    try:
+        simlib.sim_load_collective(ctx, *args, **kw)
+    except simlib.SimError as e:
+        assert e.status in (simlib.SIM_ERR_DEVICE, simlib.SIM_ERR_OOM), e
+
+
+def _step_line(coll, x, p, N, M=0):
+    """(step, offset in message) of line x from the documented id layouts."""
+    if coll in (si.COLL_RING_ALLREDUCE, si.COLL_RING_ALLGATHER, si.COLL_RING_REDUCESCATTER):
+        C = N // p
+        return x // C // p, x % C
+    if coll == si.COLL_DIRECT_ALLREDUCE or coll in (si.COLL_DIRECT_ALLGATHER, si.COLL_DIRECT_REDUCESCATTER):
+        C = N // p
+        return x // C // p, x % C
+    if coll == si.COLL_ALLTOALL:
+        return x // N // p, x % N
+    if coll == si.COLL_HIER_ALLREDUCE:
+        G = p // M
+        C1, C2 = N // M, N // M // G
+        B2 = (M - 1) * G * M * C1
+        B3 = B2 + (2 * G - 2) * M * G * C2
+        if x < B2:
+            return x // (C1 * M * G), x % C1
+        if x < B3:
+            y = x - B2
+            return (M - 1) + y // (C2 * G * M), y % C2
+        y = x - B3
+        return (M - 1) + (2 * G - 2) + y // (C1 * M * G), y % C1
+    if coll == si.COLL_RHD_ALLREDUCE:
+        K = p.bit_length() - 1
+        C = N // p
+        for j in range(K):
+            S = N >> (j + 1)
+            if p * (N - 2 * S) <= x < p * (N - S):
+                return j, (x - p * (N - 2 * S)) % S
+        for j in range(K):
+            base, A = N * (p - 1) + N * ((1 << j) - 1), C << j
+            if base <= x < base + p * A:
+                return K + j, (x - base) % A
+        raise AssertionError(x)
+    if coll == si.COLL_DBT_ALLREDUCE:
+        H = N // 2
+        return x // H // (p - 1), x % H
+    raise AssertionError(coll)
+
+
+CASES = [(si.COLL_RING_ALLREDUCE, 4, 0), (si.COLL_DIRECT_ALLREDUCE, 4, 0), (si.COLL_ALLTOALL, 1, 0),
+         (si.COLL_RING_ALLGATHER, 4, 0), (si.COLL_RING_REDUCESCATTER, 4, 0), (si.COLL_DIRECT_ALLGATHER, 4, 0),
+         (si.COLL_DIRECT_REDUCESCATTER, 4, 0), (si.COLL_RHD_ALLREDUCE, 8, 0), (si.COLL_DBT_ALLREDUCE, 6, 0),
+         (si.COLL_HIER_ALLREDUCE, 4, 4)]
+
+
+@pytest.mark.parametrize("coll,lines_per_p,M", CASES)
+def test_txn_info_matches_oracle(simlib, oracle_lib, coll, lines_per_p, M):
+    p = 8
+    w = si.full_mesh(p)
+    N = lines_per_p * (p if coll != si.COLL_ALLTOALL else 1) * (2 if M else 1)
+    order = None if coll in (si.COLL_HIER_ALLREDUCE, si.COLL_ALLTOALL) else \
+        np.random.default_rng(coll).permutation(p).astype(np.int32)
+    ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, w.arb)
+    try:
+        _load_host(simlib, ctx, coll, 128 * N, M, order)
+        rc, _, _, _, T = oracle_lib.txn(coll, 128 * N, M, p, 0, order)
+        assert rc == 0
+        for x in range(T):
+            rc, s, d, _, _ = oracle_lib.txn(coll, 128 * N, M, p, x, order)
+            got = simlib.sim_txn_info(ctx, x)
+            assert got[:2] == (s, d), (x, got, s, d)
+            assert got[2:] == _step_line(coll, x, p, N, M), (x, got)
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_txn_info(ctx, T)
+        assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+    finally:
+        simlib.sim_destroy(ctx)
+
+
+def test_txn_info_custom_memcpy_and_state(simlib, oracle_lib):
+    from sim_inputs import noc
+    w = si.full_mesh(4)
+    ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, w.arb)
+    try:
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_txn_info(ctx, 0)
+        assert e.value.status == simlib.SIM_ERR_STATE
+        try:
+            simlib.sim_load_transactions(ctx, [0, 2, 3], [1, 0, 1], [0, 0, 1, 1], [0])
+        except simlib.SimError as e:
+            assert e.status == simlib.SIM_ERR_DEVICE
+        assert [simlib.sim_txn_info(ctx, x) for x in range(3)] == [(0, 1, -1, 0), (2, 0, -1, 0), (3, 1, -1, 0)]
+    finally:
+        simlib.sim_destroy(ctx)
+    # memcpy programs: ids step-major over issue index and ascending CUs; a
+    # load takes a request id then a data id, a store one id
+    wn, lay = noc.gpu_noc(1, mesh=(2, 2), cus_per_router=1, ch_per_router=2, ports_per_router=1)
+    cus = [int(c) for c in lay.cus[0][:2]]
+    ch = lay.channels.reshape(-1)
+    mc = dict(cu=[cus[1], cus[0], cus[1]], src_space=[0, 0, 1], dst_space=[1, 1, 0], src_line=[0, 3, 5],
+              dst_line=[2, 0, 1], n_lines=[3, 5, 2], space_channels=np.concatenate([ch, ch[::-1]]), n_ch=len(ch),
+              unroll=2, window=3)
+    ctx = simlib.sim_create(wn.n_nodes, wn.n_endpoints, wn.row_ptr, wn.col_idx, 1, wn.bw, wn.lat, wn.cap, wn.arb)
+    try:
+        try:
+            simlib.sim_load_memcpy(ctx, **mc)
+        except simlib.SimError as e:
+            assert e.status == simlib.SIM_ERR_DEVICE
+        prog = {}
+        for o, c in enumerate(mc["cu"]):
+            ins = prog.setdefault(c, [])
+            for j0 in range(0, mc["n_lines"][o], mc["unroll"]):
+                gn = min(mc["unroll"], mc["n_lines"][o] - j0)
+                ins += ["load"] * gn + ["store"] * gn
+        want = []
+        for k in range(max(len(v) for v in prog.values())):
+            for c in sorted(prog):
+                if k < len(prog[c]):
+                    want.append((c, k, 0))
+                    if prog[c][k] == "load":
+                        want.append((c, k, 1))
+        src, dst, _, _ = oracle_lib.memcpy_txns(noc.Memcpy(**mc))
+        assert len(want) == len(src)
+        for x, (c, k, ln) in enumerate(want):
+            got = simlib.sim_txn_info(ctx, x)
+            assert got == (int(src[x]), int(dst[x]), k, ln), (x, got)
+            assert (got[1] if ln else got[0]) == c
+    finally:
+        simlib.sim_destroy(ctx)

@@ -130,6 +130,10 @@ def check_vs_oracle(simmod, oracle_lib, w, scenarios=None, expect_ok=True):
                 compare_scenario(r, s, want, len(want.completion))
                 n_ok += 1
         except AssertionError as e:
+            want_code = {"OK": 0, "DEADLOCK": 7}.get(want.status_name, -100)
+            if int(r.scenario_status[s]) != want_code:  # no GPU re-runs for an engine error
+                raise AssertionError(f"{e}\nscenario {s}: GPU status {int(r.scenario_status[s])}, "
+                                     f"oracle {want.status_name}") from None
             raise AssertionError(f"{e}\n{first_divergence(simmod, oracle_lib, w, s)}") from None
     return r, n_ok
 
@@ -384,6 +388,13 @@ def check_engine(simmod, oracle_lib, w, engine, txns=None):
                 compare_scenario(r, s, want, len(want.completion))
                 n_ok += 1
         except AssertionError as e:
+            # Bisect only when both sides ended the same way and only values
+            # differ; an engine watchdog or internal error is reported as is
+            # (its cause is found on the CPU, not by re-running the GPU case).
+            want_code = {"OK": 0, "DEADLOCK": 7}.get(want.status_name, -100)
+            if int(r.scenario_status[s]) != want_code:
+                raise AssertionError(f"{e}\nscenario {s}: GPU status {int(r.scenario_status[s])}, "
+                                     f"oracle {want.status_name}") from None
             old = os.environ.get("SIMGPU_ENGINE")
             if engine:
                 os.environ["SIMGPU_ENGINE"] = engine
