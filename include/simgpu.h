@@ -268,6 +268,28 @@ sim_status sim_sizes(const sim_ctx *ctx, int64_t *n_txn, int32_t *n_links, int32
 sim_status sim_run(sim_ctx *ctx, void *hip_stream, uint32_t *d_completion, uint64_t *d_tx_lines,
                    uint64_t *d_busy_cycles, uint32_t *d_makespan, uint64_t max_cycles);
 
+/*
+ * sim_run without any device allocation, for callers that cannot allocate:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, outputs and errors as sim_run; the engines'
+ * per-run scratch (per-scenario statuses and cycle counts, and the FIFO
+ * rings, per-link scalars and request records of the engines that keep
+ * them in device memory) comes from a fixed array of
+ * SIM_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends, instead of from the context.  SIM_ERR_SIZE (and
+ * nothing enqueued) if the loaded workload needs more scratch than that.
+ * The call allocates nothing; the first call on a device looks the array's
+ * address up.  Every call on a GPU uses the same array and leaves its
+ * contents behind (each run initialises what it reads): runs that overlap
+ * on one GPU -- on different streams, or from different contexts before the
+ * earlier run has finished -- race on it, and a later run overwrites the
+ * statuses sim_status_after_sync reports for an earlier one, so synchronise
+ * and read the status before the next call.
+ */
+#define SIM_NOALLOC_SCRATCH_BYTES (8u << 20)
+sim_status sim_run_noalloc(sim_ctx *ctx, void *hip_stream, uint32_t *d_completion, uint64_t *d_tx_lines,
+                           uint64_t *d_busy_cycles, uint32_t *d_makespan, uint64_t max_cycles);
+
 /* After the caller has synchronised the run's stream: SIM_OK, or the first
  * device-detected error (DEADLOCK / MAX_CYCLES) over the scenarios.  (Error
  * reporting of this library; the paper has no counterpart.)  If

@@ -12,6 +12,7 @@
 #include <cstdlib>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <map>
 #include <new>
 #include <string>
@@ -24,6 +25,24 @@
 using simgpu::DevNet;
 
 namespace {
+
+// Per-run device scratch of the engines (statuses, processed-cycle counts,
+// and the FIFO rings, per-link scalars and request records of the engines
+// that keep them in device memory) as one block: each array at an offset,
+// bound to a base address per run.
+struct StateLayout {
+    size_t bytes = 0;
+    std::vector<std::function<void(DevNet &, unsigned char *)>> bind;
+    template <class T>
+    void add(T *DevNet::*field, size_t count) {
+        const size_t off = bytes;
+        bytes += (std::max<size_t>(count * sizeof(T), 16) + 255) & ~(size_t)255;
+        bind.push_back([field, off](DevNet &d, unsigned char *base) { d.*field = reinterpret_cast<T *>(base + off); });
+    }
+    void apply(DevNet &d, unsigned char *base) const {
+        for (const auto &f : bind) f(d, base);
+    }
+};
 
 // MurmurHash3's 32-bit finalizer (Appleby): spreads (src, dst) over the
 // candidate next hops.
@@ -61,6 +80,10 @@ struct sim_ctx {
     DevNet dn{};
     std::vector<void *> dev_static;  // freed on reload / destroy
     std::vector<void *> dev_state;
+    StateLayout state;               // the engines' scratch, bound to dev_state's block in dn
+    // where the last run's statuses and cycle counts are (its scratch block)
+    int32_t *run_status = nullptr;
+    uint64_t *run_cycles = nullptr;
     std::string err = "";
     bool ran = false;
 };
@@ -1166,27 +1189,41 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
 #undef UP
     const size_t S = (size_t)c->S;
     const size_t nsrc = (size_t)m + (size_t)d.ns;
-    auto &ost = c->dev_state;
-    if ((st = alloc(c, ost, S, &d.status)) || (st = alloc(c, ost, S, &d.cycles))) return st;
-    if (engine == simgpu::kEngineLaneHbm)
-        if ((st = alloc(c, ost, S * (size_t)lf, &d.gfifo))) return st;
+    StateLayout &sl = c->state;
+    sl = StateLayout{};
+    sl.add(&DevNet::status, S);
+    sl.add(&DevNet::cycles, S);
+    if (engine == simgpu::kEngineLaneHbm) sl.add(&DevNet::gfifo, S * (size_t)lf);
     if (engine == simgpu::kEngineB1) {  // uniform rings: lane i owns entries [i << lg, (i + 1) << lg)
         d.fifo_total = nl << d.b1_ring_lg;
-        if ((st = alloc(c, ost, S * (size_t)d.fifo_total, &d.gfifo))) return st;
+        sl.add(&DevNet::gfifo, S * (size_t)d.fifo_total);
     }
-    if (engine == simgpu::kEngineWorkgroup &&
-        ((st = alloc(c, ost, S * ftot, &d.fifo_x)) || (st = alloc(c, ost, S * ftot, &d.fifo_rdy)) ||
-        (st = alloc(c, ost, S * ftot, &d.fifo_pp)) || (st = alloc(c, ost, S * m, &d.qhead)) ||
-        (st = alloc(c, ost, S * m, &d.qcred)) || (st = alloc(c, ost, S * m, &d.cptr)) ||
-        (fair && (st = alloc(c, ost, S * rtot, &d.req_aux))) ||
-        (st = alloc(c, ost, S * m, &d.qtail)) || (st = alloc(c, ost, S * m, &d.rr)) ||
-        (st = alloc(c, ost, S * d.ns, &d.cur_rng)) || (st = alloc(c, ost, S * d.ns, &d.cur_off)) ||
-        (st = alloc(c, ost, S * nflows, &d.delivered)) || (st = alloc(c, ost, S * m, &d.req_cnt)) ||
-        (st = alloc(c, ost, S * rtot, &d.req_rec)) || (st = alloc(c, ost, S * nsrc * bmax, &d.sreq_x)) ||
-        (st = alloc(c, ost, S * nsrc * bmax, &d.sreq_pp)) || (st = alloc(c, ost, S * nsrc, &d.sreq_n)) ||
-        (st = alloc(c, ost, S * nsrc * bmax, &d.grant)) || (st = alloc(c, ost, S * m, &d.gcount)) ||
-        (st = alloc(c, ost, S * m * bmax, &d.glist)) || (st = alloc(c, ost, S * m * bmax, &d.gdep))))
-        return st;
+    if (engine == simgpu::kEngineWorkgroup) {
+        sl.add(&DevNet::fifo_x, S * ftot);
+        sl.add(&DevNet::fifo_rdy, S * ftot);
+        sl.add(&DevNet::fifo_pp, S * ftot);
+        sl.add(&DevNet::qhead, S * m);
+        sl.add(&DevNet::qcred, S * m);
+        sl.add(&DevNet::cptr, S * m);
+        if (fair) sl.add(&DevNet::req_aux, S * rtot);
+        sl.add(&DevNet::qtail, S * m);
+        sl.add(&DevNet::rr, S * m);
+        sl.add(&DevNet::cur_rng, S * d.ns);
+        sl.add(&DevNet::cur_off, S * d.ns);
+        sl.add(&DevNet::delivered, S * nflows);
+        sl.add(&DevNet::req_cnt, S * m);
+        sl.add(&DevNet::req_rec, S * rtot);
+        sl.add(&DevNet::sreq_x, S * nsrc * bmax);
+        sl.add(&DevNet::sreq_pp, S * nsrc * bmax);
+        sl.add(&DevNet::sreq_n, S * nsrc);
+        sl.add(&DevNet::grant, S * nsrc * bmax);
+        sl.add(&DevNet::gcount, S * m);
+        sl.add(&DevNet::glist, S * m * bmax);
+        sl.add(&DevNet::gdep, S * m * bmax);
+    }
+    unsigned char *block = nullptr;
+    if ((st = alloc(c, c->dev_state, sl.bytes, &block))) return st;
+    sl.apply(d, block);
     c->dn = d;
     c->loaded = true;
     c->ran = false;
@@ -1359,8 +1396,11 @@ sim_status load_memcpy_impl(sim_ctx *c, int64_t n_ops, const int32_t *cu, const 
 }
 
 
+// scratch == nullptr: the engines' scratch is the context's block; else the
+// caller's scratch_bytes at scratch (nothing is allocated either way)
 sim_status run_impl(sim_ctx *c, void *stream, uint32_t *d_completion, uint64_t *d_tx_lines,
-                   uint64_t *d_busy_cycles, uint32_t *d_makespan, uint64_t max_cycles) {
+                   uint64_t *d_busy_cycles, uint32_t *d_makespan, uint64_t max_cycles,
+                   unsigned char *scratch = nullptr, size_t scratch_bytes = 0) {
     if (!c) return SIM_ERR_INVALID_ARG;
     if (!c->loaded) return fail(c, SIM_ERR_STATE, "sim_run before a workload was loaded");
     if ((!d_completion && c->T > 0) || !d_tx_lines || !d_busy_cycles || !d_makespan)
@@ -1369,6 +1409,13 @@ sim_status run_impl(sim_ctx *c, void *stream, uint32_t *d_completion, uint64_t *
     if (hipGetDevice(&dev) != hipSuccess || dev != c->device)
         return fail(c, SIM_ERR_DEVICE, "current HIP device differs from the context's device");
     DevNet d = c->dn;
+    if (scratch) {
+        if (c->state.bytes > scratch_bytes)
+            return fail(c, SIM_ERR_SIZE, "the loaded workload needs " + std::to_string(c->state.bytes) +
+                                             " B of engine scratch, more than the " + std::to_string(scratch_bytes) +
+                                             " B of the allocation-free run");
+        c->state.apply(d, scratch);
+    }
     d.completion = d_completion;
     d.tx_lines = d_tx_lines;
     d.busy = d_busy_cycles;
@@ -1380,6 +1427,8 @@ sim_status run_impl(sim_ctx *c, void *stream, uint32_t *d_completion, uint64_t *
     d.watchdog = (c->line_hops + (uint64_t)c->T + 1) * ((uint64_t)d.fifo_total + 2) + 1000000ull;
     int e = simgpu::launch_engine(d, stream);
     if (e != 0) return fail(c, SIM_ERR_DEVICE, std::string("kernel launch failed: ") + hipGetErrorString((hipError_t)e));
+    c->run_status = d.status;
+    c->run_cycles = d.cycles;
     c->ran = true;
     return SIM_OK;
 }
@@ -1388,11 +1437,11 @@ sim_status status_after_sync_impl(sim_ctx *c, int32_t *status, uint64_t *cycles)
     if (!c) return SIM_ERR_INVALID_ARG;
     if (!c->loaded || !c->ran) return fail(c, SIM_ERR_STATE, "no run to report on");
     std::vector<int32_t> st(c->S);
-    if (hipMemcpy(st.data(), c->dn.status, sizeof(int32_t) * c->S, hipMemcpyDeviceToHost) != hipSuccess)
+    if (hipMemcpy(st.data(), c->run_status, sizeof(int32_t) * c->S, hipMemcpyDeviceToHost) != hipSuccess)
         return fail(c, SIM_ERR_DEVICE, "hipMemcpy of status failed");
     if (status) std::memcpy(status, st.data(), sizeof(int32_t) * c->S);
     if (cycles &&
-        hipMemcpy(cycles, c->dn.cycles, sizeof(uint64_t) * c->S, hipMemcpyDeviceToHost) != hipSuccess)
+        hipMemcpy(cycles, c->run_cycles, sizeof(uint64_t) * c->S, hipMemcpyDeviceToHost) != hipSuccess)
         return fail(c, SIM_ERR_DEVICE, "hipMemcpy of cycles failed");
     for (int32_t s = 0; s < c->S; s++) {
         if (st[s] == simgpu::kRunDeadlock) return fail(c, SIM_ERR_DEADLOCK, "scenario " + std::to_string(s) + " deadlocked");
@@ -1471,6 +1520,20 @@ sim_status guarded(sim_ctx *c, F &&f) {
         return SIM_ERR_DEVICE;
     }
 }
+
+namespace simgpu {
+// The allocation-free run (noalloc.hip): sim_run with the engines' scratch at
+// the caller's device address.
+sim_status run_on_scratch(sim_ctx *c, void *stream, uint32_t *d_completion, uint64_t *d_tx_lines,
+                          uint64_t *d_busy_cycles, uint32_t *d_makespan, uint64_t max_cycles, void *scratch,
+                          size_t scratch_bytes) {
+    if (!scratch) return SIM_ERR_INVALID_ARG;
+    return guarded(c, [&] {
+        return run_impl(c, stream, d_completion, d_tx_lines, d_busy_cycles, d_makespan, max_cycles,
+                        static_cast<unsigned char *>(scratch), scratch_bytes);
+    });
+}
+}  // namespace simgpu
 
 extern "C" {
 

@@ -25,7 +25,7 @@ SIM_ERR_OOM, SIM_ERR_DEVICE, SIM_ERR_DEADLOCK, SIM_ERR_MAX_CYCLES, SIM_ERR_STATE
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "TOPOLOGY", 3: "UNREACHABLE", 4: "SIZE", 5: "OOM",
                 6: "DEVICE", 7: "DEADLOCK", 8: "MAX_CYCLES", 9: "STATE"}
 EXPORTS = ("sim_create", "sim_set_credit", "sim_load_collective", "sim_load_transactions", "sim_load_memcpy",
-           "sim_sizes", "sim_run",
+           "sim_sizes", "sim_run", "sim_run_noalloc",
            "sim_status_after_sync", "sim_route", "sim_txn_info", "sim_last_error", "sim_destroy")
 
 _lib = None
@@ -52,6 +52,7 @@ def lib():
         L.sim_load_memcpy.argtypes = [P, i64, P, P, P, P, P, P, C.c_int32, C.c_int32, P, C.c_int32, C.c_int32]
         L.sim_sizes.argtypes = [P, P, P, P, P]
         L.sim_run.argtypes = [P, P, P, P, P, P, u64]
+        L.sim_run_noalloc.argtypes = [P, P, P, P, P, P, u64]
         L.sim_status_after_sync.argtypes = [P, P, P]
         L.sim_route.argtypes = [P, i32, i32, P, i32, P]
         L.sim_txn_info.argtypes = [P, i64, P, P, P, P]
@@ -145,6 +146,14 @@ def sim_run(ctx, stream_ptr, d_completion, d_tx_lines, d_busy_cycles, d_makespan
     _check(ctx, lib().sim_run(ctx, C.c_void_p(stream_ptr), C.c_void_p(d_completion),
                               C.c_void_p(d_tx_lines), C.c_void_p(d_busy_cycles),
                               C.c_void_p(d_makespan), max_cycles))
+
+
+def sim_run_noalloc(ctx, stream_ptr, d_completion, d_tx_lines, d_busy_cycles, d_makespan, max_cycles=0):
+    """sim_run with the engines' scratch in the library's fixed device array
+    (no device allocation)."""
+    _check(ctx, lib().sim_run_noalloc(ctx, C.c_void_p(stream_ptr), C.c_void_p(d_completion),
+                                      C.c_void_p(d_tx_lines), C.c_void_p(d_busy_cycles),
+                                      C.c_void_p(d_makespan), max_cycles))
 
 
 def sim_status_after_sync(ctx, n_scenarios):
