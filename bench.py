@@ -31,7 +31,13 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, 8 TB/s
 COMPLETION_BYTES = 4            # u32 completion cycle written per line
+HOP_BYTES_HBM = 20              # HBM-resident queue state: per line-hop, 8 B FIFO entry read,
+                                # 8 B written into the next FIFO, 4 B path lookup
+TXN_BYTES_HBM = 12              # and per line: stream/predecessor read, completion write, release read
 KERNEL_NAME = "engine_"         # substring of the engine kernels' symbols
+# workloads whose engines keep the queue state in device memory (L2/HBM) rather
+# than in LDS and registers: their roofline counts the HBM-resident bytes
+HBM_STATE = ("C3", "C4", "NOC2_ag")
 
 DESCR = {
     "C1": "4-endpoint full mesh, direct all-reduce 64 KiB, b=1 L=10 cap=16, lowest-id",
@@ -52,10 +58,42 @@ DESCR["NOC2_ag"] = ("1024 scenarios x 2 generic GPUs as NoCs (448 nodes each) + 
 
 
 def algorithmic_bytes(T: int, S: int, m: int) -> int:
-    """Bytes the method must move per launch: one u32 completion per line
-    plus the per-link u64 counters and per-scenario makespan; scenario state
-    and routing tables are on-chip or reused and not counted."""
+    """Bytes the method must move per launch when the scenario state stays on
+    chip (LDS and registers): one u32 completion per line plus the per-link
+    u64 counters and per-scenario makespan."""
     return S * (T * COMPLETION_BYTES + m * 16 + 4)
+
+
+def algorithmic_bytes_hbm_state(T: int, S: int, m: int, line_hops: int) -> int:
+    """Bytes per launch when the queue state lives in device memory: 20 B per
+    line-hop (FIFO entry read and written on, path lookup) and 12 B per line
+    (stream or predecessor read, completion write, release read), plus the
+    per-link counters and makespans."""
+    return S * (line_hops * HOP_BYTES_HBM + T * TXN_BYTES_HBM + m * 16 + 4)
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def load_latency_profile(workload: str):
+    """Per-simulated-cycle SQ counters of the critical wave from the committed
+    profile summary, if one exists for the current engine source."""
+    path = os.path.join(ROOT, "profiles", f"engine_{workload}_sq_per_cycle.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        c = json.load(f)
+    if c.get("engine_source_hash") != engine_source_hash(c.get("kernel", KERNEL_NAME)):
+        return None
+    return c.get("per_simulated_cycle")
 
 
 def engine_source_hash(kernel: str = "") -> str:
@@ -117,6 +155,7 @@ def cpu_baseline(w, sample_seconds: float):
         hops = int(r.tx_lines.sum())
         what = "the whole scenario" if r.status == 0 else f"its first {r.processed_cycles} processed cycles"
         return {"value": hops / r.seconds, "unit": "line-hop events/s", "cores": 1, "kind": "oracle",
+                "cpu_model": cpu_model(),
                 "sample": f"1 of 1 scenario, {what}, event loop only ({hops} line-hops in {r.seconds:.1f} s)"}
     total_hops = 0
     total_s = 0.0
@@ -129,6 +168,7 @@ def cpu_baseline(w, sample_seconds: float):
         if total_s >= sample_seconds:
             break
     return {"value": total_hops / total_s, "unit": "line-hop events/s", "cores": 1, "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": f"{n} of {w.n_scenarios} scenario(s), full size, event loop only "
                       f"({total_hops} line-hops in {total_s:.1f} s)"}
 
@@ -162,7 +202,7 @@ def cpu_baseline_all_cores(name: str, n_scenarios: int, budget: float):
     with mp.get_context("spawn").Pool(n) as pool:
         res = pool.map(_oracle_worker, [(name, i, n, budget) for i in range(n)])
     rate = sum(h / sec for h, sec, _ in res if sec > 0)
-    return {"value": rate, "unit": "line-hop events/s", "cores": n, "kind": "oracle",
+    return {"value": rate, "unit": "line-hop events/s", "cores": n, "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"{sum(k for _, _, k in res)} of {n_scenarios} scenarios, full size, "
                       f"{n} processes, about {budget:.0f} s of event loop each"}
 
@@ -182,13 +222,15 @@ def copy_calibration():
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="C5", choices=sorted(DESCR))
     ap.add_argument("--cpu-sample-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-verify", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true")
+    ap.add_argument("--only-scenario", type=int, default=None,
+                    help="run one scenario of a batched workload alone (per-cycle counters of a lone wave)")
     a = ap.parse_args()
 
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -206,6 +248,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a HIP device"
     w = si.config(a.workload)
+    if a.only_scenario is not None:
+        w = si.take_scenarios(w, [a.only_scenario])
     t0 = time.time()
     s = sim.Simulator.from_workload(w)
     T, m, S, line_hops = s.sizes()
@@ -231,27 +275,30 @@ def main():
         if rc != 0:
             raise SystemExit(f"simulation failed: {sim.STATUS_NAMES[rc]} {sim.sim_last_error(s.ctx)}")
 
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    # one event between launches on the launches' own stream: the K steps back
+    # to back, and each launch's duration (median reported)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    ev0.record(stream)
+    evs[0].record(stream)
     for i in range(a.steps):
         s.enqueue(outs, stream=stream)
+        evs[i + 1].record(stream)
         if per_step:
             stream.synchronize()
             print(f"[bench] step {i} done", file=sys.stderr, flush=True)
-    ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    gpu_ms = ev0.elapsed_time(ev1)
+    gpu_ms = evs[0].elapsed_time(evs[-1])
+    launch_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(a.steps)]
+    launch_med_ms = float(np.median(launch_ms))
     rc, st, cyc = sim.sim_status_after_sync(s.ctx, S)
     if rc != 0:
         raise SystemExit(f"simulation failed: {sim.STATUS_NAMES[rc]}")
     print(f"[bench] timed {a.steps} steps: {gpu_ms:.1f} ms (wall {wall * 1e3:.1f} ms)", file=sys.stderr, flush=True)
 
     verified = None
-    if not a.no_verify:
+    if not a.no_verify and a.only_scenario is None:
         gpath = os.path.join(ROOT, "tests", "golden", f"{a.workload}.json")
         if os.path.exists(gpath):
             with open(gpath) as f:
@@ -264,10 +311,13 @@ def main():
             verified = bool(ok)
 
     ms_per_step = gpu_ms / a.steps
-    launch_s = ms_per_step / 1e3
+    launch_s = launch_med_ms / 1e3
     total_hops = line_hops * S
     value = total_hops * a.steps / (gpu_ms / 1e3)
-    alg = algorithmic_bytes(T, S, m)
+    alg_onchip = algorithmic_bytes(T, S, m)
+    alg_hbm = algorithmic_bytes_hbm_state(T, S, m, line_hops)
+    hbm_state = a.workload in HBM_STATE
+    alg = alg_hbm if hbm_state else alg_onchip
     traffic, kernel = load_traffic(a.workload, launch_s)
     achieved = alg / launch_s / 1e9
     out = {
@@ -286,11 +336,22 @@ def main():
         "config": {"workload": f"{a.workload}: {DESCR[a.workload]}", "scenarios": S, "transactions": T * S,
                    "line_hops": total_hops, "links": m,
                    "processed_cycles_max": int(cyc.max()), "processed_cycles_sum": int(cyc.sum()),
+                   "critical_scenario": int(np.argmax(cyc)),
                    "bit_exact_vs_golden": verified},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "traffic_frac": None if traffic is None else traffic / launch_s / 1e9 / HBM_PEAK_GBS,
-                     "kernel": kernel, "algorithmic_bytes_per_launch": alg},
+                     "kernel": kernel, "launch_ms_median": launch_med_ms,
+                     "launch_ms": [round(v, 3) for v in launch_ms],
+                     "accounting": ("hbm-resident queue state: 20 B per line-hop + 12 B per line" if hbm_state
+                                    else "on-chip scenario state: 4 B per line"),
+                     "algorithmic_bytes_per_launch": alg,
+                     "frac_onchip_accounting": alg_onchip / launch_s / 1e9 / HBM_PEAK_GBS,
+                     "frac_hbm_state_accounting": alg_hbm / launch_s / 1e9 / HBM_PEAK_GBS},
+        # a batch is bound by its critical scenario's chain of dependent cycles
+        "latency": {"critical_processed_cycles": int(cyc.max()),
+                    "ns_per_processed_cycle": launch_s * 1e9 / max(int(cyc.max()), 1),
+                    "sq_per_simulated_cycle": load_latency_profile(a.workload)},
     }
     s.close()
     if not a.no_cpu_baseline:

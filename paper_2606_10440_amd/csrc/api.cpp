@@ -536,6 +536,40 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     std::vector<int32_t> fsrc;
     for (int32_t l = 0; l < m; l++)
         if (used[l]) fsrc.push_back(l);
+    // Lined-up graphs: every traffic link is fed by at most one other link
+    // and sends lines on to at most one other link, and these links form
+    // paths (no cycle).  The traffic links are then ordered path by path, so
+    // that in lane order a link's feeder is the link just before it and its
+    // next link the one just after it (the wave engine's shift loop).
+    // (The wave engine's shift loop also needs, under lowest-id arbitration
+    // with several lines per cycle, one flow at most per pair of consecutive
+    // links, and no credit delays; otherwise the links keep their order.)
+    int32_t bmax_all = 1;
+    for (int32_t v : c->bw) bmax_all = std::max(bmax_all, v);
+    bool lineup = c->credit.empty();
+    {
+        std::vector<int32_t> pre(m, -1), nxt(m, -1), npair(m, 0);
+        for (size_t q = 0; q + 1 < c->path_link.size() && lineup; q++) {
+            const int32_t a = c->path_link[q], b2 = c->path_link[q + 1];
+            if (a < 0 || b2 < 0) continue;
+            if ((pre[b2] >= 0 && pre[b2] != a) || (nxt[a] >= 0 && nxt[a] != b2)) lineup = false;
+            pre[b2] = a;
+            nxt[a] = b2;
+            if (++npair[a] > 1 && c->arb == SIM_ARB_LOWEST_ID && bmax_all > 1) lineup = false;
+        }
+        std::vector<int32_t> order;
+        std::vector<char> seen(m, 0);
+        for (int32_t l : fsrc) {
+            if (!lineup || pre[l] >= 0) continue;
+            for (int32_t v = l; v >= 0; v = nxt[v]) {
+                if (seen[v]) { lineup = false; break; }
+                seen[v] = 1;
+                order.push_back(v);
+            }
+        }
+        if (lineup && order.size() == fsrc.size()) fsrc = order;
+        else lineup = false;  // a cycle of feeders (never reached from a path start)
+    }
     std::vector<int32_t> nports(c->n, 0), port_at_head(m), nports_tail(m);
     for (int32_t l = 0; l < m; l++) port_at_head[l] = nports[c->col_idx[l]]++;
     for (int32_t v = 0; v < c->E; v++) nports[v]++;  // injection port last
@@ -580,6 +614,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     // mailbox slots of the lane engine: feeders of each target lane x bmax
     std::vector<int32_t> link_lane(m, -1);
     for (int32_t i = 0; i < nl; i++) link_lane[fsrc[i]] = i;
+    const std::vector<int32_t> fsrc_pos(link_lane);  // position of a traffic link in fsrc
     std::vector<std::vector<int32_t>> feeders(nl);
     for (size_t q = 0; q + 1 < c->path_link.size(); q++) {
         const int32_t a = c->path_link[q], b2 = c->path_link[q + 1];
@@ -599,6 +634,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     // so that the longest runs start first).
     struct WaveLayout {
         bool ok = false;
+        bool lineup = false;  // the shift loop: paths of links on consecutive lanes
         int32_t G = 0, W = 0, nfs = 0;
         int32_t nblk = 0, wpb = 0;
         int64_t o_word = 0, o_red = 0, o_deliv = 0, o_req = 0, o_gnt = 0, o_gdep = 0, bytes = 0;
@@ -606,6 +642,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     WaveLayout wv;
     std::vector<uint32_t> wv_lfb, wv_lfx;
     std::vector<int32_t> wv_feed, wv_nfeed, wv_sc, r_lf, pd_dix, blk_wave, blk_off;
+    std::vector<uint32_t> wv_duo;
     constexpr int64_t kWaveBlockLds = 160 * 1024;  // LDS of a compute unit
     // compute units of the current device (256 on MI355X)
     int32_t wave_blocks = 256;
@@ -669,6 +706,27 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                 for (size_t f = 0; f < feeders[i].size(); f++)
                     wv_feed[(size_t)i * 4 + f] = feeders[i][f] | (port_at_head[fsrc[feeders[i][f]]] << 8);
             }
+            // The shift loop (no credit delays): a lane's feeder is the lane
+            // before it and the lines it sends on go to the lane after it;
+            // wv_duo[i] = the local flows bound for that lane.  Under lowest-id
+            // arbitration with several lines per cycle, one flow at most is
+            // bound for it, so that the lines it offers there are in id order.
+            wv.lineup = lineup && c->credit.empty();
+            wv_duo.assign(nl, 0);
+            for (int32_t i = 0; i < nl && wv.lineup; i++) {
+                uint32_t tm = 0;
+                for (size_t q = 0; q < lflows[i].size(); q++) {
+                    const int32_t lb = (int32_t)((wv_lfb[i] >> (8 * q)) & 63u);
+                    if (lb == i) continue;
+                    if (lb != i + 1) wv.lineup = false;
+                    tm |= 1u << q;
+                }
+                if (feeders[i].size() > 1 || (feeders[i].size() == 1 && feeders[i][0] != i - 1)) wv.lineup = false;
+                if (c->arb == SIM_ARB_LOWEST_ID && bmax > 1 && __builtin_popcount(tm) > 1) wv.lineup = false;
+                wv_duo[i] = tm;
+            }
+            if (const char *ev = std::getenv("SIMGPU_WAVE_LOOP"))
+                if (!std::strcmp(ev, "general")) wv.lineup = false;  // tests: the arbitration loops on such graphs
             r_lf.assign(nr, 0);
             for (int64_t j = 0; j < nr; j++)
                 r_lf[j] = lf_index(link_lane[c->path_link[r_path[j]]], rflow[order[j]]);
@@ -747,7 +805,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                 int64_t wb = 1;
                 while (wb < wbmax) wb <<= 1;
                 const bool fast = c->arb == SIM_ARB_LOWEST_ID && wbmax == 1;
-                wbytes[q] = align16((ringn + 64) * 8) + ((general && !fast) ? tail_gen(wb) : tail_fast);
+                wbytes[q] = align16((ringn + 64) * 8) + ((general && !fast && !wv.lineup) ? tail_gen(wb) : tail_fast);
                 if (wbytes[q] > kWaveBlockLds) fits = false;
             }
             // Estimated run time of each wave, for placement only: its longest
@@ -769,7 +827,8 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                     }
                 }
                 const bool fast = c->arb == SIM_ARB_LOWEST_ID && wbmax == 1;
-                const double per = fast ? 1.0 : wbmax <= 1 ? 1.5 : wbmax <= 2 ? 1.8 : wbmax <= 4 ? 2.9 : 5.5;
+                const double per = wv.lineup ? (wbmax <= 1 ? 0.5 : wbmax <= 2 ? 0.8 : wbmax <= 4 ? 1.2 : 2.0)
+                                   : fast ? 1.0 : wbmax <= 1 ? 1.5 : wbmax <= 2 ? 1.8 : wbmax <= 4 ? 2.9 : 5.5;
                 wtime[q] = cyc * per;
             }
             std::vector<std::vector<int32_t>> blk;
@@ -998,8 +1057,8 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
             ln_fifo[i] = (int32_t)f;
             ln_mask[i] = fifo_mask[l];
             f += fifo_mask[l] + 1;
-            // feeders were collected in ascending-link lane order
-            const int32_t nfeed = (int32_t)feeders[std::lower_bound(fsrc.begin(), fsrc.end(), l) - fsrc.begin()].size() +
+            // feeders were collected in fsrc order
+            const int32_t nfeed = (int32_t)feeders[fsrc_pos[l]].size() +
                                   (has_stream[l] ? 1 : 0);
             ln_req[i] = (int32_t)r;
             ln_reqcap[i] = nfeed * bmax;
@@ -1089,6 +1148,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     d.wv_nblk = wv.nblk;
     d.wv_wpb = wv.wpb;
     d.wv_nfs = wv.nfs;
+    d.wv_lineup = wv.lineup ? 1 : 0;
     d.o_wword = (int32_t)wv.o_word;
     d.o_wred = (int32_t)wv.o_red;
     d.o_wdeliv = (int32_t)wv.o_deliv;
@@ -1173,7 +1233,9 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     UP(in_lane, in_lane);
     UP(ln_inoff, ln_inoff);
     if (engine == simgpu::kEngineWave) {
-        uint32_t *tmp_wv_lfb, *tmp_wv_lfx;
+        uint32_t *tmp_wv_lfb, *tmp_wv_lfx, *tmp_wv_duo;
+        if (wv_duo.empty()) wv_duo.push_back(0);
+        UP(wv_duo, wv_duo);
         int32_t *tmp_wv_feed, *tmp_wv_nfeed, *tmp_wv_sc, *tmp_r_lf, *tmp_pd_dix;
         UP(wv_lfb, wv_lfb);
         UP(wv_lfx, wv_lfx);

@@ -69,6 +69,23 @@ __device__ __forceinline__ void vm_drain() { __builtin_amdgcn_s_waitcnt(0x0F70);
 
 __device__ __forceinline__ uint32_t byte_of(uint32_t v, uint32_t q) { return __builtin_amdgcn_ubfe(v, q * 8u, 8u); }
 
+// Whole-wave DPP shifts by one lane, register to register: lane w receives
+// lane w - 1's value (from_below) or lane w + 1's (from_above); the end lane
+// keeps `old`.  A lane that is inactive during the shift hands on `old`
+// instead of its value, so a shift must run with every lane active: the
+// empty volatile asm on the result pins the shift where it is written (on a
+// path every lane takes), so that the compiler cannot move it into a branch.
+__device__ __forceinline__ uint32_t from_below(uint32_t v, uint32_t old) {
+    uint32_t r = (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, 0x138, 0xF, 0xF, false);  // wave_shr:1
+    asm volatile("" : "+v"(r));
+    return r;
+}
+__device__ __forceinline__ uint32_t from_above(uint32_t v, uint32_t old) {
+    uint32_t r = (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, 0x130, 0xF, 0xF, false);  // wave_shl:1
+    asm volatile("" : "+v"(r));
+    return r;
+}
+
 __device__ __forceinline__ uint32_t wrap_add(uint32_t a, uint32_t n, uint32_t cap) {
     const uint32_t v = a + n;
     return v >= cap ? v - cap : v;
@@ -217,6 +234,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
     int R = 0, rend = 0;
     uint32_t o = 0;
     WRange cur{};
+    bool feed1 = false;  // the lane's link has exactly one feeder
     if (on) {
         link = d.ln_link[i];
         const size_t pi = (size_t)s * m + link;
@@ -235,6 +253,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
         }
         R = d.ln_srbeg[i];
         rend = d.ln_srend[i];
+        feed1 = nfeed == 1;
         if (R < rend) load_wrange(d, R, cur);
     }
     // this lane's ring: exclusive prefix sum over the wave of the capacities,
@@ -259,7 +278,8 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
     const uint32_t ring_trash = rtotal + (uint32_t)w;
     constexpr bool kFast = ARB == 0;             // the b = 1 lowest-id loop exists
     constexpr bool kGeneral = BM > 1 || ARB == 1;  // the general loop exists
-    const bool fast = kFast && (!kGeneral || __ballot(on && b != 1) == 0ull);
+    const bool lined = !CR && d.wv_lineup != 0;  // the shift loop runs instead
+    const bool fast = kFast && !lined && (!kGeneral || __ballot(on && b != 1) == 0ull);
     // the wave's bandwidth bound: its general loop is unrolled to that width
     int wbm = on ? b : 1;
 #pragma unroll
@@ -358,6 +378,362 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
             }
         }
     };
+
+    // Shift loop, for graphs whose links form paths laid out on consecutive
+    // lanes: a link is fed by the lane below it (if by any link) plus,
+    // possibly, its own injection stream, and sends the lines that go on to
+    // the lane above it.  A link's arbitration then merges two ordered
+    // lists -- its feeder's lines bound for it, in the feeder's offer order
+    // (id order: one flow under lowest id), and its stream's released lines
+    // -- and takes the first min(b, free, both); the feeder's taken lines are
+    // the first of its lines bound there, so no grant is void.  Requests move
+    // one lane up and the number taken one lane down by DPP shifts, register
+    // to register: a cycle needs no LDS round trip.  The target appends the
+    // merged lines to its ring in LDS; with one line per cycle the first two
+    // FIFO entries stay in registers and the ring is read a cycle ahead.
+    //
+    // Cycles run through a lean body while every lane's next cycle is a
+    // common one: the stream offer stays inside the current range and needs
+    // at most two predecessor counts, and every scenario moves a line and
+    // goes on.  Otherwise one cycle runs through the complete body (range
+    // changes, more predecessors, jumps over idle cycles, a scenario's end).
+    auto lineup = [&](auto bmw_tag) {
+        constexpr int BMW = decltype(bmw_tag)::value;
+        const uint32_t tmask = on ? d.wv_duo[i] : 0u;  // local flows bound for the lane above
+        const uint32_t fport = fp & 0xFFu;              // the feeder's port here
+        uint2 e[BMW];  // first FIFO entries (meaningful for k < min(occ, b))
+#pragma unroll
+        for (int k = 0; k < BMW; k++) e[k] = make_uint2(0u, 0u);
+        uint2 e1 = make_uint2(0u, 0u);   // BMW == 1: the second entry (occ >= 2) ...
+        uint2 e1l = make_uint2(0u, 0u);  // ... or, when pend, the ring read that holds it
+        bool pend = false;
+        uint32_t tx32 = 0, busy32 = 0;   // link counters of this launch (below 2^32: at most T lines)
+        // The time advance of a cycle that is not the common one: a scenario
+        // in which nothing moved jumps to its earliest future FIFO-head ready
+        // time (nxt: this lane's, as of the cycle's start); scenarios end.
+        auto slow_time = [&](bool sdep, bool sact, uint32_t nxt) {
+            uint32_t rv = kNever;
+            if (__ballot(live & !sdep) != 0ull) {
+                cbar();
+                atomicMin(&red[nxt != kNever ? (uint32_t)g : 64u + (uint32_t)w], nxt);
+                cbar();
+                rv = red[g];
+                cbar();
+                red[i == 0 ? (uint32_t)g : 64u + (uint32_t)w] = kNever;
+            }
+            const uint32_t tn = sdep ? t + 1u : rv;
+            const bool go = sact & (tn != kNever) & (tn <= maxc) & (processed <= wdog);
+            if (live & !go) {
+                int32_t st = kRunWatchdog;
+                st = (tn > maxc) ? kRunMaxCycles : st;
+                st = (!sdep & (rv == kNever)) ? kRunDeadlock : st;
+                st = !sact ? kRunOk : st;
+                state = st;
+                live = false;
+            }
+            t = live ? tn : t;
+        };
+        // One cycle.  FULL: the complete body; else the lean one, valid when
+        // no lane needs the complete one.  Returns whether the next cycle can
+        // run through the lean body.
+        auto cycle = [&](auto full_tag) -> bool {
+            constexpr bool FULL = decltype(full_tag)::value;
+            const uint32_t e_y0 = e[0].y;  // the head's ready time at the cycle's start
+            const uint32_t occ0 = occ, head0 = head;
+            // ---------------------------------------------------------- FIFO offer
+            uint32_t noff = 0, kmask = 0;
+            uint32_t up[BMW];  // offered lines as entry words at the lane above
+            {
+                bool open = live;
+#pragma unroll
+                for (int k = 0; k < BMW; k++) {
+                    open = open & (k < b) & ((uint32_t)k < occ) & (e[k].y <= t);
+                    noff += open ? 1u : 0u;
+                    const uint32_t q = (e[k].x >> 5) & 3u;
+                    kmask |= (open & (((tmask >> q) & 1u) != 0u)) ? 1u << k : 0u;
+                    up[k] = (e[k].x & ~0x7Fu) | ((byte_of(lfb, q) >> 6) << 5);
+                }
+            }
+            // ---------------------------------------------------------- the feeder's lines, up one lane
+            uint32_t fe[BMW];
+#pragma unroll
+            for (int k = 0; k < BMW; k++) fe[k] = from_below(up[k], 0u);
+            const uint32_t fkm = from_below(kmask, 0u) & (feed1 ? ~0u : 0u);
+            // ---------------------------------------------------------- stream offer
+            uint32_t sword[BMW];
+#pragma unroll
+            for (int k = 0; k < BMW; k++) sword[k] = ((cur.start + o + k) << kXs) | (cur.lf << 5);
+            uint32_t nS;
+            if constexpr (FULL) {
+                nS = (live & (R < rend)) ? released_count<CH>(d, cur, o, min((uint32_t)b, cur.len - o), dv0, dv1, deliv)
+                                         : 0u;
+                if ((nS == cur.len - o) & (nS < (uint32_t)b) & (R + 1 < rend) & live) {
+                    // the offer runs into the ranges after the current one
+                    int sR = R + 1;
+                    WRange sr;
+                    while (sR < rend && nS < (uint32_t)b) {
+                        load_wrange(d, sR, sr);
+                        const uint32_t n = released_direct<CH>(d, sr, min((uint32_t)b - nS, sr.len), deliv);
+#pragma unroll
+                        for (int k = 0; k < BMW; k++)
+                            if (((uint32_t)k >= nS) & ((uint32_t)k < nS + n))
+                                sword[k] = ((sr.start + (uint32_t)k - nS) << kXs) | (sr.lf << 5);
+                        nS += n;
+                        if (n < sr.len) break;
+                        sR++;
+                    }
+                }
+            } else {
+                // at most two predecessors, inside the range (the caller checked)
+                const uint32_t oo = CH ? 0u : o;
+                uint32_t n = (live & (R < rend)) ? (uint32_t)b : 0u;
+                n = cur.np > 0u ? min(n, pred_allows<CH>(dv0, cur.pb0 + oo)) : n;
+                n = cur.np > 1u ? min(n, pred_allows<CH>(dv1, cur.pb1 + oo)) : n;
+                nS = n;
+            }
+            // ---------------------------------------------------------- arbitration
+            const uint32_t nF = (uint32_t)__builtin_popcount(fkm);
+            const uint32_t G = live ? min(min((uint32_t)b, cap - occ), nF + nS) : 0u;
+            const uint32_t rotf = fport >= rr ? fport - rr : fport + P - rr;
+            const uint32_t rots = (P - 1u) >= rr ? P - 1u - rr : P - 1u + P - rr;
+            uint32_t gF = 0, gS = 0, lastS = 0;
+            uint32_t Ex = 0;  // BMW == 1: the entry word appended
+            const uint32_t ready = t + L;
+            // Lowest id, several lines: each list is in id order, and when the
+            // two do not interleave (the usual case: each is a run of one flow's
+            // lines) one lies wholly before the other, so the ranks need no
+            // pairwise comparisons.  first: 1 feeder's list first, 2 the
+            // stream's, 0 interleaved (compare pairwise).
+            uint32_t first = 0;
+            if constexpr (ARB == 0 && BMW > 2) {
+                uint32_t fmin = 0xFFFFFFFFu, fmax = 0u;
+#pragma unroll
+                for (int k = 0; k < BMW; k++) {
+                    const bool tb = ((fkm >> k) & 1u) != 0u;
+                    fmin = tb ? min(fmin, fe[k]) : fmin;
+                    fmax = tb ? max(fmax, fe[k]) : fmax;
+                }
+                const uint32_t smin = sword[0], smax = sword[nS > 0u ? nS - 1u : 0u];
+                first = (nS == 0u) | (fmax < smin) ? 1u : ((nF == 0u) | (smax < fmin) ? 2u : 0u);
+            }
+            const bool pairwise = ARB == 0 && (BMW <= 2 || __ballot(first == 0u) != 0ull);
+#pragma unroll
+            for (int k = 0; k < BMW; k++) {  // the feeder's lines bound here (positions in fkm)
+                const bool tb = ((fkm >> k) & 1u) != 0u;
+                const uint32_t j = (uint32_t)__builtin_popcount(fkm & ((1u << k) - 1u));
+                uint32_t ahead;
+                if constexpr (ARB == 0) {
+                    ahead = first == 2u ? nS : 0u;
+                    if (pairwise) {
+                        ahead = 0;
+#pragma unroll
+                        for (int y = 0; y < BMW; y++) ahead += (((uint32_t)y < nS) & (sword[y] < fe[k])) ? 1u : 0u;
+                    }
+                } else {
+                    ahead = min(nS, (uint32_t)k + (rots < rotf ? 1u : 0u));
+                }
+                const uint32_t rank = j + ahead;
+                const bool gk = tb & (rank < G);
+                ring[gk ? rbase + wrap_add(tail, rank, cap) : ring_trash] = make_uint2(fe[k], ready);
+                gF += gk ? 1u : 0u;
+                if (BMW == 1) Ex = gk ? fe[k] : Ex;
+            }
+#pragma unroll
+            for (int k = 0; k < BMW; k++) {  // the stream's lines
+                uint32_t ahead;
+                if constexpr (ARB == 0) {
+                    ahead = first == 1u ? nF : 0u;
+                    if (pairwise) {
+                        ahead = 0;
+#pragma unroll
+                        for (int y = 0; y < BMW; y++)
+                            ahead += ((((fkm >> y) & 1u) != 0u) & (fe[y] < sword[k])) ? 1u : 0u;
+                    }
+                } else {
+                    const uint32_t lim = (uint32_t)k + (rotf < rots ? 1u : 0u);
+                    ahead = (uint32_t)__builtin_popcount(fkm & (lim >= 32u ? ~0u : (1u << lim) - 1u));
+                }
+                const uint32_t rank = (uint32_t)k + ahead;
+                const bool gk = ((uint32_t)k < nS) & (rank < G);
+                ring[gk ? rbase + wrap_add(tail, rank, cap) : ring_trash] = make_uint2(sword[k], ready);
+                gS += gk ? 1u : 0u;
+                lastS = gk ? rank + 1u : lastS;
+                if (BMW == 1) Ex = gk ? sword[k] : Ex;
+            }
+            // ---------------------------------------------------------- the lines taken, down one lane
+            const uint32_t got = from_above(gF, 0u);
+            uint32_t gout = 0, ejd = 0;
+            {
+                bool open = true;
+#pragma unroll
+                for (int k = 0; k < BMW; k++) {
+                    const bool tb = ((kmask >> k) & 1u) != 0u;
+                    const uint32_t j = (uint32_t)__builtin_popcount(kmask & ((1u << k) - 1u));
+                    const bool dk = open & ((uint32_t)k < noff) & (!tb | (j < got));
+                    open = dk;
+                    gout += dk ? 1u : 0u;
+                    ejd |= (dk & !tb) ? 1u << k : 0u;
+                }
+            }
+            if (ejd) {
+#pragma unroll
+                for (int k = 0; k < BMW; k++) {
+                    if ((ejd >> k) & 1u) {
+                        const uint32_t x = e[k].x >> kXs;
+                        bad |= x >= Tu;
+                        comp[x < Tu ? x : 0u] = t + 1u;
+                        atomicAdd(&deliv[mydx + ((e[k].x >> 5) & 3u)], 1u);
+                    }
+                }
+            }
+            if (ARB == 1 && G != 0u) {  // past the port of the last line appended
+                const uint32_t lp = lastS == G ? P - 1u : fport;
+                rr = lp + 1u == P ? 0u : lp + 1u;
+            }
+            // ---------------------------------------------------------- FIFO and stream state
+            head = wrap_add(head, gout, cap);
+            tail = wrap_add(tail, G, cap);
+            occ = occ + G - gout;
+            tx32 += G;
+            busy32 += G ? 1u : 0u;
+            o += gS;
+            if constexpr (FULL) {
+                if (o >= cur.len) next_range();
+            }
+            if constexpr (BMW == 1) {
+                // the first two entries: kept, moved down by a pop, the line just
+                // appended, or (entry 1 after a pop with three or more lines)
+                // read from the ring now and used no earlier than the next
+                // cycle's end
+                const uint2 E = make_uint2(Ex, ready);
+                const uint2 e1v = pend ? e1l : e1;
+                const bool pop = gout != 0u;
+                const uint2 n0 = pop ? (occ0 >= 2u ? e1v : E) : (occ0 >= 1u ? e[0] : E);
+                const uint2 n1 = pop ? (occ0 == 2u ? E : e1v) : (occ0 == 1u ? E : e1v);
+                e1l = ring[rbase + wrap_add(head0, min(2u, cap - 1u), cap)];
+                e[0] = n0;
+                e1 = n1;
+                pend = pop & (occ0 >= 3u);
+            } else {
+                cbar();
+#pragma unroll
+                for (int k = 0; k < BMW; k++) e[k] = ring[rbase + wrap_add(head, min((uint32_t)k, cap - 1u), cap)];
+            }
+            dv0 = deliv[cur.ix0];  // delivered counts for the next cycle (ix0/ix1 = 0 when unused)
+            dv1 = deliv[cur.ix1];
+            // ---------------------------------------------------------- time
+            const bool dep = (gout | gS) != 0u;
+            const bool act = live & ((occ != 0u) | (R < rend));
+            const bool sdep = (__ballot(dep) & smask) != 0ull;
+            const bool sact = (__ballot(act) & smask) != 0ull;
+            processed += live ? 1u : 0u;
+            const bool common = sdep & sact & (t + 1u <= maxc) & (processed <= wdog);
+            const uint32_t nxt = (live & (occ0 != 0u) & (e_y0 > t)) ? e_y0 : kNever;
+            if (__ballot(live & !common) != 0ull) slow_time(sdep, sact, nxt);
+            else t = live ? t + 1u : t;
+            // the next cycle: the stream's offer inside its range, two predecessors at most
+            const bool lean = !live | (R >= rend) | ((o + (uint32_t)b < cur.len) & (cur.np <= 2u));
+            return __ballot(!lean) == 0ull;
+        };
+        // The lean cycle for one line per cycle: one entry word up (none
+        // when no line is bound there), one bit down.
+        auto cycle1 = [&]() -> bool {
+            constexpr uint32_t kNone = 0xFFFFFFFFu;  // above every entry word (line ids < 2^25 - 1)
+            const uint32_t hx = e[0].x, hy = e[0].y;
+            const uint32_t occ0 = occ, head0 = head;
+            const bool hrdy = live & (occ != 0u) & (hy <= t);
+            const uint32_t q = (hx >> 5) & 3u;
+            const bool upb = ((tmask >> q) & 1u) != 0u;
+            const bool tb = hrdy & upb;
+            const bool ej = hrdy & !upb;
+            const uint32_t fe = from_below(tb ? (hx & ~0x7Fu) | ((byte_of(lfb, q) >> 6) << 5) : kNone, kNone) |
+                                (feed1 ? 0u : kNone);
+            const uint32_t oo = CH ? 0u : o;
+            bool sw = live & (R < rend);
+            sw = sw & ((cur.np < 1u) | (pred_allows<CH>(dv0, cur.pb0 + oo) != 0u));
+            sw = sw & ((cur.np < 2u) | (pred_allows<CH>(dv1, cur.pb1 + oo) != 0u));
+            const uint32_t sx = sw ? ((cur.start + o) << kXs) | (cur.lf << 5) : kNone;
+            // the winner: lowest entry word (id), or the first port at or after the pointer
+            bool fwin;
+            if constexpr (ARB == 0) {
+                fwin = fe < sx;
+            } else {
+                const uint32_t rotf = fport >= rr ? fport - rr : fport + P - rr;
+                const uint32_t rots = (P - 1u) >= rr ? P - 1u - rr : P - 1u + P - rr;
+                fwin = (fe != kNone) & ((sx == kNone) | (rotf < rots));
+            }
+            const uint32_t wx = fwin ? fe : sx;
+            const bool app = live & (wx != kNone) & (occ < cap);
+            const uint32_t ready = t + L;
+            ring[app ? rbase + tail : ring_trash] = make_uint2(wx, ready);
+            const bool gF = app & fwin;
+            const bool gS = app & !fwin;
+            const bool got = from_above(gF ? 1u : 0u, 0u) != 0u;
+            const bool pop = ej | (tb & got);
+            if (ej) {
+                const uint32_t x = hx >> kXs;
+                bad |= x >= Tu;
+                comp[x < Tu ? x : 0u] = t + 1u;
+                atomicAdd(&deliv[mydx + q], 1u);
+            }
+            dv0 = deliv[cur.ix0];  // delivered counts for the next cycle (ix0/ix1 = 0 when unused)
+            dv1 = deliv[cur.ix1];
+            if (ARB == 1 && app) {
+                const uint32_t lp = gS ? P - 1u : fport;
+                rr = lp + 1u == P ? 0u : lp + 1u;
+            }
+            head = pop ? wrap_add(head, 1u, cap) : head;
+            tail = app ? wrap_add(tail, 1u, cap) : tail;
+            occ = occ + (app ? 1u : 0u) - (pop ? 1u : 0u);
+            tx32 += app ? 1u : 0u;
+            busy32 += app ? 1u : 0u;
+            o += gS ? 1u : 0u;
+            // first two entries (as in the complete cycle)
+            const uint2 E = make_uint2(wx, ready);
+            const uint2 e1v = pend ? e1l : e1;
+            const uint2 n0 = pop ? (occ0 >= 2u ? e1v : E) : (occ0 >= 1u ? e[0] : E);
+            const uint2 n1 = pop ? (occ0 == 2u ? E : e1v) : (occ0 == 1u ? E : e1v);
+            e1l = ring[rbase + wrap_add(head0, min(2u, cap - 1u), cap)];
+            e[0] = n0;
+            e1 = n1;
+            pend = pop & (occ0 >= 3u);
+            // time: the common case moves every scenario on by one cycle; any
+            // other is left to the caller (slow_time)
+            const bool act = live & ((occ != 0u) | (R < rend));
+            const bool sdep = (__ballot(pop | gS) & smask) != 0ull;
+            const bool sact = (__ballot(act) & smask) != 0ull;
+            processed += live ? 1u : 0u;
+            const bool common = sdep & sact & (t + 1u <= maxc) & (processed <= wdog);
+            if (__ballot(live & !common) != 0ull) slow_time(sdep, sact, (live & (occ0 != 0u) & (hy > t)) ? hy : kNever);
+            else t = live ? t + 1u : t;
+            const bool lean = !live | (R >= rend) | ((o + 1u < cur.len) & (cur.np <= 2u));
+            return __ballot(!lean) == 0ull;
+        };
+        while (__ballot(live) != 0ull) {
+            bool ok = cycle(std::true_type{});
+            if constexpr (BMW == 1) {
+                while (ok && __ballot(live) != 0ull) ok = cycle1();
+            } else {
+                while (ok && __ballot(live) != 0ull) ok = cycle(std::false_type{});
+            }
+        }
+        tx += tx32;
+        busy += busy32;
+        if (__ballot(bad) != 0ull) {  // engine fault: end the faulty scenarios
+            const bool sbad = (__ballot(bad) & smask) != 0ull;
+            if (sbad & on) state = kRunInternal;
+        }
+    };
+    if (lined) {
+        if (wbm <= 1) lineup(std::integral_constant<int, 1>{});
+        else if constexpr (BM >= 2) {
+            if (wbm <= 2 || BM == 2) lineup(std::integral_constant<int, 2>{});
+            else if constexpr (BM >= 4) {
+                if (wbm <= 4 || BM == 4) lineup(std::integral_constant<int, 4>{});
+                else if constexpr (BM >= 8) lineup(std::integral_constant<int, 8>{});
+            }
+        }
+    }
 
     // The head entries are re-read from the ring at the end of every cycle,
     // unconditionally: after the cycle's pops and appends the ring holds the
@@ -636,7 +1012,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
         }
     };
     if constexpr (kGeneral) {
-        if (!fast) {
+        if (!fast && !lined) {
             if constexpr (BM == 1) {
                 general(std::integral_constant<int, 1>{});
             } else {

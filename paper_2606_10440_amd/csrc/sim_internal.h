@@ -137,6 +137,8 @@ struct DevNet {
     int32_t wv_nblk;          // workgroups: up to 16 independent waves each
     int32_t wv_wpb;           // wave slots per workgroup
     int32_t wv_nfs;           // request-slot groups per target lane: feeders + the lane's own stream
+    int32_t wv_lineup;        // shift loop: a lane's feeder is lane - 1, its next link lane + 1
+    const uint32_t *wv_duo;   // [nl] shift loop: local flows bound for the next lane (bit q)
     int32_t o_wword, o_wred, o_wdeliv, o_wreq, o_wgnt, o_wgdep;  // LDS byte offsets after a wave's rings
     const int32_t *blk_wave;  // [wv_nblk*wv_wpb] wave of each slot, -1 if empty
     const int32_t *blk_off;   // [wv_nblk*wv_wpb] LDS byte offset of the slot's region

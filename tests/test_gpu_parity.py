@@ -579,3 +579,41 @@ def test_wave_all_64_links(simmod, oracle_lib, dep, arb):
     w.order = si.gray_torus_order(4, 4)
     w.dep = dep
     check_engine(simmod, oracle_lib, w, "wave")
+
+
+# ------------------------------------------------ wave engine, ring graphs
+
+@pytest.mark.parametrize("arb", [0, 1])
+@pytest.mark.parametrize("coll", [si.COLL_RING_ALLGATHER, si.COLL_DIRECT_ALLREDUCE, si.COLL_ALLTOALL])
+def test_wave_mesh_collectives_arb(simmod, oracle_lib, arb, coll):
+    """Full mesh, both policies, b = 3: one-hop flows on links of their own
+    (streams with many predecessors for the direct all-gather)."""
+    w = si.full_mesh(6, b=3, L=4, cap=5, coll=coll, nbytes=128 * 6 * 5, arb=arb)
+    assert check_engine(simmod, oracle_lib, w, "wave") == 1
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_wave_directed_ring_dags(simmod, oracle_lib, seed):
+    """A directed ring whose flows go one or two hops: every link is fed by
+    its predecessor link and by its own stream and sends lines on or out.
+    Tiny buffers (the ring's buffers form a cycle, so some scenarios
+    deadlock), mixed bandwidths, both policies, random predecessor DAGs."""
+    rng = np.random.default_rng(9100 + seed)
+    n = int(rng.integers(3, 7))
+    rp = np.arange(n + 1, dtype=np.int32)
+    ci = np.array([(v + 1) % n for v in range(n)], np.int32)
+    S = 3
+    bw = rng.choice([1, 2, 4, 8], size=S * n).astype(np.int32)
+    lat = rng.integers(1, 6, size=S * n).astype(np.int32)
+    cap = rng.integers(1, 9, size=S * n).astype(np.int32)
+    T = int(rng.integers(20, 200))
+    src = rng.integers(0, n, size=T).astype(np.int32)
+    dst = ((src + rng.integers(1, 3, size=T)) % n).astype(np.int32)
+    pptr = [0]
+    pidx = []
+    for x in range(T):
+        k = int(rng.integers(0, 3)) if x else 0
+        pidx += sorted(set(int(v) for v in rng.integers(0, x, size=k))) if x else []
+        pptr.append(len(pidx))
+    w = si.Workload("dir_ring", n, n, rp, ci, S, bw, lat, cap, seed % 2, -1, 0)
+    check_engine(simmod, oracle_lib, w, "wave", txns=(src, dst, np.array(pptr, np.int64), np.array(pidx, np.int64)))
