@@ -287,6 +287,33 @@ def test_deterministic_repeat(simmod):
     assert bool((ca == b.completion).all())
 
 
+@pytest.mark.parametrize("engine,threads", [("lane", (64, 256, 1024)), ("lanehbm", (64, 512)),
+                                            ("wave", (None,)), ("workgroup", (None,))])
+def test_launch_geometry_same_bytes(simmod, engine, threads):
+    """One workload on every engine, and on the lane engines at several
+    workgroup sizes: the outputs are the same bytes."""
+    w = si.torus2d(4, 4, n_scenarios=6, seed=77, bws=(1, 2, 4), lat_lo=1, lat_hi=20, depths=(3, 16),
+                   nbytes=128 * 16 * 8, arb=1)
+    ref = run_engine(simmod, w, "workgroup")
+    assert ref.status == 0
+    want = [t.cpu().numpy() for t in (ref.completion, ref.tx_lines, ref.busy_cycles, ref.makespan)]
+    for th in threads:
+        old = os.environ.get("SIMGPU_LANE_THREADS")
+        if th is not None:
+            os.environ["SIMGPU_LANE_THREADS"] = str(th)
+        try:
+            r = run_engine(simmod, w, engine)
+        finally:
+            if old is None:
+                os.environ.pop("SIMGPU_LANE_THREADS", None)
+            else:
+                os.environ["SIMGPU_LANE_THREADS"] = old
+        assert r.status == 0
+        got = [t.cpu().numpy() for t in (r.completion, r.tx_lines, r.busy_cycles, r.makespan)]
+        for a, b in zip(want, got):
+            assert a.tobytes() == b.tobytes(), (engine, th)
+
+
 # ----------------------------------------------------------------- full size
 
 def _digest(a: np.ndarray) -> str:
