@@ -240,6 +240,58 @@ sim_status sim_load_memcpy(sim_ctx *ctx, int64_t n_ops, const int32_t *cu, const
                            const int64_t *n_lines, int32_t n_spaces, int32_t n_ch, const int32_t *space_ch,
                            int32_t unroll, int32_t window);
 
+/* Operation kinds of sim_load_gpu_ops. */
+#define SIM_OP_COPY 0
+#define SIM_OP_RELEASE 1
+#define SIM_OP_ACQUIRE 2
+
+/*
+ * Load GPU programs with data and control operations (paper Sec. 4.1.1 GPU
+ * instructions, Sec. 4.1.2 GPU operations: memcpy, reduce, acquire and
+ * release; Sec. 4.4.2 compute unit; Sec. 4.4.3 a semaphore access is one
+ * wavefront request; Sec. 5.2 get- and put-based collectives).  Replaces any
+ * previous workload.  sim_load_memcpy is this call with one-source copies.
+ *   kind[o]: SIM_OP_COPY, SIM_OP_RELEASE or SIM_OP_ACQUIRE; cu[o] runs it (a
+ *       CU runs its operations in array order).
+ *   src_ptr[n_ops + 1] (src_ptr[0] = 0), src_space[], src_line[]: the sources
+ *       of operation o are entries src_ptr[o] .. src_ptr[o+1] - 1.
+ *   SIM_OP_COPY: n_lines[o] lines from each source (line address src_line,
+ *       address space src_space) into dst_line[o] of dst_space[o]; one source
+ *       is a memcpy, several are a reduce of the sources into the
+ *       destination.  Per group of at most U lines the CU issues the loads of
+ *       source 0, then of source 1, ..., waits for all of their data, then
+ *       issues the group's stores.  The reduce arithmetic itself is taken to
+ *       cost no cycles: only its wait for every input is modelled.
+ *   SIM_OP_RELEASE: no source, n_lines 1; one store to the semaphore line
+ *       (dst_space[o], dst_line[o]) that leaves once every earlier store of
+ *       the CU has arrived.  Each semaphore is released exactly once.
+ *   SIM_OP_ACQUIRE: no source, n_lines 1; one load of the semaphore line
+ *       (request and reply).  Of the polls of a waiting wavefront only the
+ *       successful one is simulated: its request leaves once the release of
+ *       that semaphore has arrived, and the CU's next request waits for the
+ *       reply.
+ *   n_spaces, n_ch, space_ch[n_spaces * n_ch], unroll U >= 1, window W >= 1:
+ *       as for sim_load_memcpy (W bounds every issued request: load and
+ *       acquire requests, stores and releases).
+ * Ids are step-major: for issue index k = 0, 1, ... and the CUs in ascending
+ * endpoint order, a load or acquire takes two ids (request, then data or
+ * reply), a store or release one.  Stores and data lines are data messages
+ * (class 0); load requests and every line of a release or acquire are control
+ * messages (class 1).  A memory channel returns its lines in id order: an
+ * acquire whose reply waits for a late release holds back that channel's
+ * later replies, and a program in which that closes a cycle of waits is
+ * reported as SIM_ERR_DEADLOCK by the run.  Arrays are copied.
+ * SIM_ERR_INVALID_ARG for an unknown kind, a copy without a source, a release
+ * or acquire with a source or n_lines != 1, a semaphore released twice or
+ * acquired but never released, and the errors of sim_load_memcpy;
+ * SIM_ERR_SIZE beyond 2^32 - 2 lines.
+ */
+sim_status sim_load_gpu_ops(sim_ctx *ctx, int64_t n_ops, const int32_t *kind, const int32_t *cu,
+                            const int64_t *src_ptr, const int32_t *src_space, const int64_t *src_line,
+                            const int32_t *dst_space, const int64_t *dst_line, const int64_t *n_lines,
+                            int32_t n_spaces, int32_t n_ch, const int32_t *space_ch, int32_t unroll,
+                            int32_t window);
+
 /* Sizes of the loaded problem: transactions T, links m, scenarios S and
  * line-hops per scenario (sum of path lengths; a line-hop is one admission of
  * a 128 B wavefront request onto a link, the per-line, per-hop unit of work

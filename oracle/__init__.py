@@ -64,6 +64,9 @@ def lib():
         L.oracle_memcpy.argtypes = [i64, P, P, P, P, P, P, i32, i32, P, i32, i32, i64, i64,
                                     P, P, P, P, P, P, P]
         L.oracle_memcpy.restype = C.c_int
+        L.oracle_gpu_ops.argtypes = [i64, P, P, P, P, P, P, P, P, i32, i32, P, i32, i32, i64, i64,
+                                     P, P, P, P, P, P, P]
+        L.oracle_gpu_ops.restype = C.c_int
         _lib = L
     return _lib
 
@@ -111,9 +114,16 @@ def txn(coll, nbytes, group, E, x, order=None, dep=0):
 
 
 def memcpy_txns(mc, with_class=False):
-    """Expand memcpy programs (``sim_inputs.noc.Memcpy``) into the line list
-    (src, dst, pred_ptr, pred_idx) [+ per-line class: 1 = load request]."""
+    """Expand GPU programs (``sim_inputs.noc.Memcpy``: copies, reduces,
+    releases and acquires) into the line list (src, dst, pred_ptr, pred_idx)
+    [+ per-line class: 1 = control message]."""
     n_ops = len(mc.cu)
+    if mc.kind is None:   # plain memcpy: one source per operation
+        kind = np.zeros(n_ops, np.int32)
+        sptr = np.arange(n_ops + 1, dtype=np.int64)
+    else:
+        kind = np.ascontiguousarray(mc.kind, np.int32)
+        sptr = np.ascontiguousarray(mc.src_ptr, np.int64)
     cu = np.ascontiguousarray(mc.cu, np.int32)
     ssp = np.ascontiguousarray(mc.src_space, np.int32)
     dsp = np.ascontiguousarray(mc.dst_space, np.int32)
@@ -121,20 +131,23 @@ def memcpy_txns(mc, with_class=False):
     dl = np.ascontiguousarray(mc.dst_line, np.int64)
     nl = np.ascontiguousarray(mc.n_lines, np.int64)
     ch = np.ascontiguousarray(mc.space_channels, np.int32)
+    if len(sptr) != n_ops + 1 or len(ssp) < sptr[-1] or len(sl) < sptr[-1] or len(dsp) < n_ops:
+        raise ValueError("gpu programs: inconsistent array lengths")
     n_spaces = len(ch) // mc.n_ch
     T = np.zeros(1, np.int64)
     P = np.zeros(1, np.int64)
-    args = (n_ops, _p(cu), _p(ssp), _p(dsp), _p(sl), _p(dl), _p(nl), n_spaces, mc.n_ch, _p(ch), mc.unroll, mc.window)
-    rc = lib().oracle_memcpy(*args, 0, 0, None, None, None, None, None, _p(T), _p(P))
+    args = (n_ops, _p(kind), _p(cu), _p(sptr), _p(ssp), _p(sl), _p(dsp), _p(dl), _p(nl), n_spaces, mc.n_ch,
+            _p(ch), mc.unroll, mc.window)
+    rc = lib().oracle_gpu_ops(*args, 0, 0, None, None, None, None, None, _p(T), _p(P))
     if rc:
-        raise ValueError(f"oracle_memcpy: status {rc}")
+        raise ValueError(f"oracle_gpu_ops: status {rc}")
     src = np.zeros(max(int(T[0]), 1), np.int32)
     dst = np.zeros(max(int(T[0]), 1), np.int32)
     pptr = np.zeros(int(T[0]) + 1, np.int64)
     pidx = np.zeros(max(int(P[0]), 1), np.int64)
     cls = np.zeros(max(int(T[0]), 1), np.uint8)
-    rc = lib().oracle_memcpy(*args, int(T[0]), int(P[0]), _p(src), _p(dst), _p(pptr), _p(pidx), _p(cls),
-                             _p(T), _p(P))
+    rc = lib().oracle_gpu_ops(*args, int(T[0]), int(P[0]), _p(src), _p(dst), _p(pptr), _p(pidx), _p(cls),
+                              _p(T), _p(P))
     assert rc == 0
     t = int(T[0])
     if with_class:

@@ -599,42 +599,87 @@ int oracle_txn(int coll, uint64_t bytes, int32_t group, int32_t E, const int32_t
     return rc;
 }
 
-/* ------------------------------------------------------- memcpy programs
- * The injection side of the GPU model (Sec. 4.4.3 wavefront requests, 4.4.4
- * loop unrolling; the outstanding-request limit of Sec. 5.3).  A CU runs its
- * memcpy operations in list order.  Each copied line is a load and a store;
- * unrolled by U, the loop issues U loads, waits for their data, then issues
- * the U stores (the last group of an operation may be shorter).
+/* ------------------------------------------------------------ GPU programs
+ * The injection side of the GPU model (Sec. 4.1.1 GPU instructions, 4.1.2
+ * GPU operations, 4.4.2 compute unit, 4.4.3 wavefront requests, 4.4.4 loop
+ * unrolling; the outstanding-request limit of Sec. 5.3).  A CU runs its
+ * operations in list order:
+ *   COPY    n lines from K >= 1 sources (space s_k, first line a_k) into one
+ *           destination.  Unrolled by U, each group of gn <= U lines issues
+ *           the loads of source 0 (lines j0 .. j0 + gn - 1), then of source
+ *           1, ..., waits for all of their data, then issues the gn stores.
+ *           K = 1 is memcpy; K > 1 is a reduce of the K inputs into the
+ *           destination.  The arithmetic of the reduce is taken to cost no
+ *           cycles (the paper gives no count); its effect is that the stores
+ *           wait for every input.
+ *   RELEASE one store to a semaphore line; a release completes the CU's
+ *           earlier stores first (it waits for every earlier store of the
+ *           CU), and it is a control message.
+ *   ACQUIRE one load of a semaphore line (request and reply, both control
+ *           messages).  The wavefront polls the semaphore until the release
+ *           is visible; of those polls only the one that finds it released
+ *           is simulated: its request leaves once the release of the same
+ *           semaphore has arrived.  The CU's next request waits for the
+ *           reply.
  *   load  = a request line (CU -> the channel of the source line) and a data
  *           line (that channel -> CU) that may leave once the request has
  *           arrived;
- *   store = one line (CU -> the channel of the destination line) that may
- *           leave once the data of every load of its group has arrived.
- * The CU's requests (load requests and stores) are its issued wavefront
- * requests, in program order; request k may be issued only once request
- * k - W is done (its data arrived / the store arrived): at most W
- * outstanding, retired in order.  Program order itself comes from the
- * network: all of a CU's requests leave through its one link, in id order.
- * Line a of space s lives on channel space_ch[s * n_ch + a mod n_ch].
+ *   store = one line (CU -> the channel of the destination line).
+ * The CU's requests (load requests, stores, releases, acquire requests) are
+ * its issued wavefront requests, in program order; request k may be issued
+ * only once request k - W is done (its data or reply arrived / the store
+ * arrived): at most W outstanding, retired in order.  Program order itself
+ * comes from the network: all of a CU's requests leave through its one
+ * link, in id order.  Line a of space s lives on channel
+ * space_ch[s * n_ch + a mod n_ch].  Each semaphore (space, line) is released
+ * by exactly one RELEASE; every ACQUIRE names a released semaphore.
  * Ids are step-major: for issue index k = 0, 1, ... and the CUs in ascending
- * endpoint order, a load takes two ids (request, then data), a store one.
- * A load request is a control message (class 1); data lines and stores are
- * data (class 0). */
-typedef struct { int kind; int32_t chan; int64_t g0, gn; } minstr_t;   /* kind 0 load, 1 store */
+ * endpoint order, a load or acquire takes two ids (request, then data or
+ * reply), a store or release one.  Data lines and stores are data (class
+ * 0); load requests and everything of a release or acquire are control
+ * (class 1). */
+enum { IN_LOAD = 0, IN_STORE = 1, IN_RELEASE = 2, IN_ACQUIRE = 3 };
+typedef struct {
+    int kind;
+    int32_t chan;
+    int64_t g0, gn;      /* store: the loads [g0, g0 + gn) of its group */
+    int32_t sem_sp;      /* release / acquire: the semaphore */
+    int64_t sem_ln;
+} minstr_t;
+typedef struct { int32_t sp; int64_t ln; int32_t q; int64_t k; } sem_t;
 
-int oracle_memcpy(int64_t n_ops, const int32_t *cu, const int32_t *ssp, const int32_t *dsp,
-                  const int64_t *sline, const int64_t *dline, const int64_t *nlines,
-                  int32_t n_spaces, int32_t n_ch, const int32_t *space_ch, int32_t U, int32_t W,
-                  int64_t cap_txn, int64_t cap_pred, int32_t *src, int32_t *dst,
-                  int64_t *pred_ptr, int64_t *pred_idx, uint8_t *cls, int64_t *T_out, int64_t *P_out)
+static int sem_cmp(const void *a, const void *b)
 {
-    if (n_ops < 0 || n_ch < 1 || n_spaces < 1 || U < 1 || W < 1) return OR_ERR_INVALID_ARG;
+    const sem_t *x = a, *y = b;
+    if (x->sp != y->sp) return x->sp < y->sp ? -1 : 1;
+    return x->ln < y->ln ? -1 : x->ln > y->ln;
+}
+
+int oracle_gpu_ops(int64_t n_ops, const int32_t *kind, const int32_t *cu, const int64_t *src_ptr,
+                   const int32_t *ssp, const int64_t *sline, const int32_t *dsp, const int64_t *dline,
+                   const int64_t *nlines, int32_t n_spaces, int32_t n_ch, const int32_t *space_ch, int32_t U,
+                   int32_t W, int64_t cap_txn, int64_t cap_pred, int32_t *src, int32_t *dst,
+                   int64_t *pred_ptr, int64_t *pred_idx, uint8_t *cls, int64_t *T_out, int64_t *P_out)
+{
+    if (n_ops < 0 || n_ch < 1 || n_spaces < 1 || U < 1 || W < 1 || src_ptr[0] != 0) return OR_ERR_INVALID_ARG;
+    #define CHAN(s, a) space_ch[(int64_t)(s) * n_ch + (a) % n_ch]
+    for (int64_t o = 0; o < n_ops; o++) {
+        int64_t K = src_ptr[o + 1] - src_ptr[o];
+        if (K < 0 || dsp[o] < 0 || dsp[o] >= n_spaces || dline[o] < 0 || nlines[o] < 0) return OR_ERR_INVALID_ARG;
+        if (kind[o] == 0) {
+            if (K < 1) return OR_ERR_INVALID_ARG;
+            for (int64_t s = src_ptr[o]; s < src_ptr[o + 1]; s++)
+                if (ssp[s] < 0 || ssp[s] >= n_spaces || sline[s] < 0) return OR_ERR_INVALID_ARG;
+        } else if (kind[o] == 1 || kind[o] == 2) {
+            if (K != 0 || nlines[o] != 1) return OR_ERR_INVALID_ARG;
+        } else {
+            return OR_ERR_INVALID_ARG;
+        }
+    }
     /* the CUs, ascending */
     int32_t *cus = malloc(sizeof(int32_t) * (size_t)(n_ops > 0 ? n_ops : 1));
     int32_t ncu = 0;
     for (int64_t o = 0; o < n_ops; o++) {
-        if (ssp[o] < 0 || ssp[o] >= n_spaces || dsp[o] < 0 || dsp[o] >= n_spaces || nlines[o] < 0 ||
-            sline[o] < 0 || dline[o] < 0) { free(cus); return OR_ERR_INVALID_ARG; }
         int found = 0;
         for (int32_t q = 0; q < ncu; q++) found |= cus[q] == cu[o];
         if (!found) cus[ncu++] = cu[o];
@@ -644,75 +689,126 @@ int oracle_memcpy(int64_t n_ops, const int32_t *cu, const int32_t *ssp, const in
     /* each CU's program */
     minstr_t **prog = calloc((size_t)(ncu > 0 ? ncu : 1), sizeof(minstr_t *));
     int64_t *plen = calloc((size_t)(ncu > 0 ? ncu : 1), sizeof(int64_t));
-    int64_t kmax = 0;
+    int64_t kmax = 0, nrel = 0;
+    int rc = OR_OK;
     for (int32_t q = 0; q < ncu; q++) {
         int64_t len = 0;
-        for (int64_t o = 0; o < n_ops; o++) if (cu[o] == cus[q]) len += 2 * nlines[o];
+        for (int64_t o = 0; o < n_ops; o++)
+            if (cu[o] == cus[q]) len += kind[o] == 0 ? (src_ptr[o + 1] - src_ptr[o] + 1) * nlines[o] : 1;
         prog[q] = malloc(sizeof(minstr_t) * (size_t)(len > 0 ? len : 1));
         int64_t k = 0;
         for (int64_t o = 0; o < n_ops; o++) {
             if (cu[o] != cus[q]) continue;
+            if (kind[o] != 0) {
+                prog[q][k++] = (minstr_t){kind[o] == 1 ? IN_RELEASE : IN_ACQUIRE, CHAN(dsp[o], dline[o]), 0, 0,
+                                          dsp[o], dline[o]};
+                nrel += kind[o] == 1;
+                continue;
+            }
             for (int64_t j0 = 0; j0 < nlines[o]; j0 += U) {
                 int64_t gn = nlines[o] - j0 < U ? nlines[o] - j0 : U;
                 int64_t g0 = k;                       /* first load of the group */
-                for (int64_t j = j0; j < j0 + gn; j++) {
-                    int64_t a = sline[o] + j;
-                    prog[q][k++] = (minstr_t){0, space_ch[(int64_t)ssp[o] * n_ch + a % n_ch], g0, gn};
-                }
-                for (int64_t j = j0; j < j0 + gn; j++) {
-                    int64_t a = dline[o] + j;
-                    prog[q][k++] = (minstr_t){1, space_ch[(int64_t)dsp[o] * n_ch + a % n_ch], g0, gn};
-                }
+                for (int64_t s = src_ptr[o]; s < src_ptr[o + 1]; s++)
+                    for (int64_t j = j0; j < j0 + gn; j++)
+                        prog[q][k++] = (minstr_t){IN_LOAD, CHAN(ssp[s], sline[s] + j), 0, 0, -1, -1};
+                int64_t nload = k - g0;               /* K gn loads */
+                for (int64_t j = j0; j < j0 + gn; j++)
+                    prog[q][k++] = (minstr_t){IN_STORE, CHAN(dsp[o], dline[o] + j), g0, nload, -1, -1};
             }
         }
         plen[q] = k;
         if (k > kmax) kmax = k;
+        for (int64_t j = 0; j < k; j++)
+            if (prog[q][j].chan == cus[q]) rc = OR_ERR_INVALID_ARG;   /* a line to itself */
     }
+    /* the releases, sorted by semaphore: one each */
+    sem_t *rel = malloc(sizeof(sem_t) * (size_t)(nrel > 0 ? nrel : 1));
+    int64_t nr = 0;
+    for (int32_t q = 0; q < ncu; q++)
+        for (int64_t k = 0; k < plen[q]; k++)
+            if (prog[q][k].kind == IN_RELEASE) rel[nr++] = (sem_t){prog[q][k].sem_sp, prog[q][k].sem_ln, q, k};
+    qsort(rel, (size_t)nr, sizeof(sem_t), sem_cmp);
+    for (int64_t r = 1; r < nr; r++)
+        if (sem_cmp(&rel[r - 1], &rel[r]) == 0) rc = OR_ERR_INVALID_ARG;
     /* ids: first id of every instruction */
     int64_t **id = calloc((size_t)(ncu > 0 ? ncu : 1), sizeof(int64_t *));
     for (int32_t q = 0; q < ncu; q++) id[q] = malloc(sizeof(int64_t) * (size_t)(plen[q] > 0 ? plen[q] : 1));
+    #define TWO(in) ((in)->kind == IN_LOAD || (in)->kind == IN_ACQUIRE)
     int64_t T = 0;
     for (int64_t k = 0; k < kmax; k++)
         for (int32_t q = 0; q < ncu; q++)
-            if (k < plen[q]) { id[q][k] = T; T += prog[q][k].kind == 0 ? 2 : 1; }
+            if (k < plen[q]) { id[q][k] = T; T += TWO(&prog[q][k]) ? 2 : 1; }
     /* the line that marks instruction k of CU q done */
-    #define DONE(q, k) (prog[q][k].kind == 0 ? id[q][k] + 1 : id[q][k])
+    #define DONE(q, k) (TWO(&prog[q][k]) ? id[q][k] + 1 : id[q][k])
     int64_t P = 0;
-    int rc = OR_OK;
     if (T >= (int64_t)0xFFFFFFFF) rc = OR_ERR_SIZE;
+    int64_t *pl = malloc(sizeof(int64_t) * (size_t)(kmax + 2));   /* one line's predecessors */
     for (int64_t k = 0; k < kmax && rc == OR_OK; k++)
-        for (int32_t q = 0; q < ncu; q++) {
+        for (int32_t q = 0; q < ncu && rc == OR_OK; q++) {
             if (k >= plen[q]) continue;
             const minstr_t *in = &prog[q][k];
             int64_t x = id[q][k];
-            /* the issued line: request (load) or store */
-            int64_t np = (k >= W ? 1 : 0) + (in->kind == 1 ? in->gn : 0);
-            int64_t need = np + (in->kind == 0 ? 1 : 0);
+            /* the issued line's predecessors, each once */
+            int64_t np = 0;
+            if (k >= W) pl[np++] = DONE(q, k - W);
+            if (k >= 1 && prog[q][k - 1].kind == IN_ACQUIRE && !(k >= W && W == 1))
+                pl[np++] = DONE(q, k - 1);               /* after an acquire: its reply */
+            if (in->kind == IN_STORE)
+                for (int64_t g = in->g0; g < in->g0 + in->gn; g++) pl[np++] = id[q][g] + 1;
+            if (in->kind == IN_RELEASE)                  /* stores back to the previous release, inclusive */
+                for (int64_t j = k - 1; j >= 0; j--) {
+                    if (prog[q][j].kind == IN_STORE || prog[q][j].kind == IN_RELEASE) pl[np++] = id[q][j];
+                    if (prog[q][j].kind == IN_RELEASE) break;
+                }
+            if (in->kind == IN_ACQUIRE) {
+                sem_t key = {in->sem_sp, in->sem_ln, 0, 0};
+                const sem_t *r = nr ? bsearch(&key, rel, (size_t)nr, sizeof(sem_t), sem_cmp) : NULL;
+                if (!r) { rc = OR_ERR_INVALID_ARG; break; }
+                pl[np++] = id[r->q][r->k];
+            }
+            int64_t need = np + (TWO(in) ? 1 : 0);
             if (cap_txn >= T && cap_pred >= P + need) {
                 src[x] = cus[q];
                 dst[x] = in->chan;
-                if (cls) cls[x] = in->kind == 0 ? 1 : 0;   /* a load request is a control message */
+                if (cls) cls[x] = in->kind == IN_STORE ? 0 : 1;
                 pred_ptr[x] = P;
-                int64_t w = P;
-                if (k >= W) pred_idx[w++] = DONE(q, k - W);
-                if (in->kind == 1)
-                    for (int64_t g = in->g0; g < in->g0 + in->gn; g++) pred_idx[w++] = id[q][g] + 1;
-                pred_ptr[x + 1] = w;
-                if (in->kind == 0) {       /* the data line: waits for its request */
+                for (int64_t i = 0; i < np; i++) pred_idx[P + i] = pl[i];
+                pred_ptr[x + 1] = P + np;
+                if (TWO(in)) {       /* the data line or reply: waits for its request */
                     src[x + 1] = in->chan;
                     dst[x + 1] = cus[q];
-                    if (cls) cls[x + 1] = 0;
-                    pred_idx[w++] = x;
-                    pred_ptr[x + 2] = w;
+                    if (cls) cls[x + 1] = in->kind == IN_LOAD ? 0 : 1;
+                    pred_idx[P + np] = x;
+                    pred_ptr[x + 2] = P + np + 1;
                 }
             }
             P += need;
         }
     #undef DONE
+    #undef TWO
+    #undef CHAN
     if (T_out) *T_out = T;
     if (P_out) *P_out = P;
     for (int32_t q = 0; q < ncu; q++) { free(prog[q]); free(id[q]); }
-    free(prog); free(id); free(plen); free(cus);
+    free(prog); free(id); free(plen); free(cus); free(rel); free(pl);
+    return rc;
+}
+
+/* memcpy programs: every operation a COPY from one source. */
+int oracle_memcpy(int64_t n_ops, const int32_t *cu, const int32_t *ssp, const int32_t *dsp,
+                  const int64_t *sline, const int64_t *dline, const int64_t *nlines,
+                  int32_t n_spaces, int32_t n_ch, const int32_t *space_ch, int32_t U, int32_t W,
+                  int64_t cap_txn, int64_t cap_pred, int32_t *src, int32_t *dst,
+                  int64_t *pred_ptr, int64_t *pred_idx, uint8_t *cls, int64_t *T_out, int64_t *P_out)
+{
+    if (n_ops < 0) return OR_ERR_INVALID_ARG;
+    int32_t *kind = calloc((size_t)(n_ops > 0 ? n_ops : 1), sizeof(int32_t));
+    int64_t *sp = malloc(sizeof(int64_t) * (size_t)(n_ops + 1));
+    for (int64_t o = 0; o <= n_ops; o++) sp[o] = o;
+    int rc = oracle_gpu_ops(n_ops, kind, cu, sp, ssp, sline, dsp, dline, nlines, n_spaces, n_ch, space_ch, U, W,
+                            cap_txn, cap_pred, src, dst, pred_ptr, pred_idx, cls, T_out, P_out);
+    free(kind);
+    free(sp);
     return rc;
 }
 

@@ -1371,49 +1371,93 @@ sim_status load_transactions_impl(sim_ctx *c, int64_t n, const int32_t *src, con
     return finish_load(c, R);
 }
 
-sim_status load_memcpy_impl(sim_ctx *c, int64_t n_ops, const int32_t *cu, const int32_t *src_space,
-                           const int32_t *dst_space, const int64_t *src_line, const int64_t *dst_line,
-                           const int64_t *n_lines, int32_t n_spaces, int32_t n_ch, const int32_t *space_ch,
-                           int32_t unroll, int32_t window) {
-    if (!c || n_ops < 0 || n_spaces < 1 || n_ch < 1 || !space_ch || unroll < 1 || window < 1 ||
-        (n_ops > 0 && (!cu || !src_space || !dst_space || !src_line || !dst_line || !n_lines)))
-        return c ? fail(c, SIM_ERR_INVALID_ARG, "memcpy: null array or bad n_spaces/n_ch/unroll/window")
+// GPU programs (copies with one or more sources, releases, acquires) turned
+// into lines; the rules are those of sim_load_gpu_ops.
+sim_status load_gpu_ops_impl(sim_ctx *c, int64_t n_ops, const int32_t *kind, const int32_t *cu,
+                             const int64_t *src_ptr, const int32_t *src_space, const int64_t *src_line,
+                             const int32_t *dst_space, const int64_t *dst_line, const int64_t *n_lines,
+                             int32_t n_spaces, int32_t n_ch, const int32_t *space_ch, int32_t unroll,
+                             int32_t window) {
+    if (!c || n_ops < 0 || n_spaces < 1 || n_ch < 1 || !space_ch || unroll < 1 || window < 1 || !src_ptr ||
+        (n_ops > 0 && (!kind || !cu || !dst_space || !dst_line || !n_lines)))
+        return c ? fail(c, SIM_ERR_INVALID_ARG, "gpu ops: null array or bad n_spaces/n_ch/unroll/window")
                  : SIM_ERR_INVALID_ARG;
+    if (src_ptr[0] != 0) return fail(c, SIM_ERR_INVALID_ARG, "gpu ops: src_ptr[0] must be 0");
+    if (n_ops > 0 && src_ptr[n_ops] > 0 && (!src_space || !src_line))
+        return fail(c, SIM_ERR_INVALID_ARG, "gpu ops: null source arrays");
     for (int64_t q = 0; q < (int64_t)n_spaces * n_ch; q++)
-        if (space_ch[q] < 0 || space_ch[q] >= c->E) return fail(c, SIM_ERR_INVALID_ARG, "memcpy: channel is not an endpoint");
-    // One wavefront request of a CU's program: a load (request + data) or a
-    // store waiting for the data of loads [g0, g0 + gn) of the same program.
+        if (space_ch[q] < 0 || space_ch[q] >= c->E) return fail(c, SIM_ERR_INVALID_ARG, "gpu ops: channel is not an endpoint");
+    enum : uint8_t { kLoad, kStore, kRelease, kAcquire };
+    // One wavefront request of a CU's program.  A store waits for the data of
+    // loads [g0, g0 + gn) of the same program; a release or acquire names its
+    // semaphore by its index in `sems`.
     struct Req {
-        bool store;
+        uint8_t what;
         int32_t chan;
         int64_t g0;
-        int32_t gn;
+        int64_t gn;
     };
-    std::map<int32_t, std::vector<Req>> prog;  // by CU, ascending
+    auto two = [](const Req &r) { return r.what == kLoad || r.what == kAcquire; };
+    std::map<std::pair<int32_t, int64_t>, std::pair<int32_t, int64_t>> rel_at;  // semaphore -> (CU, index)
+    std::map<int32_t, std::vector<Req>> prog;                                     // by CU, ascending
+    std::vector<std::pair<int32_t, int64_t>> sems;                                // acquires' semaphores
     uint64_t lines = 0;
+    auto chan_of = [&](int32_t s, int64_t a) { return space_ch[(int64_t)s * n_ch + a % n_ch]; };
     for (int64_t o = 0; o < n_ops; o++) {
-        if (cu[o] < 0 || cu[o] >= c->E) return fail(c, SIM_ERR_INVALID_ARG, "memcpy: CU is not an endpoint");
-        if (src_space[o] < 0 || src_space[o] >= n_spaces || dst_space[o] < 0 || dst_space[o] >= n_spaces ||
-            n_lines[o] < 0 || src_line[o] < 0 || dst_line[o] < 0)
-            return fail(c, SIM_ERR_INVALID_ARG, "memcpy: operation " + std::to_string(o) + " out of range");
-        lines += 3 * (uint64_t)n_lines[o];
-        if (lines >= 0xFFFFFFFFull) return fail(c, SIM_ERR_SIZE, "more than 2^32-2 transactions");
+        const std::string where = "gpu ops: operation " + std::to_string(o);
+        const int64_t K = src_ptr[o + 1] - src_ptr[o];
+        if (cu[o] < 0 || cu[o] >= c->E) return fail(c, SIM_ERR_INVALID_ARG, where + ": CU is not an endpoint");
+        if (K < 0 || dst_space[o] < 0 || dst_space[o] >= n_spaces || dst_line[o] < 0 || n_lines[o] < 0)
+            return fail(c, SIM_ERR_INVALID_ARG, where + " out of range");
         auto &pr = prog[cu[o]];
         const int64_t first = (int64_t)pr.size();
-        const int32_t *sch = space_ch + (int64_t)src_space[o] * n_ch;
-        const int32_t *dch = space_ch + (int64_t)dst_space[o] * n_ch;
-        for (int64_t j0 = 0; j0 < n_lines[o]; j0 += unroll) {
-            const int32_t gn = (int32_t)std::min<int64_t>(unroll, n_lines[o] - j0);
-            const int64_t g0 = (int64_t)pr.size();
-            for (int32_t u = 0; u < gn; u++) pr.push_back({false, sch[(src_line[o] + j0 + u) % n_ch], g0, gn});
-            for (int32_t u = 0; u < gn; u++) pr.push_back({true, dch[(dst_line[o] + j0 + u) % n_ch], g0, gn});
+        if (kind[o] == SIM_OP_RELEASE || kind[o] == SIM_OP_ACQUIRE) {
+            if (K != 0 || n_lines[o] != 1)
+                return fail(c, SIM_ERR_INVALID_ARG, where + ": a release or acquire has no source and one line");
+            const auto sem = std::make_pair(dst_space[o], dst_line[o]);
+            if (kind[o] == SIM_OP_RELEASE) {
+                if (!rel_at.emplace(sem, std::make_pair(cu[o], first)).second)
+                    return fail(c, SIM_ERR_INVALID_ARG, where + ": semaphore released twice");
+                pr.push_back({kRelease, chan_of(sem.first, sem.second), -1, 0});
+                lines += 1;
+            } else {
+                pr.push_back({kAcquire, chan_of(sem.first, sem.second), (int64_t)sems.size(), 0});
+                sems.push_back(sem);
+                lines += 2;
+            }
+        } else if (kind[o] == SIM_OP_COPY) {
+            if (K < 1) return fail(c, SIM_ERR_INVALID_ARG, where + ": a copy needs a source");
+            for (int64_t s = src_ptr[o]; s < src_ptr[o + 1]; s++)
+                if (src_space[s] < 0 || src_space[s] >= n_spaces || src_line[s] < 0)
+                    return fail(c, SIM_ERR_INVALID_ARG, where + ": source out of range");
+            lines += (uint64_t)(2 * K + 1) * (uint64_t)n_lines[o];
+            if (lines >= 0xFFFFFFFFull) return fail(c, SIM_ERR_SIZE, "more than 2^32-2 transactions");
+            for (int64_t j0 = 0; j0 < n_lines[o]; j0 += unroll) {
+                const int64_t gn = std::min<int64_t>(unroll, n_lines[o] - j0);
+                const int64_t g0 = (int64_t)pr.size();
+                for (int64_t s = src_ptr[o]; s < src_ptr[o + 1]; s++)
+                    for (int64_t u = 0; u < gn; u++) pr.push_back({kLoad, chan_of(src_space[s], src_line[s] + j0 + u), 0, 0});
+                const int64_t nl = (int64_t)pr.size() - g0;
+                for (int64_t u = 0; u < gn; u++) pr.push_back({kStore, chan_of(dst_space[o], dst_line[o] + j0 + u), g0, nl});
+            }
+        } else {
+            return fail(c, SIM_ERR_INVALID_ARG, where + ": unknown kind " + std::to_string(kind[o]));
         }
+        if (lines >= 0xFFFFFFFFull) return fail(c, SIM_ERR_SIZE, "more than 2^32-2 transactions");
         for (int64_t q = first; q < (int64_t)pr.size(); q++)
-            if (pr[q].chan == cu[o]) return fail(c, SIM_ERR_INVALID_ARG, "memcpy: a CU is the channel of its own line");
+            if (pr[q].chan == cu[o]) return fail(c, SIM_ERR_INVALID_ARG, where + ": a CU is the channel of its own line");
     }
+    for (const auto &s : sems)
+        if (!rel_at.count(s))
+            return fail(c, SIM_ERR_INVALID_ARG, "gpu ops: acquire of semaphore (" + std::to_string(s.first) + ", " +
+                                                    std::to_string(s.second) + ") that nothing releases");
     // ids, step-major over the CUs
     std::vector<std::pair<int32_t, std::vector<Req> *>> cus;
-    for (auto &kv : prog) cus.push_back({kv.first, &kv.second});
+    std::map<int32_t, size_t> cu_row;
+    for (auto &kv : prog) {
+        cu_row[kv.first] = cus.size();
+        cus.push_back({kv.first, &kv.second});
+    }
     std::vector<std::vector<int64_t>> id(cus.size());
     size_t kmax = 0;
     for (size_t q = 0; q < cus.size(); q++) {
@@ -1425,9 +1469,13 @@ sim_status load_memcpy_impl(sim_ctx *c, int64_t n_ops, const int32_t *cu, const 
         for (size_t q = 0; q < cus.size(); q++)
             if (k < cus[q].second->size()) {
                 id[q][k] = T;
-                T += (*cus[q].second)[k].store ? 1 : 2;
+                T += two((*cus[q].second)[k]) ? 2 : 1;
             }
-    // one range per line (consecutive ids belong to different CUs)
+    auto done = [&](size_t q, size_t k) { return id[q][k] + (two((*cus[q].second)[k]) ? 1 : 0); };
+    // Per CU: the latest store or release per channel since the CU's last
+    // release.  Lines of one (CU, channel) pair share a path, so they complete
+    // in id order and the latest one stands for all of them.
+    std::vector<std::map<int32_t, int64_t>> pending(cus.size());
     Ranges R;
     int64_t next = 0;
     for (size_t k = 0; k < kmax; k++)
@@ -1436,25 +1484,45 @@ sim_status load_memcpy_impl(sim_ctx *c, int64_t n_ops, const int32_t *cu, const 
             if (k >= pr.size()) continue;
             const Req &r = pr[k];
             const int64_t x = id[q][k];
-            if (x != next) return fail(c, SIM_ERR_INVALID_ARG, "internal: memcpy ids not dense");
+            if (x != next) return fail(c, SIM_ERR_INVALID_ARG, "internal: gpu op ids not dense");
             R.add((uint64_t)x, 1, cus[q].first, r.chan, (int64_t)k, 0);
-            if (k >= (size_t)window) {
-                const size_t kd = k - (size_t)window;  // retired before this request is issued
-                R.pred(id[q][kd] + (pr[kd].store ? 0 : 1), 0);
-            }
-            if (r.store)
+            if (k >= (size_t)window) R.pred(done(q, k - (size_t)window), 0);  // retired before this one issues
+            if (k >= 1 && pr[k - 1].what == kAcquire && window != 1) R.pred(done(q, k - 1), 0);
+            if (r.what == kStore)
                 for (int64_t g = r.g0; g < r.g0 + r.gn; g++) R.pred(id[q][g] + 1, 0);
+            if (r.what == kRelease) {
+                for (const auto &kv : pending[q]) R.pred(kv.second, 0);
+                pending[q].clear();
+            }
+            if (r.what == kStore || r.what == kRelease) pending[q][r.chan] = x;
+            if (r.what == kAcquire) {
+                const auto &at = rel_at[sems[(size_t)r.g0]];
+                R.pred(id[cu_row[at.first]][(size_t)at.second], 0);
+            }
+            R.cls.push_back(r.what == kStore ? 0 : 1);
             next = x + 1;
-            R.cls.push_back(r.store ? 0 : 1);  // a load request is a control message
-            if (!r.store) {  // the data line
+            if (two(r)) {  // the data line or reply
                 R.add((uint64_t)x + 1, 1, r.chan, cus[q].first, (int64_t)k, 1);
                 R.pred(x, 0);
-                R.cls.push_back(0);
+                R.cls.push_back(r.what == kLoad ? 0 : 1);
                 next = x + 2;
             }
         }
     R.close();
     return finish_load(c, R);
+}
+
+sim_status load_memcpy_impl(sim_ctx *c, int64_t n_ops, const int32_t *cu, const int32_t *src_space,
+                           const int32_t *dst_space, const int64_t *src_line, const int64_t *dst_line,
+                           const int64_t *n_lines, int32_t n_spaces, int32_t n_ch, const int32_t *space_ch,
+                           int32_t unroll, int32_t window) {
+    if (!c || n_ops < 0 || (n_ops > 0 && (!src_space || !src_line)))
+        return c ? fail(c, SIM_ERR_INVALID_ARG, "memcpy: null array or negative n_ops") : SIM_ERR_INVALID_ARG;
+    std::vector<int32_t> kinds((size_t)n_ops, SIM_OP_COPY);
+    std::vector<int64_t> sp((size_t)n_ops + 1);
+    for (int64_t o = 0; o <= n_ops; o++) sp[(size_t)o] = o;
+    return load_gpu_ops_impl(c, n_ops, kinds.data(), cu, sp.data(), src_space, src_line, dst_space, dst_line,
+                             n_lines, n_spaces, n_ch, space_ch, unroll, window);
 }
 
 
@@ -1624,6 +1692,13 @@ sim_status sim_load_memcpy(sim_ctx *c, int64_t n_ops, const int32_t *cu, const i
                            const int64_t *n_lines, int32_t n_spaces, int32_t n_ch, const int32_t *space_ch,
                            int32_t unroll, int32_t window) {
     return guarded(c, [&] { return load_memcpy_impl(c, n_ops, cu, src_space, dst_space, src_line, dst_line, n_lines, n_spaces, n_ch, space_ch, unroll, window); });
+}
+
+sim_status sim_load_gpu_ops(sim_ctx *c, int64_t n_ops, const int32_t *kind, const int32_t *cu,
+                            const int64_t *src_ptr, const int32_t *src_space, const int64_t *src_line,
+                            const int32_t *dst_space, const int64_t *dst_line, const int64_t *n_lines,
+                            int32_t n_spaces, int32_t n_ch, const int32_t *space_ch, int32_t unroll, int32_t window) {
+    return guarded(c, [&] { return load_gpu_ops_impl(c, n_ops, kind, cu, src_ptr, src_space, src_line, dst_space, dst_line, n_lines, n_spaces, n_ch, space_ch, unroll, window); });
 }
 
 sim_status sim_run(sim_ctx *c, void *stream, uint32_t *d_completion, uint64_t *d_tx_lines,

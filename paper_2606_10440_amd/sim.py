@@ -1,7 +1,7 @@
 """Thin ctypes binding of libsimgpu (argument marshalling only).
 
 Functions keep the C ABI's names (``sim_create``, ``sim_set_credit``, ``sim_load_collective``,
-``sim_load_transactions``, ``sim_load_memcpy``, ``sim_sizes``, ``sim_run``,
+``sim_load_transactions``, ``sim_load_memcpy``, ``sim_load_gpu_ops``, ``sim_sizes``, ``sim_run``,
 ``sim_status_after_sync``, ``sim_route``, ``sim_txn_info``, ``sim_last_error``,
 ``sim_destroy``); ``Simulator`` bundles them with torch device buffers and
 the current HIP stream.  Every step of the simulation runs in the library's
@@ -25,7 +25,7 @@ SIM_ERR_OOM, SIM_ERR_DEVICE, SIM_ERR_DEADLOCK, SIM_ERR_MAX_CYCLES, SIM_ERR_STATE
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "TOPOLOGY", 3: "UNREACHABLE", 4: "SIZE", 5: "OOM",
                 6: "DEVICE", 7: "DEADLOCK", 8: "MAX_CYCLES", 9: "STATE"}
 EXPORTS = ("sim_create", "sim_set_credit", "sim_load_collective", "sim_load_transactions", "sim_load_memcpy",
-           "sim_sizes", "sim_run", "sim_run_noalloc",
+           "sim_load_gpu_ops", "sim_sizes", "sim_run", "sim_run_noalloc",
            "sim_status_after_sync", "sim_route", "sim_txn_info", "sim_last_error", "sim_destroy")
 
 _lib = None
@@ -50,6 +50,7 @@ def lib():
         L.sim_load_collective.argtypes = [P, i32, u64, i32, P, i32]
         L.sim_load_transactions.argtypes = [P, i64, P, P, P, P]
         L.sim_load_memcpy.argtypes = [P, i64, P, P, P, P, P, P, C.c_int32, C.c_int32, P, C.c_int32, C.c_int32]
+        L.sim_load_gpu_ops.argtypes = [P, i64, P, P, P, P, P, P, P, P, i32, i32, P, i32, i32]
         L.sim_sizes.argtypes = [P, P, P, P, P]
         L.sim_run.argtypes = [P, P, P, P, P, P, u64]
         L.sim_run_noalloc.argtypes = [P, P, P, P, P, P, u64]
@@ -133,6 +134,28 @@ def sim_load_memcpy(ctx, cu, src_space, dst_space, src_line, dst_line, n_lines, 
     n_spaces = len(ch) // n_ch if n_ch > 0 else 0
     _check(ctx, lib().sim_load_memcpy(ctx, len(a32[0]), *(_ptr(v) for v in a32), *(_ptr(v) for v in a64),
                                       n_spaces, n_ch, _ptr(ch), unroll, window))
+
+
+SIM_OP_COPY, SIM_OP_RELEASE, SIM_OP_ACQUIRE = 0, 1, 2
+
+
+def sim_load_gpu_ops(ctx, kind, cu, src_ptr, src_space, src_line, dst_space, dst_line, n_lines, space_channels,
+                     n_ch, unroll, window):
+    k32 = [np.ascontiguousarray(v, np.int32) for v in (kind, cu)]
+    sp = np.ascontiguousarray(src_ptr, np.int64)
+    ssp = np.ascontiguousarray(src_space, np.int32)
+    sln = np.ascontiguousarray(src_line, np.int64)
+    if ssp.size == 0:
+        ssp, sln = np.zeros(1, np.int32), np.zeros(1, np.int64)
+    dsp = np.ascontiguousarray(dst_space, np.int32)
+    a64 = [np.ascontiguousarray(v, np.int64) for v in (dst_line, n_lines)]
+    ch = np.ascontiguousarray(space_channels, np.int32)
+    n_spaces = len(ch) // n_ch if n_ch > 0 else 0
+    if len(sp) != len(k32[0]) + 1:
+        raise ValueError("src_ptr needs n_ops + 1 entries")
+    _check(ctx, lib().sim_load_gpu_ops(ctx, len(k32[0]), *(_ptr(v) for v in k32), _ptr(sp), _ptr(ssp), _ptr(sln),
+                                       _ptr(dsp), *(_ptr(v) for v in a64), n_spaces, n_ch, _ptr(ch), unroll,
+                                       window))
 
 
 def sim_sizes(ctx):
@@ -228,9 +251,15 @@ class Simulator:
         sim_load_transactions(self.ctx, src, dst, pred_ptr, pred_idx)
 
     def load_memcpy(self, mc):
-        """Memcpy programs (fields of ``sim_inputs.noc.Memcpy``)."""
-        sim_load_memcpy(self.ctx, mc.cu, mc.src_space, mc.dst_space, mc.src_line, mc.dst_line, mc.n_lines,
-                        mc.space_channels, mc.n_ch, mc.unroll, mc.window)
+        """GPU programs (fields of ``sim_inputs.noc.Memcpy``): plain memcpy
+        programs, or copies, reduces, releases and acquires when ``kind``
+        is set."""
+        if mc.kind is None:
+            sim_load_memcpy(self.ctx, mc.cu, mc.src_space, mc.dst_space, mc.src_line, mc.dst_line, mc.n_lines,
+                            mc.space_channels, mc.n_ch, mc.unroll, mc.window)
+        else:
+            sim_load_gpu_ops(self.ctx, mc.kind, mc.cu, mc.src_ptr, mc.src_space, mc.src_line, mc.dst_space,
+                             mc.dst_line, mc.n_lines, mc.space_channels, mc.n_ch, mc.unroll, mc.window)
 
     def sizes(self):
         return sim_sizes(self.ctx)

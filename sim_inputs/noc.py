@@ -53,22 +53,34 @@ class NocLayout:
     ports: np.ndarray      # [G, 32] node ids
 
 
+OP_COPY, OP_RELEASE, OP_ACQUIRE = 0, 1, 2
+
+
 @dataclass
 class Memcpy:
-    """Memcpy operations, each run by one CU in list order per CU.
+    """GPU operations, each run by one CU in list order per CU.
+
+    Without ``kind`` every operation is a memcpy from (src_space[o],
+    src_line[o]).  With ``kind`` (OP_COPY, OP_RELEASE, OP_ACQUIRE) and
+    ``src_ptr`` the sources of operation o are entries src_ptr[o] ..
+    src_ptr[o+1] - 1 of src_space / src_line: a copy has one or more (more
+    than one: a reduce into the destination), a release or acquire none and
+    names its semaphore line as the destination, with n_lines 1.
 
     Line a of address space s (a GPU's memory) lives on memory channel
     ``space_channels[s * n_ch + a % n_ch]``."""
-    cu: np.ndarray          # int32 [n_ops] endpoint executing the copy
-    src_space: np.ndarray   # int32 [n_ops]
+    cu: np.ndarray          # int32 [n_ops] endpoint executing the operation
+    src_space: np.ndarray   # int32 [n_ops] (or [src_ptr[-1]])
     dst_space: np.ndarray   # int32 [n_ops]
-    src_line: np.ndarray    # int64 [n_ops] first source line address
+    src_line: np.ndarray    # int64 [n_ops] (or [src_ptr[-1]]) first source line address
     dst_line: np.ndarray    # int64 [n_ops]
     n_lines: np.ndarray     # int64 [n_ops]
     space_channels: np.ndarray  # int32 [n_spaces * n_ch]
     n_ch: int
     unroll: int = 4
     window: int = 64
+    kind: np.ndarray | None = None     # int32 [n_ops]
+    src_ptr: np.ndarray | None = None  # int64 [n_ops + 1]
 
 
 def gpu_noc(n_gpus: int = 1, *, mesh=(8, 4), cus_per_router=4, ch_per_router=16, ports_per_router=4,
@@ -144,6 +156,20 @@ def _ops(rows, lay, unroll, window) -> Memcpy:
                   lay.channels.shape[1], unroll, window)
 
 
+def _prog(rows, lay, unroll, window) -> Memcpy:
+    """rows: (kind, cu, [(src_space, src_line), ...], dst_space, dst_line, n_lines)."""
+    kind = np.array([r[0] for r in rows], np.int32)
+    cu = np.array([r[1] for r in rows], np.int32)
+    sptr = np.zeros(len(rows) + 1, np.int64)
+    sptr[1:] = np.cumsum([len(r[2]) for r in rows])
+    srcs = [sl for r in rows for sl in r[2]]
+    ssp = np.array([a for a, _ in srcs], np.int32)
+    sln = np.array([b for _, b in srcs], np.int64)
+    return Memcpy(cu, ssp, np.array([r[3] for r in rows], np.int32), sln, np.array([r[4] for r in rows], np.int64),
+                  np.array([r[5] for r in rows], np.int64), _space_channels(lay), lay.channels.shape[1], unroll,
+                  window, kind, sptr)
+
+
 def wg_cu(lay: NocLayout, g: int, wg: int, n_wg: int) -> int:
     """CU of workgroup wg (of n_wg) on GPU g: spread over the routers first."""
     n_cu = lay.cus.shape[1]
@@ -175,6 +201,45 @@ def allgather_ops(lay: NocLayout, out_lines: int, n_wg: int = 32, unroll=4, wind
                 else:
                     rows.append((cu, g, h, wg * c, chunk + g * chunk + wg * c, c))
     return _ops(rows, lay, unroll, window)
+
+
+def reducescatter_ops(lay: NocLayout, in_lines: int, n_wg: int = 32, unroll=4, window=64, get=True) -> Memcpy:
+    """Reduce-scatter (Sec. 5.2): every GPU holds in_lines input lines at
+    address 0, in G chunks; GPU g ends with the sum of every GPU's chunk g in
+    its output (address in_lines).  The n_wg workgroups of a GPU split each
+    chunk into slices.
+
+    Get-based: workgroup w of GPU g reads its slice of chunk g from every GPU
+    (g first, then g+1, ...: local and remote loads) and stores the reduced
+    slice; no synchronisation.
+    Put-based: workgroup w of GPU g first copies its slice of chunk h to
+    GPU h's scratch slot g (address in_lines + chunk + g chunk; remote
+    stores) and releases the semaphore (h, w, from g) on GPU h, for the peers
+    h = g+1, g+2, ...; then it acquires its own semaphores from every peer
+    and reduces its input slice with the G - 1 received slices (local loads)
+    into its output.  Semaphore (h, w, from g) is line
+    2 in_lines + chunk + g n_wg + w of GPU h."""
+    G = lay.n_gpus
+    chunk = in_lines // G
+    assert chunk * G == in_lines and chunk % n_wg == 0
+    c = chunk // n_wg
+    out, scratch, sem = in_lines, in_lines + chunk, 2 * in_lines + chunk
+    rows = []
+    for g in range(G):
+        for w in range(n_wg):
+            cu = wg_cu(lay, g, w, n_wg)
+            peers = [(g + d) % G for d in range(1, G)]
+            if get:
+                rows.append((OP_COPY, cu, [((g + d) % G, g * chunk + w * c) for d in range(G)], g, out + w * c, c))
+                continue
+            for h in peers:
+                rows.append((OP_COPY, cu, [(g, h * chunk + w * c)], h, scratch + g * chunk + w * c, c))
+                rows.append((OP_RELEASE, cu, [], h, sem + g * n_wg + w, 1))
+            for h in peers:
+                rows.append((OP_ACQUIRE, cu, [], g, sem + h * n_wg + w, 1))
+            rows.append((OP_COPY, cu, [(g, g * chunk + w * c)] + [(g, scratch + h * chunk + w * c) for h in peers],
+                         g, out + w * c, c))
+    return _prog(rows, lay, unroll, window)
 
 
 def alltoall_ops(lay: NocLayout, pair_lines: int, n_wg: int = 32, unroll=4, window=64) -> Memcpy:

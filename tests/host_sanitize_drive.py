@@ -37,6 +37,10 @@ def exercise(w, txns=None, engine=None, pairs=64):
         try:
             if txns is not None:
                 sim.sim_load_transactions(ctx, *txns)
+            elif w.meta.get("memcpy") is not None and w.meta["memcpy"].kind is not None:
+                mc = w.meta["memcpy"]
+                sim.sim_load_gpu_ops(ctx, mc.kind, mc.cu, mc.src_ptr, mc.src_space, mc.src_line, mc.dst_space,
+                                     mc.dst_line, mc.n_lines, mc.space_channels, mc.n_ch, mc.unroll, mc.window)
             elif w.meta.get("memcpy") is not None:
                 mc = w.meta["memcpy"]
                 sim.sim_load_memcpy(ctx, mc.cu, mc.src_space, mc.dst_space, mc.src_line, mc.dst_line,
@@ -86,6 +90,13 @@ def main():
             n += 1
     exercise(si.config("C4"), None, None, pairs=512)
     n += 1
+    from sim_inputs import noc
+    w, lay = noc.gpu_noc(4, mesh=(2, 2), cus_per_router=2, ch_per_router=2, ports_per_router=1)
+    for get in (True, False):
+        mc = noc.reducescatter_ops(lay, 4 * 8 * 4, n_wg=8, unroll=3, window=7, get=get)
+        for engine in ENGINES:
+            exercise(noc.memcpy_workload(w, mc), None, engine)
+            n += 1
     print(f"host builder under sanitizers: {n} workloads ok", flush=True)
 
 

@@ -187,6 +187,84 @@ def test_memcpy_argument_errors(simlib):
         simlib.sim_destroy(ctx)
 
 
+def _load_ops(simlib, ctx, mc):
+    try:
+        simlib.sim_load_gpu_ops(ctx, mc.kind, mc.cu, mc.src_ptr, mc.src_space, mc.src_line, mc.dst_space,
+                                mc.dst_line, mc.n_lines, mc.space_channels, mc.n_ch, mc.unroll, mc.window)
+    except simlib.SimError as e:   # the expansion ran; there is no device here
+        assert e.status == simlib.SIM_ERR_DEVICE, e
+
+
+@pytest.mark.parametrize("case", ["get", "put", "rand0", "rand1", "rand2", "rand3"])
+def test_gpu_ops_expansion_matches_oracle(simlib, oracle_lib, case):
+    # every line's sender, receiver, issue index and part (request / reply)
+    # through sim_txn_info, against the oracle's expansion and the program
+    # model of the oracle pins
+    from sim_inputs import noc
+    from tests.test_oracle_gpu_ops import model, random_program
+    w, lay = noc.gpu_noc(3, mesh=(2, 2), cus_per_router=2, ch_per_router=2, ports_per_router=1)
+    if case in ("get", "put"):
+        mc = noc.reducescatter_ops(lay, 3 * 4 * 3, n_wg=4, unroll=2, window=5, get=case == "get")
+    else:
+        rng = np.random.default_rng(int(case[-1]))
+        mc = noc._prog(random_program(rng, lay.cus.reshape(-1)[:6], 3, 3), lay, int(rng.integers(1, 4)),
+                       int(rng.integers(1, 7)))
+    src, dst, _, _ = oracle_lib.memcpy_txns(mc)
+    _, _, _, _, what = model(mc)
+    ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, w.arb)
+    try:
+        _load_ops(simlib, ctx, mc)
+        with pytest.raises(simlib.SimError):   # one past the last line
+            simlib.sim_txn_info(ctx, len(src))
+        k = {}
+        for x in range(len(src)):
+            got = simlib.sim_txn_info(ctx, x)
+            reply = what[x].endswith("reply")
+            cu = got[1] if reply else got[0]
+            if not reply:
+                k[cu] = k.get(cu, -1) + 1
+            assert got == (int(src[x]), int(dst[x]), k[cu], int(reply)), (x, got)
+    finally:
+        simlib.sim_destroy(ctx)
+
+
+def test_gpu_ops_argument_errors(simlib):
+    from sim_inputs import noc
+    from sim_inputs.noc import OP_ACQUIRE, OP_COPY, OP_RELEASE
+    w, lay = noc.gpu_noc(1, mesh=(2, 2), cus_per_router=1, ch_per_router=2, ports_per_router=1)
+    c0, c1 = (int(v) for v in lay.cus[0][:2])
+    ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, w.arb)
+    good = [(OP_COPY, c0, [(0, 0), (0, 9)], 0, 20, 3), (OP_RELEASE, c0, [], 0, 40, 1), (OP_ACQUIRE, c1, [], 0, 40, 1)]
+    bad = [
+        [(OP_RELEASE, c0, [], 0, 3, 1), (OP_RELEASE, c1, [], 0, 3, 1)],
+        [(OP_ACQUIRE, c0, [], 0, 3, 1)],
+        [(OP_RELEASE, c0, [(0, 1)], 0, 3, 1)],
+        [(OP_ACQUIRE, c0, [], 0, 3, 0)],
+        [(OP_COPY, c0, [], 0, 3, 2)],
+        [(5, c0, [], 0, 3, 1)],
+        [(OP_COPY, c0, [(1, 0)], 0, 3, 2)],
+        [(OP_COPY, c0, [(0, -1)], 0, 3, 2)],
+    ]
+    try:
+        _load_ops(simlib, ctx, noc._prog(good, lay, 2, 4))
+        for rows in bad:
+            mc = noc._prog(rows, lay, 2, 4)
+            with pytest.raises(simlib.SimError) as e:
+                simlib.sim_load_gpu_ops(ctx, mc.kind, mc.cu, mc.src_ptr, mc.src_space, mc.src_line, mc.dst_space,
+                                        mc.dst_line, mc.n_lines, mc.space_channels, mc.n_ch, mc.unroll,
+                                        mc.window)
+            assert e.value.status == simlib.SIM_ERR_INVALID_ARG, rows
+        mc = noc._prog(good, lay, 2, 4)
+        sp = mc.src_ptr.copy()
+        sp[0] = 1
+        with pytest.raises(simlib.SimError) as e:
+            simlib.sim_load_gpu_ops(ctx, mc.kind, mc.cu, sp, mc.src_space, mc.src_line, mc.dst_space, mc.dst_line,
+                                    mc.n_lines, mc.space_channels, mc.n_ch, mc.unroll, mc.window)
+        assert e.value.status == simlib.SIM_ERR_INVALID_ARG
+    finally:
+        simlib.sim_destroy(ctx)
+
+
 def test_set_credit_errors(simlib):
     w = si.config("C1")
     ctx = simlib.sim_create(w.n_nodes, w.n_endpoints, w.row_ptr, w.col_idx, 1, w.bw, w.lat, w.cap, w.arb)

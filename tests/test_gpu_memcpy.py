@@ -84,3 +84,50 @@ def test_memcpy_exploration_points(simmod, oracle_lib, kind, size, U, W):
     wm = noc.memcpy_workload(w, mc, name=f"two_gpu_{kind}_{size}_U{U}_W{W}")
     say(wm.name)
     check_vs_oracle(simmod, oracle_lib, wm)
+
+
+# ------------------------------------------- reduces, releases and acquires
+
+def tiny_ops(seed):
+    from tests.test_oracle_gpu_ops import random_program
+    w, lay = noc.gpu_noc(1, mesh=(2, 2), cus_per_router=2, ch_per_router=2, ports_per_router=1,
+                         noc=(4, 1, 8), cu_out=(2, 1, 4), mem=(1, 2, 3))
+    rng = np.random.default_rng(500 + seed)
+    rows = random_program(rng, lay.cus[0], 1, int(rng.integers(1, 4)))
+    mc = noc._prog(rows, lay, int(rng.integers(1, 5)), int(rng.integers(1, 9)))
+    wm = noc.memcpy_workload(w, mc, name=f"tiny_ops_{seed}")
+    wm.arb = seed % 2
+    return wm
+
+
+@pytest.mark.parametrize("engine", ENGINES)
+@pytest.mark.parametrize("seed", range(8))
+def test_gpu_ops_tiny_noc(simmod, oracle_lib, engine, seed):
+    """Random programs of copies, reduces, releases and acquires (some of
+    them deadlock: both sides must say so at the same point)."""
+    w = tiny_ops(seed)
+    if engine == "b1":
+        w.bw[:] = 1
+        w.cap[:] = np.maximum(w.cap, 2 * (w.lat + 1))
+    check_engine(simmod, oracle_lib, w, engine)
+
+
+@pytest.mark.parametrize("get", [True, False])
+@pytest.mark.parametrize("G", [2, 4])
+def test_reducescatter_generic_gpu(simmod, oracle_lib, G, get):
+    """Get- and put-based reduce-scatter (Sec. 5.2) on G generic GPUs, 32
+    workgroups per GPU, two lines per workgroup slice."""
+    w, lay = noc.gpu_noc(G)
+    mc = noc.reducescatter_ops(lay, G * 32 * 2, n_wg=32, get=get)
+    wm = noc.memcpy_workload(w, mc, name=f"rs_{'get' if get else 'put'}_G{G}")
+    say(wm.name)
+    check_vs_oracle(simmod, oracle_lib, wm)
+
+
+@pytest.mark.parametrize("engine", ["workgroup", "workgroup_scan", "lane", "lanehbm"])
+@pytest.mark.parametrize("get", [True, False])
+def test_reducescatter_engines(simmod, oracle_lib, engine, get):
+    w, lay = noc.gpu_noc(3, mesh=(2, 2), cus_per_router=2, ch_per_router=2, ports_per_router=1)
+    mc = noc.reducescatter_ops(lay, 3 * 8 * 3, n_wg=8, unroll=2, window=6, get=get)
+    wm = noc.with_scenarios(noc.memcpy_workload(w, mc, name=f"rs_small_{int(get)}"), 4, seed=11)
+    check_engine(simmod, oracle_lib, wm, engine)
