@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libsimgpu.so")
 CSRC = os.path.join(HERE, "csrc")
 SOURCES = ["api.cpp", "engine_launch.cpp", "engine_wg.hip", "engine_lane.hip", "engine_b1.hip",
-           "engine_wave.hip", "noalloc.hip"]
+           "engine_wave.hip", "engine_grid.hip", "noalloc.hip"]
 ARCH = os.environ.get("SIMGPU_ARCH", "gfx950")
 OBJDIR = os.path.join(ROOT, "_build", "simgpu")
 

@@ -431,6 +431,108 @@ sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t g
 
 // Turn ranges into device tables: flow slots, paths, streams, predecessor
 // descriptors, FIFO/request layouts; allocate per-scenario state.
+// Grid engine layout: node -> workgroup, the lanes of every workgroup as
+// source sides (head node owned) and target sides (tail node owned), request
+// slots, the flows whose delivered counts each workgroup keeps, and the LDS
+// size (the kernel carves the same arrays in the same order).
+struct GridLayout {
+    int32_t nb = 0, threads = 64, ns_max = 0, nt_max = 0, req_max = 0, fl_max = 0;
+    int64_t bytes = INT64_MAX;
+    std::vector<int32_t> sptr, slane, tptr, tlane, tloc, rqoff, floc, fptr, fown;
+};
+
+GridLayout grid_layout(const sim_ctx *c, const std::vector<int32_t> &fsrc, const std::vector<char> &has_stream,
+                       const std::vector<std::vector<int32_t>> &feeders, const std::vector<int32_t> &fsrc_pos,
+                       int32_t bmax, int32_t bm, int32_t nflows, const std::vector<int32_t> &pd_flow, int want_nb) {
+    GridLayout g;
+    const int32_t nl = (int32_t)fsrc.size();
+    std::vector<int64_t> wgt(c->n, 0);
+    for (int32_t i = 0; i < nl; i++) {
+        const int32_t l = fsrc[i];
+        wgt[c->tail[l]] += 1 + (has_stream[l] ? 1 : 0);
+        wgt[c->col_idx[l]] += 1;
+    }
+    std::vector<int32_t> nodes;
+    for (int32_t v = 0; v < c->n; v++)
+        if (wgt[v] > 0) nodes.push_back(v);
+    const int32_t nb = std::max<int32_t>(1, std::min<int32_t>(want_nb, (int32_t)nodes.size()));
+    std::stable_sort(nodes.begin(), nodes.end(), [&](int32_t a, int32_t b) { return wgt[a] > wgt[b]; });
+    std::vector<int32_t> part(c->n, 0);
+    std::vector<int64_t> load(nb, 0);
+    for (int32_t v : nodes) {
+        const int32_t w = (int32_t)(std::min_element(load.begin(), load.end()) - load.begin());
+        part[v] = w;
+        load[w] += wgt[v];
+    }
+    g.nb = nb;
+    std::vector<std::vector<int32_t>> src(nb), tgt(nb);
+    for (int32_t i = 0; i < nl; i++) {  // lanes in fsrc order
+        src[part[c->col_idx[fsrc[i]]]].push_back(i);
+        tgt[part[c->tail[fsrc[i]]]].push_back(i);
+    }
+    g.tloc.assign(nl, 0);
+    g.rqoff.assign(nl, 0);
+    g.sptr.push_back(0);
+    g.tptr.push_back(0);
+    for (int32_t w = 0; w < nb; w++) {
+        int64_t r = 0;
+        for (size_t j = 0; j < tgt[w].size(); j++) {
+            const int32_t i = tgt[w][j];
+            g.tloc[i] = (int32_t)j;
+            g.rqoff[i] = (int32_t)r;
+            r += (int64_t)((int32_t)feeders[fsrc_pos[fsrc[i]]].size() + (has_stream[fsrc[i]] ? 1 : 0)) * bmax;
+        }
+        g.slane.insert(g.slane.end(), src[w].begin(), src[w].end());
+        g.tlane.insert(g.tlane.end(), tgt[w].begin(), tgt[w].end());
+        g.sptr.push_back((int32_t)g.slane.size());
+        g.tptr.push_back((int32_t)g.tlane.size());
+        g.ns_max = std::max(g.ns_max, (int32_t)src[w].size());
+        g.nt_max = std::max(g.nt_max, (int32_t)tgt[w].size());
+        g.req_max = (int32_t)std::max<int64_t>(g.req_max, r);
+    }
+    // delivered counters: kept for the flows some line waits on, by the
+    // workgroup of the flow's destination endpoint
+    g.floc.assign(nflows, -1);
+    std::vector<char> waited(nflows, 0);
+    for (int32_t f : pd_flow) waited[f] = 1;
+    std::vector<std::vector<int32_t>> own(nb);
+    for (int32_t f = 0; f < nflows; f++) {
+        if (!waited[f]) continue;
+        int32_t q = c->flow_path[f];
+        while (c->path_link[q] >= 0) q++;
+        const int32_t w = part[c->col_idx[c->path_link[q - 1]]];
+        g.floc[f] = (int32_t)own[w].size();
+        own[w].push_back(f);
+    }
+    g.fptr.push_back(0);
+    for (int32_t w = 0; w < nb; w++) {
+        g.fown.insert(g.fown.end(), own[w].begin(), own[w].end());
+        g.fptr.push_back((int32_t)g.fown.size());
+        g.fl_max = std::max(g.fl_max, (int32_t)own[w].size());
+    }
+    if (g.fown.empty()) g.fown.push_back(0);
+    // wave 0 runs the barrier; one thread per lane after it
+    const int32_t most = std::max(g.ns_max, g.nt_max);
+    g.threads = std::min<int32_t>(1024, 64 + std::max<int32_t>(64, ((most + 63) / 64) * 64));
+    auto a16 = [](int64_t v) { return (v + 15) & ~(int64_t)15; };
+    const int64_t NS = g.ns_max, NT = g.nt_max, BM = bm, KC = 4;
+    const bool preds = !pd_flow.empty();
+    int64_t b = 0;
+    for (int q = 0; q < 11; q++) b += a16(4 * NS);     // constants, head, counts, cache fill, offers
+    for (int q = 0; q < 4; q++) b += a16(4 * NS * KC); // cached entries
+    for (int q = 0; q < 3; q++) b += a16(4 * NS * BM); // offered lines, targets, grants
+    for (int q = 0; q < 24; q++) b += a16(4 * NT);     // constants, counts, stream cursor and range
+    for (int q = 0; q < 3; q++) b += a16(preds ? 4 * NT * 2 : 0);  // stream predecessor descriptors, counts
+    for (int q = 0; q < 2; q++) b += a16(8 * NT);      // counters
+    for (int q = 0; q < 3; q++) b += a16(4 * NT * BM); // grant list, departs, stream grants
+    b += a16(16 * (int64_t)g.req_max);
+    b += a16(preds ? 4 * ((int64_t)g.fl_max + 1) : 0);  // delivered counters (+ one for the rest)
+    for (int q = 0; q < 3; q++) b += a16(preds ? 4 * (int64_t)g.fl_max : 0);  // flow ids, marks, list
+    b += a16(4 * 32);
+    g.bytes = b;
+    return g;
+}
+
 sim_status finish_load(sim_ctx *c, Ranges &R) {
     free_list(c->dev_static);
     free_list(c->dev_state);
@@ -1003,6 +1105,18 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     // arbitration by the workgroup engine
     const bool credits = !c->credit.empty();
     const bool fair = (c->arb & SIM_ARB_FAIR_CLASSES) != 0;
+    // Grid engine (one scenario over many workgroups): nodes are split over
+    // the workgroups by longest-processing-time assignment of their lanes
+    // (target sides of out-links, source sides of in-links, a stream), so
+    // that every workgroup's per-cycle work is about the same.
+    GridLayout gl;
+    const bool grid_try = c->S == 1 && !credits && !fair && nl >= 1 && bm <= 64;
+    if (grid_try) {
+        int want_nb = 32;
+        if (const char *ev = std::getenv("SIMGPU_GRID_WGS")) want_nb = std::max(1, std::min(32, std::atoi(ev)));
+        gl = grid_layout(c, fsrc, has_stream, feeders, fsrc_pos, bmax, bm, nflows, pd_flow, want_nb);
+    }
+    const bool grid_ok = grid_try && gl.bytes <= kLds;
     if ((credits && R.whole) || fair) wv.ok = false;
     const bool lane_ok = !credits && !fair && nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds;
     const bool lanehbm_ok = !credits && !fair && nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds;
@@ -1024,7 +1138,9 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         if (!std::strcmp(ev, "lanehbm")) want = simgpu::kEngineLaneHbm;
         if (!std::strcmp(ev, "b1")) want = simgpu::kEngineB1;
         if (!std::strcmp(ev, "wave")) want = simgpu::kEngineWave;
+        if (!std::strcmp(ev, "grid")) want = simgpu::kEngineGrid;
         const bool ok = want == simgpu::kEngineWorkgroup || (want == simgpu::kEngineWave && wv.ok) ||
+                        (want == simgpu::kEngineGrid && grid_ok) ||
                         (want == simgpu::kEngineLane && lane_ok) || (want == simgpu::kEngineLaneHbm && lanehbm_ok) ||
                         (want == simgpu::kEngineB1 && b1_usable);
         if (want < 0 || !ok) return fail(c, SIM_ERR_INVALID_ARG, std::string("SIMGPU_ENGINE=") + ev + " is not usable here");
@@ -1074,7 +1190,10 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     for (int32_t i = 0; i < nl; i++) ln_inoff[i] = node_inoff[c->tail[lane_link[i]]];
     const LaneLayout &lay = engine == simgpu::kEngineLane ? lay_lds : lay_hbm;
     const bool path_in_lds = lay.path_lds;
-    const int64_t lds_bytes = engine == simgpu::kEngineB1 ? b1_bytes : engine == simgpu::kEngineWave ? wv.bytes : lay.bytes;
+    const int64_t lds_bytes = engine == simgpu::kEngineB1     ? b1_bytes
+                              : engine == simgpu::kEngineWave ? wv.bytes
+                              : engine == simgpu::kEngineGrid ? gl.bytes
+                                                              : lay.bytes;
 
     // everything below touches the device
     c->expanded = true;
@@ -1232,6 +1351,36 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     UP(lane_link, ln_link);
     UP(in_lane, in_lane);
     UP(ln_inoff, ln_inoff);
+    if (engine == simgpu::kEngineGrid) {
+        // the layout was made in fsrc order; lanes are in lane_link order
+        // (the same order for this engine), and paths are re-expressed in the
+        // tail workgroups' local target indices
+        std::vector<int32_t> gpath(path_lane.size());
+        // a sink entry names the delivered counter of its flow in the
+        // destination's workgroup (the last one if nothing waits on the flow)
+        for (size_t q = 0; q < path_lane.size(); q++) {
+            const int32_t v = path_lane[q];
+            gpath[q] = v >= 0 ? gl.tloc[v] : -1 - (gl.floc[-v - 1] >= 0 ? gl.floc[-v - 1] : gl.fl_max);
+        }
+        d.gd_nb = gl.nb;
+        d.gd_stride = 8;  // blocks w * 8: one die's CUs when blocks go round-robin over the 8 dies
+        d.gd_threads = gl.threads;
+        d.gd_ns_max = gl.ns_max;
+        d.gd_nt_max = gl.nt_max;
+        d.gd_req_max = gl.req_max;
+        d.gd_fl_max = gl.fl_max;
+        int32_t *tmp_gd_sptr, *tmp_gd_slane, *tmp_gd_tptr, *tmp_gd_tlane, *tmp_gd_rqoff, *tmp_gd_path, *tmp_gd_floc,
+            *tmp_gd_fptr, *tmp_gd_fown;
+        UP(gl.sptr, gd_sptr);
+        UP(gl.slane, gd_slane);
+        UP(gl.tptr, gd_tptr);
+        UP(gl.tlane, gd_tlane);
+        UP(gl.rqoff, gd_rqoff);
+        UP(gpath, gd_path);
+        UP(gl.floc, gd_floc);
+        UP(gl.fptr, gd_fptr);
+        UP(gl.fown, gd_fown);
+    }
     if (engine == simgpu::kEngineWave) {
         uint32_t *tmp_wv_lfb, *tmp_wv_lfx, *tmp_wv_duo;
         if (wv_duo.empty()) wv_duo.push_back(0);
@@ -1255,7 +1404,12 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     sl = StateLayout{};
     sl.add(&DevNet::status, S);
     sl.add(&DevNet::cycles, S);
-    if (engine == simgpu::kEngineLaneHbm) sl.add(&DevNet::gfifo, S * (size_t)lf);
+    if (engine == simgpu::kEngineLaneHbm || engine == simgpu::kEngineGrid) sl.add(&DevNet::gfifo, S * (size_t)lf);
+    if (engine == simgpu::kEngineGrid) {
+        sl.add(&DevNet::gd_pub, 4 * (size_t)nl);
+        sl.add(&DevNet::gd_dslot, 2 * (size_t)nflows);
+        sl.add(&DevNet::gd_sync, 16);
+    }
     if (engine == simgpu::kEngineB1) {  // uniform rings: lane i owns entries [i << lg, (i + 1) << lg)
         d.fifo_total = nl << d.b1_ring_lg;
         sl.add(&DevNet::gfifo, S * (size_t)d.fifo_total);

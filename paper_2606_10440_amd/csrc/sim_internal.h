@@ -151,6 +151,23 @@ struct DevNet {
     const int32_t *wv_nfeed;  // [nl]
     const int32_t *r_lf;      // [nr] local flow index of a range's flow at its first lane
 
+    // grid engine: one scenario, its nodes split over gd_nb workgroups that run
+    // together; workgroup w is launched as block w * gd_stride
+    int32_t gd_nb, gd_stride, gd_threads;
+    int32_t gd_ns_max, gd_nt_max;  // most source / target sides of one workgroup
+    int32_t gd_req_max;            // most request slots of one workgroup
+    int32_t gd_fl_max;             // most delivered counters one workgroup keeps
+    const int32_t *gd_sptr, *gd_slane;  // [gd_nb+1] CSR: lanes whose head node the workgroup owns
+    const int32_t *gd_tptr, *gd_tlane;  // [gd_nb+1] CSR: lanes whose tail node the workgroup owns
+    const int32_t *gd_rqoff;  // [nl] first request slot of a lane in its tail workgroup's slots
+    const int32_t *gd_path;   // path table with hop lanes replaced by their index among the
+                              //   tail workgroup's target sides (sink entries unchanged)
+    const int32_t *gd_floc;   // [nflows] index of a flow's counter in its owner (-1: never waited on)
+    const int32_t *gd_fptr, *gd_fown;  // [gd_nb+1] CSR: the flows each workgroup keeps counters of
+    uint32_t *gd_pub;         // [4*nl] appended counts (cycle parity 0, 1), popped counts (0, 1)
+    unsigned long long *gd_dslot;  // [2*nflows] delivered counts: (first cycle valid << 32) | count
+    uint32_t *gd_sync;        // [16] barrier count, next-cycle offers [3], flags [3]
+
     // outputs
     uint32_t *completion; // [S*T]
     uint64_t *tx_lines;   // [S*m]
@@ -160,7 +177,8 @@ struct DevNet {
     uint64_t *cycles;     // [S] processed cycles
 };
 
-enum : int32_t { kEngineWorkgroup = 0, kEngineLane = 1, kEngineLaneHbm = 2, kEngineB1 = 3, kEngineWave = 4 };
+enum : int32_t { kEngineWorkgroup = 0, kEngineLane = 1, kEngineLaneHbm = 2, kEngineB1 = 3, kEngineWave = 4,
+                 kEngineGrid = 5 };
 // Wave engine entry words: line id << kWaveXShift | local-flow index (0..3)
 // << 5, the low five bits free for a request slot number (so line ids must
 // be below 2^25 - 1).
@@ -186,5 +204,6 @@ hipError_t launch_workgroup(const DevNet &d, hipStream_t st);
 hipError_t launch_lane_any(const DevNet &d, hipStream_t st);
 hipError_t launch_b1_any(const DevNet &d, hipStream_t st);
 hipError_t launch_wave_any(const DevNet &d, hipStream_t st);
+hipError_t launch_grid_any(const DevNet &d, hipStream_t st);
 
 }  // namespace simgpu

@@ -20,7 +20,7 @@ import sim_inputs as si  # noqa: E402
 from paper_2606_10440_amd import sim  # noqa: E402
 from tests.test_gpu_fuzz import draw  # noqa: E402
 
-ENGINES = [None, "workgroup", "workgroup_scan", "lane", "lanehbm", "b1", "wave"]
+ENGINES = [None, "workgroup", "workgroup_scan", "lane", "lanehbm", "b1", "wave", "grid"]
 HOST_DONE = (sim.SIM_ERR_DEVICE, sim.SIM_ERR_OOM)
 
 
@@ -89,7 +89,8 @@ def main():
             exercise(w, None, engine)
             n += 1
     exercise(si.config("C4"), None, None, pairs=512)
-    n += 1
+    exercise(si.config("C4"), None, "grid", pairs=64)
+    n += 2
     from sim_inputs import noc
     w, lay = noc.gpu_noc(4, mesh=(2, 2), cus_per_router=2, ch_per_router=2, ports_per_router=1)
     for get in (True, False):

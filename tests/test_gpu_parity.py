@@ -369,7 +369,7 @@ def test_full_size_batched_digest(simmod, torch_cuda, name):
 
 # ----------------------------------------------------------------- every engine
 
-ENGINES = ["workgroup", "workgroup_scan", "lane", "lanehbm", "b1", "wave"]
+ENGINES = ["workgroup", "workgroup_scan", "lane", "lanehbm", "b1", "wave", "grid"]
 
 
 def run_engine(simmod, w, engine, txns=None):
@@ -644,3 +644,30 @@ def test_wave_directed_ring_dags(simmod, oracle_lib, seed):
         pptr.append(len(pidx))
     w = si.Workload("dir_ring", n, n, rp, ci, S, bw, lat, cap, seed % 2, -1, 0)
     check_engine(simmod, oracle_lib, w, "wave", txns=(src, dst, np.array(pptr, np.int64), np.array(pidx, np.int64)))
+
+
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C1_chunk", "C2_chunk", "C4"])
+def test_full_size_digest_grid(simmod, torch_cuda, name):
+    """The device-wide engine (one topology over many workgroups) on the
+    single-topology benchmark workloads: the same bytes as the oracle's
+    golden digests."""
+    g = _golden(name)
+    w = si.config(name)
+    say(f"full-size {name}: grid engine")
+    old = os.environ.get("SIMGPU_ENGINE")
+    os.environ["SIMGPU_ENGINE"] = "grid"
+    try:
+        r = run_gpu(simmod, w)
+    finally:
+        if old is None:
+            os.environ.pop("SIMGPU_ENGINE", None)
+        else:
+            os.environ["SIMGPU_ENGINE"] = old
+    assert r.status == 0, simmod.STATUS_NAMES[r.status]
+    comp = r.completion[0].cpu().numpy().view(np.uint32)
+    idx = np.array(g["sample_idx"])
+    assert np.array_equal(comp[idx].astype(np.int64), np.array(g["sample_completion"]))
+    assert int(r.makespan[0]) == g["makespan"][0]
+    assert _digest(comp.astype("<u4")) == g["completion_sha256"][0]
+    assert _digest(r.tx_lines[0].cpu().numpy().astype("<u8")) == g["tx_lines_sha256"][0]
+    assert _digest(r.busy_cycles[0].cpu().numpy().astype("<u8")) == g["busy_cycles_sha256"][0]
