@@ -429,8 +429,6 @@ sim_status expand_collective(sim_ctx *c, int32_t coll, uint64_t bytes, int32_t g
     return SIM_OK;
 }
 
-// Turn ranges into device tables: flow slots, paths, streams, predecessor
-// descriptors, FIFO/request layouts; allocate per-scenario state.
 // Grid engine layout: node -> workgroup, the lanes of every workgroup as
 // source sides (head node owned) and target sides (tail node owned), request
 // slots, the flows whose delivered counts each workgroup keeps, and the LDS
@@ -439,11 +437,17 @@ struct GridLayout {
     int32_t nb = 0, threads = 64, ns_max = 0, nt_max = 0, req_max = 0, fl_max = 0;
     int64_t bytes = INT64_MAX;
     std::vector<int32_t> sptr, slane, tptr, tlane, tloc, rqoff, floc, fptr, fown;
+    // one-line-per-cycle form
+    bool one = false;
+    int32_t one_threads = 64, inl_max = 0;
+    int64_t one_bytes = INT64_MAX;
+    std::vector<int32_t> toff, iptr, inl;
 };
 
 GridLayout grid_layout(const sim_ctx *c, const std::vector<int32_t> &fsrc, const std::vector<char> &has_stream,
                        const std::vector<std::vector<int32_t>> &feeders, const std::vector<int32_t> &fsrc_pos,
-                       int32_t bmax, int32_t bm, int32_t nflows, const std::vector<int32_t> &pd_flow, int want_nb) {
+                       int32_t bmax, int32_t bm, int32_t nflows, const std::vector<int32_t> &pd_flow, int want_nb,
+                       const std::vector<int32_t> &port_at_head, const std::vector<int32_t> &nports) {
     GridLayout g;
     const int32_t nl = (int32_t)fsrc.size();
     std::vector<int64_t> wgt(c->n, 0);
@@ -530,9 +534,52 @@ GridLayout grid_layout(const sim_ctx *c, const std::vector<int32_t> &fsrc, const
     for (int q = 0; q < 3; q++) b += a16(preds ? 4 * (int64_t)g.fl_max : 0);  // flow ids, marks, list
     b += a16(4 * 32);
     g.bytes = b;
+    // one-line-per-cycle form: one source and one target side per thread
+    // after the barrier wave, and every input-port set in one 64-bit mask
+    if (bmax == 1 && most <= 960) {
+        g.one = true;
+        g.one_threads = 64 + std::max<int32_t>(64, ((most + 63) / 64) * 64);
+        std::vector<int32_t> sloc(nl, -1);
+        for (int32_t w = 0; w < nb; w++)
+            for (int32_t q = g.sptr[w]; q < g.sptr[w + 1]; q++) sloc[g.slane[q]] = q - g.sptr[w];
+        std::vector<int32_t> lane_of(c->m, -1);
+        for (int32_t i = 0; i < nl; i++) lane_of[fsrc[i]] = i;
+        std::vector<std::vector<int32_t>> in_links(c->n);
+        for (int32_t l = 0; l < c->m; l++) in_links[c->col_idx[l]].push_back(l);
+        g.toff.assign(nl, 0);
+        g.iptr.push_back(0);
+        std::vector<int32_t> node_off(c->n, -1);
+        for (int32_t w = 0; w < nb; w++) {
+            const size_t base = g.inl.size();
+            for (int32_t q = g.tptr[w]; q < g.tptr[w + 1]; q++) {
+                const int32_t i = g.tlane[q];
+                const int32_t u = c->tail[fsrc[i]];
+                if (node_off[u] < 0) {
+                    node_off[u] = (int32_t)(g.inl.size() - base);
+                    if (nports[u] > 64) g.one = false;
+                    std::vector<int32_t> tab(nports[u], -1);
+                    for (int32_t l : in_links[u])
+                        if (lane_of[l] >= 0) tab[port_at_head[l]] = sloc[lane_of[l]];
+                    g.inl.insert(g.inl.end(), tab.begin(), tab.end());
+                }
+                g.toff[i] = node_off[u];
+            }
+            g.iptr.push_back((int32_t)g.inl.size());
+            g.inl_max = std::max(g.inl_max, (int32_t)(g.inl.size() - base));
+        }
+        if (g.inl.empty()) g.inl.push_back(-1);
+        int64_t b1 = a16(8 * NT * (c->arb == SIM_ARB_LOWEST_ID ? 2 : 1));
+        if (c->arb == SIM_ARB_ROUND_ROBIN) b1 += a16(8 * NS) + a16(4 * (int64_t)g.inl_max);
+        b1 += a16(preds ? 4 * ((int64_t)g.fl_max + 1) : 0);
+        for (int q = 0; q < 3; q++) b1 += a16(preds ? 4 * (int64_t)g.fl_max : 0);
+        b1 += a16(4 * 32);
+        g.one_bytes = b1;
+    }
     return g;
 }
 
+// Turn ranges into device tables: flow slots, paths, streams, predecessor
+// descriptors, FIFO/request layouts; allocate per-scenario state.
 sim_status finish_load(sim_ctx *c, Ranges &R) {
     free_list(c->dev_static);
     free_list(c->dev_state);
@@ -1114,7 +1161,15 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     if (grid_try) {
         int want_nb = 32;
         if (const char *ev = std::getenv("SIMGPU_GRID_WGS")) want_nb = std::max(1, std::min(32, std::atoi(ev)));
-        gl = grid_layout(c, fsrc, has_stream, feeders, fsrc_pos, bmax, bm, nflows, pd_flow, want_nb);
+        gl = grid_layout(c, fsrc, has_stream, feeders, fsrc_pos, bmax, bm, nflows, pd_flow, want_nb, port_at_head,
+                         nports);
+        if (std::getenv("SIMGPU_GRID_GENERAL")) gl.one = false;  // tests: the general form on b = 1 graphs
+        if (gl.one && gl.one_bytes <= kLds) {
+            gl.bytes = gl.one_bytes;
+            gl.threads = gl.one_threads;
+        } else {
+            gl.one = false;
+        }
     }
     const bool grid_ok = grid_try && gl.bytes <= kLds;
     if ((credits && R.whole) || fair) wv.ok = false;
@@ -1126,6 +1181,12 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     else if (lane_ok) engine = simgpu::kEngineLane;
     else if (b1_usable) engine = simgpu::kEngineB1;
     else if (lanehbm_ok) engine = simgpu::kEngineLaneHbm;
+    // One large topology whose lines move one per cycle per link: the grid
+    // engine's one-line form spreads it over many CUs at a lower time per
+    // processed cycle than the single-workgroup compact and HBM engines.
+    if (grid_ok && gl.one && (engine == simgpu::kEngineB1 || engine == simgpu::kEngineLaneHbm ||
+                              engine == simgpu::kEngineWorkgroup))
+        engine = simgpu::kEngineGrid;
     bool wg_scan = false;  // workgroup engine without active sets (tests)
     if (const char *ev = std::getenv("SIMGPU_ENGINE")) {
         int want = -1;
@@ -1369,6 +1430,8 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         d.gd_nt_max = gl.nt_max;
         d.gd_req_max = gl.req_max;
         d.gd_fl_max = gl.fl_max;
+        d.gd_one = gl.one ? 1 : 0;
+        d.gd_inl_max = gl.inl_max;
         int32_t *tmp_gd_sptr, *tmp_gd_slane, *tmp_gd_tptr, *tmp_gd_tlane, *tmp_gd_rqoff, *tmp_gd_path, *tmp_gd_floc,
             *tmp_gd_fptr, *tmp_gd_fown;
         UP(gl.sptr, gd_sptr);
@@ -1380,6 +1443,12 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         UP(gl.floc, gd_floc);
         UP(gl.fptr, gd_fptr);
         UP(gl.fown, gd_fown);
+        if (gl.one) {
+            int32_t *tmp_gd_toff, *tmp_gd_iptr, *tmp_gd_inl;
+            UP(gl.toff, gd_toff);
+            UP(gl.iptr, gd_iptr);
+            UP(gl.inl, gd_inl);
+        }
     }
     if (engine == simgpu::kEngineWave) {
         uint32_t *tmp_wv_lfb, *tmp_wv_lfx, *tmp_wv_duo;
@@ -1407,6 +1476,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     if (engine == simgpu::kEngineLaneHbm || engine == simgpu::kEngineGrid) sl.add(&DevNet::gfifo, S * (size_t)lf);
     if (engine == simgpu::kEngineGrid) {
         sl.add(&DevNet::gd_pub, 4 * (size_t)nl);
+        if (gl.one) sl.add(&DevNet::gd_tpub, 4 * (size_t)nl);
         sl.add(&DevNet::gd_dslot, 2 * (size_t)nflows);
         sl.add(&DevNet::gd_sync, 16);
     }

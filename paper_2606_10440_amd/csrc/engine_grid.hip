@@ -80,6 +80,8 @@ __global__ void grid_init(DevNet d) {
     const size_t i0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const size_t step = (size_t)gridDim.x * blockDim.x;
     for (size_t j = i0; j < (size_t)4 * d.nl; j += step) d.gd_pub[j] = 0u;
+    if (d.gd_tpub)  // tagged counts: no cycle's tag yet
+        for (size_t j = i0; j < (size_t)4 * d.nl; j += step) d.gd_tpub[j] = 0xFFFFFFFFull << 32;
     for (size_t j = i0; j < (size_t)2 * d.nflows; j += step) d.gd_dslot[j] = 0ull;
     // [0..5] arrival words of three successive cycles (64 bits each), [6..8]
     // the earliest future ready time offered by workgroups that moved nothing
@@ -668,14 +670,451 @@ __global__ void __launch_bounds__(1024) engine_grid(DevNet d) {
     }
 }
 
+// ----------------------------------------------------------------------------
+// Grid engine for graphs whose every link moves one line per cycle (b = 1),
+// with one source side and one target side per thread, kept in registers.
+// Then a FIFO offers at most its head, a link grants at most one request and
+// a grant always departs (no void grants), so a cycle needs one exchange of
+// LDS words, as in the compact single-workgroup engine:
+//   round-robin  the source posts {line, path index} in its own LDS slot and
+//                sets its port's bit in the target's word; the target picks
+//                the first set bit at or after its pointer, appends the
+//                winner and marks the winner's post as won;
+//   lowest-id    the source takes the atomic minimum of {line, path index}
+//                in the target's word (two words, by cycle parity); the
+//                target appends the winner and a source has departed when the
+//                word still holds its line.
+// The target appends in the grant phase, so a cycle has two LDS phase
+// boundaries.  The appended and popped counts cross workgroups as 64-bit
+// words tagged with the processed-cycle index (a slot per cycle parity): the
+// thread that owns a side waits for the tag of the cycle it needs while wave
+// 0 waits at the barrier, so the barrier itself carries no data and nothing
+// waits for all stores before arriving.  A count is stored only after the
+// entries it covers (the appending thread waits for its entry stores first),
+// so an entry below a count read with the right tag is complete.  The head
+// entry is fetched, and its next hop looked up, in the same wait.
+template <int ARB, bool PREDS>
+__global__ void __launch_bounds__(1024) engine_grid1(DevNet d) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    if (blockIdx.x % (unsigned)d.gd_stride) return;
+    const int w = (int)(blockIdx.x / (unsigned)d.gd_stride);
+    if (w >= d.gd_nb) return;
+    const int tid = threadIdx.x;
+    const int j = tid - 64;  // this thread's source side and target side (wave 0 runs the barrier)
+    const int nl = d.nl, m = d.m, NB = d.gd_nb;
+    const int sb = d.gd_sptr[w], ns = d.gd_sptr[w + 1] - sb;
+    const int tb = d.gd_tptr[w], nt = d.gd_tptr[w + 1] - tb;
+    const int NT = d.gd_nt_max, NS = d.gd_ns_max;
+    const bool hs = j >= 0 && j < ns, ht = j >= 0 && j < nt;
+
+    size_t off = 0;
+    auto carve = [&](size_t bytes) {
+        unsigned char *p = smem + off;
+        off = (off + bytes + 15) & ~(size_t)15;
+        return p;
+    };
+    unsigned long long *word = (unsigned long long *)carve(8 * (size_t)NT * (ARB == 0 ? 2 : 1));
+    unsigned long long *post = (unsigned long long *)carve(ARB == 1 ? 8 * (size_t)NS : 0);
+    int32_t *inl = (int32_t *)carve(ARB == 1 ? 4 * (size_t)d.gd_inl_max : 0);
+    uint32_t *deliv = (uint32_t *)carve(PREDS ? 4 * ((size_t)d.gd_fl_max + 1) : 0);
+    int32_t *dflow = (int32_t *)carve(PREDS ? 4 * (size_t)d.gd_fl_max : 0);
+    uint32_t *dmark = (uint32_t *)carve(PREDS ? 4 * (size_t)d.gd_fl_max : 0);
+    uint32_t *dlist = (uint32_t *)carve(PREDS ? 4 * (size_t)d.gd_fl_max : 0);
+    uint32_t *red = (uint32_t *)carve(4 * 32);
+    constexpr unsigned long long kNone = ARB == 0 ? ~0ull : 0ull;
+    constexpr unsigned long long kWon = ~0ull;
+
+    const int32_t *path = d.gd_path;
+    uint32_t *ring = reinterpret_cast<uint32_t *>(d.gfifo);
+    uint32_t *comp = d.completion;
+    unsigned long long *tpub = d.gd_tpub;  // [parity][tail | head][nl]: (cycle index << 32) | count
+
+    for (int q = tid; q < NT * (ARB == 0 ? 2 : 1); q += blockDim.x) word[q] = kNone;
+    if (ARB == 1) {
+        const int i0 = d.gd_iptr[w], ni = d.gd_iptr[w + 1] - i0;
+        for (int q = tid; q < ni; q += blockDim.x) inl[q] = d.gd_inl[i0 + q];
+    }
+    if (PREDS) {
+        for (int q = tid; q <= d.gd_fl_max; q += blockDim.x) deliv[q] = 0;
+        const int f0 = d.gd_fptr[w], nf = d.gd_fptr[w + 1] - f0;
+        for (int q = tid; q < d.gd_fl_max; q += blockDim.x) {
+            dmark[q] = 0;
+            dflow[q] = q < nf ? d.gd_fown[f0 + q] : 0;
+        }
+    }
+    if (tid < 32) red[tid] = tid < 16 ? kNever : 0u;
+    if (w == 0)
+        for (int q = tid; q < m; q += blockDim.x)
+            if (d.link_lane[q] < 0) {
+                d.tx_lines[q] = 0;
+                d.busy[q] = 0;
+            }
+
+    // source side: the in-link's FIFO as seen from its head node
+    uint32_t s_lane = 0, s_fb = 0, s_fm = 0, s_L = 0, s_port = 0;
+    uint32_t head = 0, tkn = 0, tkp = 0;
+    bool cval = false;               // head entry cached
+    uint32_t cx = 0, cr = 0, cpp = 0;
+    int32_t ct = kUnresolved;        // cached entry's next hop
+    if (hs) {
+        s_lane = (uint32_t)d.gd_slane[sb + j];
+        const int link = d.ln_link[s_lane];
+        s_fb = (uint32_t)d.ln_fifo[s_lane];
+        s_fm = (uint32_t)d.ln_mask[s_lane];
+        s_L = (uint32_t)d.lat[link];
+        s_port = (uint32_t)d.ln_port[s_lane];
+    }
+    // target side: the out-link's arbitration, appends and stream
+    uint32_t t_lane = 0, t_link = 0, t_L = 0, t_cap = 0, t_P = 1, t_fb = 0, t_fm = 0, t_toff = 0;
+    uint32_t tail = 0, khead = 0, rr = 0;
+    unsigned long long tx = 0;
+    int R = 0, rend = 0;
+    uint32_t o = 0, r_st = 0, r_len = 0;
+    int r_path = 0, pd0 = 0, pd1 = 0;
+    int32_t pf[kPDesc];
+    uint32_t pb[kPDesc];
+#pragma unroll
+    for (int q = 0; q < kPDesc; q++) pf[q] = 0, pb[q] = 0;
+    auto set_range = [&](int Rn) {
+        r_st = d.r_start[Rn];
+        r_len = d.r_len[Rn];
+        r_path = d.r_path[Rn];
+        pd0 = d.r_pd[Rn];
+        pd1 = d.r_pd[Rn + 1];
+        if (PREDS)
+#pragma unroll
+            for (int q = 0; q < kPDesc; q++)
+                if (pd0 + q < pd1) {
+                    pf[q] = d.pd_flow[pd0 + q];
+                    pb[q] = d.pd_base[pd0 + q];
+                }
+    };
+    if (ht) {
+        t_lane = (uint32_t)d.gd_tlane[tb + j];
+        t_link = (uint32_t)d.ln_link[t_lane];
+        t_L = (uint32_t)d.lat[t_link];
+        t_cap = (uint32_t)d.cap[t_link];
+        t_P = (uint32_t)d.ln_P[t_lane];
+        t_fb = (uint32_t)d.ln_fifo[t_lane];
+        t_fm = (uint32_t)d.ln_mask[t_lane];
+        t_toff = ARB == 1 ? (uint32_t)d.gd_toff[t_lane] : 0u;
+        R = d.ln_srbeg[t_lane];
+        rend = d.ln_srend[t_lane];
+        if (R < rend) set_range(R);
+    }
+    __syncthreads();
+
+    uint32_t t = 0, t_prev = 0;
+    uint64_t k = 0;
+    int32_t state = d.T > 0 ? kRunRunning : kRunOk;
+
+    while (state == kRunRunning) {
+        const int par = (int)(k & 1u);
+        unsigned long long *wcur = ARB == 0 ? word + (size_t)par * NT : word;
+        uint32_t next = kNever;
+        int dep = 0;
+        bool act = false;
+        // -------------------------------------------------------------- R
+        bool req_f = false, sink_f = false;  // the head requests a link / the sink
+        if (hs && tkn != head) {
+            uint32_t x = cx, rdy = cr, pp = cpp;
+            int32_t tg = ct;
+            bool known = cval;
+            if (!cval && head >= tkp) {  // appended at the last processed cycle
+                rdy = t_prev + s_L;
+                known = rdy > t;         // not ready yet: its contents can wait
+            }
+            if (!known) {
+                uint32_t *e = ring + 4 * (size_t)(s_fb + (head & s_fm));
+                cx = x = ld_dev(e);
+                cr = rdy = ld_dev(e + 1);
+                cpp = pp = ld_dev(e + 2);
+                ct = tg = kUnresolved;
+                cval = true;
+            }
+            if (rdy <= t && tg == kUnresolved) ct = tg = path[pp + 1];
+            if (rdy > t) {
+                next = rdy;
+            } else if (tg < 0) {
+                sink_f = true;
+            } else {
+                req_f = true;
+                const unsigned long long key = ((unsigned long long)x << 32) | (pp + 1u);
+                if (ARB == 1) {
+                    post[j] = key;
+                    atomicOr(&wcur[tg], 1ull << s_port);
+                } else {
+                    atomicMin(&wcur[tg], key);
+                }
+            }
+        }
+        bool sreq = false;
+        if (ht && R < rend) {
+            bool ok = true;
+            if (PREDS) {
+                const int npd = pd1 - pd0;
+                if (npd > kPDesc) {
+                    ok = stream_allow<PREDS>(d, pd0, pd1, o, t) > 0;
+                } else {
+#pragma unroll
+                    for (int q = 0; q < kPDesc; q++)
+                        if (q < npd) ok = ok && deliv_at(d.gd_dslot, pf[q], t) > pb[q] + (o & d.pd_omask);
+                }
+            }
+            if (ok) {
+                sreq = true;
+                if (ARB == 1)
+                    atomicOr(&wcur[j], 1ull << (t_P - 1u));
+                else
+                    atomicMin(&wcur[j], ((unsigned long long)(r_st + o) << 32) | (uint32_t)r_path);
+            }
+        }
+        __syncthreads();
+        // ------------------------------------------------ G (and append)
+        bool sdep = false;
+        bool appended = false;
+        if (ht) {
+            if (ARB == 0) word[(size_t)(par ^ 1) * NT + j] = kNone;  // the word of the next cycle
+            const unsigned long long wv = wcur[j];
+            if (wv != kNone) {
+                if (ARB == 1) wcur[j] = 0ull;
+                if (tail - khead >= t_cap) {
+                    if (ARB == 0) wcur[j] = kNone;  // full: nobody moves
+                } else {
+                    uint32_t x, pp;
+                    if (ARB == 1) {
+                        const unsigned long long hi = wv >> rr;
+                        const uint32_t p = hi ? rr + (uint32_t)__builtin_ctzll(hi) : (uint32_t)__builtin_ctzll(wv);
+                        const int src = inl[t_toff + p];
+                        if (src < 0) {  // the injection port: this thread's own stream
+                            x = r_st + o;
+                            pp = (uint32_t)r_path;
+                            sdep = true;
+                        } else {
+                            const unsigned long long pw = post[src];
+                            post[src] = kWon;
+                            x = (uint32_t)(pw >> 32);
+                            pp = (uint32_t)pw;
+                        }
+                        rr = p + 1u == t_P ? 0u : p + 1u;
+                    } else {
+                        x = (uint32_t)(wv >> 32);
+                        pp = (uint32_t)wv;
+                    }
+                    uint32_t *e = ring + 4 * (size_t)(t_fb + (tail & t_fm));
+                    st_dev(e, x);
+                    st_dev(e + 1, t + t_L);
+                    st_dev(e + 2, pp);
+                    tail++;
+                    tx++;
+                    appended = true;
+                }
+            }
+        }
+        __syncthreads();
+        // -------------------------------------------------------------- D
+        if (hs) {
+            bool gone = sink_f;
+            if (sink_f) {
+                comp[cx] = t + 1;
+                const int fl = -ct - 1;
+                if (PREDS && fl < d.gd_fl_max) {
+                    deliv[fl] += 1u;
+                    if ((dmark[fl] & 0x7FFFFFFFu) != (uint32_t)(k & 0x7FFFFFFFu) + 1u) {
+                        dmark[fl] = (dmark[fl] & 0x80000000u) | ((uint32_t)(k & 0x7FFFFFFFu) + 1u);
+                        dlist[atomicAdd(&red[24 + par], 1u)] = (uint32_t)fl;
+                    }
+                }
+            } else if (req_f) {
+                gone = ARB == 1 ? post[j] == kWon : (uint32_t)(wcur[ct] >> 32) == cx;
+            }
+            if (gone) {
+                head++;
+                cval = false;
+                ct = kUnresolved;
+                dep++;
+            }
+            st_dev(&tpub[((size_t)par * 2 + 1) * nl + s_lane], ((unsigned long long)(uint32_t)k << 32) | head);
+            if (head != tkn) act = true;
+        }
+        if (ht) {
+            if (sreq && (ARB == 1 ? sdep : (uint32_t)(wcur[j] >> 32) == r_st + o)) {
+                dep++;
+                if (++o == r_len) {
+                    o = 0;
+                    R++;
+                    if (R < rend) set_range(R);
+                }
+            }
+            if (appended) {
+                act = true;
+                __builtin_amdgcn_s_waitcnt(0x0F70);  // the entry is stored before the count that covers it
+            }
+            st_dev(&tpub[((size_t)par * 2) * nl + t_lane], ((unsigned long long)(uint32_t)k << 32) | tail);
+            if (R < rend) act = true;
+        }
+        if (PREDS) {
+            __syncthreads();  // the list of flows that delivered
+            const uint32_t nch = red[24 + par];
+            for (int q = j; q >= 0 && q < (int)nch; q += (int)blockDim.x - 64) {
+                const int fl = (int)dlist[q];
+                const int f = dflow[fl];
+                const uint32_t mk = dmark[fl];
+                const int slot = (mk >> 31) ? 0 : 1;
+                st_dev(&d.gd_dslot[2 * f + slot], ((unsigned long long)(t + 1) << 32) | deliv[fl]);
+                dmark[fl] = (mk & 0x7FFFFFFFu) | (slot ? 0x80000000u : 0u);
+            }
+            // delivered counts are read after the barrier: they are complete
+            // before this workgroup arrives
+            __builtin_amdgcn_s_waitcnt(0x0F70);
+        }
+        // -------------------------------------------------------------- time
+        const int p4 = par * 4;
+        {
+            const bool wdep = __ballot(dep > 0) != 0, wact = __ballot(act) != 0;
+            uint32_t v = next;
+#pragma unroll
+            for (int sh = 32; sh >= 1; sh >>= 1) {
+                const uint32_t u = (uint32_t)__shfl_xor((int)v, sh);
+                v = u < v ? u : v;
+            }
+            if ((tid & 63) == 0) {
+                if (wdep) red[p4] = 1u;
+                if (wact) red[p4 + 1] = 1u;
+                if (v != kNever) atomicMin(&red[p4 + 2], v);
+            }
+        }
+        __syncthreads();
+        bool stuck = false;
+        if (tid == 0) {
+            const bool any_dep = red[p4] != kNever;
+            const bool any_act = red[p4 + 1] != kNever;
+            const int r3 = (int)(k % 3u);
+            unsigned long long *wordg = reinterpret_cast<unsigned long long *>(d.gd_sync) + r3;
+            uint32_t *nxtw = d.gd_sync + 6 + r3;
+            if (!any_dep && red[p4 + 2] != kNever)
+                __hip_atomic_fetch_min(nxtw, red[p4 + 2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __builtin_amdgcn_s_waitcnt(0x0F70);  // the offer, and the last reset of the words, have landed
+            const unsigned long long mine = 1ull | (any_dep ? 1ull << 16 : 0ull) | (any_act ? 1ull << 32 : 0ull);
+            unsigned long long v = __hip_atomic_fetch_add(wordg, mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + mine;
+            uint32_t spins = 0;
+            while ((v & 0xFFFFull) < (unsigned long long)NB) {
+                if (++spins > kSpinLimit) {
+                    stuck = true;
+                    break;
+                }
+                v = ld_dev(wordg);
+            }
+            const bool movers = ((v >> 16) & 0xFFFFull) != 0, active = ((v >> 32) & 0xFFFFull) != 0;
+            red[16] = movers ? t + 1 : (active && !stuck ? ld_dev(nxtw) : kNever);
+            red[17] = (active ? 1u : 0u);
+            if (w == 0 && !stuck) {
+                const int r5 = (int)((k + 2) % 3u);
+                st_dev(reinterpret_cast<unsigned long long *>(d.gd_sync) + r5, 0ull);
+                st_dev(d.gd_sync + 6 + r5, kNever);
+            }
+            red[(4 - p4)] = kNever;
+            red[(4 - p4) + 1] = kNever;
+            red[(4 - p4) + 2] = kNever;
+            red[24 + (par ^ 1)] = 0u;
+        } else if (j >= 0) {
+            // While wave 0 waits: this cycle's counts of this thread's sides
+            // (the producers store them before they arrive), the head entry
+            // and its next hop.
+            const unsigned long long tagk = (unsigned long long)(uint32_t)k;
+            bool need_e = hs && !cval && head != tkn;  // an entry known before this cycle
+            uint32_t ex = 0, er = 0, ep = 0;
+            int32_t nh = kUnresolved;
+            if (need_e) {
+                uint32_t *e = ring + 4 * (size_t)(s_fb + (head & s_fm));
+                ex = ld_dev(e);
+                er = ld_dev(e + 1);
+                ep = ld_dev(e + 2);
+            }
+            if (hs && cval && ct == kUnresolved) nh = path[cpp + 1];
+            uint32_t ntail = tkn, nkhead = khead;
+            uint32_t spins = 0;
+            if (hs) {
+                unsigned long long *pw = &tpub[((size_t)par * 2) * nl + s_lane];
+                unsigned long long v;
+                while (((v = ld_dev(pw)) >> 32) != tagk) {
+                    if (++spins > kSpinLimit) {
+                        stuck = true;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(2);
+                }
+                ntail = (uint32_t)v;
+            }
+            if (ht) {
+                unsigned long long *pw = &tpub[((size_t)par * 2 + 1) * nl + t_lane];
+                unsigned long long v;
+                while (((v = ld_dev(pw)) >> 32) != tagk) {
+                    if (++spins > kSpinLimit) {
+                        stuck = true;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(2);
+                }
+                nkhead = (uint32_t)v;
+            }
+            if (need_e) {
+                cx = ex, cr = er, cpp = ep;
+                ct = kUnresolved;
+                cval = true;
+            }
+            if (nh != kUnresolved) ct = nh;
+            // an entry appended this cycle is fetched in the next wait (its
+            // ready time, t + L, is known without it)
+            tkp = tkn;
+            tkn = ntail;
+            khead = nkhead;
+        }
+        if (stuck) red[20] = 1u;
+        __syncthreads();
+        const uint32_t nxt = red[16];
+        const uint32_t flags = red[17];
+        k++;
+        if (red[20]) {
+            state = kRunWatchdog;
+        } else if (!(flags & 1u)) {
+            state = kRunOk;
+        } else if (nxt == kNever) {
+            state = kRunDeadlock;
+        } else {
+            t_prev = t;
+            t = nxt;
+        }
+        if (state == kRunRunning && (uint64_t)t > d.max_cycles) state = kRunMaxCycles;
+        if (state == kRunRunning && k > d.watchdog) state = kRunWatchdog;
+        __syncthreads();
+    }
+    if (ht) {
+        d.tx_lines[t_link] = tx;
+        d.busy[t_link] = tx;  // one line per cycle at most: busy cycles = lines
+    }
+    if (tid == 0) {
+        atomicMax(&d.status[0], state);
+        if (w == 0) {
+            d.makespan[0] = d.T > 0 ? t + 1 : 0;
+            d.cycles[0] = k;
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_grid_any(const DevNet &d, hipStream_t st) {
     hipLaunchKernelGGL(grid_init, dim3(64), dim3(256), 0, st, d);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const void *k = d.arb == 0 ? (d.has_preds ? (const void *)engine_grid<0, true> : (const void *)engine_grid<0, false>)
-                               : (d.has_preds ? (const void *)engine_grid<1, true> : (const void *)engine_grid<1, false>);
+    const void *k;
+    if (d.gd_one)
+        k = d.arb == 0 ? (d.has_preds ? (const void *)engine_grid1<0, true> : (const void *)engine_grid1<0, false>)
+                       : (d.has_preds ? (const void *)engine_grid1<1, true> : (const void *)engine_grid1<1, false>);
+    else
+        k = d.arb == 0 ? (d.has_preds ? (const void *)engine_grid<0, true> : (const void *)engine_grid<0, false>)
+                       : (d.has_preds ? (const void *)engine_grid<1, true> : (const void *)engine_grid<1, false>);
     if (d.lds_bytes > 65536) (void)hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
     DevNet arg = d;
     void *args[] = {&arg};

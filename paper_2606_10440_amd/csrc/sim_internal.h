@@ -166,7 +166,15 @@ struct DevNet {
     const int32_t *gd_fptr, *gd_fown;  // [gd_nb+1] CSR: the flows each workgroup keeps counters of
     uint32_t *gd_pub;         // [4*nl] appended counts (cycle parity 0, 1), popped counts (0, 1)
     unsigned long long *gd_dslot;  // [2*nflows] delivered counts: (first cycle valid << 32) | count
-    uint32_t *gd_sync;        // [16] barrier count, next-cycle offers [3], flags [3]
+    uint32_t *gd_sync;        // [16] arrival words [3 x 64 bit], next-cycle offers [3]
+    // one-line-per-cycle form (every bandwidth 1; one source and one target
+    // side per thread, in registers)
+    int32_t gd_one;
+    unsigned long long *gd_tpub;  // [2 parities x (appended, popped) x nl]: (cycle index << 32) | count
+    int32_t gd_inl_max;       // most in-port table entries of one workgroup
+    const int32_t *gd_toff;   // [nl] offset of a lane's tail node in its workgroup's in-port table
+    const int32_t *gd_iptr, *gd_inl;  // [gd_nb+1] CSR: per node of the workgroup, for each input
+                                      //   port the local source side feeding it (-1: stream or none)
 
     // outputs
     uint32_t *completion; // [S*T]

@@ -646,23 +646,32 @@ def test_wave_directed_ring_dags(simmod, oracle_lib, seed):
     check_engine(simmod, oracle_lib, w, "wave", txns=(src, dst, np.array(pptr, np.int64), np.array(pidx, np.int64)))
 
 
-@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C1_chunk", "C2_chunk", "C4"])
-def test_full_size_digest_grid(simmod, torch_cuda, name):
+@pytest.mark.parametrize("name,general", [("C1", False), ("C2", False), ("C3", False), ("C1_chunk", False),
+                                          ("C2_chunk", False), ("C4", False), ("C1", True), ("C2", True),
+                                          ("C2_chunk", True)])
+def test_full_size_digest_grid(simmod, torch_cuda, name, general):
     """The device-wide engine (one topology over many workgroups) on the
     single-topology benchmark workloads: the same bytes as the oracle's
-    golden digests."""
+    golden digests.  Graphs with every bandwidth 1 run its one-line form
+    unless the general form is asked for."""
     g = _golden(name)
     w = si.config(name)
-    say(f"full-size {name}: grid engine")
-    old = os.environ.get("SIMGPU_ENGINE")
-    os.environ["SIMGPU_ENGINE"] = "grid"
+    say(f"full-size {name}: grid engine{' (general form)' if general else ''}")
+    env = {"SIMGPU_ENGINE": "grid", "SIMGPU_GRID_GENERAL": "1" if general else None}
+    old = {k: os.environ.get(k) for k in env}
+    for k, v in env.items():
+        if v is None:
+            os.environ.pop(k, None)
+        else:
+            os.environ[k] = v
     try:
         r = run_gpu(simmod, w)
     finally:
-        if old is None:
-            os.environ.pop("SIMGPU_ENGINE", None)
-        else:
-            os.environ["SIMGPU_ENGINE"] = old
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
     assert r.status == 0, simmod.STATUS_NAMES[r.status]
     comp = r.completion[0].cpu().numpy().view(np.uint32)
     idx = np.array(g["sample_idx"])
