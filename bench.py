@@ -219,6 +219,55 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
 
 
+def sweep_allgather(points, n_wg=32, seconds_cap=120.0):
+    """The scalability measurement of the paper's Sec. 5.4: a put-based
+    all-gather with n_wg workgroups per GPU on G generic GPUs, for several
+    output buffer sizes per GPU.  Per point one JSON line: host setup time
+    (expansion and tables, not simulated time), the launch's wall time
+    (device events around sim_run), the makespan in cycles and in simulated
+    nanoseconds (one cycle = one line on one memory channel), and simulated
+    nanoseconds per wall-clock second.  A GPU count's larger sizes are
+    skipped once a launch took longer than seconds_cap."""
+    import torch
+    from sim_inputs import noc
+    from paper_2606_10440_amd import sim
+    stop = set()
+    for G, mib in points:
+        if G in stop:
+            continue
+        chunk = int(mib * 2 ** 20 / 128) // G
+        chunk = max(n_wg, chunk // n_wg * n_wg)
+        t0 = time.time()
+        w, lay = noc.gpu_noc(G)
+        wm = noc.memcpy_workload(w, noc.allgather_ops(lay, chunk * G, n_wg=n_wg), name=f"ag_{G}gpu")
+        s = sim.Simulator.from_workload(wm)
+        T, m, S, line_hops = s.sizes()
+        outs = s.alloc_outputs()
+        torch.cuda.synchronize()
+        setup = time.time() - t0
+        stream = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        s.enqueue(outs, stream=stream)
+        e1.record(stream)
+        stream.synchronize()
+        run_s = e0.elapsed_time(e1) / 1e3
+        rc, st, cyc = sim.sim_status_after_sync(s.ctx, S)
+        mk = int(outs[3][0])
+        sim_ns = mk * noc.CYCLE_NS
+        print(json.dumps({"sweep": "allgather", "gpus": G, "endpoints": G * 448, "out_mib_per_gpu": chunk * G * 128 / 2 ** 20,
+                          "workgroups_per_gpu": n_wg, "lines": T, "line_hops": line_hops, "status": sim.STATUS_NAMES[rc],
+                          "setup_s": round(setup, 3), "run_s": run_s, "processed_cycles": int(cyc[0]),
+                          "makespan_cycles": mk, "simulated_ns": sim_ns,
+                          "simulated_ns_per_wall_s": sim_ns / run_s if run_s > 0 else None,
+                          "line_hops_per_s": line_hops / run_s if run_s > 0 else None}), flush=True)
+        s.close()
+        del outs
+        torch.cuda.empty_cache()
+        if run_s > seconds_cap:
+            stop.add(G)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -231,6 +280,8 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true")
     ap.add_argument("--only-scenario", type=int, default=None,
                     help="run one scenario of a batched workload alone (per-cycle counters of a lone wave)")
+    ap.add_argument("--sweep-allgather", default=None,
+                    help="instead of the benchmark line: the Sec. 5.4 all-gather sweep, points 'G:MiB,G:MiB,...'")
     a = ap.parse_args()
 
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -240,6 +291,10 @@ def main():
         sys.exit(2)
     if a.calibrate_copy:
         copy_calibration()
+        return
+    if a.sweep_allgather:
+        pts = [(int(g), float(mb)) for g, mb in (p.split(":") for p in a.sweep_allgather.split(","))]
+        sweep_allgather(pts)
         return
 
     import torch

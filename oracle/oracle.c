@@ -172,6 +172,116 @@ int oracle_paths(int32_t n, int32_t E, const int32_t *row_ptr,
     return rc;
 }
 
+/* Routes of the (source, destination) pairs one workload uses, for graphs
+ * whose all-pairs table would not fit: an open-addressing hash from the key
+ * s * E + d to the pair's path, each traced as above, destination by
+ * destination so that one distance array is alive at a time. */
+typedef struct {
+    int64_t cap;        /* hash slots (power of two) */
+    int64_t *key;       /* -1: empty */
+    int64_t *idx;       /* pair index of the slot */
+    int64_t np;         /* pairs */
+    int64_t *pkey;      /* [np] keys in insertion order */
+    int64_t *ptr;       /* [np + 1] path start in link */
+    int32_t *link;
+} routes_t;
+
+static int64_t route_slot(const routes_t *r, int64_t key)
+{
+    uint64_t h = (uint64_t)key * 0x9E3779B97F4A7C15ull;   /* Fibonacci hashing */
+    int64_t i = (int64_t)(h >> 20) & (r->cap - 1);
+    while (r->key[i] != -1 && r->key[i] != key) i = (i + 1) & (r->cap - 1);
+    return i;
+}
+
+static int routes_add(routes_t *r, int64_t key)
+{
+    if (2 * (r->np + 1) > r->cap) {                    /* grow to keep the load under one half */
+        routes_t g = *r;
+        g.cap = r->cap ? 2 * r->cap : 1024;
+        g.key = malloc(sizeof(int64_t) * (size_t)g.cap);
+        g.idx = malloc(sizeof(int64_t) * (size_t)g.cap);
+        g.pkey = realloc(r->pkey, sizeof(int64_t) * (size_t)g.cap);
+        if (!g.key || !g.idx || !g.pkey) return OR_ERR_OOM;
+        for (int64_t i = 0; i < g.cap; i++) g.key[i] = -1;
+        for (int64_t q = 0; q < r->np; q++) {
+            int64_t i = route_slot(&g, g.pkey[q]);
+            g.key[i] = g.pkey[q];
+            g.idx[i] = q;
+        }
+        free(r->key); free(r->idx);
+        *r = g;
+    }
+    int64_t i = route_slot(r, key);
+    if (r->key[i] == -1) {
+        r->key[i] = key;
+        r->idx[i] = r->np;
+        r->pkey[r->np++] = key;
+    }
+    return OR_OK;
+}
+
+static int64_t routes_find(const routes_t *r, int64_t key)
+{
+    if (!r->cap) return -1;
+    int64_t i = route_slot(r, key);
+    return r->key[i] == key ? r->idx[i] : -1;
+}
+
+/* Trace every pair (unreachable: empty path). */
+static int routes_trace(routes_t *r, int32_t n, int32_t E, const int32_t *row_ptr, const int32_t *col_idx)
+{
+    int32_t m = row_ptr[n];
+    int32_t maxdeg = 1;
+    for (int32_t u = 0; u < n; u++)
+        if (row_ptr[u + 1] - row_ptr[u] > maxdeg) maxdeg = row_ptr[u + 1] - row_ptr[u];
+    int32_t *dist = malloc(sizeof(int32_t) * (size_t)n), *queue = malloc(sizeof(int32_t) * (size_t)n);
+    int32_t *cand = malloc(sizeof(int32_t) * (size_t)maxdeg);
+    int32_t *in_ptr = calloc((size_t)n + 1, sizeof(int32_t)), *in_tail = malloc(sizeof(int32_t) * (size_t)(m + 1));
+    int32_t *fill = calloc((size_t)n, sizeof(int32_t));
+    int64_t *order = malloc(sizeof(int64_t) * (size_t)(r->np > 0 ? r->np : 1));
+    int32_t *len = malloc(sizeof(int32_t) * (size_t)(r->np > 0 ? r->np : 1));
+    r->ptr = malloc(sizeof(int64_t) * (size_t)(r->np + 1));
+    if (!dist || !queue || !cand || !in_ptr || !in_tail || !fill || !order || !len || !r->ptr) return OR_ERR_OOM;
+    for (int32_t l = 0; l < m; l++) in_ptr[col_idx[l] + 1]++;
+    for (int32_t v = 0; v < n; v++) in_ptr[v + 1] += in_ptr[v];
+    for (int32_t u = 0; u < n; u++)
+        for (int32_t l = row_ptr[u]; l < row_ptr[u + 1]; l++)
+            in_tail[in_ptr[col_idx[l]] + fill[col_idx[l]]++] = u;
+    /* pairs grouped by destination (counting sort) */
+    int64_t *dcnt = calloc((size_t)E + 1, sizeof(int64_t));
+    if (!dcnt) return OR_ERR_OOM;
+    for (int64_t q = 0; q < r->np; q++) dcnt[r->pkey[q] % E + 1]++;
+    for (int32_t d = 0; d < E; d++) dcnt[d + 1] += dcnt[d];
+    for (int64_t q = 0; q < r->np; q++) order[dcnt[r->pkey[q] % E]++] = q;
+    free(dcnt);
+    /* path lengths are the distances: a first pass sizes the table */
+    int64_t total = 0;
+    for (int64_t a = 0; a < r->np; a++) {
+        int32_t d = (int32_t)(r->pkey[order[a]] % E), s = (int32_t)(r->pkey[order[a]] / E);
+        if (a == 0 || r->pkey[order[a - 1]] % E != d) bfs_to(n, in_ptr, in_tail, d, dist, queue);
+        len[order[a]] = s == d || dist[s] < 0 ? 0 : dist[s];
+        total += len[order[a]];
+    }
+    r->ptr[0] = 0;
+    for (int64_t q = 0; q < r->np; q++) r->ptr[q + 1] = r->ptr[q] + len[q];
+    r->link = malloc(sizeof(int32_t) * (size_t)(total > 0 ? total : 1));
+    if (!r->link) return OR_ERR_OOM;
+    for (int64_t a = 0; a < r->np; a++) {
+        int32_t d = (int32_t)(r->pkey[order[a]] % E), s = (int32_t)(r->pkey[order[a]] / E);
+        if (a == 0 || r->pkey[order[a - 1]] % E != d) bfs_to(n, in_ptr, in_tail, d, dist, queue);
+        if (len[order[a]]) trace_path(row_ptr, col_idx, dist, s, d, r->link + r->ptr[order[a]], cand);
+    }
+    free(dist); free(queue); free(cand); free(in_ptr); free(in_tail); free(fill); free(order); free(len);
+    return OR_OK;
+}
+
+static void routes_free(routes_t *r)
+{
+    free(r->key); free(r->idx); free(r->pkey); free(r->ptr); free(r->link);
+    memset(r, 0, sizeof(*r));
+}
+
 /* ------------------------------------------------------ workload expansion */
 
 enum {
@@ -847,7 +957,7 @@ typedef struct {
 } hcache_t;
 
 static const hcache_t *head_info(hcache_t *c, int64_t *slot, const work_t *w, uint32_t x,
-                                 const int64_t *path_ptr, int32_t E)
+                                 const routes_t *rt, int32_t E)
 {
     if (c->x == x) return c;
     int32_t s, d;
@@ -861,8 +971,9 @@ static const hcache_t *head_info(hcache_t *c, int64_t *slot, const work_t *w, ui
         c->preds = slot;
     }
     c->np = decode(w, x, &s, &d, slot);
-    c->pp = path_ptr[(int64_t)s * E + d];
-    c->plen = (int32_t)(path_ptr[(int64_t)s * E + d + 1] - c->pp);
+    const int64_t q = routes_find(rt, (int64_t)s * E + d);
+    c->pp = rt->ptr[q];
+    c->plen = (int32_t)(rt->ptr[q + 1] - c->pp);
     c->x = x;
     return c;
 }
@@ -964,19 +1075,22 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     int64_t *chunk_done = nchunks ? calloc((size_t)nchunks, sizeof(int64_t)) : NULL;
     uint32_t *chunk_max = nchunks ? calloc((size_t)nchunks, sizeof(uint32_t)) : NULL;
 
-    /* routes */
-    int64_t *path_ptr = malloc(sizeof(int64_t) * ((size_t)E * E + 1));
-    if (!path_ptr) return OR_ERR_OOM;
-    int64_t pcap = (int64_t)E * (E - 1) * 8 + 16;
-    int32_t *path_link = malloc(sizeof(int32_t) * (size_t)pcap);
-    rc = oracle_paths(n, E, row_ptr, col_idx, path_ptr, path_link, pcap);
-    if (rc == OR_ERR_SIZE) {
-        pcap = path_ptr[(int64_t)E * E];
-        free(path_link);
-        path_link = malloc(sizeof(int32_t) * (size_t)pcap);
-        rc = oracle_paths(n, E, row_ptr, col_idx, path_ptr, path_link, pcap);
+    /* routes of the pairs the workload uses */
+    routes_t rt;
+    memset(&rt, 0, sizeof(rt));
+    int64_t *preds = malloc(sizeof(int64_t) * (size_t)pred_bound(&w));
+    for (int64_t x = 0; x < T && rc == OR_OK; x++) {
+        int32_t s, d;
+        decode(&w, x, &s, &d, preds);
+        rc = routes_add(&rt, (int64_t)s * E + d);
     }
-    if (rc) { free(path_ptr); free(path_link); return rc; }
+    if (rc == OR_OK) rc = routes_trace(&rt, n, E, row_ptr, col_idx);
+    if (rc) { routes_free(&rt); free(preds); free(chunk_done); free(chunk_max); return rc; }
+    const int64_t *path_ptr = rt.ptr;
+    const int32_t *path_link = rt.link;
+    /* the path of flow (s, d): start and one past its end in path_link */
+    #define PATH_LO(s, d) path_ptr[routes_find(&rt, (int64_t)(s) * E + (d))]
+    #define PATH_HI(s, d) path_ptr[routes_find(&rt, (int64_t)(s) * E + (d)) + 1]
 
     /* input ports: in-links of v sorted by id, then the injection port */
     int32_t *port_of = malloc(sizeof(int32_t) * (size_t)(m + 1));
@@ -991,23 +1105,22 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     int64_t *s_ptr = calloc((size_t)m + 1, sizeof(int64_t));
     uint32_t *s_list = malloc(sizeof(uint32_t) * (size_t)(T > 0 ? T : 1));
     int64_t *s_cur = calloc((size_t)m, sizeof(int64_t));
-    int64_t *preds = malloc(sizeof(int64_t) * (size_t)pred_bound(&w));
     int64_t line_hops = 0;
     int32_t maxp = 1;   /* most predecessors of any line (sizes the head cache) */
     for (int64_t x = 0; x < T; x++) {
         int32_t s, d;
         int32_t np = decode(&w, x, &s, &d, preds);
         if (np > maxp) maxp = np;
-        int64_t f0 = path_ptr[(int64_t)s * E + d];
-        if (path_ptr[(int64_t)s * E + d + 1] == f0) {   /* needed pair without a path */
+        int64_t f0 = PATH_LO(s, d);
+        if (PATH_HI(s, d) == f0) {   /* needed pair without a path */
             rc = OR_ERR_UNREACHABLE;
             break;
         }
         s_ptr[path_link[f0] + 1]++;
-        line_hops += path_ptr[(int64_t)s * E + d + 1] - f0;
+        line_hops += PATH_HI(s, d) - f0;
     }
     if (rc) {
-        free(path_ptr); free(path_link); free(port_of); free(nports); free(tail_of);
+        routes_free(&rt); free(port_of); free(nports); free(tail_of);
         free(s_ptr); free(s_list); free(s_cur); free(preds); free(chunk_done); free(chunk_max);
         return rc;
     }
@@ -1015,7 +1128,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
     for (int64_t x = 0; x < T; x++) {
         int32_t s, d;
         decode(&w, x, &s, &d, preds);
-        int32_t f = path_link[path_ptr[(int64_t)s * E + d]];
+        int32_t f = path_link[PATH_LO(s, d)];
         s_list[s_ptr[f] + s_cur[f]++] = (uint32_t)x;
     }
     memset(s_cur, 0, sizeof(int64_t) * (size_t)m);
@@ -1111,7 +1224,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
             for (int32_t k = 0; k < bw[f] && s_cur[f] + k < len; k++) {
                 uint32_t x = s_list[s_ptr[f] + s_cur[f] + k];
                 const hcache_t *hc = head_info(&hcache[(size_t)f * bmax + k], hpred + ((size_t)f * bmax + k) * maxp,
-                                               &w, x, path_ptr, E);
+                                               &w, x, &rt, E);
                 uint64_t rel = release_of(hc, completion, chunk_done, chunk_max, &w);
                 if (rel > t) break;
                 req_t *r = &reqs[nr++];
@@ -1278,7 +1391,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
             for (int32_t k = 0; k < bw[f] && s_cur[f] + k < len; k++) {
                 uint32_t x = s_list[s_ptr[f] + s_cur[f] + k];
                 const hcache_t *hc = head_info(&hcache[(size_t)f * bmax + k], hpred + ((size_t)f * bmax + k) * maxp,
-                                               &w, x, path_ptr, E);
+                                               &w, x, &rt, E);
                 uint64_t rel = release_of(hc, completion, chunk_done, chunk_max, &w);
                 if (rel > t) { if (rel < next) next = rel; break; }
             }
@@ -1316,7 +1429,7 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
                     if (completion[y] > rel) rel = completion[y];
             }
             uint64_t lsum = 0;
-            for (int64_t q = path_ptr[(int64_t)s * E + d]; q < path_ptr[(int64_t)s * E + d + 1]; q++)
+            for (int64_t q = PATH_LO(s, d); q < PATH_HI(s, d); q++)
                 lsum += (uint64_t)lat[path_link[q]];
             if (admit0[x] < rel) rc = OR_ERR_INVARIANT;
             if ((uint64_t)completion[x] < rel + lsum + 1) rc = OR_ERR_INVARIANT;
@@ -1339,8 +1452,10 @@ int oracle_simulate(int32_t n, int32_t E, const int32_t *row_ptr, const int32_t 
         stats->line_hops = (uint64_t)line_hops;
         stats->seconds = (double)(t1.tv_sec - t0.tv_sec) + 1e-9 * (double)(t1.tv_nsec - t0.tv_nsec);
     }
-    free(path_ptr); free(path_link); free(port_of); free(nports); free(tail_of);
+    routes_free(&rt); free(port_of); free(nports); free(tail_of);
     free(s_ptr); free(s_list); free(s_cur); free(preds); free(q_off); free(qbuf);
+    #undef PATH_LO
+    #undef PATH_HI
     free(qhead); free(qocc); free(owe_t); free(owe_n); free(owe_h); free(owe_c); free(owed); free(cptr); free(rr);
     free(fair_a); free(reqs); free(bucket_n); free(bucket_off);
     free(bucket); free(touched); free(active);

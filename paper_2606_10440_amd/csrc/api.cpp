@@ -63,7 +63,12 @@ struct sim_ctx {
     std::vector<int32_t> row_ptr, col_idx, tail;
     std::vector<int32_t> bw, lat, cap;
     std::vector<int32_t> credit;  // [S*m] credit return delays; empty = all 1
-    std::vector<int32_t> hops;  // [E*n]: hop count from node v to endpoint d (-1 none)
+    // minimal-hop routing: the reversed links, and the hop counts from every
+    // node to one destination endpoint at a time (computed when needed)
+    std::vector<int32_t> in_ptr, in_src;
+    mutable std::vector<int32_t> hop_to;
+    mutable std::vector<int32_t> hop_frontier;
+    mutable int32_t hop_dst = -1;
 
     // loaded workload
     bool loaded = false;
@@ -122,34 +127,41 @@ sim_status alloc(sim_ctx *c, std::vector<void *> &owner, size_t count, T **out) 
     return SIM_OK;
 }
 
-// Hop distances to every endpoint: breadth-first search from the endpoint
-// over reversed links.
-void build_hops(sim_ctx *c) {
+// The reversed links (for each node, the tails of its in-links).
+void build_in_links(sim_ctx *c) {
     const int32_t n = c->n, m = c->m;
-    std::vector<int32_t> in_ptr(n + 1, 0), in_src(m);
-    for (int32_t l = 0; l < m; l++) in_ptr[c->col_idx[l] + 1]++;
-    for (int32_t v = 0; v < n; v++) in_ptr[v + 1] += in_ptr[v];
-    std::vector<int32_t> fill(in_ptr.begin(), in_ptr.end() - 1);
-    for (int32_t l = 0; l < m; l++) in_src[fill[c->col_idx[l]]++] = c->tail[l];
-    c->hops.assign((size_t)c->E * n, -1);
-    std::vector<int32_t> frontier;
-    frontier.reserve(n);
-    for (int32_t d = 0; d < c->E; d++) {
-        int32_t *h = &c->hops[(size_t)d * n];
-        frontier.clear();
-        frontier.push_back(d);
-        h[d] = 0;
-        for (size_t q = 0; q < frontier.size(); q++) {
-            int32_t w = frontier[q];
-            for (int32_t e = in_ptr[w]; e < in_ptr[w + 1]; e++) {
-                int32_t u = in_src[e];
-                if (h[u] < 0) {
-                    h[u] = h[w] + 1;
-                    frontier.push_back(u);
-                }
+    c->in_ptr.assign(n + 1, 0);
+    c->in_src.assign(m, 0);
+    for (int32_t l = 0; l < m; l++) c->in_ptr[c->col_idx[l] + 1]++;
+    for (int32_t v = 0; v < n; v++) c->in_ptr[v + 1] += c->in_ptr[v];
+    std::vector<int32_t> fill(c->in_ptr.begin(), c->in_ptr.end() - 1);
+    for (int32_t l = 0; l < m; l++) c->in_src[fill[c->col_idx[l]]++] = c->tail[l];
+    c->hop_dst = -1;
+}
+
+// Hop distances from every node to endpoint d (-1: unreachable): a
+// breadth-first search from d over the reversed links, kept until the next
+// destination is asked for.
+const int32_t *hops_to(const sim_ctx *c, int32_t d) {
+    if (c->hop_dst == d) return c->hop_to.data();
+    c->hop_to.assign(c->n, -1);
+    int32_t *h = c->hop_to.data();
+    auto &frontier = c->hop_frontier;
+    frontier.clear();
+    frontier.push_back(d);
+    h[d] = 0;
+    for (size_t q = 0; q < frontier.size(); q++) {
+        const int32_t w = frontier[q];
+        for (int32_t e = c->in_ptr[w]; e < c->in_ptr[w + 1]; e++) {
+            const int32_t u = c->in_src[e];
+            if (h[u] < 0) {
+                h[u] = h[w] + 1;
+                frontier.push_back(u);
             }
         }
     }
+    c->hop_dst = d;
+    return h;
 }
 
 // Minimal-hop route of flow s -> d.  Among out-links whose head is one hop
@@ -158,7 +170,7 @@ void build_hops(sim_ctx *c) {
 // after the first.
 bool trace_route(const sim_ctx *c, int32_t s, int32_t d, std::vector<int32_t> &out) {
     out.clear();
-    const int32_t *h = &c->hops[(size_t)d * c->n];
+    const int32_t *h = hops_to(c, d);
     if (h[s] < 0) return false;
     uint32_t key = finalize32(((uint32_t)s << 16) | (uint32_t)d);
     int32_t ties = 0;
@@ -442,6 +454,9 @@ struct GridLayout {
     int32_t one_threads = 64, inl_max = 0;
     int64_t one_bytes = INT64_MAX;
     std::vector<int32_t> toff, iptr, inl;
+    // windowed form
+    int32_t window = 0, sring_max = 0, cring_max = 0;
+    std::vector<int32_t> sro, tro;
 };
 
 GridLayout grid_layout(const sim_ctx *c, const std::vector<int32_t> &fsrc, const std::vector<char> &has_stream,
@@ -604,25 +619,42 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     c->flow_path.clear();
     c->path_link.clear();
     std::vector<int32_t> rflow(nr);
-    std::vector<int32_t> hopsv;
     std::vector<int32_t> flow_hops;
+    // flow slots in order of first appearance; their routes are traced
+    // destination by destination (one hop table alive at a time)
+    std::vector<std::pair<int32_t, int32_t>> fpair;
     for (int64_t i = 0; i < nr; i++) {
         uint64_t key = ((uint64_t)(uint32_t)R.src[i] << 32) | (uint32_t)R.dst[i];
         auto it = c->flow_slot.find(key);
         if (it == c->flow_slot.end()) {
-            if (!trace_route(c, R.src[i], R.dst[i], hopsv))
-                return fail(c, SIM_ERR_UNREACHABLE, "no path from endpoint " + std::to_string(R.src[i]) +
-                                                        " to endpoint " + std::to_string(R.dst[i]));
-            int32_t slot = (int32_t)c->flow_path.size();
-            c->flow_path.push_back((int32_t)c->path_link.size());
-            c->path_link.insert(c->path_link.end(), hopsv.begin(), hopsv.end());
-            c->path_link.push_back(-(1 + slot));
-            flow_hops.push_back((int32_t)hopsv.size());
-            it = c->flow_slot.emplace(key, slot).first;
+            it = c->flow_slot.emplace(key, (int32_t)fpair.size()).first;
+            fpair.emplace_back(R.src[i], R.dst[i]);
         }
         rflow[i] = it->second;
     }
-    const int32_t nflows = (int32_t)c->flow_path.size();
+    const int32_t nflows = (int32_t)fpair.size();
+    {
+        std::vector<int32_t> by_dst(nflows);
+        for (int32_t f = 0; f < nflows; f++) by_dst[f] = f;
+        std::stable_sort(by_dst.begin(), by_dst.end(),
+                         [&](int32_t a, int32_t b) { return fpair[a].second < fpair[b].second; });
+        std::vector<std::vector<int32_t>> routes(nflows);
+        for (int32_t f : by_dst) {
+            if (!trace_route(c, fpair[f].first, fpair[f].second, routes[f]))
+                return fail(c, SIM_ERR_UNREACHABLE, "no path from endpoint " + std::to_string(fpair[f].first) +
+                                                        " to endpoint " + std::to_string(fpair[f].second));
+        }
+        size_t total = 0;
+        for (const auto &r : routes) total += r.size() + 1;
+        if (total >= (size_t)INT32_MAX) return fail(c, SIM_ERR_SIZE, "path table too large");
+        c->path_link.reserve(total);
+        for (int32_t f = 0; f < nflows; f++) {
+            c->flow_path.push_back((int32_t)c->path_link.size());
+            c->path_link.insert(c->path_link.end(), routes[f].begin(), routes[f].end());
+            c->path_link.push_back(-(1 + f));
+            flow_hops.push_back((int32_t)routes[f].size());
+        }
+    }
     if (c->path_link.size() >= (size_t)INT32_MAX) return fail(c, SIM_ERR_SIZE, "path table too large");
 
     // per-flow sequence numbers (flows deliver in id order) and predecessor descriptors
@@ -1157,7 +1189,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     // (target sides of out-links, source sides of in-links, a stream), so
     // that every workgroup's per-cycle work is about the same.
     GridLayout gl;
-    const bool grid_try = c->S == 1 && !credits && !fair && nl >= 1 && bm <= 64;
+    const bool grid_try = c->S == 1 && !fair && nl >= 1 && bm <= 64;
     if (grid_try) {
         int want_nb = 32;
         if (const char *ev = std::getenv("SIMGPU_GRID_WGS")) want_nb = std::max(1, std::min(32, std::atoi(ev)));
@@ -1169,6 +1201,42 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
             gl.threads = gl.one_threads;
         } else {
             gl.one = false;
+        }
+        // Credit delays: the windowed form, when every traffic link has
+        // latency and credit delay of at least 2 and no line waits on another.
+        if (credits) {
+            int32_t win = INT32_MAX;
+            for (int32_t l : fsrc) win = std::min(win, std::min(c->lat[l], c->credit[l]));
+            if (gl.one && !any_preds && win >= 2) {
+                std::vector<int32_t> ring_of(nl);
+                for (int32_t i = 0; i < nl; i++) ring_of[i] = fifo_mask[fsrc[i]] + 1;
+                gl.sro.assign(nl, 0);
+                gl.tro.assign(nl, 0);
+                int64_t smax = 0, tmax = 0;
+                for (int32_t w = 0; w < gl.nb; w++) {
+                    int64_t so = 0, to = 0;
+                    for (int32_t q = gl.sptr[w]; q < gl.sptr[w + 1]; q++) {
+                        gl.sro[gl.slane[q]] = (int32_t)so;
+                        so += ring_of[gl.slane[q]];
+                    }
+                    for (int32_t q = gl.tptr[w]; q < gl.tptr[w + 1]; q++) {
+                        gl.tro[gl.tlane[q]] = (int32_t)to;
+                        to += ring_of[gl.tlane[q]];
+                    }
+                    smax = std::max(smax, so);
+                    tmax = std::max(tmax, to);
+                }
+                auto a16 = [](int64_t v) { return (v + 15) & ~(int64_t)15; };
+                int64_t b = a16(8 * (int64_t)gl.nt_max * (c->arb == SIM_ARB_LOWEST_ID ? 2 : 1));
+                if (c->arb == SIM_ARB_ROUND_ROBIN) b += a16(8 * (int64_t)gl.ns_max) + a16(4 * (int64_t)gl.inl_max);
+                b += a16(16 * smax) + a16(4 * tmax) + a16(4 * 4 * 2 * 16) + a16(4 * 32);
+                gl.window = win;
+                gl.sring_max = (int32_t)smax;
+                gl.cring_max = (int32_t)tmax;
+                gl.bytes = b;
+            } else {
+                gl.bytes = INT64_MAX;  // credit delays need the windowed form
+            }
         }
     }
     const bool grid_ok = grid_try && gl.bytes <= kLds;
@@ -1432,6 +1500,9 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         d.gd_fl_max = gl.fl_max;
         d.gd_one = gl.one ? 1 : 0;
         d.gd_inl_max = gl.inl_max;
+        d.gd_window = gl.window;
+        d.gd_sring_max = gl.sring_max;
+        d.gd_cring_max = gl.cring_max;
         int32_t *tmp_gd_sptr, *tmp_gd_slane, *tmp_gd_tptr, *tmp_gd_tlane, *tmp_gd_rqoff, *tmp_gd_path, *tmp_gd_floc,
             *tmp_gd_fptr, *tmp_gd_fown;
         UP(gl.sptr, gd_sptr);
@@ -1448,6 +1519,11 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
             UP(gl.toff, gd_toff);
             UP(gl.iptr, gd_iptr);
             UP(gl.inl, gd_inl);
+        }
+        if (gl.window > 0) {
+            int32_t *tmp_gd_sro, *tmp_gd_tro;
+            UP(gl.sro, gd_sro);
+            UP(gl.tro, gd_tro);
         }
     }
     if (engine == simgpu::kEngineWave) {
@@ -1558,7 +1634,7 @@ sim_status create_impl(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_
     c->bw.assign(bw, bw + pm);
     c->lat.assign(lat, lat + pm);
     c->cap.assign(cap, cap + pm);
-    build_hops(c);
+    build_in_links(c);
     *out = c;
     return SIM_OK;
 }

@@ -86,7 +86,11 @@ __global__ void grid_init(DevNet d) {
     // [0..5] arrival words of three successive cycles (64 bits each), [6..8]
     // the earliest future ready time offered by workgroups that moved nothing
     if (i0 < 16) d.gd_sync[i0] = (i0 >= 6 && i0 <= 8) ? kNever : 0u;
-    if (i0 == 0) d.status[0] = kRunRunning;
+    if (i0 == 0) {
+        d.status[0] = kRunRunning;
+        d.makespan[0] = 0;
+        d.cycles[0] = 0;
+    }
 }
 
 // Lines of a stream's current range that may be offered this cycle, from
@@ -1102,6 +1106,429 @@ __global__ void __launch_bounds__(1024) engine_grid1(DevNet d) {
     }
 }
 
+// ----------------------------------------------------------------------------
+// Windowed form (credit delays): when every traffic link has latency L >= 2
+// and credit delay D >= 2, a line appended at cycle t may leave at t + L and
+// a slot freed at t is usable from t + D, so within a window of
+// W = min(L, D) cycles (over all traffic links) no workgroup's work can
+// depend on another's.  Each workgroup then runs its own cycles of a window
+// with LDS-only phases and its own event skipping; the workgroups exchange
+// once per window:
+//   - a source side mirrors the FIFO entries appended in earlier windows into
+//     an LDS ring (with their next hops) and publishes its popped count; the
+//     cycle each entry left is written into the entry's slot;
+//   - a target side reads the cycles its popped entries left at (its credit
+//     returns) and publishes its appended count;
+//   - the next window starts at the earliest event any workgroup offers: its
+//     next local event, the ready time of a line it appended, or the return
+//     of a credit it freed (all at or after the window's end).
+// Lines that cross no window boundary never leave the workgroup's LDS copy;
+// the result is the same as the cycle-by-cycle model, because whatever one
+// workgroup does inside a window reaches another only from the next window.
+// Every bandwidth is 1 and no line has predecessors.
+template <int ARB>
+__global__ void __launch_bounds__(1024) engine_gridw(DevNet d) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    if (blockIdx.x % (unsigned)d.gd_stride) return;
+    const int w = (int)(blockIdx.x / (unsigned)d.gd_stride);
+    if (w >= d.gd_nb) return;
+    const int tid = threadIdx.x;
+    const int j = tid - 64;
+    const int nl = d.nl, m = d.m, NB = d.gd_nb;
+    const int sb = d.gd_sptr[w], ns = d.gd_sptr[w + 1] - sb;
+    const int tb = d.gd_tptr[w], nt = d.gd_tptr[w + 1] - tb;
+    const int NT = d.gd_nt_max, NS = d.gd_ns_max;
+    const bool hs = j >= 0 && j < ns, ht = j >= 0 && j < nt;
+    const uint32_t W = (uint32_t)d.gd_window;
+    const int nwave = (int)(blockDim.x >> 6);
+
+    size_t off = 0;
+    auto carve = [&](size_t bytes) {
+        unsigned char *p = smem + off;
+        off = (off + bytes + 15) & ~(size_t)15;
+        return p;
+    };
+    unsigned long long *word = (unsigned long long *)carve(8 * (size_t)NT * (ARB == 0 ? 2 : 1));
+    unsigned long long *post = (unsigned long long *)carve(ARB == 1 ? 8 * (size_t)NS : 0);
+    int32_t *inl = (int32_t *)carve(ARB == 1 ? 4 * (size_t)d.gd_inl_max : 0);
+    uint4 *sring = (uint4 *)carve(16 * (size_t)d.gd_sring_max);     // {line, ready, path index, next hop}
+    uint32_t *cring = (uint32_t *)carve(4 * (size_t)d.gd_cring_max);  // cycles popped entries left at
+    uint32_t *wred = (uint32_t *)carve(4 * 4 * 2 * 16);              // per wave: moved, next (two parities)
+    uint32_t *red = (uint32_t *)carve(4 * 32);
+    constexpr unsigned long long kNone = ARB == 0 ? ~0ull : 0ull;
+    constexpr unsigned long long kWon = ~0ull;
+
+    const int32_t *path = d.gd_path;
+    uint32_t *ring = reinterpret_cast<uint32_t *>(d.gfifo);  // {line, ready, path index, cycle it left}
+    uint32_t *comp = d.completion;
+    unsigned long long *tpub = d.gd_tpub;
+
+    for (int q = tid; q < NT * (ARB == 0 ? 2 : 1); q += blockDim.x) word[q] = kNone;
+    if (ARB == 1) {
+        const int i0 = d.gd_iptr[w], ni = d.gd_iptr[w + 1] - i0;
+        for (int q = tid; q < ni; q += blockDim.x) inl[q] = d.gd_inl[i0 + q];
+    }
+    if (tid < 32) red[tid] = tid == 2 ? kNever : 0u;  // [0] flags, [2] earliest offer
+    if (w == 0)
+        for (int q = tid; q < m; q += blockDim.x)
+            if (d.link_lane[q] < 0) {
+                d.tx_lines[q] = 0;
+                d.busy[q] = 0;
+            }
+
+    // source side
+    uint32_t s_lane = 0, s_fb = 0, s_fm = 0, s_D = 1, s_port = 0, s_lo = 0;
+    uint32_t head = 0, tkn = 0;
+    if (hs) {
+        s_lane = (uint32_t)d.gd_slane[sb + j];
+        const int link = d.ln_link[s_lane];
+        s_fb = (uint32_t)d.ln_fifo[s_lane];
+        s_fm = (uint32_t)d.ln_mask[s_lane];
+        s_D = (uint32_t)d.credit[link];
+        s_port = (uint32_t)d.ln_port[s_lane];
+        s_lo = (uint32_t)d.gd_sro[s_lane];
+    }
+    // target side
+    uint32_t t_lane = 0, t_link = 0, t_L = 0, t_cap = 0, t_P = 1, t_fb = 0, t_fm = 0, t_toff = 0, t_D = 1, t_co = 0;
+    uint32_t tail = 0, ret = 0, pk = 0, rr = 0;  // appended, credits back, pops known
+    unsigned long long tx = 0;
+    int R = 0, rend = 0;
+    uint32_t o = 0, r_st = 0, r_len = 0;
+    int r_path = 0;
+    if (ht) {
+        t_lane = (uint32_t)d.gd_tlane[tb + j];
+        t_link = (uint32_t)d.ln_link[t_lane];
+        t_L = (uint32_t)d.lat[t_link];
+        t_cap = (uint32_t)d.cap[t_link];
+        t_P = (uint32_t)d.ln_P[t_lane];
+        t_fb = (uint32_t)d.ln_fifo[t_lane];
+        t_fm = (uint32_t)d.ln_mask[t_lane];
+        t_D = (uint32_t)d.credit[t_link];
+        t_toff = ARB == 1 ? (uint32_t)d.gd_toff[t_lane] : 0u;
+        t_co = (uint32_t)d.gd_tro[t_lane];
+        R = d.ln_srbeg[t_lane];
+        rend = d.ln_srend[t_lane];
+        if (R < rend) {
+            r_st = d.r_start[R];
+            r_len = d.r_len[R];
+            r_path = d.r_path[R];
+        }
+    }
+    __syncthreads();
+
+    uint32_t T0 = 0, maxcomp = 0;
+    uint64_t widx = 0, local_cycles = 0;
+    int32_t state = d.T > 0 ? kRunRunning : kRunOk;
+    uint32_t lpar = 0;  // parity of the per-wave reduction slots
+
+    while (state == kRunRunning) {
+        const uint32_t wend = T0 + W;  // this window: cycles T0 .. wend - 1
+        uint32_t t = T0;
+        uint32_t offer = kNever;       // this thread's events at or after wend
+        bool over = false;
+        // ------------------------------------------------ cycles of the window
+        for (;;) {
+            unsigned long long *wcur = ARB == 0 ? word + (size_t)(lpar & 1u) * NT : word;
+            uint32_t next = kNever;
+            bool moved = false;
+            bool req_f = false, sink_f = false;
+            uint4 he = make_uint4(0, 0, 0, 0);
+            if (hs && head != tkn) {
+                he = sring[s_lo + (head & s_fm)];
+                if (he.y > t) {
+                    next = he.y;
+                } else if ((int32_t)he.w < 0) {
+                    sink_f = true;
+                } else {
+                    req_f = true;
+                    const unsigned long long key = ((unsigned long long)he.x << 32) | (he.z + 1u);
+                    if (ARB == 1) {
+                        post[j] = key;
+                        atomicOr(&wcur[he.w], 1ull << s_port);
+                    } else {
+                        atomicMin(&wcur[he.w], key);
+                    }
+                }
+            }
+            bool sreq = false;
+            if (ht && R < rend) {
+                sreq = true;
+                if (ARB == 1)
+                    atomicOr(&wcur[j], 1ull << (t_P - 1u));
+                else
+                    atomicMin(&wcur[j], ((unsigned long long)(r_st + o) << 32) | (uint32_t)r_path);
+            }
+            __syncthreads();
+            // ---- grants and appends
+            bool sdep = false;
+            if (ht) {
+                if (ARB == 0) word[(size_t)((lpar & 1u) ^ 1u) * NT + j] = kNone;
+                while (ret != pk && cring[t_co + (ret & t_fm)] + t_D <= t) ret++;  // credits back by t
+                const unsigned long long wv = wcur[j];
+                if (wv != kNone) {
+                    if (ARB == 1) wcur[j] = 0ull;
+                    if (tail - ret >= t_cap) {
+                        if (ARB == 0) wcur[j] = kNone;
+                    } else {
+                        uint32_t x, pp;
+                        if (ARB == 1) {
+                            const unsigned long long hi = wv >> rr;
+                            const uint32_t p = hi ? rr + (uint32_t)__builtin_ctzll(hi) : (uint32_t)__builtin_ctzll(wv);
+                            const int src = inl[t_toff + p];
+                            if (src < 0) {
+                                x = r_st + o;
+                                pp = (uint32_t)r_path;
+                                sdep = true;
+                            } else {
+                                const unsigned long long pw = post[src];
+                                post[src] = kWon;
+                                x = (uint32_t)(pw >> 32);
+                                pp = (uint32_t)pw;
+                            }
+                            rr = p + 1u == t_P ? 0u : p + 1u;
+                        } else {
+                            x = (uint32_t)(wv >> 32);
+                            pp = (uint32_t)wv;
+                        }
+                        uint32_t *e = ring + 4 * (size_t)(t_fb + (tail & t_fm));
+                        st_dev(e, x);
+                        st_dev(e + 1, t + t_L);
+                        st_dev(e + 2, pp);
+                        tail++;
+                        tx++;
+                        moved = true;
+                        offer = min(offer, t + t_L);  // its consumer's event
+                    }
+                }
+                if (ret != pk) next = min(next, cring[t_co + (ret & t_fm)] + t_D);  // a credit coming back
+            }
+            __syncthreads();
+            // ---- departures
+            if (hs) {
+                bool gone = sink_f;
+                if (sink_f) {
+                    comp[he.x] = t + 1;
+                    maxcomp = max(maxcomp, t + 1);
+                } else if (req_f) {
+                    gone = ARB == 1 ? post[j] == kWon : (uint32_t)(wcur[he.w] >> 32) == he.x;
+                }
+                if (gone) {
+                    st_dev(ring + 4 * (size_t)(s_fb + (head & s_fm)) + 3, t);  // the cycle it left
+                    head++;
+                    moved = true;
+                    offer = min(offer, t + s_D);  // its credit comes back
+                    if (head != tkn) {
+                        const uint32_t r2 = sring[s_lo + (head & s_fm)].y;
+                        next = min(next, r2 > t ? r2 : t + 1);
+                    }
+                }
+            }
+            if (ht && sreq && (ARB == 1 ? sdep : (uint32_t)(wcur[j] >> 32) == r_st + o)) {
+                moved = true;
+                if (++o == r_len) {
+                    o = 0;
+                    R++;
+                    if (R < rend) {
+                        r_st = d.r_start[R];
+                        r_len = d.r_len[R];
+                        r_path = d.r_path[R];
+                    }
+                }
+            }
+            // ---- local time advance
+            {
+                const bool wm = __ballot(moved) != 0;
+                uint32_t v = next;
+#pragma unroll
+                for (int sh = 32; sh >= 1; sh >>= 1) {
+                    const uint32_t u = (uint32_t)__shfl_xor((int)v, sh);
+                    v = u < v ? u : v;
+                }
+                if ((tid & 63) == 0) {
+                    wred[(lpar & 1u) * 32 + (tid >> 6) * 2] = wm ? 1u : 0u;
+                    wred[(lpar & 1u) * 32 + (tid >> 6) * 2 + 1] = v;
+                }
+            }
+            __syncthreads();
+            bool any_moved = false;
+            uint32_t nx = kNever;
+            for (int q = 0; q < nwave; q++) {
+                any_moved = any_moved || wred[(lpar & 1u) * 32 + q * 2] != 0u;
+                nx = min(nx, wred[(lpar & 1u) * 32 + q * 2 + 1]);
+            }
+            lpar++;
+            local_cycles++;
+            if (any_moved) nx = t + 1;
+            if (nx >= wend || nx == kNever) {
+                offer = min(offer, nx);
+                break;
+            }
+            if ((uint64_t)nx > d.max_cycles) {
+                over = true;
+                break;
+            }
+            t = nx;
+        }
+        // ------------------------------------------------ exchange
+        const unsigned long long tagw = (unsigned long long)(uint32_t)widx;
+        const int par = (int)(widx & 1u);
+        if (hs) {
+            __builtin_amdgcn_s_waitcnt(0x0F70);  // the cycles entries left at, before the count
+            st_dev(&tpub[((size_t)par * 2 + 1) * nl + s_lane], (tagw << 32) | head);
+        }
+        if (ht) {
+            __builtin_amdgcn_s_waitcnt(0x0F70);  // the entries, before the count
+            st_dev(&tpub[((size_t)par * 2) * nl + t_lane], (tagw << 32) | tail);
+        }
+        // lines left (offer already covers their events)
+        bool act = (hs && head != tkn) || (ht && (R < rend || tail != pk));
+        {
+            const bool wact = __ballot(act) != 0, wover = __ballot(over) != 0;
+            uint32_t v = offer;
+#pragma unroll
+            for (int sh = 32; sh >= 1; sh >>= 1) {
+                const uint32_t u = (uint32_t)__shfl_xor((int)v, sh);
+                v = u < v ? u : v;
+            }
+            if ((tid & 63) == 0) {
+                if (wact) atomicOr(&red[0], 1u);
+                if (wover) atomicOr(&red[0], 2u);
+                if (v != kNever) atomicMin(&red[2], v);
+            }
+        }
+        __syncthreads();
+        bool stuck = false;
+        if (tid == 0) {
+            const uint32_t flags = red[0];
+            const int r3 = (int)(widx % 3u);
+            unsigned long long *wordg = reinterpret_cast<unsigned long long *>(d.gd_sync) + r3;
+            uint32_t *nxtw = d.gd_sync + 6 + r3;
+            if (red[2] != kNever) __hip_atomic_fetch_min(nxtw, red[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __builtin_amdgcn_s_waitcnt(0x0F70);
+            const unsigned long long mine = 1ull | ((flags & 1u) ? 1ull << 32 : 0ull) | ((flags & 2u) ? 1ull << 48 : 0ull);
+            unsigned long long v = __hip_atomic_fetch_add(wordg, mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + mine;
+            uint32_t spins = 0;
+            while ((v & 0xFFFFull) < (unsigned long long)NB) {
+                if (++spins > kSpinLimit) {
+                    stuck = true;
+                    break;
+                }
+                v = ld_dev(wordg);
+            }
+            red[16] = stuck ? kNever : ld_dev(nxtw);
+            red[17] = (((v >> 32) & 0xFFFFull) ? 1u : 0u) | ((v >> 48) ? 2u : 0u);
+            if (w == 0 && !stuck) {
+                const int r5 = (int)((widx + 2) % 3u);
+                st_dev(reinterpret_cast<unsigned long long *>(d.gd_sync) + r5, 0ull);
+                st_dev(d.gd_sync + 6 + r5, kNever);
+            }
+            red[0] = 0u;
+            red[2] = kNever;
+        } else if (j >= 0) {
+            // the counts of this window; then the new entries (with their next
+            // hops) and the cycles the newly popped entries left at
+            uint32_t ntail = tkn, npk = pk;
+            uint32_t spins = 0;
+            if (hs) {
+                unsigned long long *pw = &tpub[((size_t)par * 2) * nl + s_lane];
+                unsigned long long v;
+                while (((v = ld_dev(pw)) >> 32) != tagw) {
+                    if (++spins > kSpinLimit) {
+                        stuck = true;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(2);
+                }
+                ntail = (uint32_t)v;
+            }
+            if (ht) {
+                unsigned long long *pw = &tpub[((size_t)par * 2 + 1) * nl + t_lane];
+                unsigned long long v;
+                while (((v = ld_dev(pw)) >> 32) != tagw) {
+                    if (++spins > kSpinLimit) {
+                        stuck = true;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(2);
+                }
+                npk = (uint32_t)v;
+            }
+            // in batches, so that the loads of a batch are in flight together
+            constexpr int kB = 8;
+            for (uint32_t i0 = tkn; hs && i0 != ntail;) {
+                const uint32_t nb = ntail - i0 < (uint32_t)kB ? ntail - i0 : (uint32_t)kB;
+                uint32_t ex[kB], er[kB], ep[kB];
+                int32_t nh[kB];
+#pragma unroll
+                for (int q = 0; q < kB; q++)
+                    if ((uint32_t)q < nb) {
+                        uint32_t *e = ring + 4 * (size_t)(s_fb + ((i0 + q) & s_fm));
+                        ex[q] = ld_dev(e);
+                        er[q] = ld_dev(e + 1);
+                        ep[q] = ld_dev(e + 2);
+                    }
+#pragma unroll
+                for (int q = 0; q < kB; q++)
+                    if ((uint32_t)q < nb) nh[q] = path[ep[q] + 1];
+#pragma unroll
+                for (int q = 0; q < kB; q++)
+                    if ((uint32_t)q < nb) sring[s_lo + ((i0 + q) & s_fm)] = make_uint4(ex[q], er[q], ep[q], (uint32_t)nh[q]);
+                i0 += nb;
+            }
+            for (uint32_t i0 = pk; ht && i0 != npk;) {
+                const uint32_t nb = npk - i0 < (uint32_t)kB ? npk - i0 : (uint32_t)kB;
+                uint32_t dc[kB];
+#pragma unroll
+                for (int q = 0; q < kB; q++)
+                    if ((uint32_t)q < nb) dc[q] = ld_dev(ring + 4 * (size_t)(t_fb + ((i0 + q) & t_fm)) + 3);
+#pragma unroll
+                for (int q = 0; q < kB; q++)
+                    if ((uint32_t)q < nb) cring[t_co + ((i0 + q) & t_fm)] = dc[q];
+                i0 += nb;
+            }
+            tkn = ntail;
+            pk = npk;
+        }
+        if (stuck) red[20] = 1u;
+        __syncthreads();
+        const uint32_t nxt = red[16];
+        const uint32_t flags = red[17];
+        widx++;
+        if (red[20]) {
+            state = kRunWatchdog;
+        } else if (flags & 2u) {
+            state = kRunMaxCycles;
+        } else if (!(flags & 1u)) {
+            state = kRunOk;
+        } else if (nxt == kNever) {
+            state = kRunDeadlock;
+        } else {
+            T0 = nxt;
+        }
+        if (state == kRunRunning && (uint64_t)T0 > d.max_cycles) state = kRunMaxCycles;
+        if (state == kRunRunning && local_cycles > d.watchdog) state = kRunWatchdog;
+        __syncthreads();
+    }
+    if (ht) {
+        d.tx_lines[t_link] = tx;
+        d.busy[t_link] = tx;
+    }
+    // makespan: the largest completion of any workgroup
+    {
+        uint32_t v = maxcomp;
+#pragma unroll
+        for (int sh = 32; sh >= 1; sh >>= 1) {
+            const uint32_t u = (uint32_t)__shfl_xor((int)v, sh);
+            v = u > v ? u : v;
+        }
+        if ((tid & 63) == 0 && v) atomicMax(&d.makespan[0], v);
+    }
+    if (tid == 0) {
+        atomicMax(&d.status[0], state);
+        atomicMax(reinterpret_cast<unsigned long long *>(&d.cycles[0]), (unsigned long long)local_cycles);
+    }
+}
+
 }  // namespace
 
 hipError_t launch_grid_any(const DevNet &d, hipStream_t st) {
@@ -1109,7 +1536,9 @@ hipError_t launch_grid_any(const DevNet &d, hipStream_t st) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const void *k;
-    if (d.gd_one)
+    if (d.gd_window > 0)
+        k = d.arb == 0 ? (const void *)engine_gridw<0> : (const void *)engine_gridw<1>;
+    else if (d.gd_one)
         k = d.arb == 0 ? (d.has_preds ? (const void *)engine_grid1<0, true> : (const void *)engine_grid1<0, false>)
                        : (d.has_preds ? (const void *)engine_grid1<1, true> : (const void *)engine_grid1<1, false>);
     else

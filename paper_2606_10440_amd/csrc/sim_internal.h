@@ -171,6 +171,11 @@ struct DevNet {
     // side per thread, in registers)
     int32_t gd_one;
     unsigned long long *gd_tpub;  // [2 parities x (appended, popped) x nl]: (cycle index << 32) | count
+    // windowed form (every traffic link with latency and credit delay >= 2):
+    // window length (0: not windowed), per-lane LDS ring offsets
+    int32_t gd_window;
+    int32_t gd_sring_max, gd_cring_max;  // most LDS ring entries of one workgroup's source / target sides
+    const int32_t *gd_sro, *gd_tro;      // [nl] offset of a lane's mirrored entries / credit cycles
     int32_t gd_inl_max;       // most in-port table entries of one workgroup
     const int32_t *gd_toff;   // [nl] offset of a lane's tail node in its workgroup's in-port table
     const int32_t *gd_iptr, *gd_inl;  // [gd_nb+1] CSR: per node of the workgroup, for each input

@@ -95,3 +95,26 @@ def test_credit_with_chunk_dependencies_not_on_wave(simmod, oracle_lib):
     check_vs_oracle(simmod, oracle_lib, w)
     with pytest.raises(pytest.skip.Exception):
         check_engine(simmod, oracle_lib, w, "wave")
+
+
+@pytest.mark.parametrize("arb", [0, 1])
+@pytest.mark.parametrize("seed", range(8))
+def test_windowed_grid(simmod, oracle_lib, arb, seed):
+    """The grid engine's windowed form: one-line-per-cycle graphs whose links
+    all have latency and credit delay of at least 2 (a k = 4 fat tree, or a
+    one-scenario torus), delays below, at and above the latency; every line,
+    counter and the makespan against the oracle."""
+    rng = np.random.default_rng(13000 + seed)
+    if seed % 2 == 0:
+        w = si.fat_tree(4, lat_seed=seed, lat_lo=2, lat_hi=int(rng.integers(3, 16)), cap=int(rng.integers(2, 9)),
+                        nbytes=128 * 16 * int(rng.integers(1, 4)), arb=arb,
+                        coll=int(rng.choice([si.COLL_ALLTOALL, si.COLL_ALLTOALL])))
+    else:
+        # shallow buffers deadlock this all-to-all (both sides must stop at the
+        # same point); deep ones finish
+        w = si.torus2d(4, 4, n_scenarios=1, seed=seed, bws=(1, 1), lat_lo=2, lat_hi=int(rng.integers(3, 12)),
+                       depths=(2, 4, 9) if seed < 4 else (24, 32, 48), nbytes=128 * 16 * 2, coll=si.COLL_ALLTOALL,
+                       arb=arb)
+    lo = np.maximum(2, w.lat - 3)
+    w.credit = rng.integers(lo, w.lat + 4).astype(np.int32)
+    check_engine(simmod, oracle_lib, w, "grid")
