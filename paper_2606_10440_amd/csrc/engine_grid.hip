@@ -950,11 +950,7 @@ __global__ void __launch_bounds__(1024) engine_grid1(DevNet d) {
                     if (R < rend) set_range(R);
                 }
             }
-            if (appended) {
-                act = true;
-                __builtin_amdgcn_s_waitcnt(0x0F70);  // the entry is stored before the count that covers it
-            }
-            st_dev(&tpub[((size_t)par * 2) * nl + t_lane], ((unsigned long long)(uint32_t)k << 32) | tail);
+            if (appended) act = true;
             if (R < rend) act = true;
         }
         if (PREDS) {
@@ -1022,10 +1018,14 @@ __global__ void __launch_bounds__(1024) engine_grid1(DevNet d) {
             red[(4 - p4) + 2] = kNever;
             red[24 + (par ^ 1)] = 0u;
         } else if (j >= 0) {
-            // While wave 0 waits: this cycle's counts of this thread's sides
-            // (the producers store them before they arrive), the head entry
-            // and its next hop.
+            // While wave 0 waits: this thread's appended count (once the
+            // entries it covers are stored), then this cycle's counts of this
+            // thread's sides, the head entry and its next hop.
             const unsigned long long tagk = (unsigned long long)(uint32_t)k;
+            if (ht) {
+                if (appended) __builtin_amdgcn_s_waitcnt(0x0F70);
+                st_dev(&tpub[((size_t)par * 2) * nl + t_lane], (tagk << 32) | tail);
+            }
             bool need_e = hs && !cval && head != tkn;  // an entry known before this cycle
             uint32_t ex = 0, er = 0, ep = 0;
             int32_t nh = kUnresolved;
