@@ -37,7 +37,7 @@ TXN_BYTES_HBM = 12              # and per line: stream/predecessor read, complet
 KERNEL_NAME = "engine_"         # substring of the engine kernels' symbols
 # workloads whose engines keep the queue state in device memory (L2/HBM) rather
 # than in LDS and registers: their roofline counts the HBM-resident bytes
-HBM_STATE = ("C3", "C4", "NOC2_ag")
+HBM_STATE = ("C3", "C4", "C4_credit", "NOC2_ag")
 
 DESCR = {
     "C1": "4-endpoint full mesh, direct all-reduce 64 KiB, b=1 L=10 cap=16, lowest-id",
@@ -52,6 +52,7 @@ for _k, _c in (("rhd", "recursive halving-doubling all-reduce"), ("dbt", "double
                ("ag", "ring all-gather")):
     DESCR["C5_" + _k] = DESCR["C5"].replace("ring all-reduce", _c)
 DESCR["C5_credit"] = DESCR["C5"] + "; credit delay = link latency"
+DESCR["C4_credit"] = DESCR["C4"] + "; credit delay = link latency"
 DESCR["NOC2_ag"] = ("1024 scenarios x 2 generic GPUs as NoCs (448 nodes each) + 32 scale-up switches, "
                     "put-based all-gather 2 MiB out per GPU as memcpy programs (32 WGs/GPU, unroll 4, "
                     "64 outstanding), channel latency in {1,2,4,8}, scale-up cable latency in {40,67,134}")

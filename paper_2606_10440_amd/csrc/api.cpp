@@ -1493,6 +1493,10 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         }
         d.gd_nb = gl.nb;
         d.gd_stride = 8;  // blocks w * 8: one die's CUs when blocks go round-robin over the 8 dies
+        if (const char *ev = std::getenv("SIMGPU_GRID_STRIDE")) {  // tests: workgroups spread over the dies
+            const int v = std::atoi(ev);
+            if (v >= 1 && v <= 8) d.gd_stride = v;
+        }
         d.gd_threads = gl.threads;
         d.gd_ns_max = gl.ns_max;
         d.gd_nt_max = gl.nt_max;

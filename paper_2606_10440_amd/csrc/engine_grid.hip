@@ -1227,18 +1227,56 @@ __global__ void __launch_bounds__(1024) engine_gridw(DevNet d) {
         uint32_t offer = kNever;       // this thread's events at or after wend
         bool over = false;
         // ------------------------------------------------ cycles of the window
+        // A cycle's departures are committed at the start of the next
+        // iteration (or before the exchange): whether anything moved is
+        // known after the grants (every departure other than to the sink is
+        // an append here, and a sink departure is decided with the request),
+        // so the workgroup's decision on its next cycle shares the barrier
+        // between grants and departures.
+        bool pend = false, req_f = false, sink_f = false, sreq = false, sdep = false;
+        uint4 he = make_uint4(0, 0, 0, 0);
+        uint32_t tD = t;
+        unsigned long long *wD = word;
+        auto depart = [&]() {
+            if (hs && (sink_f || req_f)) {
+                bool gone = sink_f;
+                if (sink_f) {
+                    comp[he.x] = tD + 1;
+                    maxcomp = max(maxcomp, tD + 1);
+                } else {
+                    gone = ARB == 1 ? post[j] == kWon : (uint32_t)(wD[he.w] >> 32) == he.x;
+                }
+                if (gone) {
+                    ring[4 * (size_t)(s_fb + (head & s_fm)) + 3] = tD;  // the cycle it left
+                    head++;
+                    offer = min(offer, tD + s_D);  // its credit comes back
+                }
+            }
+            if (ht && sreq && (ARB == 1 ? sdep : (uint32_t)(wD[j] >> 32) == r_st + o)) {
+                if (++o == r_len) {
+                    o = 0;
+                    R++;
+                    if (R < rend) {
+                        r_st = d.r_start[R];
+                        r_len = d.r_len[R];
+                        r_path = d.r_path[R];
+                    }
+                }
+            }
+        };
         for (;;) {
+            if (pend) depart();
             unsigned long long *wcur = ARB == 0 ? word + (size_t)(lpar & 1u) * NT : word;
             uint32_t next = kNever;
             bool moved = false;
-            bool req_f = false, sink_f = false;
-            uint4 he = make_uint4(0, 0, 0, 0);
+            req_f = sink_f = false;
             if (hs && head != tkn) {
                 he = sring[s_lo + (head & s_fm)];
                 if (he.y > t) {
                     next = he.y;
                 } else if ((int32_t)he.w < 0) {
                     sink_f = true;
+                    moved = true;
                 } else {
                     req_f = true;
                     const unsigned long long key = ((unsigned long long)he.x << 32) | (he.z + 1u);
@@ -1250,7 +1288,7 @@ __global__ void __launch_bounds__(1024) engine_gridw(DevNet d) {
                     }
                 }
             }
-            bool sreq = false;
+            sreq = false;
             if (ht && R < rend) {
                 sreq = true;
                 if (ARB == 1)
@@ -1260,7 +1298,7 @@ __global__ void __launch_bounds__(1024) engine_gridw(DevNet d) {
             }
             __syncthreads();
             // ---- grants and appends
-            bool sdep = false;
+            sdep = false;
             if (ht) {
                 if (ARB == 0) word[(size_t)((lpar & 1u) ^ 1u) * NT + j] = kNone;
                 while (ret != pk && cring[t_co + (ret & t_fm)] + t_D <= t) ret++;  // credits back by t
@@ -1290,10 +1328,9 @@ __global__ void __launch_bounds__(1024) engine_gridw(DevNet d) {
                             x = (uint32_t)(wv >> 32);
                             pp = (uint32_t)wv;
                         }
-                        uint32_t *e = ring + 4 * (size_t)(t_fb + (tail & t_fm));
-                        st_dev(e, x);
-                        st_dev(e + 1, t + t_L);
-                        st_dev(e + 2, pp);
+                        // plain stores: they are made visible, all at once, before the exchange
+                        *reinterpret_cast<uint4 *>(ring + 4 * (size_t)(t_fb + (tail & t_fm))) =
+                            make_uint4(x, t + t_L, pp, 0u);
                         tail++;
                         tx++;
                         moved = true;
@@ -1302,40 +1339,7 @@ __global__ void __launch_bounds__(1024) engine_gridw(DevNet d) {
                 }
                 if (ret != pk) next = min(next, cring[t_co + (ret & t_fm)] + t_D);  // a credit coming back
             }
-            __syncthreads();
-            // ---- departures
-            if (hs) {
-                bool gone = sink_f;
-                if (sink_f) {
-                    comp[he.x] = t + 1;
-                    maxcomp = max(maxcomp, t + 1);
-                } else if (req_f) {
-                    gone = ARB == 1 ? post[j] == kWon : (uint32_t)(wcur[he.w] >> 32) == he.x;
-                }
-                if (gone) {
-                    st_dev(ring + 4 * (size_t)(s_fb + (head & s_fm)) + 3, t);  // the cycle it left
-                    head++;
-                    moved = true;
-                    offer = min(offer, t + s_D);  // its credit comes back
-                    if (head != tkn) {
-                        const uint32_t r2 = sring[s_lo + (head & s_fm)].y;
-                        next = min(next, r2 > t ? r2 : t + 1);
-                    }
-                }
-            }
-            if (ht && sreq && (ARB == 1 ? sdep : (uint32_t)(wcur[j] >> 32) == r_st + o)) {
-                moved = true;
-                if (++o == r_len) {
-                    o = 0;
-                    R++;
-                    if (R < rend) {
-                        r_st = d.r_start[R];
-                        r_len = d.r_len[R];
-                        r_path = d.r_path[R];
-                    }
-                }
-            }
-            // ---- local time advance
+            // ---- the workgroup's next cycle
             {
                 const bool wm = __ballot(moved) != 0;
                 uint32_t v = next;
@@ -1356,30 +1360,36 @@ __global__ void __launch_bounds__(1024) engine_gridw(DevNet d) {
                 any_moved = any_moved || wred[(lpar & 1u) * 32 + q * 2] != 0u;
                 nx = min(nx, wred[(lpar & 1u) * 32 + q * 2 + 1]);
             }
+            pend = true;
+            tD = t;
+            wD = wcur;
             lpar++;
             local_cycles++;
             if (any_moved) nx = t + 1;
             if (nx >= wend || nx == kNever) {
+                depart();
                 offer = min(offer, nx);
                 break;
             }
             if ((uint64_t)nx > d.max_cycles) {
+                depart();
                 over = true;
                 break;
             }
             t = nx;
         }
         // ------------------------------------------------ exchange
+        // the window's entries and departure cycles (plain stores) reach
+        // device scope before the counts that cover them: every thread's
+        // stores are done, then one write-back of the die's cache
         const unsigned long long tagw = (unsigned long long)(uint32_t)widx;
         const int par = (int)(widx & 1u);
-        if (hs) {
-            __builtin_amdgcn_s_waitcnt(0x0F70);  // the cycles entries left at, before the count
-            st_dev(&tpub[((size_t)par * 2 + 1) * nl + s_lane], (tagw << 32) | head);
-        }
-        if (ht) {
-            __builtin_amdgcn_s_waitcnt(0x0F70);  // the entries, before the count
-            st_dev(&tpub[((size_t)par * 2) * nl + t_lane], (tagw << 32) | tail);
-        }
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        __syncthreads();
+        if (tid == 0) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __syncthreads();
+        if (hs) st_dev(&tpub[((size_t)par * 2 + 1) * nl + s_lane], (tagw << 32) | head);
+        if (ht) st_dev(&tpub[((size_t)par * 2) * nl + t_lane], (tagw << 32) | tail);
         // lines left (offer already covers their events)
         bool act = (hs && head != tkn) || (ht && (R < rend || tail != pk));
         {

@@ -118,3 +118,17 @@ def test_windowed_grid(simmod, oracle_lib, arb, seed):
     lo = np.maximum(2, w.lat - 3)
     w.credit = rng.integers(lo, w.lat + 4).astype(np.int32)
     check_engine(simmod, oracle_lib, w, "grid")
+
+
+@pytest.mark.parametrize("stride", [1, 8])
+@pytest.mark.parametrize("seed", [0, 2])
+def test_windowed_grid_placement(simmod, oracle_lib, stride, seed, monkeypatch):
+    """The windowed form with its workgroups launched as consecutive blocks
+    (spread over the dies) or every eighth block: the same bytes."""
+    monkeypatch.setenv("SIMGPU_GRID_STRIDE", str(stride))
+    monkeypatch.setenv("SIMGPU_GRID_WGS", "32")
+    rng = np.random.default_rng(14000 + seed)
+    w = si.fat_tree(4, lat_seed=seed, lat_lo=2, lat_hi=int(rng.integers(3, 16)), cap=int(rng.integers(2, 9)),
+                    nbytes=128 * 16 * 3, arb=seed % 2, coll=si.COLL_ALLTOALL)
+    w.credit = rng.integers(np.maximum(2, w.lat - 2), w.lat + 3).astype(np.int32)
+    check_engine(simmod, oracle_lib, w, "grid")

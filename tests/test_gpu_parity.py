@@ -680,3 +680,21 @@ def test_full_size_digest_grid(simmod, torch_cuda, name, general):
     assert _digest(comp.astype("<u4")) == g["completion_sha256"][0]
     assert _digest(r.tx_lines[0].cpu().numpy().astype("<u8")) == g["tx_lines_sha256"][0]
     assert _digest(r.busy_cycles[0].cpu().numpy().astype("<u8")) == g["busy_cycles_sha256"][0]
+
+
+@pytest.mark.parametrize("stride", [1, 8])
+@pytest.mark.parametrize("name", ["C2", "C3"])
+def test_grid_placement_same_bytes(simmod, torch_cuda, name, stride, monkeypatch):
+    """The grid engine with its workgroups launched as consecutive blocks
+    (spread over the dies) or every eighth block: the golden digests either
+    way (C2: the one-line form, C3: the general form)."""
+    monkeypatch.setenv("SIMGPU_ENGINE", "grid")
+    monkeypatch.setenv("SIMGPU_GRID_STRIDE", str(stride))
+    g = _golden(name)
+    w = si.config(name)
+    r = run_gpu(simmod, w)
+    assert r.status == 0, simmod.STATUS_NAMES[r.status]
+    comp = r.completion[0].cpu().numpy().view(np.uint32)
+    assert _digest(comp.astype("<u4")) == g["completion_sha256"][0]
+    assert _digest(r.tx_lines[0].cpu().numpy().astype("<u8")) == g["tx_lines_sha256"][0]
+    assert _digest(r.busy_cycles[0].cpu().numpy().astype("<u8")) == g["busy_cycles_sha256"][0]
