@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libsimgpu.so")
 CSRC = os.path.join(HERE, "csrc")
 SOURCES = ["api.cpp", "engine_launch.cpp", "engine_wg.hip", "engine_lane.hip", "engine_b1.hip",
-           "engine_wave.hip", "engine_grid.hip", "noalloc.hip"]
+           "engine_wave.hip", "engine_grid.hip", "engine_res.hip", "noalloc.hip"]
 ARCH = os.environ.get("SIMGPU_ARCH", "gfx950")
 OBJDIR = os.path.join(ROOT, "_build", "simgpu")
 
@@ -39,12 +39,18 @@ def _run(cmd, verbose):
         raise subprocess.CalledProcessError(r.returncode, cmd)
 
 
+# per-source flags: the resident engine's same-address LDS atomics with
+# lane-varying operands are combined per wave by a DPP scan instead of a
+# scalar loop over the active lanes
+EXTRA = {"engine_res.hip": ["-mllvm", "-amdgpu-atomic-optimizer-strategy=DPP"]}
+
+
 def build(verbose: bool = False) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     os.makedirs(OBJDIR, exist_ok=True)
     srcs = [s for s in SOURCES if os.path.exists(os.path.join(CSRC, s))]
     objs = [os.path.join(OBJDIR, s + ".o") for s in srcs]
-    jobs = [[hipcc, *FLAGS, "-c", "-o", o, os.path.join(CSRC, s)] for s, o in zip(srcs, objs)]
+    jobs = [[hipcc, *FLAGS, *EXTRA.get(s, []), "-c", "-o", o, os.path.join(CSRC, s)] for s, o in zip(srcs, objs)]
     with ThreadPoolExecutor(max_workers=min(len(jobs), 8)) as ex:
         list(ex.map(lambda c: _run(c, verbose), jobs))
     tmp = LIB + ".tmp"

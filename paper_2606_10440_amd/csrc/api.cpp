@@ -1240,6 +1240,61 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         }
     }
     const bool grid_ok = grid_try && gl.bytes <= kLds;
+    // Resident workgroup engine: a scenario's per-link state and parameters
+    // and the cycle's request records in LDS.  16-bit positions and counts
+    // (rings of at most 2^15 entries, fewer than 2^16 requests per target
+    // and cycle, links and sources below 2^16, latencies and credit delays
+    // below 2^16), records past the LDS capacity in HBM.  Workgroups per CU:
+    // the most (up to 4, as many as the batch needs) whose LDS leaves room
+    // for at least 256 records.
+    struct ResLayout {
+        bool ok = false;
+        int64_t off[20] = {};
+        int64_t bytes = 0, rcap = 0, scap = 0, ovf = 0;
+        int32_t threads = 256;
+    } res;
+    {
+        const int64_t nsrc_all = (int64_t)m + (int64_t)s_link.size();
+        bool ok = !fair && m <= 65535 && nsrc_all <= 65535 && bmax <= 255;
+        int64_t qmax = 0;  // request records one cycle can need
+        for (int32_t l : fsrc) {
+            ok = ok && fifo_mask[l] + 1 <= 32768 && (int64_t)nports_tail[l] * bmax <= 65533 && nports_tail[l] <= 255;
+            int32_t bl = 1;
+            for (int32_t sc = 0; sc < c->S; sc++) bl = std::max(bl, c->bw[(size_t)sc * m + l]);
+            qmax += std::min<int64_t>(bl, fifo_mask[l] + 1) + (has_stream[l] ? bl : 0);
+        }
+        for (size_t i = 0; i < c->lat.size() && ok; i++) ok = c->lat[i] <= 65535;
+        for (size_t i = 0; i < c->credit.size() && ok; i++) ok = c->credit[i] <= 65535;
+        ok = ok && qmax < (1 << 24);
+        auto a4 = [](int64_t v) { return (v + 3) & ~(int64_t)3; };
+        const int64_t scap = bmax > 4 ? std::min<int64_t>(512, (int64_t)m * ((bmax - 1) / 4)) : 0;
+        const int64_t sizes[17] = {2 * (int64_t)m, 2 * (int64_t)m, credits ? 2 * (int64_t)m : 0, 2 * (int64_t)m,
+                                   4 * (int64_t)m, m, (c->arb & SIM_ARB_ROUND_ROBIN) ? m : 0, 2 * (int64_t)m,
+                                   2 * (int64_t)m, credits ? 2 * (int64_t)m : 0, 4 * nsrc_all,
+                                   4 * (int64_t)s_link.size(), 4 * (int64_t)s_link.size(),
+                                   4 * ((nsrc_all + 31) / 32), 2 * nsrc_all, 2 * (int64_t)m, 4 * scap};
+        int64_t o = 0;
+        for (int i = 0; i < 17; i++) {
+            res.off[i] = o;
+            o += a4(sizes[i]);
+        }
+        res.off[18] = o;  // input ports per link (round-robin)
+        o += a4((c->arb & SIM_ARB_ROUND_ROBIN) ? m : 0);
+        res.off[17] = o;  // request records last
+        const int64_t room = kLds - 1024;  // room for the static LDS
+        const int want = c->S > 512 ? 4 : c->S > 256 ? 2 : 1;
+        for (int k = want; k >= 1 && ok && !res.ok; k--) {
+            const int64_t avail = room / k - o;
+            const int64_t rcap = std::min<int64_t>({qmax, avail / 28, 4096});
+            if (rcap < std::min<int64_t>(qmax, 256)) continue;
+            res.ok = true;
+            res.rcap = std::max<int64_t>(rcap, 1);
+            res.scap = scap;
+            res.ovf = std::max<int64_t>(0, qmax - res.rcap);
+            res.bytes = o + 28 * res.rcap;
+            res.threads = k == 1 ? 1024 : k == 2 ? 512 : 256;
+        }
+    }
     if ((credits && R.whole) || fair) wv.ok = false;
     const bool lane_ok = !credits && !fair && nl >= 1 && nl <= 1024 && bm <= 64 && lay_lds.bytes <= kLds;
     const bool lanehbm_ok = !credits && !fair && nl >= 1 && nl <= 1024 && bm <= 64 && lay_hbm.bytes <= kLds;
@@ -1255,6 +1310,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     if (grid_ok && gl.one && (engine == simgpu::kEngineB1 || engine == simgpu::kEngineLaneHbm ||
                               engine == simgpu::kEngineWorkgroup))
         engine = simgpu::kEngineGrid;
+    if (engine == simgpu::kEngineWorkgroup && res.ok) engine = simgpu::kEngineResident;
     bool wg_scan = false;  // workgroup engine without active sets (tests)
     if (const char *ev = std::getenv("SIMGPU_ENGINE")) {
         int want = -1;
@@ -1268,7 +1324,9 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         if (!std::strcmp(ev, "b1")) want = simgpu::kEngineB1;
         if (!std::strcmp(ev, "wave")) want = simgpu::kEngineWave;
         if (!std::strcmp(ev, "grid")) want = simgpu::kEngineGrid;
+        if (!std::strcmp(ev, "resident")) want = simgpu::kEngineResident;
         const bool ok = want == simgpu::kEngineWorkgroup || (want == simgpu::kEngineWave && wv.ok) ||
+                        (want == simgpu::kEngineResident && res.ok) ||
                         (want == simgpu::kEngineGrid && grid_ok) ||
                         (want == simgpu::kEngineLane && lane_ok) || (want == simgpu::kEngineLaneHbm && lanehbm_ok) ||
                         (want == simgpu::kEngineB1 && b1_usable);
@@ -1322,6 +1380,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     const int64_t lds_bytes = engine == simgpu::kEngineB1     ? b1_bytes
                               : engine == simgpu::kEngineWave ? wv.bytes
                               : engine == simgpu::kEngineGrid ? gl.bytes
+                              : engine == simgpu::kEngineResident ? res.bytes
                                                               : lay.bytes;
 
     // everything below touches the device
@@ -1352,12 +1411,15 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         // in LDS too when they fit and every scenario's workgroup is resident at once
         // (else fewer resident workgroups hide less HBM latency than the LDS saves)
         const int64_t nsrc_all = (int64_t)m + (int64_t)s_link.size();
-        const int64_t rcap = std::min<int64_t>(2048, nsrc_all * bmax);  // request list (8 B each)
+        const int64_t rcap = std::min<int64_t>(1024, nsrc_all * bmax);  // request list (8 B each)
+        // spill list (4 B each): the chunks after the first of FIFO offers longer than one chunk
+        const int64_t scap = bmax > 4 ? std::min<int64_t>(512, (int64_t)m * ((bmax - 1) / 4)) : 0;
         // (+ one word: the request list is 8-byte aligned)
-        const int64_t act = 4 * ((nsrc_all + 31) / 32 + nsrc_all + (int64_t)m + 1) + 8 * rcap;
+        const int64_t act = 4 * ((nsrc_all + 31) / 32 + nsrc_all + (int64_t)m + 1) + 8 * rcap + 4 * scap;
         const int64_t room = kLds - 1024;  // room for the static LDS
         d.wg_act = (act <= room / 2 && !wg_scan) ? (int32_t)act : 0;
         d.wg_rcap = (int32_t)rcap;
+        d.wg_scap = (int32_t)scap;
         const int64_t words = 7 * (int64_t)m + nsrc_all + 2 * (int64_t)s_link.size();
         const int64_t bytes = words * 4 + d.wg_act;
         const int64_t per_cu = bytes <= room ? room / bytes : 0;
@@ -1407,7 +1469,12 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     d.path_in_lds = path_in_lds ? 1 : 0;
     d.req_slots = (int32_t)lr;
     // lane engines: rings of the traffic links only, in lane order
-    if (engine != simgpu::kEngineWorkgroup) d.fifo_total = (int32_t)lf;
+    if (engine != simgpu::kEngineWorkgroup && engine != simgpu::kEngineResident) d.fifo_total = (int32_t)lf;
+    for (int i = 0; i < 20; i++) d.wr_off[i] = (int32_t)res.off[i];
+    d.wr_rcap = (int32_t)res.rcap;
+    d.wr_scap = (int32_t)res.scap;
+    d.wr_ovf = res.ovf;
+    d.wr_threads = res.threads;
     sim_status st;
     auto &own = c->dev_static;
 #define UP(vec, field)                                         \
@@ -1440,7 +1507,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         int32_t *tmp_credit;
         UP(c->credit, credit);
     }
-    if (engine == simgpu::kEngineWorkgroup) {
+    if (engine == simgpu::kEngineWorkgroup || engine == simgpu::kEngineResident) {
         // streams to wake when a flow delivers: every flow that a range of the
         // stream waits on (flow-major CSR, each stream once per flow)
         std::vector<std::pair<int32_t, int32_t>> fs;
@@ -1563,6 +1630,21 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     if (engine == simgpu::kEngineB1) {  // uniform rings: lane i owns entries [i << lg, (i + 1) << lg)
         d.fifo_total = nl << d.b1_ring_lg;
         sl.add(&DevNet::gfifo, S * (size_t)d.fifo_total);
+    }
+    if (engine == simgpu::kEngineResident) {
+        sl.add(&DevNet::wr_frec, S * ftot);
+        sl.add(&DevNet::delivered, S * nflows);
+        if (res.ovf > 0) {
+            const size_t ov = S * (size_t)res.ovf;
+            sl.add(&DevNet::wr_ox, ov);
+            sl.add(&DevNet::wr_opp, ov);
+            sl.add(&DevNet::wr_okey, ov);
+            sl.add(&DevNet::wr_ots, ov);
+            sl.add(&DevNet::wr_osidx, ov);
+            sl.add(&DevNet::wr_ogl, ov);
+            sl.add(&DevNet::wr_osrc, ov);
+            sl.add(&DevNet::wr_og, ov);
+        }
     }
     if (engine == simgpu::kEngineWorkgroup) {
         sl.add(&DevNet::fifo_x, S * ftot);

@@ -11,6 +11,7 @@ int launch_engine(const DevNet &d, void *stream) {
     case kEngineB1: return (int)launch_b1_any(d, st);
     case kEngineWave: return (int)launch_wave_any(d, st);
     case kEngineGrid: return (int)launch_grid_any(d, st);
+    case kEngineResident: return (int)launch_resident(d, st);
     case kEngineLane:
     case kEngineLaneHbm: return (int)launch_lane_any(d, st);
     default: return (int)launch_workgroup(d, st);

@@ -1,0 +1,695 @@
+// Device engine of libsimgpu for large graphs batched over many scenarios:
+// the workgroup engine's phases with a scenario's per-link state, its link
+// parameters and the cycle's requests resident in LDS.
+//
+// One workgroup owns one scenario and runs it to completion in one launch.
+// LDS holds, per link: head and tail positions (with credit delays also the
+// credit position) as 16-bit counters over rings of at most 2^15 entries,
+// the number of requests received this cycle, bandwidth, capacity, latency,
+// the round-robin pointer and input-port count and this cycle's (segment
+// offset, grant count);
+// per source: where its block of request records starts and how many of them
+// it made; per stream: its cursor; the active sets (a live-source bitmap and
+// the cycle's source and target lists); the cycle's request records (line,
+// path index, key, target and slot, input port, grant) and the index lists of
+// the grant phase.  Records and index entries past the LDS capacity go to a
+// per-scenario overflow area in HBM.  FIFO entries stay in HBM, one 16-byte
+// record {line, ready cycle, path index} each.
+//
+// A cycle, each step ended by a workgroup barrier:
+//   A   the live-source bitmap is compacted into the source list;
+//   R   every listed source reserves a contiguous block of request records
+//       and fills it.  A FIFO link offers its ready heads (ready times never
+//       decrease along a FIFO, so the ready heads are a prefix and each
+//       chunk of heads can be tested alone): the first chunk inline, the
+//       later ones through a spill list, one chunk per thread after a
+//       barrier.  A stream offers its released lines: its ranges are read a
+//       window at a time with every predecessor count of the window, then
+//       the lines are counted, reserved and written in a second walk;
+//   G0  every target that received requests gets a segment of the sorted
+//       index list and its grant count g = min(b, free slots, requests);
+//   G1  every request drops its record index into its target's segment;
+//   G2  every request ranks itself by the keys in its segment (keys are
+//       distinct per target) and, with rank r < g, takes grant rank r;
+//   D   every source departs its longest granted prefix; lines leaving their
+//       last hop complete (cycle + 1) and bump their flow's delivered count;
+//   E   every target appends its departing grants in rank order
+//       (ready = cycle + L).
+// Then the time advance of the workgroup engine: the next cycle is t + 1 if
+// anything departed, else the earliest FIFO-head ready time or credit
+// return, else the scenario has deadlocked.
+#include <hip/hip_runtime.h>
+
+#include "sim_internal.h"
+
+namespace simgpu {
+
+namespace {
+
+constexpr int kC = 4;                        // FIFO heads per chunk (loads in flight together)
+constexpr int kW = 4;                        // stream ranges per window
+constexpr int kE = 6;                        // predecessor descriptors per load batch
+constexpr int kB = 4;                        // grants per batch in the departure and append steps
+constexpr uint32_t kNoSpill = 0xFFFFFFFFu;   // spill entry that holds no chunk
+// rts (target << 16 | slot) of records that no target ranks
+constexpr uint32_t kTsSink = 0xFFFFFFFFu;    // leaves the network: the sink takes it
+constexpr uint32_t kTsHole = 0xFFFFFFFEu;    // reserved for a head that was not ready
+// rg: grant rank (< 256), with kDep set once the source lets it depart
+constexpr uint16_t kNoGrant = 0xFFFFu;
+constexpr uint16_t kSinkGrant = 0x7FFFu;
+constexpr uint16_t kDep = 0x8000u;
+
+// A record field: entries below cap in LDS, the rest in HBM.
+template <typename T>
+struct Split {
+    T *lds;
+    T *hbm;  // entry q >= cap at hbm[q - cap]
+    uint32_t cap;
+    __device__ __forceinline__ T &operator[](uint32_t q) const { return q < cap ? lds[q] : hbm[q - cap]; }
+};
+
+template <int ARB, bool CR, int kThreads>
+__global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
+    extern __shared__ __align__(16) unsigned char res_lds[];
+    const int s = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int m = d.m;
+    const int ns = d.ns;
+    const int nsrc = m + ns;
+    const size_t sm = (size_t)s * m;
+    const int32_t *__restrict__ path = d.path_link;
+
+    uint16_t *qh = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[0]);
+    uint16_t *qt = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[1]);
+    uint16_t *qc = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[2]);   // CR
+    uint32_t *rqw = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[3]);  // two 16-bit counts per word
+    uint16_t *rq = reinterpret_cast<uint16_t *>(rqw);
+    uint32_t *kg = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[4]);   // segment | g << 24
+    uint8_t *bwl = res_lds + d.wr_off[5];
+    uint8_t *rrl = res_lds + d.wr_off[6];                                  // ARB == 1
+    uint8_t *npl = res_lds + d.wr_off[18];                                 // ARB == 1: input ports at the tail
+    uint16_t *capl = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[7]);
+    uint16_t *latl = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[8]);
+    uint16_t *crl = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[9]);  // CR: credit delay
+    uint32_t *sqn = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[10]); // first record << 8 | count
+    int32_t *cur_rng = reinterpret_cast<int32_t *>(res_lds + d.wr_off[11]);
+    uint32_t *cur_off = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[12]);
+    uint32_t *livew = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[13]);
+    uint16_t *alist = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[14]);
+    uint16_t *tlist = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[15]);
+    uint32_t *spill = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[16]);
+    const uint32_t rcap = (uint32_t)d.wr_rcap;
+    const uint32_t scap = (uint32_t)d.wr_scap;
+    const size_t ov = (size_t)s * d.wr_ovf;
+    unsigned char *rb = res_lds + d.wr_off[17];
+    const Split<uint32_t> rx{reinterpret_cast<uint32_t *>(rb), d.wr_ox + ov, rcap};
+    const Split<int32_t> rpp{reinterpret_cast<int32_t *>(rb + 4 * rcap), d.wr_opp + ov, rcap};
+    const Split<uint32_t> rkey{reinterpret_cast<uint32_t *>(rb + 8 * rcap), d.wr_okey + ov, rcap};
+    const Split<uint32_t> rts{reinterpret_cast<uint32_t *>(rb + 12 * rcap), d.wr_ots + ov, rcap};
+    const Split<uint32_t> sidx{reinterpret_cast<uint32_t *>(rb + 16 * rcap), d.wr_osidx + ov, rcap};
+    const Split<uint32_t> gl{reinterpret_cast<uint32_t *>(rb + 20 * rcap), d.wr_ogl + ov, rcap};
+    const Split<uint16_t> rport{reinterpret_cast<uint16_t *>(rb + 24 * rcap), d.wr_osrc + ov, rcap};  // ARB == 1
+    const Split<uint16_t> rg{reinterpret_cast<uint16_t *>(rb + 26 * rcap), d.wr_og + ov, rcap};
+
+    uint4 *frec = d.wr_frec + (size_t)s * d.fifo_total;
+    uint32_t *delivered = d.delivered + (size_t)s * d.nflows;
+    uint32_t *comp = d.completion + (size_t)s * d.T;
+    uint64_t *tx = d.tx_lines + sm;
+    uint64_t *busy = d.busy + sm;
+
+    __shared__ uint32_t sh_t, sh_next, sh_anydep, sh_ndone, sh_nalive, sh_nalive_s, sh_ntgt, sh_nreq, sh_nspill, sh_koff;
+    __shared__ int32_t sh_state;
+    const int nw = (nsrc + 31) / 32;
+    auto set_live = [&](int src) { atomicOr(&livew[src >> 5], 1u << (src & 31)); };
+    auto clear_live = [&](int src) { atomicAnd(&livew[src >> 5], ~(1u << (src & 31))); };
+    // n requests to target f: their first slot (16-bit count inside a 32-bit word)
+    auto take_slots = [&](int f, uint32_t n) -> uint32_t {
+        const uint32_t sh = 16u * (uint32_t)(f & 1);
+        return (atomicAdd(&rqw[f >> 1], n << sh) >> sh) & 0xFFFFu;
+    };
+
+    for (int l = tid; l < m; l += kThreads) {
+        qh[l] = 0;
+        qt[l] = 0;
+        if (CR) {
+            qc[l] = 0;
+            crl[l] = (uint16_t)d.credit[sm + l];
+        }
+        rq[l] = 0;
+        kg[l] = 0;
+        bwl[l] = (uint8_t)d.bw[sm + l];
+        if (ARB == 1) {
+            rrl[l] = 0;
+            npl[l] = (uint8_t)d.nports_tail[l];
+        }
+        capl[l] = (uint16_t)d.cap[sm + l];
+        latl[l] = (uint16_t)d.lat[sm + l];
+        tx[l] = 0;
+        busy[l] = 0;
+    }
+    for (int i = tid; i < nsrc; i += kThreads) sqn[i] = 0;
+    for (int j = tid; j < ns; j += kThreads) {
+        cur_rng[j] = d.s_rbeg[j];
+        cur_off[j] = 0;
+    }
+    for (int f = tid; f < d.nflows; f += kThreads) delivered[f] = 0;
+    for (int j = tid; j < nw; j += kThreads) livew[j] = 0;
+    if (tid == 0) {
+        sh_t = 0;
+        sh_state = d.T > 0 ? kRunRunning : kRunOk;
+        sh_next = kNever;
+        sh_anydep = 0;
+        sh_ndone = 0;
+        sh_nalive = 0;
+        sh_nalive_s = 0;
+        sh_ntgt = 0;
+        sh_nreq = 0;
+        sh_nspill = 0;
+        sh_koff = 0;
+    }
+    __syncthreads();
+    for (int j = tid; j < ns; j += kThreads)  // streams with lines are live from the start
+        if (d.s_rbeg[j] < d.s_rend[j]) set_live(m + j);
+    __syncthreads();
+
+    uint64_t done = 0, processed = 0;  // meaningful in thread 0
+    while (sh_state == kRunRunning) {
+        const uint32_t t = sh_t;
+        // ---------------------------------------------------------------- A
+        // one source per thread: live FIFO links from the front of the list,
+        // live streams from its back (a slot is a wave-wide count of one per
+        // live lane)
+        for (int i = tid; i < nsrc; i += kThreads)
+            if ((livew[i >> 5] >> (i & 31)) & 1u) {
+                if (i < m) alist[atomicAdd(&sh_nalive, 1u)] = (uint16_t)i;
+                else alist[nsrc - 1 - (int)atomicAdd(&sh_nalive_s, 1u)] = (uint16_t)i;
+            }
+        __syncthreads();
+        // FIFO links and streams take different code paths: the first half of
+        // the workgroup's waves walks the links, the second half the streams
+        const int nfl = (int)sh_nalive, nst = (int)sh_nalive_s;
+        constexpr int kF = kThreads / 2;
+        const bool fside = tid < kF;
+        const int a0 = fside ? tid : tid - kF;
+        const int na = fside ? nfl : nst;
+        auto src_at = [&](int a) -> int { return fside ? (int)alist[a] : (int)alist[nsrc - 1 - a]; };
+        // ---------------------------------------------------------------- R
+        // Heads k0 .. k0 + kC - 1 (below lim) of FIFO link l with head
+        // position h: their entries, and how many of them are ready (the
+        // first that is not offers its ready time as the next event).
+        auto load_heads = [&](int l, uint32_t h, int k0, int lim, uint4 *e) -> int {
+            const int base = d.fifo_off[l], mask = d.fifo_mask[l];
+#pragma unroll
+            for (int u = 0; u < kC; u++)
+                if (k0 + u < lim) e[u] = frec[base + (int)((h + (uint32_t)(k0 + u)) & (uint32_t)mask)];
+            int nrd = 0;
+            bool run = true;
+#pragma unroll
+            for (int u = 0; u < kC; u++) {
+                if (run && k0 + u < lim && e[u].y > t) atomicMin(&sh_next, e[u].y);  // first head not ready
+                run = run && k0 + u < lim && e[u].y <= t;
+                nrd += run ? 1 : 0;
+            }
+            return nrd;
+        };
+        // Records q0 + k0 + u of those heads: requests for u < nrd, holes for
+        // nrd <= u < nfill.
+        auto post_heads = [&](int l, int k0, int nrd, int nfill, const uint4 *e, uint32_t q0) {
+            int tg[kC];
+#pragma unroll
+            for (int u = 0; u < kC; u++)
+                if (u < nrd) tg[u] = path[(int)e[u].z + 1];
+            uint32_t P[kC];
+            if (ARB == 1) {
+#pragma unroll
+                for (int u = 0; u < kC; u++)
+                    if (u < nrd && tg[u] >= 0) P[u] = (uint32_t)npl[tg[u]];
+            }
+            const uint32_t ph = ARB == 1 ? (uint32_t)d.port_at_head[l] : 0u;
+#pragma unroll
+            for (int u = 0; u < kC; u++) {
+                const int k = k0 + u;
+                const uint32_t q = q0 + (uint32_t)k;
+                if (u >= nrd) {
+                    if (u < nfill) rts[q] = kTsHole;
+                    continue;
+                }
+                rx[q] = e[u].x;
+                if (ARB == 1) rport[q] = (uint16_t)ph;
+                if (tg[u] < 0) {  // the sink takes everything
+                    rpp[q] = -tg[u] - 1;  // the flow
+                    rts[q] = kTsSink;
+                    rg[q] = kSinkGrant;
+                } else {
+                    rpp[q] = (int)e[u].z + 1;
+                    uint32_t key;
+                    if (ARB == 0) {
+                        key = e[u].x;
+                    } else {
+                        const uint32_t rot = (ph + P[u] - (uint32_t)rrl[tg[u]]) % P[u];
+                        key = (uint32_t)k * P[u] + rot;
+                    }
+                    rkey[q] = key;
+                    const uint32_t slot = take_slots(tg[u], 1u);
+                    rts[q] = ((uint32_t)tg[u] << 16) | slot;
+                    if (slot == 0u) tlist[atomicAdd(&sh_ntgt, 1u)] = (uint16_t)tg[u];
+                }
+            }
+        };
+        for (int a = a0; a < na; a += kF) {
+            const int sid = src_at(a);
+            if (fside) {
+                const int l = sid;
+                const uint32_t h = qh[l];
+                const uint32_t occ = (uint16_t)(qt[l] - h);
+                const int b = bwl[l];
+                if (CR) {
+                    // slots of lines that left at least credit cycles ago are free
+                    // again; the next return is an event of the time advance
+                    const int base = d.fifo_off[l], mask = d.fifo_mask[l];
+                    const uint32_t D = crl[l];
+                    uint32_t c = qc[l];
+                    while ((uint16_t)c != (uint16_t)h && frec[base + (int)(c & (uint32_t)mask)].y + D <= t) c++;
+                    qc[l] = (uint16_t)c;
+                    if ((uint16_t)c != (uint16_t)h) atomicMin(&sh_next, frec[base + (int)(c & (uint32_t)mask)].y + D);
+                    if ((uint16_t)c == qt[l]) clear_live(l);  // nothing held: every credit is back
+                }
+                const int lim = b < (int)occ ? b : (int)occ;
+                if (lim == 0) {
+                    sqn[l] = 0;
+                    continue;
+                }
+                // the first chunk's readiness decides the reservation: its ready
+                // heads, or (all of it ready) every head up to lim
+                uint4 e[kC];
+                const int nrd0 = load_heads(l, h, 0, lim, e);
+                const bool more = nrd0 == kC && lim > kC;
+                const uint32_t nres = more ? (uint32_t)lim : (uint32_t)nrd0;
+                const uint32_t q0 = nres ? atomicAdd(&sh_nreq, nres) : 0u;
+                post_heads(l, 0, nrd0, nrd0, e, q0);
+                int nr = nrd0;
+                if (more) {
+                    const uint32_t nch = (uint32_t)((lim - 1) / kC);
+                    const uint32_t s0 = atomicAdd(&sh_nspill, nch);
+                    if (s0 + nch <= scap) {
+                        for (uint32_t c = 0; c < nch; c++) spill[s0 + c] = ((uint32_t)l << 8) | (uint32_t)(kC * (c + 1));
+                    } else {  // the list is full: the later chunks inline
+                        for (uint32_t c = 0; s0 + c < scap && c < nch; c++) spill[s0 + c] = kNoSpill;
+                        bool open = true;
+                        for (int k0 = kC; k0 < lim; k0 += kC) {
+                            const int nfill = lim - k0 < kC ? lim - k0 : kC;
+                            int n = 0;
+                            if (open) {
+                                uint4 e2[kC];
+                                n = load_heads(l, h, k0, lim, e2);
+                                post_heads(l, k0, n, nfill, e2, q0);
+                            } else {  // past the first head that is not ready
+                                for (int u = 0; u < nfill; u++) rts[q0 + (uint32_t)(k0 + u)] = kTsHole;
+                            }
+                            nr += n;
+                            open = n == kC;
+                        }
+                    }
+                }
+                sqn[l] = (q0 << 8) | (uint32_t)nr;
+            } else {
+                const int j = sid - m;
+                const int f = d.s_link[j];
+                const int src = m + j;
+                const int R0 = cur_rng[j];
+                const uint32_t o0 = cur_off[j];
+                const int rend = d.s_rend[j];
+                const int b = bwl[f];
+                if (R0 >= rend) {
+                    clear_live(src);
+                    sqn[src] = 0;
+                    continue;
+                }
+                // count: ranges in order, kW at a time, with every predecessor
+                // count of the window; the lines from o0 on whose predecessors
+                // have all delivered (a prefix), at most b
+                int R = R0;
+                uint32_t o = o0;
+                int cnt = 0;
+                bool go = true;
+                while (go && cnt < b) {
+                    const int nwr = rend - R < kW ? rend - R : kW;
+                    uint32_t len[kW];
+                    int pq[kW + 1];
+#pragma unroll
+                    for (int u = 0; u < kW; u++)
+                        if (u < nwr) {
+                            len[u] = d.r_len[R + u];
+                            pq[u] = d.r_pd[R + u];
+                        }
+                    pq[kW] = d.r_pd[R + nwr];
+#pragma unroll
+                    for (int u = 1; u < kW; u++)
+                        if (u >= nwr) pq[u] = pq[kW];
+                    uint32_t A[kW];
+#pragma unroll
+                    for (int u = 0; u < kW; u++) A[u] = 0xFFFFFFFFu;
+                    // the first batch holds only the first range's descriptors, so
+                    // that a stream held back at its first line (the usual case)
+                    // stops after one batch
+                    const int qe0 = pq[1] - pq[0] < kE ? pq[1] : pq[0] + kE;
+                    for (int q0 = pq[0], qe = qe0; q0 < pq[kW];
+                         q0 = qe, qe = pq[kW] - qe < kE ? pq[kW] : qe + kE) {
+                        int fl[kE];
+                        uint32_t bs[kE], dv[kE];
+#pragma unroll
+                        for (int v = 0; v < kE; v++)
+                            if (q0 + v < qe) {
+                                fl[v] = d.pd_flow[q0 + v];
+                                bs[v] = d.pd_base[q0 + v];
+                            }
+#pragma unroll
+                        for (int v = 0; v < kE; v++)
+                            if (q0 + v < qe) dv[v] = delivered[fl[v]];
+#pragma unroll
+                        for (int v = 0; v < kE; v++) {
+                            const int q = q0 + v;
+                            if (q >= qe) continue;
+                            // lines o + i (first range) or i with delivered > base + i
+                            // (per line) or > base (per chunk)
+                            const uint32_t b0 = bs[v] + (q < pq[1] ? (o & d.pd_omask) : 0u);
+                            const uint32_t allow = dv[v] > b0 ? (d.pd_omask ? dv[v] - b0 : 0xFFFFFFFFu) : 0u;
+#pragma unroll
+                            for (int u = 0; u < kW; u++)
+                                if (q >= pq[u] && q < pq[u + 1]) A[u] = A[u] < allow ? A[u] : allow;
+                        }
+                        if (q0 == pq[0] && qe >= pq[1]) {  // the first range is known: taken whole?
+                            const uint32_t need = (uint32_t)(b - cnt) < len[0] - o ? (uint32_t)(b - cnt) : len[0] - o;
+                            if (A[0] < need) break;
+                        }
+                    }
+                    bool stop = false;
+#pragma unroll
+                    for (int u = 0; u < kW; u++) {
+                        if (u >= nwr || stop) continue;
+                        const uint32_t off = u == 0 ? o : 0u;
+                        uint32_t n = (uint32_t)(b - cnt) < len[u] - off ? (uint32_t)(b - cnt) : len[u] - off;
+                        n = n < A[u] ? n : A[u];
+                        cnt += (int)n;
+                        if (n == 0u || off + n < len[u]) stop = true;  // held back by a predecessor or by b
+                    }
+                    go = !stop && R + nwr < rend;
+                    R += nwr;
+                    o = 0;
+                }
+                if (cnt == 0) {
+                    clear_live(src);  // asleep until a flow it waits on delivers
+                    sqn[src] = 0;
+                    continue;
+                }
+                // reserve and write: the same walk takes whole ranges until cnt lines
+                const uint32_t q0 = atomicAdd(&sh_nreq, (uint32_t)cnt);
+                const uint32_t slot0 = take_slots(f, (uint32_t)cnt);
+                if (slot0 == 0u) tlist[atomicAdd(&sh_ntgt, 1u)] = (uint16_t)f;
+                uint32_t rot = 0;
+                uint32_t P = 1;
+                if (ARB == 1) {
+                    P = (uint32_t)npl[f];
+                    rot = ((P - 1u) + P - (uint32_t)rrl[f]) % P;  // a stream is the link's last port
+                }
+                R = R0;
+                o = o0;
+                int k = 0;
+                while (k < cnt && R < rend) {
+                    const int nwr = rend - R < kW ? rend - R : kW;
+                    uint32_t len[kW], st[kW];
+                    int rp[kW];
+#pragma unroll
+                    for (int u = 0; u < kW; u++)
+                        if (u < nwr) {
+                            len[u] = d.r_len[R + u];
+                            st[u] = d.r_start[R + u];
+                            rp[u] = d.r_path[R + u];
+                        }
+#pragma unroll
+                    for (int u = 0; u < kW; u++) {
+                        if (u >= nwr || k >= cnt) continue;
+                        const uint32_t off = u == 0 ? o : 0u;
+                        const uint32_t n = (uint32_t)(cnt - k) < len[u] - off ? (uint32_t)(cnt - k) : len[u] - off;
+                        for (uint32_t i = 0; i < n; i++) {
+                            const uint32_t q = q0 + (uint32_t)k + i;
+                            const uint32_t x = st[u] + off + i;
+                            rx[q] = x;
+                            rpp[q] = rp[u];
+                            if (ARB == 1) rport[q] = (uint16_t)(P - 1u);
+                            rkey[q] = ARB == 0 ? x : ((uint32_t)k + i) * P + rot;
+                            rts[q] = ((uint32_t)f << 16) | (slot0 + (uint32_t)k + i);
+                        }
+                        k += (int)n;
+                    }
+                    R += nwr;
+                    o = 0;
+                }
+                sqn[src] = (q0 << 8) | (uint32_t)cnt;
+            }
+        }
+        __syncthreads();
+        {   // the spilled chunks of long FIFO offers
+            const uint32_t nsp = sh_nspill < scap ? sh_nspill : scap;
+            for (uint32_t i = (uint32_t)tid; i < nsp; i += kThreads) {
+                const uint32_t v = spill[i];
+                if (v == kNoSpill) continue;
+                const int l = (int)(v >> 8), k0 = (int)(v & 255u);
+                const uint32_t h = qh[l];
+                const uint32_t occ = (uint16_t)(qt[l] - h);
+                const int b = bwl[l];
+                const int lim = b < (int)occ ? b : (int)occ;
+                const uint32_t q0 = sqn[l] >> 8;
+                uint4 e[kC];
+                const int n = load_heads(l, h, k0, lim, e);
+                post_heads(l, k0, n, lim - k0 < kC ? lim - k0 : kC, e, q0);
+                if (n) atomicMax(&sqn[l], (q0 << 8) | (uint32_t)(k0 + n));
+            }
+        }
+        __syncthreads();
+        // ---------------------------------------------------------------- G
+        const int ntgt = (int)sh_ntgt;
+        const uint32_t nreq = sh_nreq;
+        for (int a = tid; a < ntgt; a += kThreads) {  // G0: segments and grant counts
+            const int f = (int)tlist[a];
+            const uint32_t c = rq[f];
+            const int occ = (int)(uint16_t)(qt[f] - (CR ? qc[f] : qh[f]));
+            int g = bwl[f];
+            if ((int)capl[f] - occ < g) g = (int)capl[f] - occ;
+            if ((int)c < g) g = (int)c;
+            kg[f] = atomicAdd(&sh_koff, c) | ((uint32_t)(g > 0 ? g : 0) << 24);
+        }
+        __syncthreads();
+        for (uint32_t q = (uint32_t)tid; q < nreq; q += kThreads) {  // G1: indices into the segments
+            const uint32_t ts = rts[q];
+            if (ts >= kTsHole) continue;
+            sidx[(kg[ts >> 16] & 0xFFFFFFu) + (ts & 0xFFFFu)] = q;
+        }
+        __syncthreads();
+        for (uint32_t q = (uint32_t)tid; q < nreq; q += kThreads) {  // G2: ranks and grants
+            const uint32_t ts = rts[q];
+            if (ts >= kTsHole) continue;
+            const int f = (int)(ts >> 16);
+            const uint32_t v = kg[f];
+            const uint32_t seg = v & 0xFFFFFFu, g = v >> 24;
+            const uint32_t c = rq[f];
+            const uint32_t ki = rkey[q];
+            uint32_t rank = 0;
+            for (uint32_t jj = 0; jj < c; jj++) rank += rkey[sidx[seg + jj]] < ki ? 1u : 0u;
+            if (rank < g) {
+                gl[seg + rank] = q;
+                rg[q] = (uint16_t)rank;
+            } else {
+                rg[q] = kNoGrant;
+            }
+        }
+        __syncthreads();
+        // ---------------------------------------------------------------- D
+        for (int a = a0; a < na; a += kF) {
+            const int src = src_at(a);
+            const uint32_t v = sqn[src];
+            const int nr = (int)(v & 255u);
+            if (nr == 0) continue;
+            const uint32_t q0 = v >> 8;
+            // the longest granted prefix departs, kB grants read at a time
+            int dep = 0, sinks = 0;
+            for (int k0 = 0; k0 < nr; k0 += kB) {
+                uint16_t gr[kB];
+#pragma unroll
+                for (int u = 0; u < kB; u++) gr[u] = k0 + u < nr ? rg[q0 + (uint32_t)(k0 + u)] : kNoGrant;
+                int n = 0;
+                bool run = true;
+#pragma unroll
+                for (int u = 0; u < kB; u++) {
+                    run = run && gr[u] != kNoGrant;
+                    n += run ? 1 : 0;
+                }
+#pragma unroll
+                for (int u = 0; u < kB; u++) {
+                    if (u >= n) continue;
+                    const uint32_t q = q0 + (uint32_t)(k0 + u);
+                    if (gr[u] == kSinkGrant) {
+                        const int fl = rpp[q];
+                        comp[rx[q]] = t + 1;
+                        atomicAdd(&delivered[fl], 1u);
+                        sinks++;
+                        for (int w = d.fw_ptr[fl]; w < d.fw_ptr[fl + 1]; w++) set_live(m + d.fw_str[w]);
+                    } else {
+                        rg[q] = (uint16_t)(gr[u] | kDep);
+                    }
+                }
+                dep += n;
+                if (n < kB) break;
+            }
+            if (dep == 0) continue;
+            sh_anydep = 1;
+            if (fside) {
+                const uint32_t h = qh[src];
+                if (CR) {  // a left entry keeps its slot until its credit is back
+                    const int base = d.fifo_off[src], mask = d.fifo_mask[src];
+                    for (int k = 0; k < dep; k++) frec[base + (int)((h + (uint32_t)k) & (uint32_t)mask)].y = t;
+                }
+                const uint16_t nh = (uint16_t)(h + (uint32_t)dep);
+                qh[src] = nh;
+                if (!CR && nh == qt[src]) clear_live(src);  // emptied
+            } else {
+                const int j = src - m;
+                int R = cur_rng[j];
+                uint32_t o = cur_off[j] + (uint32_t)dep;
+                const int rend = d.s_rend[j];
+                bool go = R < rend;
+                while (go) {  // past the ranges it finished, kW lengths read at a time
+                    uint32_t len[kW];
+#pragma unroll
+                    for (int u = 0; u < kW; u++)
+                        if (R + u < rend) len[u] = d.r_len[R + u];
+#pragma unroll
+                    for (int u = 0; u < kW; u++) {
+                        if (!go) continue;
+                        if (R < rend && o >= len[u]) {
+                            o -= len[u];
+                            R++;
+                        } else {
+                            go = false;
+                        }
+                    }
+                    go = go && R < rend;
+                }
+                cur_rng[j] = R;
+                cur_off[j] = o;
+                if (R == rend) clear_live(src);
+            }
+            if (sinks) atomicAdd(&sh_ndone, (uint32_t)sinks);
+        }
+        __syncthreads();
+        // ---------------------------------------------------------------- E
+        for (int a = tid; a < ntgt; a += kThreads) {
+            const int f = (int)tlist[a];
+            rq[f] = 0;
+            const uint32_t v = kg[f];
+            const uint32_t seg = v & 0xFFFFFFu, g = v >> 24;
+            if (g == 0u) continue;
+            const int base = d.fifo_off[f], mask = d.fifo_mask[f];
+            const uint32_t ready = t + (uint32_t)latl[f];
+            uint32_t tl = qt[f];
+            uint32_t cnt = 0, last = 0;
+            for (uint32_t r0 = 0; r0 < g; r0 += kB) {  // the grants in rank order, kB at a time
+                uint32_t q[kB];
+                bool dp[kB];
+#pragma unroll
+                for (int u = 0; u < kB; u++) q[u] = r0 + u < g ? gl[seg + r0 + u] : 0u;
+#pragma unroll
+                for (int u = 0; u < kB; u++) dp[u] = r0 + u < g && (rg[q[u]] & kDep) != 0;
+                uint32_t x[kB], pp[kB];
+#pragma unroll
+                for (int u = 0; u < kB; u++)
+                    if (dp[u]) {
+                        x[u] = rx[q[u]];
+                        pp[u] = (uint32_t)rpp[q[u]];
+                    }
+#pragma unroll
+                for (int u = 0; u < kB; u++)
+                    if (dp[u]) {
+                        frec[base + (int)(tl & (uint32_t)mask)] = make_uint4(x[u], ready, pp[u], 0u);
+                        last = q[u];
+                        tl++;
+                        cnt++;
+                    }
+            }
+            if (cnt) {
+                set_live(f);
+                qt[f] = (uint16_t)tl;
+                atomicAdd(&tx[f], (unsigned long long)cnt);  // no read back: the counters only grow
+                atomicAdd(&busy[f], 1ull);
+                if (ARB == 1) {
+                    const uint32_t P = (uint32_t)npl[f];
+                    const uint32_t lp = rport[last];
+                    rrl[f] = (uint8_t)((lp + 1u) % P);
+                }
+            }
+        }
+        __syncthreads();
+        // ---------------------------------------------------------------- time
+        if (tid == 0) {
+            processed++;
+            done += sh_ndone;
+            uint32_t nt = t;
+            int32_t state = kRunRunning;
+            if (done == (uint64_t)d.T) {
+                state = kRunOk;
+                d.makespan[s] = t + 1;
+            } else if (sh_anydep) {
+                nt = t + 1;
+            } else if (sh_next == kNever) {
+                state = kRunDeadlock;
+            } else {
+                nt = sh_next;
+            }
+            if (state == kRunRunning && (uint64_t)nt > d.max_cycles) state = kRunMaxCycles;
+            if (state == kRunRunning && processed > d.watchdog) state = kRunWatchdog;
+            sh_t = nt;
+            sh_state = state;
+            sh_next = kNever;
+            sh_anydep = 0;
+            sh_ndone = 0;
+            sh_nalive = 0;
+            sh_nalive_s = 0;
+            sh_ntgt = 0;
+            sh_nreq = 0;
+            sh_nspill = 0;
+            sh_koff = 0;
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        if (d.T == 0) d.makespan[s] = 0;
+        d.status[s] = sh_state;
+        d.cycles[s] = processed;
+    }
+}
+
+template <int ARB, bool CR, int NT>
+hipError_t launch_res3(const DevNet &d, hipStream_t st) {
+    auto k = engine_res<ARB, CR, NT>;
+    if (d.lds_bytes > 65536)
+        (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
+    hipLaunchKernelGGL(k, dim3((unsigned)d.S), dim3(NT), (unsigned)d.lds_bytes, st, d);
+    return hipGetLastError();
+}
+
+template <int ARB, bool CR>
+hipError_t launch_res2(const DevNet &d, hipStream_t st) {
+    if (d.wr_threads >= 1024) return launch_res3<ARB, CR, 1024>(d, st);
+    if (d.wr_threads >= 512) return launch_res3<ARB, CR, 512>(d, st);
+    return launch_res3<ARB, CR, 256>(d, st);
+}
+
+}  // namespace
+
+hipError_t launch_resident(const DevNet &d, hipStream_t st) {
+    const bool cr = d.credit != nullptr;
+    if (d.arb & 1) return cr ? launch_res2<1, true>(d, st) : launch_res2<1, false>(d, st);
+    return cr ? launch_res2<0, true>(d, st) : launch_res2<0, false>(d, st);
+}
+
+}  // namespace simgpu

@@ -47,6 +47,11 @@ namespace {
 // FIFO heads, requests and grants of one source or target are handled kC at
 // a time, so that their memory loads are in flight together.
 constexpr int kC = 4;
+// Stream offers read kW ranges at a time and their predecessor descriptors
+// kE at a time.
+constexpr int kW = 4;
+constexpr int kE = 8;
+constexpr uint32_t kNoSpill = 0xFFFFFFFFu;  // a spill-list entry that holds no chunk
 
 // SM: the per-link and per-stream scalars (queue pointers, request and grant
 // counts, round-robin and class pointers, stream cursors) live in LDS, so
@@ -115,10 +120,10 @@ __global__ void __launch_bounds__(kThreads, 4) engine_wg(DevNet d) {
     uint64_t *busy = d.busy + sm;
     const int32_t *__restrict__ path = d.path_link;
 
-    __shared__ uint32_t sh_t, sh_next, sh_anydep, sh_ndone, sh_nalive, sh_ntgt, sh_nreq;
+    __shared__ uint32_t sh_t, sh_next, sh_anydep, sh_ndone, sh_nalive, sh_ntgt, sh_nreq, sh_nspill;
     __shared__ int32_t sh_state;
     // active sets: live-source bitmap [nw], live-source list [m + ns], target list [m],
-    // request list [wg_rcap] of (target, slot)
+    // request list [wg_rcap] of (target, slot), spill list [wg_scap]
     const int nw = (int)((nsrc + 31) / 32);
     const size_t aoff = SM ? (size_t)d.wg_lds : 0;
     uint32_t *livew = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(wg_lds) + aoff);
@@ -127,6 +132,9 @@ __global__ void __launch_bounds__(kThreads, 4) engine_wg(DevNet d) {
     uint2 *rlist = reinterpret_cast<uint2 *>(reinterpret_cast<unsigned char *>(wg_lds) +
                                              ((aoff + 4 * ((size_t)nw + nsrc + (size_t)m) + 7) & ~(size_t)7));
     const uint32_t rcap = (uint32_t)d.wg_rcap;
+    // spill list [wg_scap]: chunks of long FIFO offers, (link << 8 | first head)
+    uint32_t *spill = reinterpret_cast<uint32_t *>(rlist + rcap);
+    const uint32_t scap = ACT ? (uint32_t)d.wg_scap : 0u;
     auto post = [&](int tgt, uint32_t slot) {  // a request's place in the active sets
         if (slot == 0u) tlist[atomicAdd(&sh_ntgt, 1u)] = tgt;
         const uint32_t q = atomicAdd(&sh_nreq, 1u);
@@ -165,6 +173,7 @@ __global__ void __launch_bounds__(kThreads, 4) engine_wg(DevNet d) {
         sh_nalive = 0;
         sh_ntgt = 0;
         sh_nreq = 0;
+        sh_nspill = 0;
     }
     __syncthreads();
     if constexpr (ACT) {  // streams with lines are live from the start; links start empty
@@ -191,6 +200,71 @@ __global__ void __launch_bounds__(kThreads, 4) engine_wg(DevNet d) {
         }
         const int nsrc_now = ACT ? (int)sh_nalive : nact;
         // ---------------------------------------------------------------- R
+        // The ready heads of FIFO link l from head k0 on (below lim), kC of
+        // them with their loads in flight together, post their requests;
+        // returns how many were ready.  Ready times never decrease along a
+        // FIFO, so the ready heads are a prefix and a chunk needs no
+        // knowledge of the chunks before it: the first head that is not
+        // ready offers the next event, and a later one offers no earlier one.
+        auto offer_heads = [&](int l, uint32_t h, int k0, int lim) -> int {
+            const int base = d.fifo_off[l], mask = d.fifo_mask[l];
+            int e[kC];
+            uint32_t rdy[kC];
+#pragma unroll
+            for (int u = 0; u < kC; u++) {
+                e[u] = base + (int)((h + (uint32_t)(k0 + u)) & (uint32_t)mask);
+                rdy[u] = k0 + u < lim ? frdy[e[u]] : kNever;
+            }
+            int nrd = 0;
+            bool run = true;
+#pragma unroll
+            for (int u = 0; u < kC; u++) {
+                if (run && k0 + u < lim && rdy[u] > t) atomicMin(&sh_next, rdy[u]);  // first head not ready
+                run = run && k0 + u < lim && rdy[u] <= t;
+                nrd += run ? 1 : 0;
+            }
+            uint32_t x[kC];
+            int pp[kC], tg[kC];
+#pragma unroll
+            for (int u = 0; u < kC; u++)
+                if (u < nrd) {
+                    x[u] = fx[e[u]];
+                    pp[u] = fpp[e[u]] + 1;
+                }
+#pragma unroll
+            for (int u = 0; u < kC; u++)
+                if (u < nrd) tg[u] = path[pp[u]];
+            uint32_t P[kC], rot[kC];
+            if (d.arb & 1) {
+                const uint32_t ph = (uint32_t)d.port_at_head[l];
+#pragma unroll
+                for (int u = 0; u < kC; u++)
+                    if (u < nrd && tg[u] >= 0) {
+                        P[u] = (uint32_t)d.nports_tail[tg[u]];
+                        rot[u] = rr[tg[u]];
+                    }
+#pragma unroll
+                for (int u = 0; u < kC; u++)
+                    if (u < nrd && tg[u] >= 0) rot[u] = (ph + P[u] - rot[u]) % P[u];
+            }
+#pragma unroll
+            for (int u = 0; u < kC; u++) {
+                if (u >= nrd) continue;
+                const int k = k0 + u;
+                const size_t si = (size_t)l * bmax + k;
+                sreq_x[si] = x[u];
+                sreq_pp[si] = pp[u];
+                if (tg[u] < 0) {
+                    grant[si] = -2;  // the sink takes everything
+                } else {
+                    const uint32_t key = (d.arb & 1) == 0 ? x[u] : (uint32_t)k * P[u] + rot[u];
+                    const uint32_t slot = atomicAdd(&req_cnt[tg[u]], 1u);
+                    req_rec[d.req_off[tg[u]] + slot] = ((uint64_t)key << 32) | ((uint32_t)l << 8) | (uint32_t)k;
+                    if (ACT) post(tg[u], slot);
+                }
+            }
+            return nrd;
+        };
         for (int a = tid; a < nsrc_now; a += kThreads) {
             const int sid = ACT ? alist[a] : (a < d.n_fsrc ? d.fsrc_link[a] : m + (a - d.n_fsrc));
             if (sid < m) {
@@ -198,10 +272,10 @@ __global__ void __launch_bounds__(kThreads, 4) engine_wg(DevNet d) {
                 const uint32_t h = qhead[l];
                 const uint32_t occ = qtail[l] - h;
                 const int b = bw[l];
-                const int base = d.fifo_off[l], mask = d.fifo_mask[l];
                 if (cred) {
                     // slots of lines that left at least credit cycles ago are free
                     // again; the next return is an event of the time advance
+                    const int base = d.fifo_off[l], mask = d.fifo_mask[l];
                     const uint32_t D = (uint32_t)cred[l];
                     uint32_t qc = qcred[l];
                     while (qc != h && frdy[base + (int)(qc & (uint32_t)mask)] + D <= t) qc++;
@@ -209,66 +283,24 @@ __global__ void __launch_bounds__(kThreads, 4) engine_wg(DevNet d) {
                     if (qc != h) atomicMin(&sh_next, frdy[base + (int)(qc & (uint32_t)mask)] + D);
                     if (ACT && qc == qtail[l]) clear_live(l);  // nothing held: every credit is back
                 }
-                // the ready heads, kC at a time (their loads in flight together)
                 const int lim = b < (int)occ ? b : (int)occ;
-                int nr = 0;
-                bool run = true;
-                for (int k0 = 0; run && k0 < lim; k0 += kC) {
-                    int e[kC];
-                    uint32_t rdy[kC];
-#pragma unroll
-                    for (int u = 0; u < kC; u++) {
-                        e[u] = base + (int)((h + (uint32_t)(k0 + u)) & (uint32_t)mask);
-                        rdy[u] = k0 + u < lim ? frdy[e[u]] : kNever;
-                    }
-                    int nrd = 0;
-#pragma unroll
-                    for (int u = 0; u < kC; u++) {
-                        if (run && k0 + u < lim && rdy[u] > t) atomicMin(&sh_next, rdy[u]);  // first head not ready
-                        run = run && k0 + u < lim && rdy[u] <= t;
-                        nrd += run ? 1 : 0;
-                    }
-                    uint32_t x[kC];
-                    int pp[kC], tg[kC];
-#pragma unroll
-                    for (int u = 0; u < kC; u++)
-                        if (u < nrd) {
-                            x[u] = fx[e[u]];
-                            pp[u] = fpp[e[u]] + 1;
-                        }
-#pragma unroll
-                    for (int u = 0; u < kC; u++)
-                        if (u < nrd) tg[u] = path[pp[u]];
-                    uint32_t P[kC], rot[kC];
-                    if (d.arb & 1) {
-                        const uint32_t ph = (uint32_t)d.port_at_head[l];
-#pragma unroll
-                        for (int u = 0; u < kC; u++)
-                            if (u < nrd && tg[u] >= 0) {
-                                P[u] = (uint32_t)d.nports_tail[tg[u]];
-                                rot[u] = rr[tg[u]];
-                            }
-#pragma unroll
-                        for (int u = 0; u < kC; u++)
-                            if (u < nrd && tg[u] >= 0) rot[u] = (ph + P[u] - rot[u]) % P[u];
-                    }
-#pragma unroll
-                    for (int u = 0; u < kC; u++) {
-                        if (u >= nrd) continue;
-                        const int k = k0 + u;
-                        const size_t si = (size_t)l * bmax + k;
-                        sreq_x[si] = x[u];
-                        sreq_pp[si] = pp[u];
-                        if (tg[u] < 0) {
-                            grant[si] = -2;  // the sink takes everything
-                        } else {
-                            const uint32_t key = (d.arb & 1) == 0 ? x[u] : (uint32_t)k * P[u] + rot[u];
-                            const uint32_t slot = atomicAdd(&req_cnt[tg[u]], 1u);
-                            req_rec[d.req_off[tg[u]] + slot] = ((uint64_t)key << 32) | ((uint32_t)l << 8) | (uint32_t)k;
-                            if (ACT) post(tg[u], slot);
+                int nr = lim > 0 ? offer_heads(l, h, 0, lim) : 0;
+                if (nr == kC && lim > kC) {
+                    // every head of the first chunk is ready: the later chunks go
+                    // to the spill list, one per thread after the next barrier
+                    // (inline if the list is full)
+                    const uint32_t nch = (uint32_t)((lim - 1) / kC);
+                    const uint32_t s0 = ACT ? atomicAdd(&sh_nspill, nch) : scap;
+                    if (s0 + nch <= scap) {
+                        for (uint32_t c = 0; c < nch; c++) spill[s0 + c] = ((uint32_t)l << 8) | (uint32_t)(kC * (c + 1));
+                    } else {
+                        for (uint32_t c = 0; ACT && s0 + c < scap && c < nch; c++) spill[s0 + c] = kNoSpill;
+                        for (int k0 = kC; k0 < lim; k0 += kC) {
+                            const int n = offer_heads(l, h, k0, lim);
+                            nr += n;
+                            if (n < kC) break;
                         }
                     }
-                    nr += nrd;
                 }
                 sreq_n[l] = nr;
             } else {
@@ -281,62 +313,129 @@ __global__ void __launch_bounds__(kThreads, 4) engine_wg(DevNet d) {
                 const int b = bw[f];
                 const uint32_t P = (uint32_t)d.nports_tail[f];
                 if (ACT && R >= rend) clear_live(src);
-                // each range in turn: the lines from o on whose predecessors have all
-                // delivered (a prefix), all requested at once from the stream's link
+                // ranges in order, kW at a time (their lengths, first lines,
+                // paths and predecessor descriptors read together, then every
+                // predecessor count of the window): the lines from o on whose
+                // predecessors have all delivered (a prefix), all requested at
+                // once from the stream's link
                 const uint32_t rot = (d.arb & 1) ? ((P - 1) + P - rr[f]) % P : 0u;
                 int nr = 0;
-                while (nr < b && R < rend) {
-                    const int q0 = d.r_pd[R], q1 = d.r_pd[R + 1];
-                    const uint32_t len = d.r_len[R];
-                    uint32_t n = (uint32_t)(b - nr) < len - o ? (uint32_t)(b - nr) : len - o;
-                    for (int q = q0; q < q1 && n != 0u; q += kC) {
-                        int fl[kC];
-                        uint32_t bs[kC], dv[kC];
+                bool go = R < rend;
+                while (go && nr < b) {
+                    const int nw = rend - R < kW ? rend - R : kW;
+                    uint32_t len[kW], st[kW];
+                    int rp[kW], pq[kW + 1];
 #pragma unroll
-                        for (int u = 0; u < kC; u++)
-                            if (q + u < q1) {
-                                fl[u] = d.pd_flow[q + u];
-                                bs[u] = d.pd_base[q + u] + (o & d.pd_omask);
+                    for (int u = 0; u < kW; u++)
+                        if (u < nw) {
+                            len[u] = d.r_len[R + u];
+                            st[u] = d.r_start[R + u];
+                            rp[u] = d.r_path[R + u];
+                            pq[u] = d.r_pd[R + u];
+                        }
+                    pq[kW] = d.r_pd[R + nw];
+#pragma unroll
+                    for (int u = 1; u < kW; u++)
+                        if (u >= nw) pq[u] = pq[kW];  // empty spans past the window
+                    // allowance per range: lines o + i (range 0) or i (later
+                    // ranges) with delivered > base + i (per line) or > base
+                    uint32_t A[kW];
+#pragma unroll
+                    for (int u = 0; u < kW; u++) A[u] = 0xFFFFFFFFu;
+                    for (int q0 = pq[0]; q0 < pq[kW]; q0 += kE) {
+                        int fl[kE];
+                        uint32_t bs[kE], dv[kE];
+#pragma unroll
+                        for (int v = 0; v < kE; v++)
+                            if (q0 + v < pq[kW]) {
+                                fl[v] = d.pd_flow[q0 + v];
+                                bs[v] = d.pd_base[q0 + v];
                             }
 #pragma unroll
-                        for (int u = 0; u < kC; u++)
-                            if (q + u < q1) dv[u] = delivered[fl[u]];
+                        for (int v = 0; v < kE; v++)
+                            if (q0 + v < pq[kW]) dv[v] = delivered[fl[v]];
 #pragma unroll
-                        for (int u = 0; u < kC; u++)
-                            if (q + u < q1) {
-                                // lines o + i with delivered > base + i (per line) or > base (per chunk)
-                                const uint32_t allow = dv[u] > bs[u] ? (d.pd_omask ? dv[u] - bs[u] : 0xFFFFFFFFu) : 0u;
-                                n = n < allow ? n : allow;
-                            }
+                        for (int v = 0; v < kE; v++) {
+                            const int q = q0 + v;
+                            if (q >= pq[kW]) continue;
+                            const uint32_t b0 = bs[v] + (q < pq[1] ? (o & d.pd_omask) : 0u);
+                            const uint32_t allow = dv[v] > b0 ? (d.pd_omask ? dv[v] - b0 : 0xFFFFFFFFu) : 0u;
+#pragma unroll
+                            for (int u = 0; u < kW; u++)
+                                if (q >= pq[u] && q < pq[u + 1]) A[u] = A[u] < allow ? A[u] : allow;
+                        }
                     }
-                    if (n == 0u) {
+                    // take the ranges' lines in order
+                    const uint32_t o0 = o;
+                    uint32_t nu[kW];
+                    int cnt = 0;
+                    bool stop = false;
+#pragma unroll
+                    for (int u = 0; u < kW; u++) {
+                        nu[u] = 0;
+                        if (u >= nw || stop) continue;
+                        const uint32_t off = u == 0 ? o0 : 0u;
+                        uint32_t n = (uint32_t)(b - nr - cnt) < len[u] - off ? (uint32_t)(b - nr - cnt) : len[u] - off;
+                        n = n < A[u] ? n : A[u];
+                        nu[u] = n;
+                        cnt += (int)n;
+                        if (n == 0u || off + n < len[u]) {  // held back by a predecessor or by the bandwidth
+                            stop = true;
+                            R += u;
+                            o = off + n;
+                        }
+                    }
+                    if (!stop) {
+                        R += nw;
+                        o = 0;
+                    }
+                    go = !stop && R < rend;
+                    if (cnt == 0) {
                         if (ACT && nr == 0) clear_live(src);  // asleep until a flow it waits on delivers
                         break;
                     }
-                    const uint32_t x0 = d.r_start[R] + o;
-                    const int rp = d.r_path[R];
-                    const uint32_t slot0 = atomicAdd(&req_cnt[f], n);
+                    const uint32_t slot0 = atomicAdd(&req_cnt[f], (uint32_t)cnt);
                     uint64_t *rec = req_rec + d.req_off[f] + slot0;
-                    for (uint32_t i = 0; i < n; i++) {
-                        const uint32_t k = (uint32_t)nr + i;
-                        const size_t si = (size_t)src * bmax + k;
-                        sreq_x[si] = x0 + i;
-                        sreq_pp[si] = rp;
-                        const uint32_t key = (d.arb & 1) == 0 ? x0 + i : k * P + rot;
-                        rec[i] = ((uint64_t)key << 32) | ((uint32_t)src << 8) | k;
+                    uint32_t i0 = 0;
+#pragma unroll
+                    for (int u = 0; u < kW; u++) {
+                        const uint32_t x0 = st[u] + (u == 0 ? o0 : 0u);
+                        for (uint32_t i = 0; i < nu[u]; i++) {
+                            const uint32_t k = (uint32_t)nr + i0 + i;
+                            const size_t si = (size_t)src * bmax + k;
+                            const uint32_t x = x0 + i;
+                            sreq_x[si] = x;
+                            sreq_pp[si] = rp[u];
+                            const uint32_t key = (d.arb & 1) == 0 ? x : k * P + rot;
+                            rec[i0 + i] = ((uint64_t)key << 32) | ((uint32_t)src << 8) | k;
+                        }
+                        i0 += nu[u];
                     }
                     if (ACT) {
                         if (slot0 == 0u) tlist[atomicAdd(&sh_ntgt, 1u)] = f;
-                        const uint32_t q = atomicAdd(&sh_nreq, n);
-                        for (uint32_t i = 0; i < n && q + i < rcap; i++) rlist[q + i] = make_uint2((uint32_t)f, slot0 + i);
+                        const uint32_t q = atomicAdd(&sh_nreq, (uint32_t)cnt);
+                        for (uint32_t i = 0; i < (uint32_t)cnt && q + i < rcap; i++)
+                            rlist[q + i] = make_uint2((uint32_t)f, slot0 + i);
                     }
-                    nr += (int)n;
-                    o += n;
-                    if (o < len) break;  // held back by a predecessor or by the bandwidth
-                    R++;
-                    o = 0;
+                    nr += cnt;
                 }
                 sreq_n[src] = nr;
+            }
+        }
+        if constexpr (ACT) {
+            // the spilled chunks of long FIFO offers
+            __syncthreads();
+            const uint32_t ns_ = sh_nspill < scap ? sh_nspill : scap;
+            for (uint32_t i = (uint32_t)tid; i < ns_; i += kThreads) {
+                const uint32_t v = spill[i];
+                if (v == kNoSpill) continue;
+                const int l = (int)(v >> 8), k0 = (int)(v & 255u);
+                const uint32_t h = qhead[l];
+                const uint32_t occ = qtail[l] - h;
+                const int b = bw[l];
+                const int lim = b < (int)occ ? b : (int)occ;
+                const int n = offer_heads(l, h, k0, lim);
+                if (n) atomicMax(&sreq_n[l], k0 + n);
             }
         }
         __syncthreads();
@@ -590,6 +689,7 @@ __global__ void __launch_bounds__(kThreads, 4) engine_wg(DevNet d) {
             sh_nalive = 0;
             sh_ntgt = 0;
             sh_nreq = 0;
+            sh_nspill = 0;
         }
         __syncthreads();
     }

@@ -78,6 +78,7 @@ struct DevNet {
     int32_t wg_lds;       // workgroup engine: bytes of per-scenario scalars kept in LDS (0: in HBM)
     int32_t wg_act;       // workgroup engine: bytes of the active sets in LDS after them (0: full scans)
     int32_t wg_rcap;      // workgroup engine: capacity of the active sets' request list
+    int32_t wg_scap;      // workgroup engine: capacity of the active sets' spill list (chunks of long FIFO offers)
     uint32_t *qcred;      // [S*m] popped entries whose slot is free again (credit returned);
                           // a popped entry's fifo_rdy then holds the cycle it left
     uint32_t *rr;         // [S*m] round-robin pointer
@@ -181,6 +182,18 @@ struct DevNet {
     const int32_t *gd_iptr, *gd_inl;  // [gd_nb+1] CSR: per node of the workgroup, for each input
                                       //   port the local source side feeding it (-1: stream or none)
 
+    // resident workgroup engine: per-link state, link parameters and the
+    // cycle's request records of a scenario in LDS (byte offsets wr_off),
+    // records past wr_rcap in a per-scenario HBM overflow area of wr_ovf
+    // entries per field
+    int32_t wr_off[20];
+    int32_t wr_rcap, wr_scap, wr_threads;
+    int64_t wr_ovf;
+    uint4 *wr_frec;           // [S*fifo_total] FIFO entries {line, ready, path index, 0}
+    uint32_t *wr_ox, *wr_okey, *wr_ots, *wr_osidx, *wr_ogl;  // [S*wr_ovf] overflow records
+    int32_t *wr_opp;
+    uint16_t *wr_osrc, *wr_og;
+
     // outputs
     uint32_t *completion; // [S*T]
     uint64_t *tx_lines;   // [S*m]
@@ -191,7 +204,7 @@ struct DevNet {
 };
 
 enum : int32_t { kEngineWorkgroup = 0, kEngineLane = 1, kEngineLaneHbm = 2, kEngineB1 = 3, kEngineWave = 4,
-                 kEngineGrid = 5 };
+                 kEngineGrid = 5, kEngineResident = 6 };
 // Wave engine entry words: line id << kWaveXShift | local-flow index (0..3)
 // << 5, the low five bits free for a request slot number (so line ids must
 // be below 2^25 - 1).
@@ -218,5 +231,6 @@ hipError_t launch_lane_any(const DevNet &d, hipStream_t st);
 hipError_t launch_b1_any(const DevNet &d, hipStream_t st);
 hipError_t launch_wave_any(const DevNet &d, hipStream_t st);
 hipError_t launch_grid_any(const DevNet &d, hipStream_t st);
+hipError_t launch_resident(const DevNet &d, hipStream_t st);
 
 }  // namespace simgpu

@@ -20,7 +20,7 @@ import sim_inputs as si  # noqa: E402
 from paper_2606_10440_amd import sim  # noqa: E402
 from tests.test_gpu_fuzz import draw  # noqa: E402
 
-ENGINES = [None, "workgroup", "workgroup_scan", "lane", "lanehbm", "b1", "wave", "grid"]
+ENGINES = [None, "workgroup", "workgroup_scan", "lane", "lanehbm", "b1", "wave", "grid", "resident"]
 HOST_DONE = (sim.SIM_ERR_DEVICE, sim.SIM_ERR_OOM)
 
 

@@ -80,7 +80,7 @@ def test_credit_wave_torus(simmod, oracle_lib, arb, bws):
     check_engine(simmod, oracle_lib, w, "wave")
 
 
-@pytest.mark.parametrize("engine", ["wave", "workgroup", "workgroup_scan"])
+@pytest.mark.parametrize("engine", ["wave", "workgroup", "workgroup_scan", "resident"])
 def test_credit_wave_full_size_sample(simmod, oracle_lib, engine):
     w = si.take_scenarios(si.config("C5"), [3, 7, 2048, 4000])
     w.credit = w.lat.copy()

@@ -44,7 +44,7 @@ def test_memcpy_generic_gpu_local_copy(simmod, oracle_lib, U, W):
     check_vs_oracle(simmod, oracle_lib, wm)
 
 
-@pytest.mark.parametrize("engine", ["workgroup", "workgroup_scan", "lane", "lanehbm"])
+@pytest.mark.parametrize("engine", ["workgroup", "workgroup_scan", "lane", "lanehbm", "resident"])
 def test_memcpy_generic_gpu_sweep(simmod, oracle_lib, engine):
     w, lay = noc.gpu_noc(1)
     wm = noc.memcpy_workload(w, noc.local_copy_ops(lay, 32 * 8, n_wg=32, unroll=4, window=8), name="gpu_sweep")
@@ -124,7 +124,7 @@ def test_reducescatter_generic_gpu(simmod, oracle_lib, G, get):
     check_vs_oracle(simmod, oracle_lib, wm)
 
 
-@pytest.mark.parametrize("engine", ["workgroup", "workgroup_scan", "lane", "lanehbm"])
+@pytest.mark.parametrize("engine", ["workgroup", "workgroup_scan", "lane", "lanehbm", "resident"])
 @pytest.mark.parametrize("get", [True, False])
 def test_reducescatter_engines(simmod, oracle_lib, engine, get):
     w, lay = noc.gpu_noc(3, mesh=(2, 2), cus_per_router=2, ch_per_router=2, ports_per_router=1)

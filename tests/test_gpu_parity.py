@@ -369,7 +369,7 @@ def test_full_size_batched_digest(simmod, torch_cuda, name):
 
 # ----------------------------------------------------------------- every engine
 
-ENGINES = ["workgroup", "workgroup_scan", "lane", "lanehbm", "b1", "wave", "grid"]
+ENGINES = ["workgroup", "workgroup_scan", "lane", "lanehbm", "b1", "wave", "grid", "resident"]
 
 
 def run_engine(simmod, w, engine, txns=None):
@@ -465,7 +465,7 @@ def test_engines_random_dag_b1(simmod, oracle_lib, engine, seed):
     check_engine(simmod, oracle_lib, w, engine, txns=(src, dst, pptr, pidx))
 
 
-@pytest.mark.parametrize("engine", ["workgroup", "workgroup_scan", "lane", "lanehbm", "wave"])
+@pytest.mark.parametrize("engine", ["workgroup", "workgroup_scan", "lane", "lanehbm", "wave", "resident"])
 @pytest.mark.parametrize("seed", range(12))
 def test_engines_random_dag_multirate(simmod, oracle_lib, engine, seed):
     rng = np.random.default_rng(6000 + seed)
