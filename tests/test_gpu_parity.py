@@ -647,13 +647,14 @@ def test_wave_directed_ring_dags(simmod, oracle_lib, seed):
 
 
 @pytest.mark.parametrize("name,general", [("C1", False), ("C2", False), ("C3", False), ("C1_chunk", False),
-                                          ("C2_chunk", False), ("C4", False), ("C1", True), ("C2", True),
-                                          ("C2_chunk", True)])
+                                          ("C2_chunk", False), ("C4", False), ("C4_credit", False), ("C1", True),
+                                          ("C2", True), ("C2_chunk", True)])
 def test_full_size_digest_grid(simmod, torch_cuda, name, general):
     """The device-wide engine (one topology over many workgroups) on the
     single-topology benchmark workloads: the same bytes as the oracle's
     golden digests.  Graphs with every bandwidth 1 run its one-line form
-    unless the general form is asked for."""
+    unless the general form is asked for; C4 with credit delays its
+    windowed form."""
     g = _golden(name)
     w = si.config(name)
     say(f"full-size {name}: grid engine{' (general form)' if general else ''}")
