@@ -1249,13 +1249,13 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     // for at least 256 records.
     struct ResLayout {
         bool ok = false;
-        int64_t off[20] = {};
-        int64_t bytes = 0, rcap = 0, scap = 0, ovf = 0;
-        int32_t threads = 256;
+        int64_t off[24] = {};
+        int64_t bytes = 0, rcap = 0, scap = 0, ovf = 0, tcap = 0, tovf = 0;
+        int32_t threads = 256, nw = 1;
     } res;
     {
         const int64_t nsrc_all = (int64_t)m + (int64_t)s_link.size();
-        bool ok = !fair && m <= 65535 && nsrc_all <= 65535 && bmax <= 255;
+        bool ok = !fair && m <= 65535 && nsrc_all <= 65535 && bmax <= 64;
         int64_t qmax = 0;  // request records one cycle can need
         for (int32_t l : fsrc) {
             ok = ok && fifo_mask[l] + 1 <= 32768 && (int64_t)nports_tail[l] * bmax <= 65533 && nports_tail[l] <= 255;
@@ -1280,18 +1280,30 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         }
         res.off[18] = o;  // input ports per link (round-robin)
         o += a4((c->arb & SIM_ARB_ROUND_ROBIN) ? m : 0);
+        int32_t sbw = 1;  // widest stream link: windows of ranges per stream
+        for (int32_t f : s_link)
+            for (int32_t sc = 0; sc < c->S; sc++) sbw = std::max(sbw, c->bw[(size_t)sc * m + f]);
+        res.nw = (sbw + simgpu::kResWindow - 1) / simgpu::kResWindow;
+        res.off[19] = o;  // a check result per stream window
+        o += a4(2 * (int64_t)s_link.size() * res.nw);
+        res.tcap = std::min<int64_t>(m, 256);  // per-target words of a cycle's targets
+        res.tovf = (int64_t)m - res.tcap;
+        o = (o + 7) & ~(int64_t)7;  // 64-bit words first
+        res.off[20] = o;
+        o += 14 * res.tcap;
+        o = (o + 7) & ~(int64_t)7;
         res.off[17] = o;  // request records last
         const int64_t room = kLds - 1024;  // room for the static LDS
         const int want = c->S > 512 ? 4 : c->S > 256 ? 2 : 1;
         for (int k = want; k >= 1 && ok && !res.ok; k--) {
             const int64_t avail = room / k - o;
-            const int64_t rcap = std::min<int64_t>({qmax, avail / 28, 4096});
+            const int64_t rcap = std::min<int64_t>({qmax, avail / 30, 4096});
             if (rcap < std::min<int64_t>(qmax, 256)) continue;
             res.ok = true;
             res.rcap = std::max<int64_t>(rcap, 1);
             res.scap = scap;
             res.ovf = std::max<int64_t>(0, qmax - res.rcap);
-            res.bytes = o + 28 * res.rcap;
+            res.bytes = o + 30 * res.rcap;
             res.threads = k == 1 ? 1024 : k == 2 ? 512 : 256;
         }
     }
@@ -1470,11 +1482,14 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     d.req_slots = (int32_t)lr;
     // lane engines: rings of the traffic links only, in lane order
     if (engine != simgpu::kEngineWorkgroup && engine != simgpu::kEngineResident) d.fifo_total = (int32_t)lf;
-    for (int i = 0; i < 20; i++) d.wr_off[i] = (int32_t)res.off[i];
+    for (int i = 0; i < 24; i++) d.wr_off[i] = (int32_t)res.off[i];
     d.wr_rcap = (int32_t)res.rcap;
     d.wr_scap = (int32_t)res.scap;
     d.wr_ovf = res.ovf;
     d.wr_threads = res.threads;
+    d.wr_nw = res.nw;
+    d.wr_tcap = (int32_t)res.tcap;
+    d.wr_tovf = res.tovf;
     sim_status st;
     auto &own = c->dev_static;
 #define UP(vec, field)                                         \
@@ -1644,6 +1659,13 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
             sl.add(&DevNet::wr_ogl, ov);
             sl.add(&DevNet::wr_osrc, ov);
             sl.add(&DevNet::wr_og, ov);
+            sl.add(&DevNet::wr_osrcid, ov);
+        }
+        if (res.tovf > 0) {
+            const size_t tv = S * (size_t)res.tovf;
+            sl.add(&DevNet::wr_otmask, tv);
+            sl.add(&DevNet::wr_otseg, tv);
+            sl.add(&DevNet::wr_otq, tv);
         }
     }
     if (engine == simgpu::kEngineWorkgroup) {

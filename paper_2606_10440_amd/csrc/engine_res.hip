@@ -19,13 +19,16 @@
 // A cycle, each step ended by a workgroup barrier:
 //   A   the live-source bitmap is compacted into the source list;
 //   R   every listed source reserves a contiguous block of request records
-//       and fills it.  A FIFO link offers its ready heads (ready times never
+//       and fills it (FIFO links on the first half of the waves, streams on
+//       the second).  A FIFO link offers its ready heads (ready times never
 //       decrease along a FIFO, so the ready heads are a prefix and each
 //       chunk of heads can be tested alone): the first chunk inline, the
 //       later ones through a spill list, one chunk per thread after a
-//       barrier.  A stream offers its released lines: its ranges are read a
-//       window at a time with every predecessor count of the window, then
-//       the lines are counted, reserved and written in a second walk;
+//       barrier.  A stream offers its released lines: each window of its
+//       next ranges is checked by its own thread (lines released in order
+//       from the window's start, and whether all are), and after the
+//       barrier the stream adds the windows up to the first one held back,
+//       reserves, and writes its records in a second walk;
 //   G0  every target that received requests gets a segment of the sorted
 //       index list and its grant count g = min(b, free slots, requests);
 //   G1  every request drops its record index into its target's segment;
@@ -47,17 +50,15 @@ namespace simgpu {
 namespace {
 
 constexpr int kC = 4;                        // FIFO heads per chunk (loads in flight together)
-constexpr int kW = 4;                        // stream ranges per window
+constexpr int kW = kResWindow;               // stream ranges per window
 constexpr int kE = 6;                        // predecessor descriptors per load batch
-constexpr int kB = 4;                        // grants per batch in the departure and append steps
 constexpr uint32_t kNoSpill = 0xFFFFFFFFu;   // spill entry that holds no chunk
 // rts (target << 16 | slot) of records that no target ranks
 constexpr uint32_t kTsSink = 0xFFFFFFFFu;    // leaves the network: the sink takes it
 constexpr uint32_t kTsHole = 0xFFFFFFFEu;    // reserved for a head that was not ready
-// rg: grant rank (< 256), with kDep set once the source lets it depart
+// rg: grant rank (< 64)
 constexpr uint16_t kNoGrant = 0xFFFFu;
 constexpr uint16_t kSinkGrant = 0x7FFFu;
-constexpr uint16_t kDep = 0x8000u;
 
 // A record field: entries below cap in LDS, the rest in HBM.
 template <typename T>
@@ -88,6 +89,8 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
     uint8_t *bwl = res_lds + d.wr_off[5];
     uint8_t *rrl = res_lds + d.wr_off[6];                                  // ARB == 1
     uint8_t *npl = res_lds + d.wr_off[18];                                 // ARB == 1: input ports at the tail
+    uint16_t *sres = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[19]); // stream window checks
+    const int nwin = d.wr_nw;                                              // windows per stream
     uint16_t *capl = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[7]);
     uint16_t *latl = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[8]);
     uint16_t *crl = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[9]);  // CR: credit delay
@@ -110,6 +113,15 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
     const Split<uint32_t> gl{reinterpret_cast<uint32_t *>(rb + 20 * rcap), d.wr_ogl + ov, rcap};
     const Split<uint16_t> rport{reinterpret_cast<uint16_t *>(rb + 24 * rcap), d.wr_osrc + ov, rcap};  // ARB == 1
     const Split<uint16_t> rg{reinterpret_cast<uint16_t *>(rb + 26 * rcap), d.wr_og + ov, rcap};
+    const Split<uint16_t> rsrc{reinterpret_cast<uint16_t *>(rb + 28 * rcap), d.wr_osrcid + ov, rcap};
+    // per target of the cycle (index in the target list): its segment, its
+    // tail at the cycle's start, and the grant ranks that depart
+    const uint32_t tcap = (uint32_t)d.wr_tcap;
+    const size_t tov = (size_t)s * d.wr_tovf;
+    unsigned char *tb = res_lds + d.wr_off[20];
+    const Split<unsigned long long> tmask{reinterpret_cast<unsigned long long *>(tb), d.wr_otmask + tov, tcap};
+    const Split<uint32_t> tseg{reinterpret_cast<uint32_t *>(tb + 8 * tcap), d.wr_otseg + tov, tcap};
+    const Split<uint16_t> tq{reinterpret_cast<uint16_t *>(tb + 12 * tcap), d.wr_otq + tov, tcap};
 
     uint4 *frec = d.wr_frec + (size_t)s * d.fifo_total;
     uint32_t *delivered = d.delivered + (size_t)s * d.nflows;
@@ -191,8 +203,6 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
         constexpr int kF = kThreads / 2;
         const bool fside = tid < kF;
         const int a0 = fside ? tid : tid - kF;
-        const int na = fside ? nfl : nst;
-        auto src_at = [&](int a) -> int { return fside ? (int)alist[a] : (int)alist[nsrc - 1 - a]; };
         // ---------------------------------------------------------------- R
         // Heads k0 .. k0 + kC - 1 (below lim) of FIFO link l with head
         // position h: their entries, and how many of them are ready (the
@@ -235,6 +245,7 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                     continue;
                 }
                 rx[q] = e[u].x;
+                rsrc[q] = (uint16_t)l;
                 if (ARB == 1) rport[q] = (uint16_t)ph;
                 if (tg[u] < 0) {  // the sink takes everything
                     rpp[q] = -tg[u] - 1;  // the flow
@@ -256,93 +267,88 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                 }
             }
         };
-        for (int a = a0; a < na; a += kF) {
-            const int sid = src_at(a);
-            if (fside) {
+        if (fside) {
+            for (int a = a0; a < nfl; a += kF) {
+                const int sid = (int)alist[a];
                 const int l = sid;
-                const uint32_t h = qh[l];
-                const uint32_t occ = (uint16_t)(qt[l] - h);
-                const int b = bwl[l];
-                if (CR) {
-                    // slots of lines that left at least credit cycles ago are free
-                    // again; the next return is an event of the time advance
-                    const int base = d.fifo_off[l], mask = d.fifo_mask[l];
-                    const uint32_t D = crl[l];
-                    uint32_t c = qc[l];
-                    while ((uint16_t)c != (uint16_t)h && frec[base + (int)(c & (uint32_t)mask)].y + D <= t) c++;
-                    qc[l] = (uint16_t)c;
-                    if ((uint16_t)c != (uint16_t)h) atomicMin(&sh_next, frec[base + (int)(c & (uint32_t)mask)].y + D);
-                    if ((uint16_t)c == qt[l]) clear_live(l);  // nothing held: every credit is back
-                }
-                const int lim = b < (int)occ ? b : (int)occ;
-                if (lim == 0) {
-                    sqn[l] = 0;
-                    continue;
-                }
-                // the first chunk's readiness decides the reservation: its ready
-                // heads, or (all of it ready) every head up to lim
-                uint4 e[kC];
-                const int nrd0 = load_heads(l, h, 0, lim, e);
-                const bool more = nrd0 == kC && lim > kC;
-                const uint32_t nres = more ? (uint32_t)lim : (uint32_t)nrd0;
-                const uint32_t q0 = nres ? atomicAdd(&sh_nreq, nres) : 0u;
-                post_heads(l, 0, nrd0, nrd0, e, q0);
-                int nr = nrd0;
-                if (more) {
-                    const uint32_t nch = (uint32_t)((lim - 1) / kC);
-                    const uint32_t s0 = atomicAdd(&sh_nspill, nch);
-                    if (s0 + nch <= scap) {
-                        for (uint32_t c = 0; c < nch; c++) spill[s0 + c] = ((uint32_t)l << 8) | (uint32_t)(kC * (c + 1));
-                    } else {  // the list is full: the later chunks inline
-                        for (uint32_t c = 0; s0 + c < scap && c < nch; c++) spill[s0 + c] = kNoSpill;
-                        bool open = true;
-                        for (int k0 = kC; k0 < lim; k0 += kC) {
-                            const int nfill = lim - k0 < kC ? lim - k0 : kC;
-                            int n = 0;
-                            if (open) {
-                                uint4 e2[kC];
-                                n = load_heads(l, h, k0, lim, e2);
-                                post_heads(l, k0, n, nfill, e2, q0);
-                            } else {  // past the first head that is not ready
-                                for (int u = 0; u < nfill; u++) rts[q0 + (uint32_t)(k0 + u)] = kTsHole;
+                    const uint32_t h = qh[l];
+                    const uint32_t occ = (uint16_t)(qt[l] - h);
+                    const int b = bwl[l];
+                    if (CR) {
+                        // slots of lines that left at least credit cycles ago are free
+                        // again; the next return is an event of the time advance
+                        const int base = d.fifo_off[l], mask = d.fifo_mask[l];
+                        const uint32_t D = crl[l];
+                        uint32_t c = qc[l];
+                        while ((uint16_t)c != (uint16_t)h && frec[base + (int)(c & (uint32_t)mask)].y + D <= t) c++;
+                        qc[l] = (uint16_t)c;
+                        if ((uint16_t)c != (uint16_t)h) atomicMin(&sh_next, frec[base + (int)(c & (uint32_t)mask)].y + D);
+                        if ((uint16_t)c == qt[l]) clear_live(l);  // nothing held: every credit is back
+                    }
+                    const int lim = b < (int)occ ? b : (int)occ;
+                    if (lim == 0) {
+                        sqn[l] = 0;
+                        continue;
+                    }
+                    // the first chunk's readiness decides the reservation: its ready
+                    // heads, or (all of it ready) every head up to lim
+                    uint4 e[kC];
+                    const int nrd0 = load_heads(l, h, 0, lim, e);
+                    const bool more = nrd0 == kC && lim > kC;
+                    const uint32_t nres = more ? (uint32_t)lim : (uint32_t)nrd0;
+                    const uint32_t q0 = nres ? atomicAdd(&sh_nreq, nres) : 0u;
+                    post_heads(l, 0, nrd0, nrd0, e, q0);
+                    int nr = nrd0;
+                    if (more) {
+                        const uint32_t nch = (uint32_t)((lim - 1) / kC);
+                        const uint32_t s0 = atomicAdd(&sh_nspill, nch);
+                        if (s0 + nch <= scap) {
+                            for (uint32_t c = 0; c < nch; c++) spill[s0 + c] = ((uint32_t)l << 8) | (uint32_t)(kC * (c + 1));
+                        } else {  // the list is full: the later chunks inline
+                            for (uint32_t c = 0; s0 + c < scap && c < nch; c++) spill[s0 + c] = kNoSpill;
+                            bool open = true;
+                            for (int k0 = kC; k0 < lim; k0 += kC) {
+                                const int nfill = lim - k0 < kC ? lim - k0 : kC;
+                                int n = 0;
+                                if (open) {
+                                    uint4 e2[kC];
+                                    n = load_heads(l, h, k0, lim, e2);
+                                    post_heads(l, k0, n, nfill, e2, q0);
+                                } else {  // past the first head that is not ready
+                                    for (int u = 0; u < nfill; u++) rts[q0 + (uint32_t)(k0 + u)] = kTsHole;
+                                }
+                                nr += n;
+                                open = n == kC;
                             }
-                            nr += n;
-                            open = n == kC;
                         }
                     }
-                }
-                sqn[l] = (q0 << 8) | (uint32_t)nr;
-            } else {
-                const int j = sid - m;
+                    sqn[l] = (q0 << 8) | (uint32_t)nr;
+            }
+        } else {
+            // stream windows: window w of a live stream is its ranges
+            // R0 + w kW ... (at most kW, the first from the cursor's offset);
+            // each is checked by its own thread: how many lines from its
+            // start are released in order (capped at b), and whether all are
+            for (int i = a0; i < nst * nwin; i += kThreads - kF) {
+                const int a = i / nwin, w = i - a * nwin;
+                const int j = (int)alist[nsrc - 1 - a] - m;
                 const int f = d.s_link[j];
-                const int src = m + j;
-                const int R0 = cur_rng[j];
-                const uint32_t o0 = cur_off[j];
                 const int rend = d.s_rend[j];
                 const int b = bwl[f];
-                if (R0 >= rend) {
-                    clear_live(src);
-                    sqn[src] = 0;
-                    continue;
-                }
-                // count: ranges in order, kW at a time, with every predecessor
-                // count of the window; the lines from o0 on whose predecessors
-                // have all delivered (a prefix), at most b
-                int R = R0;
-                uint32_t o = o0;
-                int cnt = 0;
-                bool go = true;
-                while (go && cnt < b) {
-                    const int nwr = rend - R < kW ? rend - R : kW;
+                const int Rw = cur_rng[j] + w * kW;
+                uint32_t res = 0;
+                if (Rw < rend && w * kW < b) {
+                    const int nwr = rend - Rw < kW ? rend - Rw : kW;
+                    const uint32_t ow = w == 0 ? cur_off[j] : 0u;
                     uint32_t len[kW];
                     int pq[kW + 1];
 #pragma unroll
                     for (int u = 0; u < kW; u++)
                         if (u < nwr) {
-                            len[u] = d.r_len[R + u];
-                            pq[u] = d.r_pd[R + u];
+                            len[u] = d.r_len[Rw + u];
+                            pq[u] = d.r_pd[Rw + u];
                         }
-                    pq[kW] = d.r_pd[R + nwr];
+                    pq[kW] = d.r_pd[Rw + nwr];
 #pragma unroll
                     for (int u = 1; u < kW; u++)
                         if (u >= nwr) pq[u] = pq[kW];
@@ -350,7 +356,7 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
 #pragma unroll
                     for (int u = 0; u < kW; u++) A[u] = 0xFFFFFFFFu;
                     // the first batch holds only the first range's descriptors, so
-                    // that a stream held back at its first line (the usual case)
+                    // that a window held back at its first line (the usual case)
                     // stops after one batch
                     const int qe0 = pq[1] - pq[0] < kE ? pq[1] : pq[0] + kE;
                     for (int q0 = pq[0], qe = qe0; q0 < pq[kW];
@@ -370,38 +376,74 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                         for (int v = 0; v < kE; v++) {
                             const int q = q0 + v;
                             if (q >= qe) continue;
-                            // lines o + i (first range) or i with delivered > base + i
+                            // lines ow + i (first range) or i with delivered > base + i
                             // (per line) or > base (per chunk)
-                            const uint32_t b0 = bs[v] + (q < pq[1] ? (o & d.pd_omask) : 0u);
+                            const uint32_t b0 = bs[v] + (q < pq[1] ? (ow & d.pd_omask) : 0u);
                             const uint32_t allow = dv[v] > b0 ? (d.pd_omask ? dv[v] - b0 : 0xFFFFFFFFu) : 0u;
 #pragma unroll
                             for (int u = 0; u < kW; u++)
                                 if (q >= pq[u] && q < pq[u + 1]) A[u] = A[u] < allow ? A[u] : allow;
                         }
                         if (q0 == pq[0] && qe >= pq[1]) {  // the first range is known: taken whole?
-                            const uint32_t need = (uint32_t)(b - cnt) < len[0] - o ? (uint32_t)(b - cnt) : len[0] - o;
+                            const uint32_t need = (uint32_t)b < len[0] - ow ? (uint32_t)b : len[0] - ow;
                             if (A[0] < need) break;
                         }
                     }
-                    bool stop = false;
+                    uint32_t cnt = 0;
+                    bool whole = true;
 #pragma unroll
                     for (int u = 0; u < kW; u++) {
-                        if (u >= nwr || stop) continue;
-                        const uint32_t off = u == 0 ? o : 0u;
-                        uint32_t n = (uint32_t)(b - cnt) < len[u] - off ? (uint32_t)(b - cnt) : len[u] - off;
-                        n = n < A[u] ? n : A[u];
-                        cnt += (int)n;
-                        if (n == 0u || off + n < len[u]) stop = true;  // held back by a predecessor or by b
+                        if (u >= nwr || !whole || cnt >= (uint32_t)b) continue;
+                        const uint32_t off = u == 0 ? ow : 0u;
+                        const uint32_t n = len[u] - off < A[u] ? len[u] - off : A[u];
+                        cnt += n;
+                        if (n == 0u || n < len[u] - off) whole = false;  // held back by a predecessor
                     }
-                    go = !stop && R + nwr < rend;
-                    R += nwr;
-                    o = 0;
+                    res = (cnt < (uint32_t)b ? cnt : (uint32_t)b) | (whole ? 0x8000u : 0u);
                 }
+                sres[i] = (uint16_t)res;
+            }
+        }
+        __syncthreads();
+        if (fside) {  // the spilled chunks of long FIFO offers
+            const uint32_t nsp = sh_nspill < scap ? sh_nspill : scap;
+            for (uint32_t i = (uint32_t)a0; i < nsp; i += kF) {
+                const uint32_t v = spill[i];
+                if (v == kNoSpill) continue;
+                const int l = (int)(v >> 8), k0 = (int)(v & 255u);
+                const uint32_t h = qh[l];
+                const uint32_t occ = (uint16_t)(qt[l] - h);
+                const int b = bwl[l];
+                const int lim = b < (int)occ ? b : (int)occ;
+                const uint32_t q0 = sqn[l] >> 8;
+                uint4 e[kC];
+                const int n = load_heads(l, h, k0, lim, e);
+                post_heads(l, k0, n, lim - k0 < kC ? lim - k0 : kC, e, q0);
+                if (n) atomicMax(&sqn[l], (q0 << 8) | (uint32_t)(k0 + n));
+            }
+        } else {  // streams: their windows combined, records reserved and written
+            for (int a = a0; a < nst; a += kThreads - kF) {
+                const int src = (int)alist[nsrc - 1 - a];
+                const int j = src - m;
+                const int f = d.s_link[j];
+                const int R0 = cur_rng[j];
+                const uint32_t o0 = cur_off[j];
+                const int rend = d.s_rend[j];
+                const int b = bwl[f];
+                int cnt = 0;
+                for (int w = 0; w < nwin && w * kW < b && R0 + w * kW < rend; w++) {
+                    const uint32_t v = sres[a * nwin + w];
+                    cnt += (int)(v & 0x7FFFu);
+                    if (cnt >= b || (v & 0x8000u) == 0u) break;
+                }
+                if (cnt > b) cnt = b;
                 if (cnt == 0) {
-                    clear_live(src);  // asleep until a flow it waits on delivers
+                    clear_live(src);  // done, or asleep until a flow it waits on delivers
                     sqn[src] = 0;
                     continue;
                 }
+                int R;
+                uint32_t o;
                 // reserve and write: the same walk takes whole ranges until cnt lines
                 const uint32_t q0 = atomicAdd(&sh_nreq, (uint32_t)cnt);
                 const uint32_t slot0 = take_slots(f, (uint32_t)cnt);
@@ -435,6 +477,7 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                             const uint32_t q = q0 + (uint32_t)k + i;
                             const uint32_t x = st[u] + off + i;
                             rx[q] = x;
+                            rsrc[q] = (uint16_t)src;
                             rpp[q] = rp[u];
                             if (ARB == 1) rport[q] = (uint16_t)(P - 1u);
                             rkey[q] = ARB == 0 ? x : ((uint32_t)k + i) * P + rot;
@@ -449,49 +492,37 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
             }
         }
         __syncthreads();
-        {   // the spilled chunks of long FIFO offers
-            const uint32_t nsp = sh_nspill < scap ? sh_nspill : scap;
-            for (uint32_t i = (uint32_t)tid; i < nsp; i += kThreads) {
-                const uint32_t v = spill[i];
-                if (v == kNoSpill) continue;
-                const int l = (int)(v >> 8), k0 = (int)(v & 255u);
-                const uint32_t h = qh[l];
-                const uint32_t occ = (uint16_t)(qt[l] - h);
-                const int b = bwl[l];
-                const int lim = b < (int)occ ? b : (int)occ;
-                const uint32_t q0 = sqn[l] >> 8;
-                uint4 e[kC];
-                const int n = load_heads(l, h, k0, lim, e);
-                post_heads(l, k0, n, lim - k0 < kC ? lim - k0 : kC, e, q0);
-                if (n) atomicMax(&sqn[l], (q0 << 8) | (uint32_t)(k0 + n));
-            }
-        }
-        __syncthreads();
         // ---------------------------------------------------------------- G
         const int ntgt = (int)sh_ntgt;
         const uint32_t nreq = sh_nreq;
         for (int a = tid; a < ntgt; a += kThreads) {  // G0: segments and grant counts
             const int f = (int)tlist[a];
             const uint32_t c = rq[f];
-            const int occ = (int)(uint16_t)(qt[f] - (CR ? qc[f] : qh[f]));
+            const uint16_t tl = qt[f];
+            const int occ = (int)(uint16_t)(tl - (CR ? qc[f] : qh[f]));
             int g = bwl[f];
             if ((int)capl[f] - occ < g) g = (int)capl[f] - occ;
             if ((int)c < g) g = (int)c;
-            kg[f] = atomicAdd(&sh_koff, c) | ((uint32_t)(g > 0 ? g : 0) << 24);
+            kg[f] = (uint32_t)a | ((uint32_t)(g > 0 ? g : 0) << 24);
+            tseg[a] = atomicAdd(&sh_koff, c);
+            tq[a] = tl;
+            tmask[a] = 0ull;
         }
         __syncthreads();
         for (uint32_t q = (uint32_t)tid; q < nreq; q += kThreads) {  // G1: indices into the segments
             const uint32_t ts = rts[q];
             if (ts >= kTsHole) continue;
-            sidx[(kg[ts >> 16] & 0xFFFFFFu) + (ts & 0xFFFFu)] = q;
+            sidx[tseg[kg[ts >> 16] & 0xFFFFFFu] + (ts & 0xFFFFu)] = q;
         }
         __syncthreads();
-        for (uint32_t q = (uint32_t)tid; q < nreq; q += kThreads) {  // G2: ranks and grants
+        // G2: ranks and grants; a request left without a grant cuts its
+        // source's departing prefix there (the count in sqn drops to its index)
+        for (uint32_t q = (uint32_t)tid; q < nreq; q += kThreads) {
             const uint32_t ts = rts[q];
             if (ts >= kTsHole) continue;
             const int f = (int)(ts >> 16);
             const uint32_t v = kg[f];
-            const uint32_t seg = v & 0xFFFFFFu, g = v >> 24;
+            const uint32_t seg = tseg[v & 0xFFFFFFu], g = v >> 24;
             const uint32_t c = rq[f];
             const uint32_t ki = rkey[q];
             uint32_t rank = 0;
@@ -501,61 +532,46 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                 rg[q] = (uint16_t)rank;
             } else {
                 rg[q] = kNoGrant;
+                const int src = (int)rsrc[q];
+                const uint32_t q0 = sqn[src] >> 8;
+                atomicMin(&sqn[src], (q0 << 8) | (q - q0));
             }
         }
         __syncthreads();
         // ---------------------------------------------------------------- D
-        for (int a = a0; a < na; a += kF) {
-            const int src = src_at(a);
+        // one request per thread: those before the first without a grant
+        // depart; the first request of a source moves the source on
+        for (uint32_t q = (uint32_t)tid; q < nreq; q += kThreads) {
+            const uint32_t ts = rts[q];
+            if (ts == kTsHole) continue;
+            const int src = (int)rsrc[q];
             const uint32_t v = sqn[src];
-            const int nr = (int)(v & 255u);
-            if (nr == 0) continue;
-            const uint32_t q0 = v >> 8;
-            // the longest granted prefix departs, kB grants read at a time
-            int dep = 0, sinks = 0;
-            for (int k0 = 0; k0 < nr; k0 += kB) {
-                uint16_t gr[kB];
-#pragma unroll
-                for (int u = 0; u < kB; u++) gr[u] = k0 + u < nr ? rg[q0 + (uint32_t)(k0 + u)] : kNoGrant;
-                int n = 0;
-                bool run = true;
-#pragma unroll
-                for (int u = 0; u < kB; u++) {
-                    run = run && gr[u] != kNoGrant;
-                    n += run ? 1 : 0;
-                }
-#pragma unroll
-                for (int u = 0; u < kB; u++) {
-                    if (u >= n) continue;
-                    const uint32_t q = q0 + (uint32_t)(k0 + u);
-                    if (gr[u] == kSinkGrant) {
-                        const int fl = rpp[q];
-                        comp[rx[q]] = t + 1;
-                        atomicAdd(&delivered[fl], 1u);
-                        sinks++;
-                        for (int w = d.fw_ptr[fl]; w < d.fw_ptr[fl + 1]; w++) set_live(m + d.fw_str[w]);
-                    } else {
-                        rg[q] = (uint16_t)(gr[u] | kDep);
-                    }
-                }
-                dep += n;
-                if (n < kB) break;
+            const uint32_t q0 = v >> 8, dep = v & 255u, k = q - q0;
+            if (k >= dep) continue;
+            if (ts == kTsSink) {
+                const int fl = rpp[q];
+                comp[rx[q]] = t + 1;
+                atomicAdd(&delivered[fl], 1u);
+                atomicAdd(&sh_ndone, 1u);
+                for (int w = d.fw_ptr[fl]; w < d.fw_ptr[fl + 1]; w++) set_live(m + d.fw_str[w]);
+            } else {
+                atomicOr(&tmask[kg[ts >> 16] & 0xFFFFFFu], 1ull << rg[q]);
             }
-            if (dep == 0) continue;
+            if (k != 0u) continue;
             sh_anydep = 1;
-            if (fside) {
+            if (src < m) {
                 const uint32_t h = qh[src];
                 if (CR) {  // a left entry keeps its slot until its credit is back
                     const int base = d.fifo_off[src], mask = d.fifo_mask[src];
-                    for (int k = 0; k < dep; k++) frec[base + (int)((h + (uint32_t)k) & (uint32_t)mask)].y = t;
+                    for (uint32_t i = 0; i < dep; i++) frec[base + (int)((h + i) & (uint32_t)mask)].y = t;
                 }
-                const uint16_t nh = (uint16_t)(h + (uint32_t)dep);
+                const uint16_t nh = (uint16_t)(h + dep);
                 qh[src] = nh;
                 if (!CR && nh == qt[src]) clear_live(src);  // emptied
             } else {
                 const int j = src - m;
                 int R = cur_rng[j];
-                uint32_t o = cur_off[j] + (uint32_t)dep;
+                uint32_t o = cur_off[j] + dep;
                 const int rend = d.s_rend[j];
                 bool go = R < rend;
                 while (go) {  // past the ranges it finished, kW lengths read at a time
@@ -579,53 +595,40 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                 cur_off[j] = o;
                 if (R == rend) clear_live(src);
             }
-            if (sinks) atomicAdd(&sh_ndone, (uint32_t)sinks);
         }
         __syncthreads();
         // ---------------------------------------------------------------- E
-        for (int a = tid; a < ntgt; a += kThreads) {
+        // one request per thread: a departing grant of rank r enters its
+        // target's FIFO at the tail the cycle started with plus the number of
+        // departing grants ranked before it
+        for (uint32_t q = (uint32_t)tid; q < nreq; q += kThreads) {
+            const uint32_t ts = rts[q];
+            if (ts >= kTsHole) continue;
+            const uint16_t r = rg[q];
+            if (r == kNoGrant) continue;
+            const int f = (int)(ts >> 16);
+            const uint32_t a = kg[f] & 0xFFFFFFu;
+            const unsigned long long dm = tmask[a];
+            if (((dm >> r) & 1ull) == 0ull) continue;
+            const uint32_t pos = (uint32_t)__popcll(dm & ((1ull << r) - 1ull));
+            const int base = d.fifo_off[f], mask = d.fifo_mask[f];
+            frec[base + (int)(((uint32_t)tq[a] + pos) & (uint32_t)mask)] =
+                make_uint4(rx[q], t + (uint32_t)latl[f], (uint32_t)rpp[q], 0u);
+        }
+        for (int a = tid; a < ntgt; a += kThreads) {  // and per target its tail and counters
             const int f = (int)tlist[a];
             rq[f] = 0;
-            const uint32_t v = kg[f];
-            const uint32_t seg = v & 0xFFFFFFu, g = v >> 24;
-            if (g == 0u) continue;
-            const int base = d.fifo_off[f], mask = d.fifo_mask[f];
-            const uint32_t ready = t + (uint32_t)latl[f];
-            uint32_t tl = qt[f];
-            uint32_t cnt = 0, last = 0;
-            for (uint32_t r0 = 0; r0 < g; r0 += kB) {  // the grants in rank order, kB at a time
-                uint32_t q[kB];
-                bool dp[kB];
-#pragma unroll
-                for (int u = 0; u < kB; u++) q[u] = r0 + u < g ? gl[seg + r0 + u] : 0u;
-#pragma unroll
-                for (int u = 0; u < kB; u++) dp[u] = r0 + u < g && (rg[q[u]] & kDep) != 0;
-                uint32_t x[kB], pp[kB];
-#pragma unroll
-                for (int u = 0; u < kB; u++)
-                    if (dp[u]) {
-                        x[u] = rx[q[u]];
-                        pp[u] = (uint32_t)rpp[q[u]];
-                    }
-#pragma unroll
-                for (int u = 0; u < kB; u++)
-                    if (dp[u]) {
-                        frec[base + (int)(tl & (uint32_t)mask)] = make_uint4(x[u], ready, pp[u], 0u);
-                        last = q[u];
-                        tl++;
-                        cnt++;
-                    }
-            }
-            if (cnt) {
-                set_live(f);
-                qt[f] = (uint16_t)tl;
-                atomicAdd(&tx[f], (unsigned long long)cnt);  // no read back: the counters only grow
-                atomicAdd(&busy[f], 1ull);
-                if (ARB == 1) {
-                    const uint32_t P = (uint32_t)npl[f];
-                    const uint32_t lp = rport[last];
-                    rrl[f] = (uint8_t)((lp + 1u) % P);
-                }
+            const unsigned long long dm = tmask[a];
+            if (dm == 0ull) continue;
+            const uint32_t cnt = (uint32_t)__popcll(dm);
+            set_live(f);
+            qt[f] = (uint16_t)(tq[a] + cnt);
+            atomicAdd(&tx[f], (unsigned long long)cnt);  // no read back: the counters only grow
+            atomicAdd(&busy[f], 1ull);
+            if (ARB == 1) {  // past the port of the last line appended
+                const uint32_t P = (uint32_t)npl[f];
+                const uint32_t lp = rport[gl[tseg[a] + (63u - (uint32_t)__clzll(dm))]];
+                rrl[f] = (uint8_t)((lp + 1u) % P);
             }
         }
         __syncthreads();

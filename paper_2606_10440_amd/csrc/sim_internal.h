@@ -186,13 +186,17 @@ struct DevNet {
     // cycle's request records of a scenario in LDS (byte offsets wr_off),
     // records past wr_rcap in a per-scenario HBM overflow area of wr_ovf
     // entries per field
-    int32_t wr_off[20];
-    int32_t wr_rcap, wr_scap, wr_threads;
-    int64_t wr_ovf;
+    int32_t wr_off[24];
+    int32_t wr_rcap, wr_scap, wr_threads, wr_nw;  // wr_nw: windows of kResWindow ranges per stream
+    int32_t wr_tcap;          // targets of a cycle whose per-target words are in LDS
+    int64_t wr_ovf, wr_tovf;  // overflow entries per scenario: records, targets
     uint4 *wr_frec;           // [S*fifo_total] FIFO entries {line, ready, path index, 0}
     uint32_t *wr_ox, *wr_okey, *wr_ots, *wr_osidx, *wr_ogl;  // [S*wr_ovf] overflow records
     int32_t *wr_opp;
-    uint16_t *wr_osrc, *wr_og;
+    uint16_t *wr_osrc, *wr_og, *wr_osrcid;
+    unsigned long long *wr_otmask;  // [S*wr_tovf] overflow per-target words
+    uint32_t *wr_otseg;
+    uint16_t *wr_otq;
 
     // outputs
     uint32_t *completion; // [S*T]
@@ -216,6 +220,9 @@ constexpr int kWaveMaxNF = 4;
 constexpr int kWaveMaxWpb = 8;
 // Registers cache up to this many predecessor descriptors of a stream's range.
 constexpr int kPredCache = 8;
+// Resident workgroup engine: a stream's ranges are checked this many at a time
+// (one thread per window).
+constexpr int kResWindow = 4;
 
 // Launch the engine for all scenarios on `stream`; returns a hipError_t value.
 int launch_engine(const DevNet &d, void *stream);
