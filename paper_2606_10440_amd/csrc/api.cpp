@@ -784,10 +784,13 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         if (nports_tail[l] > 64) rr_ports_fit = false;
     const bool any_preds = !pd_flow.empty();
 
-    // Engine choice.  Lane engine with FIFO rings in LDS when a scenario fits
-    // a workgroup's LDS; the compact b = 1 engine for large single-line-rate
+    // Engine choice.  Wave engine for small graphs batched many to a
+    // wavefront; lane engine with FIFO rings in LDS when a scenario fits a
+    // workgroup's LDS; the compact b = 1 engine for large single-line-rate
     // graphs; the lane engine with FIFO rings in HBM when only its mailboxes
-    // fit; else the generic workgroup engine.
+    // fit; else the workgroup engine, resident in LDS when its per-scenario
+    // state fits.  One large topology goes to the grid engine when its
+    // one-line or windowed form applies.
     auto align16 = [](int64_t v) { return (v + 15) & ~(int64_t)15; };
     const int64_t kLds = 160 * 1024;
     int64_t lf = 0;
@@ -1180,8 +1183,9 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                        (!any_preds || b1_deliv_lds) &&
                        (c->arb == SIM_ARB_LOWEST_ID || (rr_ports_fit && m < 65536));
     // credit delays above 1 are simulated by the wave engine (not together
-    // with per-chunk dependencies) and the workgroup engine; class-fair
-    // arbitration by the workgroup engine
+    // with per-chunk dependencies), the workgroup engine (both forms) and the
+    // grid engine's windowed form; class-fair arbitration by the generic
+    // workgroup engine
     const bool credits = !c->credit.empty();
     const bool fair = (c->arb & SIM_ARB_FAIR_CLASSES) != 0;
     // Grid engine (one scenario over many workgroups): nodes are split over
