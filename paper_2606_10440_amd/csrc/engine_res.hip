@@ -185,9 +185,38 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
     __syncthreads();
 
     uint64_t done = 0, processed = 0;  // meaningful in thread 0
-    while (sh_state == kRunRunning) {
-        const uint32_t t = sh_t;
-        // ---------------------------------------------------------------- A
+    uint32_t t = 0;
+    for (bool started = false;; started = true) {
+        // ------------------------------------------------------- time and A
+        // thread 0 advances the clock past the cycle just processed while
+        // every thread compacts the live sources of the next one
+        if (tid == 0 && started) {
+            processed++;
+            done += sh_ndone;
+            uint32_t nt = t;
+            int32_t state = kRunRunning;
+            if (done == (uint64_t)d.T) {
+                state = kRunOk;
+                d.makespan[s] = t + 1;
+            } else if (sh_anydep) {
+                nt = t + 1;
+            } else if (sh_next == kNever) {
+                state = kRunDeadlock;
+            } else {
+                nt = sh_next;
+            }
+            if (state == kRunRunning && (uint64_t)nt > d.max_cycles) state = kRunMaxCycles;
+            if (state == kRunRunning && processed > d.watchdog) state = kRunWatchdog;
+            sh_t = nt;
+            sh_state = state;
+            sh_next = kNever;
+            sh_anydep = 0;
+            sh_ndone = 0;
+            sh_ntgt = 0;
+            sh_nreq = 0;
+            sh_nspill = 0;
+            sh_koff = 0;
+        }
         // one source per thread: live FIFO links from the front of the list,
         // live streams from its back (a slot is a wave-wide count of one per
         // live lane)
@@ -197,6 +226,8 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                 else alist[nsrc - 1 - (int)atomicAdd(&sh_nalive_s, 1u)] = (uint16_t)i;
             }
         __syncthreads();
+        if (sh_state != kRunRunning) break;
+        t = sh_t;
         // FIFO links and streams take different code paths: the first half of
         // the workgroup's waves walks the links, the second half the streams
         const int nfl = (int)sh_nalive, nst = (int)sh_nalive_s;
@@ -632,35 +663,9 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
             }
         }
         __syncthreads();
-        // ---------------------------------------------------------------- time
-        if (tid == 0) {
-            processed++;
-            done += sh_ndone;
-            uint32_t nt = t;
-            int32_t state = kRunRunning;
-            if (done == (uint64_t)d.T) {
-                state = kRunOk;
-                d.makespan[s] = t + 1;
-            } else if (sh_anydep) {
-                nt = t + 1;
-            } else if (sh_next == kNever) {
-                state = kRunDeadlock;
-            } else {
-                nt = sh_next;
-            }
-            if (state == kRunRunning && (uint64_t)nt > d.max_cycles) state = kRunMaxCycles;
-            if (state == kRunRunning && processed > d.watchdog) state = kRunWatchdog;
-            sh_t = nt;
-            sh_state = state;
-            sh_next = kNever;
-            sh_anydep = 0;
-            sh_ndone = 0;
+        if (tid == 0) {  // the compaction counts start over (read into registers above)
             sh_nalive = 0;
             sh_nalive_s = 0;
-            sh_ntgt = 0;
-            sh_nreq = 0;
-            sh_nspill = 0;
-            sh_koff = 0;
         }
         __syncthreads();
     }
