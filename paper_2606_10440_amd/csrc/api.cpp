@@ -1546,6 +1546,41 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         UP(fw_ptr, fw_ptr);
         UP(fw_str, fw_str);
     }
+    if (engine == simgpu::kEngineResident) {
+        // descriptor spans shared by consecutive ranges of a stream whose
+        // descriptors are equal
+        std::vector<char> first(r_start.size() + 1, 0);
+        for (int32_t b0 : s_rbeg) first[b0] = 1;
+        std::vector<int32_t> rpb(r_start.size() + 1, 0), rpe(r_start.size() + 1, 0), pdf;
+        std::vector<uint32_t> pdb;
+        for (size_t j = 0; j < r_start.size(); j++) {
+            const int32_t a1 = r_pd[j], b1 = r_pd[j + 1];
+            bool same = j > 0 && !first[j] && a1 - r_pd[j - 1] == b1 - a1;
+            for (int32_t q = 0; same && q < b1 - a1; q++)
+                same = pd_flow[r_pd[j - 1] + q] == pd_flow[a1 + q] && pd_base[r_pd[j - 1] + q] == pd_base[a1 + q];
+            if (same) {
+                rpb[j] = rpb[j - 1];
+                rpe[j] = rpe[j - 1];
+                continue;
+            }
+            rpb[j] = (int32_t)pdf.size();
+            for (int32_t q = a1; q < b1; q++) {
+                pdf.push_back(pd_flow[q]);
+                pdb.push_back(pd_base[q]);
+            }
+            rpe[j] = (int32_t)pdf.size();
+        }
+        if (pdf.empty()) {
+            pdf.push_back(0);
+            pdb.push_back(0);
+        }
+        int32_t *tmp_wr_rpb, *tmp_wr_rpe, *tmp_wr_pdf;
+        uint32_t *tmp_wr_pdb;
+        UP(rpb, wr_rpb);
+        UP(rpe, wr_rpe);
+        UP(pdf, wr_pdf);
+        UP(pdb, wr_pdb);
+    }
     if (fair && !R.cls.empty()) {
         uint8_t *tmp_line_cls;
         UP(R.cls, line_cls);

@@ -372,33 +372,37 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                     const int nwr = rend - Rw < kW ? rend - Rw : kW;
                     const uint32_t ow = w == 0 ? cur_off[j] : 0u;
                     uint32_t len[kW];
-                    int pq[kW + 1];
+                    int pb[kW], pe[kW];  // descriptor spans (repeated ones shared)
 #pragma unroll
                     for (int u = 0; u < kW; u++)
                         if (u < nwr) {
                             len[u] = d.r_len[Rw + u];
-                            pq[u] = d.r_pd[Rw + u];
+                            pb[u] = d.wr_rpb[Rw + u];
+                            pe[u] = d.wr_rpe[Rw + u];
                         }
-                    pq[kW] = d.r_pd[Rw + nwr];
+                    int qend = pe[0];  // spans never go back: the window's are [pb[0], qend)
 #pragma unroll
-                    for (int u = 1; u < kW; u++)
-                        if (u >= nwr) pq[u] = pq[kW];
+                    for (int u = 1; u < kW; u++) {
+                        if (u < nwr) qend = pe[u];
+                        else pb[u] = pe[u] = qend;
+                    }
+                    // allowance per range: lines ow + i (first range) or i with
+                    // delivered > base + i (per line) or > base (per chunk)
                     uint32_t A[kW];
 #pragma unroll
                     for (int u = 0; u < kW; u++) A[u] = 0xFFFFFFFFu;
                     // the first batch holds only the first range's descriptors, so
                     // that a window held back at its first line (the usual case)
                     // stops after one batch
-                    const int qe0 = pq[1] - pq[0] < kE ? pq[1] : pq[0] + kE;
-                    for (int q0 = pq[0], qe = qe0; q0 < pq[kW];
-                         q0 = qe, qe = pq[kW] - qe < kE ? pq[kW] : qe + kE) {
+                    const int qe0 = pe[0] - pb[0] < kE ? pe[0] : pb[0] + kE;
+                    for (int q0 = pb[0], qe = qe0; q0 < qend; q0 = qe, qe = qend - qe < kE ? qend : qe + kE) {
                         int fl[kE];
                         uint32_t bs[kE], dv[kE];
 #pragma unroll
                         for (int v = 0; v < kE; v++)
                             if (q0 + v < qe) {
-                                fl[v] = d.pd_flow[q0 + v];
-                                bs[v] = d.pd_base[q0 + v];
+                                fl[v] = d.wr_pdf[q0 + v];
+                                bs[v] = d.wr_pdb[q0 + v];
                             }
 #pragma unroll
                         for (int v = 0; v < kE; v++)
@@ -407,15 +411,16 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                         for (int v = 0; v < kE; v++) {
                             const int q = q0 + v;
                             if (q >= qe) continue;
-                            // lines ow + i (first range) or i with delivered > base + i
-                            // (per line) or > base (per chunk)
-                            const uint32_t b0 = bs[v] + (q < pq[1] ? (ow & d.pd_omask) : 0u);
-                            const uint32_t allow = dv[v] > b0 ? (d.pd_omask ? dv[v] - b0 : 0xFFFFFFFFu) : 0u;
+                            const uint32_t b0 = bs[v] + (ow & d.pd_omask);
+                            const uint32_t al0 = dv[v] > b0 ? (d.pd_omask ? dv[v] - b0 : 0xFFFFFFFFu) : 0u;
+                            const uint32_t al1 = dv[v] > bs[v] ? (d.pd_omask ? dv[v] - bs[v] : 0xFFFFFFFFu) : 0u;
 #pragma unroll
-                            for (int u = 0; u < kW; u++)
-                                if (q >= pq[u] && q < pq[u + 1]) A[u] = A[u] < allow ? A[u] : allow;
+                            for (int u = 0; u < kW; u++) {
+                                const uint32_t al = u == 0 ? al0 : al1;
+                                if (q >= pb[u] && q < pe[u]) A[u] = A[u] < al ? A[u] : al;
+                            }
                         }
-                        if (q0 == pq[0] && qe >= pq[1]) {  // the first range is known: taken whole?
+                        if (q0 == pb[0] && qe >= pe[0]) {  // the first range is known: taken whole?
                             const uint32_t need = (uint32_t)b < len[0] - ow ? (uint32_t)b : len[0] - ow;
                             if (A[0] < need) break;
                         }

@@ -50,6 +50,12 @@ struct DevNet {
     const uint32_t *r_len;        // [nr] lines in range
     const int32_t *r_path;        // [nr] index of the range's first hop in path_link
     const int32_t *r_pd;          // [nr+1] predecessor descriptors of the range
+    // resident engine: the same descriptors with a range that repeats the
+    // descriptors of the range before it in its stream sharing that range's
+    // span (a group's stores all wait on the group's loads): range j's
+    // descriptors are wr_pdf/wr_pdb[wr_rpb[j] .. wr_rpe[j] - 1]
+    const int32_t *wr_rpb, *wr_rpe, *wr_pdf;
+    const uint32_t *wr_pdb;
     // predecessor descriptor: line start+o may be injected once flow pd_flow has
     // delivered more than pd_base + (o & pd_omask) lines (flows deliver in id
     // order).  pd_omask is all ones for per-line dependencies; 0 for per-chunk
