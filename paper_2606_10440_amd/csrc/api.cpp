@@ -1292,6 +1292,10 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         o += a4(2 * (int64_t)s_link.size() * res.nw);
         res.tcap = std::min<int64_t>(m, 256);  // per-target words of a cycle's targets
         res.tovf = (int64_t)m - res.tcap;
+        res.off[21] = o;  // per stream: its link, one past its last range
+        o += 4 * (int64_t)s_link.size();
+        res.off[22] = o;
+        o += 4 * (int64_t)s_link.size();
         o = (o + 7) & ~(int64_t)7;  // 64-bit words first
         res.off[20] = o;
         o += 14 * res.tcap;

@@ -97,6 +97,8 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
     uint32_t *sqn = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[10]); // first record << 8 | count
     int32_t *cur_rng = reinterpret_cast<int32_t *>(res_lds + d.wr_off[11]);
     uint32_t *cur_off = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[12]);
+    int32_t *s_lnk = reinterpret_cast<int32_t *>(res_lds + d.wr_off[21]);  // a stream's link
+    int32_t *s_end = reinterpret_cast<int32_t *>(res_lds + d.wr_off[22]);  // one past its last range
     uint32_t *livew = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[13]);
     uint16_t *alist = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[14]);
     uint16_t *tlist = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[15]);
@@ -163,6 +165,8 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
     for (int j = tid; j < ns; j += kThreads) {
         cur_rng[j] = d.s_rbeg[j];
         cur_off[j] = 0;
+        s_lnk[j] = d.s_link[j];
+        s_end[j] = d.s_rend[j];
     }
     for (int f = tid; f < d.nflows; f += kThreads) delivered[f] = 0;
     for (int j = tid; j < nw; j += kThreads) livew[j] = 0;
@@ -363,8 +367,8 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
             for (int i = a0; i < nst * nwin; i += kThreads - kF) {
                 const int a = i / nwin, w = i - a * nwin;
                 const int j = (int)alist[nsrc - 1 - a] - m;
-                const int f = d.s_link[j];
-                const int rend = d.s_rend[j];
+                const int f = s_lnk[j];
+                const int rend = s_end[j];
                 const int b = bwl[f];
                 const int Rw = cur_rng[j] + w * kW;
                 uint32_t res = 0;
@@ -391,10 +395,9 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                     uint32_t A[kW];
 #pragma unroll
                     for (int u = 0; u < kW; u++) A[u] = 0xFFFFFFFFu;
-                    // the first batch holds only the first range's descriptors, so
-                    // that a window held back at its first line (the usual case)
-                    // stops after one batch
-                    const int qe0 = pe[0] - pb[0] < kE ? pe[0] : pb[0] + kE;
+                    // a window held back at its first line (the usual case) stops
+                    // after the batch that holds the first range's descriptors
+                    const int qe0 = qend - pb[0] < kE ? qend : pb[0] + kE;
                     for (int q0 = pb[0], qe = qe0; q0 < qend; q0 = qe, qe = qend - qe < kE ? qend : qe + kE) {
                         int fl[kE];
                         uint32_t bs[kE], dv[kE];
@@ -461,10 +464,10 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
             for (int a = a0; a < nst; a += kThreads - kF) {
                 const int src = (int)alist[nsrc - 1 - a];
                 const int j = src - m;
-                const int f = d.s_link[j];
+                const int f = s_lnk[j];
                 const int R0 = cur_rng[j];
                 const uint32_t o0 = cur_off[j];
-                const int rend = d.s_rend[j];
+                const int rend = s_end[j];
                 const int b = bwl[f];
                 int cnt = 0;
                 for (int w = 0; w < nwin && w * kW < b && R0 + w * kW < rend; w++) {
@@ -608,7 +611,7 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                 const int j = src - m;
                 int R = cur_rng[j];
                 uint32_t o = cur_off[j] + dep;
-                const int rend = d.s_rend[j];
+                const int rend = s_end[j];
                 bool go = R < rend;
                 while (go) {  // past the ranges it finished, kW lengths read at a time
                     uint32_t len[kW];
