@@ -69,7 +69,7 @@ def _torus(S, seed, nbytes):
                       nbytes=nbytes)
 
 
-@pytest.mark.parametrize("engine", ["wave", "lane", "lanehbm", "workgroup"])
+@pytest.mark.parametrize("engine", ["wave", "lane", "lanehbm", "workgroup", "resident"])
 def test_noalloc_matches_run_twice(simmod, engine):
     _pair(simmod, _torus(24, 300, 128 * 16 * 24), engine)
     _pair(simmod, _torus(5, 301, 128 * 16 * 6), engine)
