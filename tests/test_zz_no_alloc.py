@@ -80,6 +80,13 @@ def test_noalloc_compact_engine_twice(simmod):
     _pair(simmod, si.fat_tree(4, nbytes=128 * 7, cap=3, lat_lo=1, lat_hi=4, arb=0), "b1")
 
 
+def test_noalloc_grid_engine_twice(simmod):
+    # one topology over several cooperating workgroups (one-line form), then
+    # a smaller one
+    _pair(simmod, si.scaled(si.config("C2"), bytes=128 * 8 * 40), "grid")
+    _pair(simmod, si.scaled(si.config("C1"), bytes=128 * 4 * 6), "grid")
+
+
 def test_noalloc_c5_then_smaller(simmod):
     w = si.take_scenarios(si.config("C5"), range(0, 4096, 16))
     _pair(simmod, si.scaled(w, bytes=128 * 16 * 64), "wave")
