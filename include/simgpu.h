@@ -170,8 +170,9 @@ sim_status sim_create(int32_t n_nodes, int32_t n_endpoints, const int32_t *row_p
  * the base model): credits that travel back to the sender take time, which
  * also bounds how soon a link's state can affect its upstream neighbours.
  * Returns of owed credits are events of the time advance.  Delays above 1
- * are simulated by the wave engine (not together with SIM_DEP_CHUNK) and the
- * workgroup engine.  Any loaded workload is dropped:
+ * are simulated by the wave engine (not together with SIM_DEP_CHUNK), the
+ * workgroup engine (generic and LDS-resident) and, for one large topology,
+ * the grid engine's windowed form.  Any loaded workload is dropped:
  * call sim_load_* again before sim_run.  The array is copied.
  */
 sim_status sim_set_credit(sim_ctx *ctx, const int32_t *credit);
