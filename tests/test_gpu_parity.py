@@ -341,11 +341,19 @@ def test_full_size_digest(simmod, torch_cuda, name):
     assert _digest(r.busy_cycles[0].cpu().numpy().astype("<u8")) == g["busy_cycles_sha256"][0]
 
 
-@pytest.mark.parametrize("name", ["C5", "C5_chunk", "C5_rhd", "C5_dbt", "C5_ag", "C5_credit", "NOC2_ag"])
-def test_full_size_batched_digest(simmod, torch_cuda, name):
+@pytest.mark.parametrize("name,engine", [("C5", None), ("C5_chunk", None), ("C5_rhd", None), ("C5_dbt", None),
+                                         ("C5_ag", None), ("C5_credit", None), ("NOC2_ag", None),
+                                         ("C5_credit", "resident"), ("C5_rhd", "resident"),
+                                         ("NOC2_ag", "workgroup")])
+def test_full_size_batched_digest(simmod, torch_cuda, name, engine, monkeypatch):
+    """Every scenario of the batched workloads against the oracle's golden
+    digests: on the engine the library picks, and on the LDS-resident and
+    generic workgroup engines where another one is picked."""
     g = _golden(name)
     w = si.config(name)
-    say(f"full-size {name}: running 4096 scenarios on GPU")
+    if engine:
+        monkeypatch.setenv("SIMGPU_ENGINE", engine)
+    say(f"full-size {name}: running {w.n_scenarios} scenarios on GPU ({engine or 'default engine'})")
     r = run_gpu(simmod, w)
     assert r.status == 0
     mk = r.makespan.cpu().numpy()
