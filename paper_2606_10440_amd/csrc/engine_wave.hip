@@ -514,7 +514,7 @@ __global__ void __launch_bounds__(64 * kWaveMaxWpb) engine_wave(DevNet d) {
                     fmax = tb ? max(fmax, fe[k]) : fmax;
                 }
                 const uint32_t smin = sword[0], smax = sword[nS > 0u ? nS - 1u : 0u];
-                first = (nS == 0u) | (fmax < smin) ? 1u : ((nF == 0u) | (smax < fmin) ? 2u : 0u);
+                first = ((nS == 0u) | (fmax < smin)) ? 1u : (((nF == 0u) | (smax < fmin)) ? 2u : 0u);
             }
             const bool pairwise = ARB == 0 && (BMW <= 2 || __ballot(first == 0u) != 0ull);
 #pragma unroll
