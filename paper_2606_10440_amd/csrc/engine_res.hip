@@ -6,18 +6,21 @@
 // LDS holds, per link: head and tail positions (with credit delays also the
 // credit position) as 16-bit counters over rings of at most 2^15 entries,
 // the number of requests received this cycle, bandwidth, capacity, latency,
-// the round-robin pointer and input-port count and this cycle's (segment
-// offset, grant count);
-// per source: where its block of request records starts and how many of them
-// it made; per stream: its cursor; the active sets (a live-source bitmap and
-// the cycle's source and target lists); the cycle's request records (line,
-// path index, key, target and slot, input port, grant) and the index lists of
-// the grant phase.  Records and index entries past the LDS capacity go to a
-// per-scenario overflow area in HBM.  FIFO entries stay in HBM, one 16-byte
-// record {line, ready cycle, path index} each.
+// the round-robin pointer and input-port count, and this cycle's target-list
+// index and grant count; per source: where its block of request records
+// starts and how many of them depart; per stream: its cursor, link and last
+// range; the active sets (a live-source bitmap and the cycle's source and
+// target lists); per target of the cycle: its index segment, its tail at the
+// cycle's start and the mask of departing grant ranks; the cycle's request
+// records (line, path index, key, target and slot, source, input port,
+// grant rank) and the grant step's two index lists.  Records, index entries
+// and per-target words past their LDS capacity go to a per-scenario
+// overflow area in HBM.  FIFO entries stay in HBM, one 16-byte record
+// {line, ready cycle, path index} each.
 //
 // A cycle, each step ended by a workgroup barrier:
-//   A   the live-source bitmap is compacted into the source list;
+//   A   thread 0 advances the clock past the previous cycle while every
+//       thread compacts the live-source bitmap into the source list;
 //   R   every listed source reserves a contiguous block of request records
 //       and fills it (FIFO links on the first half of the waves, streams on
 //       the second).  A FIFO link offers its ready heads (ready times never
@@ -33,12 +36,18 @@
 //       index list and its grant count g = min(b, free slots, requests);
 //   G1  every request drops its record index into its target's segment;
 //   G2  every request ranks itself by the keys in its segment (keys are
-//       distinct per target) and, with rank r < g, takes grant rank r;
-//   D   every source departs its longest granted prefix; lines leaving their
-//       last hop complete (cycle + 1) and bump their flow's delivered count;
-//   E   every target appends its departing grants in rank order
-//       (ready = cycle + L).
-// Then the time advance of the workgroup engine: the next cycle is t + 1 if
+//       distinct per target) and, with rank r < g, takes grant rank r; one
+//       left without a grant cuts its source's departing count to its own
+//       index (the source's longest granted prefix departs);
+//   D   one request per thread: it departs if its index is below its
+//       source's count; a line leaving its last hop completes (cycle + 1)
+//       and bumps its flow's delivered count, any other sets its rank's bit
+//       in its target's mask; a source's first request moves the source on;
+//   E   one request per thread: a departing grant enters its target's FIFO
+//       (ready = cycle + L) at the tail the cycle started with plus the
+//       number of departing grants ranked before it; per target, the tail,
+//       the link counters and the round-robin pointer move on.
+// The time advance is the workgroup engine's: the next cycle is t + 1 if
 // anything departed, else the earliest FIFO-head ready time or credit
 // return, else the scenario has deadlocked.
 #include <hip/hip_runtime.h>
@@ -85,7 +94,7 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
     uint16_t *qc = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[2]);   // CR
     uint32_t *rqw = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[3]);  // two 16-bit counts per word
     uint16_t *rq = reinterpret_cast<uint16_t *>(rqw);
-    uint32_t *kg = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[4]);   // segment | g << 24
+    uint32_t *kg = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[4]);   // target-list index | g << 24
     uint8_t *bwl = res_lds + d.wr_off[5];
     uint8_t *rrl = res_lds + d.wr_off[6];                                  // ARB == 1
     uint8_t *npl = res_lds + d.wr_off[18];                                 // ARB == 1: input ports at the tail
@@ -94,7 +103,7 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
     uint16_t *capl = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[7]);
     uint16_t *latl = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[8]);
     uint16_t *crl = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[9]);  // CR: credit delay
-    uint32_t *sqn = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[10]); // first record << 8 | count
+    uint32_t *sqn = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[10]); // first record << 8 | count (departing, after G2)
     int32_t *cur_rng = reinterpret_cast<int32_t *>(res_lds + d.wr_off[11]);
     uint32_t *cur_off = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[12]);
     int32_t *s_lnk = reinterpret_cast<int32_t *>(res_lds + d.wr_off[21]);  // a stream's link
