@@ -67,7 +67,8 @@ typedef enum {
  * and hands the turn to the other class.  After a cycle in which it appended
  * lines, the pointer names the class other than that of the last line
  * appended.  Load requests of sim_load_memcpy are control messages; every
- * other line is data.  The workgroup engine simulates SIM_ARB_FAIR_CLASSES. */
+ * other line is data.  The workgroup engine (generic and LDS-resident)
+ * simulates SIM_ARB_FAIR_CLASSES. */
 typedef enum { SIM_ARB_LOWEST_ID = 0, SIM_ARB_ROUND_ROBIN = 1, SIM_ARB_FAIR_CLASSES = 2 } sim_arb;
 
 /* Collectives (the paper's textbook algorithms, Sec. 1 and 2.2: ring,

@@ -1184,8 +1184,8 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
                        (c->arb == SIM_ARB_LOWEST_ID || (rr_ports_fit && m < 65536));
     // credit delays above 1 are simulated by the wave engine (not together
     // with per-chunk dependencies), the workgroup engine (both forms) and the
-    // grid engine's windowed form; class-fair arbitration by the generic
-    // workgroup engine
+    // grid engine's windowed form; class-fair arbitration by the workgroup
+    // engine (both forms)
     const bool credits = !c->credit.empty();
     const bool fair = (c->arb & SIM_ARB_FAIR_CLASSES) != 0;
     // Grid engine (one scenario over many workgroups): nodes are split over
@@ -1259,7 +1259,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
     } res;
     {
         const int64_t nsrc_all = (int64_t)m + (int64_t)s_link.size();
-        bool ok = !fair && m <= 65535 && nsrc_all <= 65535 && bmax <= 64;
+        bool ok = m <= 65535 && nsrc_all <= 65535 && bmax <= 64;
         int64_t qmax = 0;  // request records one cycle can need
         for (int32_t l : fsrc) {
             ok = ok && fifo_mask[l] + 1 <= 32768 && (int64_t)nports_tail[l] * bmax <= 65533 && nports_tail[l] <= 255;
@@ -1296,6 +1296,8 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         o += 4 * (int64_t)s_link.size();
         res.off[22] = o;
         o += 4 * (int64_t)s_link.size();
+        res.off[23] = o;  // class-fair arbitration: the class whose turn it is per link
+        o += a4(fair ? m : 0);
         o = (o + 7) & ~(int64_t)7;  // 64-bit words first
         res.off[20] = o;
         o += 14 * res.tcap;
@@ -1305,13 +1307,14 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         const int want = c->S > 512 ? 4 : c->S > 256 ? 2 : 1;
         for (int k = want; k >= 1 && ok && !res.ok; k--) {
             const int64_t avail = room / k - o;
-            const int64_t rcap = std::min<int64_t>({qmax, avail / 30, 4096});
+            const int64_t rb = fair ? 32 : 30;  // record bytes (class-fair: a count of requests ahead)
+            const int64_t rcap = std::min<int64_t>({qmax, avail / rb, 4096});
             if (rcap < std::min<int64_t>(qmax, 256)) continue;
             res.ok = true;
             res.rcap = std::max<int64_t>(rcap, 1);
             res.scap = scap;
             res.ovf = std::max<int64_t>(0, qmax - res.rcap);
-            res.bytes = o + 30 * res.rcap;
+            res.bytes = o + rb * res.rcap;
             res.threads = k == 1 ? 1024 : k == 2 ? 512 : 256;
         }
     }
@@ -1703,6 +1706,7 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
             sl.add(&DevNet::wr_osrc, ov);
             sl.add(&DevNet::wr_og, ov);
             sl.add(&DevNet::wr_osrcid, ov);
+            if (fair) sl.add(&DevNet::wr_oaux, ov);
         }
         if (res.tovf > 0) {
             const size_t tv = S * (size_t)res.tovf;

@@ -78,7 +78,9 @@ struct Split {
     __device__ __forceinline__ T &operator[](uint32_t q) const { return q < cap ? lds[q] : hbm[q - cap]; }
 };
 
-template <int ARB, bool CR, int kThreads>
+// FAIR: class-fair arbitration (control and data lines take turns at a
+// link), picked target by target instead of ranked request by request.
+template <int ARB, bool CR, bool FAIR, int kThreads>
 __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
     extern __shared__ __align__(16) unsigned char res_lds[];
     const int s = blockIdx.x;
@@ -108,6 +110,8 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
     uint32_t *cur_off = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[12]);
     int32_t *s_lnk = reinterpret_cast<int32_t *>(res_lds + d.wr_off[21]);  // a stream's link
     int32_t *s_end = reinterpret_cast<int32_t *>(res_lds + d.wr_off[22]);  // one past its last range
+    uint8_t *cpl = res_lds + d.wr_off[23];  // FAIR: the class whose turn it is at each link
+    const uint8_t *__restrict__ lcls = d.line_cls;  // FAIR: 1 control, 0 data (null: all data)
     uint32_t *livew = reinterpret_cast<uint32_t *>(res_lds + d.wr_off[13]);
     uint16_t *alist = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[14]);
     uint16_t *tlist = reinterpret_cast<uint16_t *>(res_lds + d.wr_off[15]);
@@ -125,6 +129,8 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
     const Split<uint16_t> rport{reinterpret_cast<uint16_t *>(rb + 24 * rcap), d.wr_osrc + ov, rcap};  // ARB == 1
     const Split<uint16_t> rg{reinterpret_cast<uint16_t *>(rb + 26 * rcap), d.wr_og + ov, rcap};
     const Split<uint16_t> rsrc{reinterpret_cast<uint16_t *>(rb + 28 * rcap), d.wr_osrcid + ov, rcap};
+    // FAIR: a request's count of requests of its source ahead of it at its target
+    const Split<uint16_t> raux{reinterpret_cast<uint16_t *>(rb + 30 * rcap), d.wr_oaux + ov, rcap};
     // per target of the cycle (index in the target list): its segment, its
     // tail at the cycle's start, and the grant ranks that depart
     const uint32_t tcap = (uint32_t)d.wr_tcap;
@@ -165,6 +171,7 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
             rrl[l] = 0;
             npl[l] = (uint8_t)d.nports_tail[l];
         }
+        if (FAIR) cpl[l] = 0;
         capl[l] = (uint16_t)d.cap[sm + l];
         latl[l] = (uint16_t)d.lat[sm + l];
         tx[l] = 0;
@@ -565,6 +572,62 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
         __syncthreads();
         // G2: ranks and grants; a request left without a grant cuts its
         // source's departing prefix there (the count in sqn drops to its index)
+        if constexpr (FAIR) {
+            // target by target, picks in turn: each takes, among the requests
+            // with no request of the same source ahead of them at this link,
+            // the lowest key of the class whose turn it is (of either class if
+            // none), and hands the turn to the other class
+            auto cls_of = [&](uint32_t q) -> uint32_t { return lcls ? (uint32_t)lcls[rx[q]] : 0u; };
+            for (int a = tid; a < ntgt; a += kThreads) {
+                const int f = (int)tlist[a];
+                const uint32_t seg = tseg[a], g = kg[f] >> 24, c = rq[f];
+                for (uint32_t i = 0; i < c; i++) {
+                    const uint32_t qi = sidx[seg + i];
+                    const uint16_t si = rsrc[qi];
+                    uint32_t ahead = 0;
+                    for (uint32_t jj = 0; jj < c; jj++) {
+                        const uint32_t qj = sidx[seg + jj];
+                        ahead += (rsrc[qj] == si && qj < qi) ? 1u : 0u;
+                    }
+                    raux[qi] = (uint16_t)ahead;
+                }
+                uint32_t turn = cpl[f];
+                for (uint32_t pos = 0; pos < g; pos++) {
+                    uint32_t best = 0xFFFFFFFFu, any = 0xFFFFFFFFu, kb = 0xFFFFFFFFu, ka = 0xFFFFFFFFu;
+                    for (uint32_t i = 0; i < c; i++) {
+                        const uint32_t qi = sidx[seg + i];
+                        if (raux[qi] != 0u) continue;  // picked, or not yet its source's head
+                        const uint32_t ki = rkey[qi];
+                        if (ki < ka) {
+                            ka = ki;
+                            any = qi;
+                        }
+                        if (ki < kb && cls_of(qi) == turn) {
+                            kb = ki;
+                            best = qi;
+                        }
+                    }
+                    const uint32_t qp = best != 0xFFFFFFFFu ? best : any;
+                    raux[qp] = 0xFFFFu;
+                    const uint16_t sp = rsrc[qp];
+                    for (uint32_t i = 0; i < c; i++) {  // the source's next request moves up
+                        const uint32_t qi = sidx[seg + i];
+                        if (raux[qi] != 0xFFFFu && rsrc[qi] == sp) raux[qi] = (uint16_t)(raux[qi] - 1u);
+                    }
+                    gl[seg + pos] = qp;
+                    rg[qp] = (uint16_t)pos;
+                    turn = 1u - cls_of(qp);
+                }
+                for (uint32_t i = 0; i < c; i++) {  // the others get no grant
+                    const uint32_t qi = sidx[seg + i];
+                    if (raux[qi] == 0xFFFFu) continue;
+                    rg[qi] = kNoGrant;
+                    const int src = (int)rsrc[qi];
+                    const uint32_t q0 = sqn[src] >> 8;
+                    atomicMin(&sqn[src], (q0 << 8) | (qi - q0));
+                }
+            }
+        } else
         for (uint32_t q = (uint32_t)tid; q < nreq; q += kThreads) {
             const uint32_t ts = rts[q];
             if (ts >= kTsHole) continue;
@@ -678,6 +741,10 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
                 const uint32_t lp = rport[gl[tseg[a] + (63u - (uint32_t)__clzll(dm))]];
                 rrl[f] = (uint8_t)((lp + 1u) % P);
             }
+            if (FAIR) {  // the other class than the last line appended
+                const uint32_t ql = gl[tseg[a] + (63u - (uint32_t)__clzll(dm))];
+                cpl[f] = (uint8_t)(1u - (lcls ? (uint32_t)lcls[rx[ql]] : 0u));
+            }
         }
         __syncthreads();
         if (tid == 0) {  // the compaction counts start over (read into registers above)
@@ -693,28 +760,33 @@ __global__ void __launch_bounds__(kThreads, 4) engine_res(DevNet d) {
     }
 }
 
-template <int ARB, bool CR, int NT>
+template <int ARB, bool CR, bool FAIR, int NT>
 hipError_t launch_res3(const DevNet &d, hipStream_t st) {
-    auto k = engine_res<ARB, CR, NT>;
+    auto k = engine_res<ARB, CR, FAIR, NT>;
     if (d.lds_bytes > 65536)
         (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
     hipLaunchKernelGGL(k, dim3((unsigned)d.S), dim3(NT), (unsigned)d.lds_bytes, st, d);
     return hipGetLastError();
 }
 
-template <int ARB, bool CR>
+template <int ARB, bool CR, bool FAIR>
 hipError_t launch_res2(const DevNet &d, hipStream_t st) {
-    if (d.wr_threads >= 1024) return launch_res3<ARB, CR, 1024>(d, st);
-    if (d.wr_threads >= 512) return launch_res3<ARB, CR, 512>(d, st);
-    return launch_res3<ARB, CR, 256>(d, st);
+    if (d.wr_threads >= 1024) return launch_res3<ARB, CR, FAIR, 1024>(d, st);
+    if (d.wr_threads >= 512) return launch_res3<ARB, CR, FAIR, 512>(d, st);
+    return launch_res3<ARB, CR, FAIR, 256>(d, st);
+}
+
+template <int ARB, bool CR>
+hipError_t launch_res1(const DevNet &d, hipStream_t st) {
+    return (d.arb & 2) ? launch_res2<ARB, CR, true>(d, st) : launch_res2<ARB, CR, false>(d, st);
 }
 
 }  // namespace
 
 hipError_t launch_resident(const DevNet &d, hipStream_t st) {
     const bool cr = d.credit != nullptr;
-    if (d.arb & 1) return cr ? launch_res2<1, true>(d, st) : launch_res2<1, false>(d, st);
-    return cr ? launch_res2<0, true>(d, st) : launch_res2<0, false>(d, st);
+    if (d.arb & 1) return cr ? launch_res1<1, true>(d, st) : launch_res1<1, false>(d, st);
+    return cr ? launch_res1<0, true>(d, st) : launch_res1<0, false>(d, st);
 }
 
 }  // namespace simgpu

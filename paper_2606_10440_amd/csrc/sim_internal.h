@@ -199,7 +199,7 @@ struct DevNet {
     uint4 *wr_frec;           // [S*fifo_total] FIFO entries {line, ready, path index, 0}
     uint32_t *wr_ox, *wr_okey, *wr_ots, *wr_osidx, *wr_ogl;  // [S*wr_ovf] overflow records
     int32_t *wr_opp;
-    uint16_t *wr_osrc, *wr_og, *wr_osrcid;
+    uint16_t *wr_osrc, *wr_og, *wr_osrcid, *wr_oaux;
     unsigned long long *wr_otmask;  // [S*wr_tovf] overflow per-target words
     uint32_t *wr_otseg;
     uint16_t *wr_otq;
