@@ -77,14 +77,14 @@ def test_credit_wave_torus(simmod, oracle_lib, arb, bws):
     w = si.torus2d(4, 4, n_scenarios=13, seed=170 + arb + len(bws), bws=bws, lat_lo=1, lat_hi=25,
                    depths=(1, 2, 3, 7, 32), nbytes=128 * 16 * 6, arb=arb)
     w.credit = np.random.default_rng(arb + 7 * len(bws)).integers(1, 14, size=len(w.bw)).astype(np.int32)
-    check_engine(simmod, oracle_lib, w, "wave")
+    check_engine(simmod, oracle_lib, w, "wave", must_run=True)
 
 
 @pytest.mark.parametrize("engine", ["wave", "workgroup", "workgroup_scan", "resident"])
 def test_credit_wave_full_size_sample(simmod, oracle_lib, engine):
     w = si.take_scenarios(si.config("C5"), [3, 7, 2048, 4000])
     w.credit = w.lat.copy()
-    check_engine(simmod, oracle_lib, w, engine)
+    check_engine(simmod, oracle_lib, w, engine, must_run=True)
 
 
 def test_credit_with_chunk_dependencies_not_on_wave(simmod, oracle_lib):
@@ -117,7 +117,7 @@ def test_windowed_grid(simmod, oracle_lib, arb, seed):
                        arb=arb)
     lo = np.maximum(2, w.lat - 3)
     w.credit = rng.integers(lo, w.lat + 4).astype(np.int32)
-    check_engine(simmod, oracle_lib, w, "grid")
+    check_engine(simmod, oracle_lib, w, "grid", must_run=True)
 
 
 @pytest.mark.parametrize("stride", [1, 8])
@@ -131,4 +131,4 @@ def test_windowed_grid_placement(simmod, oracle_lib, stride, seed, monkeypatch):
     w = si.fat_tree(4, lat_seed=seed, lat_lo=2, lat_hi=int(rng.integers(3, 16)), cap=int(rng.integers(2, 9)),
                     nbytes=128 * 16 * 3, arb=seed % 2, coll=si.COLL_ALLTOALL)
     w.credit = rng.integers(np.maximum(2, w.lat - 2), w.lat + 3).astype(np.int32)
-    check_engine(simmod, oracle_lib, w, "grid")
+    check_engine(simmod, oracle_lib, w, "grid", must_run=True)

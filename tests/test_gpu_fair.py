@@ -18,7 +18,8 @@ pytestmark = pytest.mark.gpu
 def test_fair_tiny_noc(simmod, oracle_lib, engine, seed):
     w = tiny_noc(100 + seed)
     w.arb |= si.ARB_FAIR_CLASSES
-    check_engine(simmod, oracle_lib, w, engine)
+    # both forms of the workgroup engine take class-fair arbitration
+    check_engine(simmod, oracle_lib, w, engine, must_run=engine in ("workgroup", "resident"))
 
 
 @pytest.mark.parametrize("get", [False, True])
@@ -48,4 +49,4 @@ def test_fair_noc_allgather_512k(simmod, oracle_lib, engine):
     wm = noc.memcpy_workload(w, noc.allgather_ops(lay, 4096, n_wg=32, unroll=4, window=64), name="ag_fair_512k")
     wm.arb = 1 | si.ARB_FAIR_CLASSES
     wm = noc.with_scenarios(wm, 4, seed=9)
-    check_engine(simmod, oracle_lib, wm, engine)
+    check_engine(simmod, oracle_lib, wm, engine, must_run=True)

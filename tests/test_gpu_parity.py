@@ -380,10 +380,11 @@ def test_full_size_batched_digest(simmod, torch_cuda, name, engine, monkeypatch)
 ENGINES = ["workgroup", "workgroup_scan", "lane", "lanehbm", "b1", "wave", "grid", "resident"]
 
 
-def run_engine(simmod, w, engine, txns=None):
+def run_engine(simmod, w, engine, txns=None, must_run=False):
     """Run with the engine forced; skip if the library refuses that engine
     for this workload (the wave engine's limits: at most 64 traffic links,
-    four flows per link, three feeders per link)."""
+    four flows per link, three feeders per link), or fail if must_run (the
+    engine is documented to take such workloads)."""
     old = os.environ.get("SIMGPU_ENGINE")
     if engine:
         os.environ["SIMGPU_ENGINE"] = engine
@@ -393,7 +394,7 @@ def run_engine(simmod, w, engine, txns=None):
         try:
             return run_gpu(simmod, w, txns=txns)
         except simmod.SimError as e:
-            if e.status == simmod.SIM_ERR_INVALID_ARG and "SIMGPU_ENGINE" in str(e):
+            if e.status == simmod.SIM_ERR_INVALID_ARG and "SIMGPU_ENGINE" in str(e) and not must_run:
                 pytest.skip(f"engine {engine} not usable for {w.name}")
             raise
     finally:
@@ -403,9 +404,9 @@ def run_engine(simmod, w, engine, txns=None):
             os.environ["SIMGPU_ENGINE"] = old
 
 
-def check_engine(simmod, oracle_lib, w, engine, txns=None):
+def check_engine(simmod, oracle_lib, w, engine, txns=None, must_run=False):
     say(f"engine {engine}: {w.name} S={w.n_scenarios}")
-    r = run_engine(simmod, w, engine, txns)
+    r = run_engine(simmod, w, engine, txns, must_run=must_run)
     m = w.n_links
     n_ok = 0
     for s in range(w.n_scenarios):
