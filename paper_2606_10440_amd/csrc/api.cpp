@@ -1291,6 +1291,8 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         res.off[19] = o;  // a check result per stream window
         o += a4(2 * (int64_t)s_link.size() * res.nw);
         res.tcap = std::min<int64_t>(m, 256);  // per-target words of a cycle's targets
+        if (const char *ev = std::getenv("SIMGPU_RES_TCAP"))  // tests: later targets' words in HBM
+            res.tcap = std::max<int64_t>(1, std::min<int64_t>(res.tcap, std::atoll(ev)));
         res.tovf = (int64_t)m - res.tcap;
         res.off[21] = o;  // per stream: its link, one past its last range
         o += 4 * (int64_t)s_link.size();
@@ -1312,6 +1314,8 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
             if (rcap < std::min<int64_t>(qmax, 256)) continue;
             res.ok = true;
             res.rcap = std::max<int64_t>(rcap, 1);
+            if (const char *ev = std::getenv("SIMGPU_RES_RCAP"))  // tests: later request records in HBM
+                res.rcap = std::max<int64_t>(1, std::min<int64_t>(res.rcap, std::atoll(ev)));
             res.scap = scap;
             res.ovf = std::max<int64_t>(0, qmax - res.rcap);
             res.bytes = o + rb * res.rcap;
