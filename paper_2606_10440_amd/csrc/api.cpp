@@ -1271,7 +1271,9 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         for (size_t i = 0; i < c->credit.size() && ok; i++) ok = c->credit[i] <= 65535;
         ok = ok && qmax < (1 << 24);
         auto a4 = [](int64_t v) { return (v + 3) & ~(int64_t)3; };
-        const int64_t scap = bmax > 4 ? std::min<int64_t>(512, (int64_t)m * ((bmax - 1) / 4)) : 0;
+        int64_t scap = bmax > 4 ? std::min<int64_t>(512, (int64_t)m * ((bmax - 1) / 4)) : 0;
+        if (const char *ev = std::getenv("SIMGPU_SPILL_CAP"))  // tests: a short spill list (later chunks inline)
+            scap = std::max<int64_t>(0, std::min<int64_t>(scap, std::atoll(ev)));
         const int64_t sizes[17] = {2 * (int64_t)m, 2 * (int64_t)m, credits ? 2 * (int64_t)m : 0, 2 * (int64_t)m,
                                    4 * (int64_t)m, m, (c->arb & SIM_ARB_ROUND_ROBIN) ? m : 0, 2 * (int64_t)m,
                                    2 * (int64_t)m, credits ? 2 * (int64_t)m : 0, 4 * nsrc_all,
@@ -1440,7 +1442,9 @@ sim_status finish_load(sim_ctx *c, Ranges &R) {
         const int64_t nsrc_all = (int64_t)m + (int64_t)s_link.size();
         const int64_t rcap = std::min<int64_t>(1024, nsrc_all * bmax);  // request list (8 B each)
         // spill list (4 B each): the chunks after the first of FIFO offers longer than one chunk
-        const int64_t scap = bmax > 4 ? std::min<int64_t>(512, (int64_t)m * ((bmax - 1) / 4)) : 0;
+        int64_t scap = bmax > 4 ? std::min<int64_t>(512, (int64_t)m * ((bmax - 1) / 4)) : 0;
+        if (const char *ev = std::getenv("SIMGPU_SPILL_CAP"))  // tests: a short spill list (later chunks inline)
+            scap = std::max<int64_t>(0, std::min<int64_t>(scap, std::atoll(ev)));
         // (+ one word: the request list is 8-byte aligned)
         const int64_t act = 4 * ((nsrc_all + 31) / 32 + nsrc_all + (int64_t)m + 1) + 8 * rcap + 4 * scap;
         const int64_t room = kLds - 1024;  // room for the static LDS

@@ -63,3 +63,20 @@ def test_resident_overflow_credit(simmod, oracle_lib, monkeypatch):
     w = si.take_scenarios(si.config("C5"), [5, 1000, 3001])
     w.credit = w.lat.copy()
     check_engine(simmod, oracle_lib, w, "resident", must_run=True)
+
+
+@pytest.mark.parametrize("engine", ["resident", "workgroup"])
+@pytest.mark.parametrize("scap", [0, 3])
+@pytest.mark.parametrize("fair", [False, True])
+def test_short_spill_list(simmod, oracle_lib, monkeypatch, engine, scap, fair):
+    """A FIFO offer longer than one chunk hands its later chunks to other
+    threads through a spill list; with the list cut short (SIMGPU_SPILL_CAP)
+    the chunks that do not fit are read inline by the link's own thread.
+    Router links of b = 64 on two generic GPUs make such offers."""
+    monkeypatch.setenv("SIMGPU_SPILL_CAP", str(scap))
+    w, lay = noc.gpu_noc(2)
+    wm = noc.memcpy_workload(w, noc.allgather_ops(lay, 512, n_wg=32, unroll=4, window=64), name="ag_64k_short_spill")
+    wm.arb = (si.ARB_FAIR_CLASSES | 1) if fair else 0
+    wm = noc.with_scenarios(wm, 3, seed=23)
+    say(f"{wm.name} {engine} scap={scap}")
+    check_engine(simmod, oracle_lib, wm, engine, must_run=True)
