@@ -93,6 +93,20 @@ def test_noalloc_c5_then_smaller(simmod):
     _pair(simmod, si.scaled(si.take_scenarios(w, range(7)), bytes=128 * 16 * 8), "wave")
 
 
+@pytest.mark.parametrize("engine", ["resident", "workgroup"])
+def test_noalloc_noc_fair_then_credit(simmod, engine):
+    """Class-fair arbitration on a small NoC running memcpy programs (four
+    scenarios), then a torus with credit delays, on both workgroup engines."""
+    from sim_inputs import noc
+    from tests.test_gpu_memcpy import tiny_noc
+    wm = tiny_noc(105, n_ops=8, max_lines=24)
+    wm.arb = 1 | si.ARB_FAIR_CLASSES
+    _pair(simmod, noc.with_scenarios(wm, 4, seed=3), engine)
+    t = _torus(4, 303, 128 * 16 * 4)
+    t.credit = t.lat.copy()
+    _pair(simmod, t, engine)
+
+
 def test_noalloc_rejects_oversized_scratch(simmod):
     w = _torus(4096, 302, 128 * 16)
     old = os.environ.get("SIMGPU_ENGINE")
