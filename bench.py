@@ -28,6 +28,7 @@ import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
+from paper_2606_10440_amd import build as _build  # noqa: E402  (compile flags, for the profile digests)
 
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, 8 TB/s
 COMPLETION_BYTES = 4            # u32 completion cycle written per line
@@ -100,7 +101,8 @@ def load_latency_profile(workload: str):
 def engine_source_hash(kernel: str = "") -> str:
     """Digest of the device sources a kernel is built from: its engine's
     .hip file (named after the kernel symbol, e.g. engine_wave) and the
-    headers it includes, transitively.  With no kernel name, every engine
+    headers it includes, transitively, with the flags each is compiled
+    with.  With no kernel name, every engine
     source.  Counters taken on other sources are not reported."""
     csrc = os.path.join(ROOT, "paper_2606_10440_amd", "csrc")
     m = re.search(r"(engine_[a-z0-9]+)", kernel or "")
@@ -120,6 +122,8 @@ def engine_source_hash(kernel: str = "") -> str:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode())
             h.update(fh.read())
+        # the flags it is compiled with
+        h.update(" ".join(_build.FLAGS[:4] + _build.EXTRA.get(f, [])).encode())
     return h.hexdigest()[:16]
 
 
